@@ -1,0 +1,455 @@
+"""Pins of the fp64 oracle against facts fixed outside it: closed forms,
+invariants, special cases that reduce to textbook definitions, hand-derived
+fixtures (tests/golden/) and brute force on tiny inputs.
+
+Each test names the plausible oracle mistake it would catch.
+"""
+import itertools
+import math
+import os
+
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import vla_oracle as O
+
+GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
+
+TINY = wl.ExpertConfig(
+    name="pin_tiny", n_layers=2, d_model=8, n_heads=2, head_dim=4, n_kv_heads=1,
+    d_ff=16, d_prefix=6, n_action=3, d_action=2, d_state=3,
+    pattern="self_cross", mlp="gelu", wtype="f32", prefix_len=3, n_steps=3, seed_base=77)
+
+
+def _rng(seed=0):
+    return np.random.default_rng(seed)
+
+
+# --- brute-force evaluators (pure-Python loops, tiny shapes only) ------------
+
+def bf_linear(u, W):
+    n, k = len(u), len(u[0])
+    return [[sum(float(u[i][j]) * float(W[o][j]) for j in range(k)) for o in range(len(W))]
+            for i in range(n)]
+
+
+def bf_attention(q, k, v, H, G, hd):
+    """Textbook softmax attention per head; head i uses K/V head i // (H/G)."""
+    n = len(q)
+    per = H // G
+    out = [[0.0] * (H * hd) for _ in range(n)]
+    for i in range(H):
+        g = i // per
+        for r in range(n):
+            scores = []
+            for key in range(len(k[g])):
+                s = sum(float(q[r][i * hd + c]) * float(k[g][key][c]) for c in range(hd))
+                scores.append(s / math.sqrt(hd))
+            mx = max(scores)
+            w = [math.exp(s - mx) for s in scores]
+            z = sum(w)
+            for c in range(hd):
+                out[r][i * hd + c] = sum(w[key] * float(v[g][key][c]) for key in range(len(w))) / z
+    return np.array(out)
+
+
+# --- Euler integrator (explicit Euler, t = 1 -> 0) -------------------------
+
+SCHED = np.array([1.0, 0.7, 0.45, 0.1, 0.0])   # non-uniform, decreasing
+
+
+def test_euler_zero_field_returns_noise():
+    """v = 0 must leave a0 untouched (catches a stray additive term)."""
+    a0 = _rng(1).standard_normal((5, 3))
+    out = O.euler_integrate(lambda a, k, t: np.zeros_like(a), a0, SCHED)
+    assert np.array_equal(out, a0)
+
+
+def test_euler_constant_field_endpoint():
+    """v = c gives a_T = a0 + (tau_T - tau_0) c exactly up to rounding
+    (catches a wrong sign of the step or a missing step)."""
+    a0 = _rng(2).standard_normal((5, 3))
+    c = _rng(3).standard_normal((5, 3))
+    out = O.euler_integrate(lambda a, k, t: c, a0, SCHED)
+    np.testing.assert_allclose(out, a0 + (SCHED[-1] - SCHED[0]) * c, rtol=0, atol=1e-14)
+
+
+def test_euler_linear_field_product():
+    """v = lam a gives a_T = prod_k (1 + lam dt_k) a0 (catches evaluating v at
+    the end of the interval instead of the start)."""
+    a0 = _rng(4).standard_normal((4, 2))
+    lam = -0.8
+    out = O.euler_integrate(lambda a, k, t: lam * a, a0, SCHED)
+    fac = np.prod([1 + lam * (SCHED[i + 1] - SCHED[i]) for i in range(len(SCHED) - 1)])
+    np.testing.assert_allclose(out, fac * a0, rtol=1e-14)
+
+
+def test_euler_time_argument_is_interval_start():
+    """v = t: a_T - a0 = sum_k dt_k tau_k (left Riemann sum)."""
+    a0 = np.zeros((1, 1))
+    out = O.euler_integrate(lambda a, k, t: np.full_like(a, t), a0, SCHED)
+    expect = sum((SCHED[i + 1] - SCHED[i]) * SCHED[i] for i in range(len(SCHED) - 1))
+    assert abs(out[0, 0] - expect) < 1e-15
+
+
+# --- time embedding --------------------------------------------------------------
+
+def test_time_embedding_golden():
+    """Hand-derived d = 4 values (catches a swapped sin/cos half or wrong periods)."""
+    rows = np.loadtxt(os.path.join(GOLDEN, "time_embedding.txt"))
+    for t, *e in rows:
+        np.testing.assert_allclose(O.time_embedding(t, 4), e, atol=1e-12)
+
+
+def test_time_embedding_zero_and_norm():
+    d = 1024
+    e0 = O.time_embedding(0.0, d)
+    assert np.array_equal(e0, np.concatenate([np.zeros(d // 2), np.ones(d // 2)]))
+    for t in (0.1, 0.37, 0.9, 1.0):
+        assert abs(np.sum(O.time_embedding(t, d) ** 2) - d / 2) < 1e-9
+
+
+def test_time_embedding_period_endpoints():
+    """First pair uses period 4e-3, last pair period 4 (geometric ends)."""
+    d, t = 16, 0.3
+    e = O.time_embedding(t, d)
+    assert abs(e[0] - math.sin(2 * math.pi * t / 4e-3)) < 1e-9
+    assert abs(e[d // 2 - 1] - math.sin(2 * math.pi * t / 4.0)) < 1e-12
+    assert abs(e[d - 1] - math.cos(2 * math.pi * t / 4.0)) < 1e-12
+
+
+# --- adaRMS -------------------------------------------------------------------------
+
+def test_adarms_unit_mean_square():
+    """gamma = beta = 0: mean(u^2) = m / (m + eps), m = mean(x^2)."""
+    x = _rng(5).standard_normal((6, 32))
+    eps = 1e-3
+    u = O.ada_rms(x, np.zeros(32), np.zeros(32), eps)
+    m = np.mean(x * x, axis=-1)
+    np.testing.assert_allclose(np.mean(u * u, axis=-1), m / (m + eps), rtol=1e-13)
+
+
+def test_adarms_scale_invariance_and_affine():
+    """u(kx) = u(x) at eps = 0, and gamma, beta enter as (1+gamma) and +beta."""
+    x = _rng(6).standard_normal((3, 16))
+    g, b = np.zeros(16), np.zeros(16)
+    base = O.ada_rms(x, g, b, 0.0)
+    np.testing.assert_allclose(O.ada_rms(7.5 * x, g, b, 0.0), base, rtol=1e-13)
+    np.testing.assert_allclose(O.ada_rms(x, np.ones(16), np.full(16, 0.5), 0.0), 2 * base + 0.5,
+                               rtol=1e-13)
+
+
+# --- activations ---------------------------------------------------------------------
+
+def test_activations_closed_forms():
+    from scipy.special import erf
+    x = np.linspace(-6, 6, 241)
+    exact_gelu = 0.5 * x * (1 + erf(x / np.sqrt(2)))
+    # the tanh form stays within 1e-3 of the erf form everywhere
+    assert np.max(np.abs(O.gelu_tanh(x) - exact_gelu)) < 1e-3
+    assert O.gelu_tanh(0.0) == 0.0
+    assert abs(O.silu(1.0) - 1.0 / (1.0 + math.exp(-1.0))) < 1e-15
+    assert O.silu(0.0) == 0.0
+    # gate vs up roles: the activation applies to the gate only
+    assert O.mlp_activation("geglu", 0.0, 5.0) == 0.0
+    assert O.mlp_activation("swiglu", 0.0, 5.0) == 0.0
+    assert O.mlp_activation("relu2glu", -1.0, 3.0) == 0.0
+    assert O.mlp_activation("relu2glu", 2.0, 3.0) == 12.0
+    assert abs(O.mlp_activation("swiglu", 1.0, 2.0) - 2.0 / (1.0 + math.exp(-1.0))) < 1e-15
+
+
+# --- linear / attention -----------------------------------------------------------
+
+def test_linear_bruteforce():
+    """[out][in] convention: y = u W^T (catches a transposed operand)."""
+    u = _rng(7).standard_normal((3, 5))
+    W = _rng(8).standard_normal((4, 5))
+    np.testing.assert_allclose(O.linear(u, W), bf_linear(u, W), rtol=1e-13)
+
+
+def test_softmax_rows_sum_to_one():
+    s = _rng(9).standard_normal((7, 40)) * 30
+    p = O.softmax_rows(s)
+    assert np.max(np.abs(p.sum(-1) - 1)) < 1e-15 * 40
+    assert np.all(p >= 0)
+
+
+@pytest.mark.parametrize("H,G", [(2, 1), (4, 2), (6, 3), (3, 3)])
+def test_attention_bruteforce_gqa(H, G):
+    """Grouped K/V heads: consecutive query heads share one K/V head."""
+    hd, n, keys = 4, 3, 5
+    r = _rng(10 + H + G)
+    q = r.standard_normal((n, H * hd))
+    k = r.standard_normal((G, keys, hd))
+    v = r.standard_normal((G, keys, hd))
+    np.testing.assert_allclose(O.attention(q, k, v, H, G, hd), bf_attention(q, k, v, H, G, hd),
+                               rtol=1e-12, atol=1e-14)
+
+
+def test_attention_single_key_returns_v():
+    r = _rng(11)
+    q = r.standard_normal((4, 2 * 8))
+    k = r.standard_normal((1, 1, 8))
+    v = r.standard_normal((1, 1, 8))
+    out = O.attention(q, k, v, 2, 1, 8)
+    for i in range(2):
+        np.testing.assert_allclose(out[:, i * 8:(i + 1) * 8], np.repeat(v[0], 4, axis=0), rtol=1e-15)
+
+
+def test_attention_zero_query_is_mean_of_values():
+    r = _rng(12)
+    k = r.standard_normal((2, 9, 4))
+    v = r.standard_normal((2, 9, 4))
+    out = O.attention(np.zeros((3, 4 * 4)), k, v, 4, 2, 4)
+    for i in range(4):
+        np.testing.assert_allclose(out[:, i * 4:(i + 1) * 4],
+                                   np.repeat(v[i // 2].mean(0, keepdims=True), 3, 0), rtol=1e-13)
+
+
+def test_attention_key_permutation_invariance():
+    r = _rng(13)
+    q = r.standard_normal((5, 8))
+    k = r.standard_normal((1, 11, 4))
+    v = r.standard_normal((1, 11, 4))
+    perm = r.permutation(11)
+    np.testing.assert_allclose(O.attention(q, k[:, perm], v[:, perm], 2, 1, 4),
+                               O.attention(q, k, v, 2, 1, 4), rtol=1e-12)
+
+
+def test_attention_query_permutation_equivariance():
+    r = _rng(14)
+    q = r.standard_normal((6, 8))
+    k = r.standard_normal((2, 6, 4))
+    v = r.standard_normal((2, 6, 4))
+    perm = r.permutation(6)
+    np.testing.assert_allclose(O.attention(q[perm], k, v, 2, 2, 4),
+                               O.attention(q, k, v, 2, 2, 4)[perm], rtol=1e-12)
+
+
+# --- ternary / quantiser ------------------------------------------------------------
+
+def test_pack_golden_and_unpack_roundtrip():
+    rows = np.loadtxt(os.path.join(GOLDEN, "ternary_pack.txt"), dtype=np.int64)
+    w = rows[:, :4]
+    packed = wl.pack_ternary(w)
+    assert packed[:, 0].tolist() == rows[:, 4].tolist()
+    assert np.array_equal(O.unpack_ternary(packed, 4), w)
+    big = wl.random_ternary((7, 64), 3)
+    assert np.array_equal(O.unpack_ternary(wl.pack_ternary(big), 64), big)
+
+
+def test_ternary_gemm_bruteforce_and_special_cases():
+    x = wl.random_int8((5, 32), 1)
+    w = wl.random_ternary((6, 32), 2)
+    acc = O.ternary_gemm(x, wl.pack_ternary(w), 32)
+    bf = [[sum(int(x[m, k]) * int(w[n, k]) for k in range(32)) for n in range(6)] for m in range(5)]
+    assert acc.tolist() == bf
+    ones = np.ones((3, 32), np.int8)
+    assert np.array_equal(O.ternary_gemm(x, wl.pack_ternary(0 * ones), 32), np.zeros((5, 3)))
+    assert np.array_equal(O.ternary_gemm(x, wl.pack_ternary(ones), 32)[:, 0], x.astype(np.int64).sum(1))
+    assert np.array_equal(O.ternary_gemm(x, wl.pack_ternary(-ones), 32)[:, 2], -x.astype(np.int64).sum(1))
+    onehot = np.zeros((2, 32), np.int8)
+    onehot[0, 5] = 1
+    onehot[1, 31] = -1
+    acc = O.ternary_gemm(x, wl.pack_ternary(onehot), 32)
+    assert np.array_equal(acc[:, 0], x[:, 5]) and np.array_equal(acc[:, 1], -x[:, 31].astype(np.int64))
+
+
+def test_ternary_gemm_extreme_fits_int32():
+    k = 6912
+    x = np.full((2, k), -128, np.int8)
+    w = np.ones((1, k), np.int8)
+    assert O.ternary_gemm(x, wl.pack_ternary(w), k)[0, 0] == -128 * k
+
+
+def _read_quant_golden():
+    rows, codes = [], []
+    for line in open(os.path.join(GOLDEN, "quantizer_ties.txt")):
+        if line.startswith("row:"):
+            rows.append([float(v) for v in line.split()[1:]])
+        elif line.startswith("codes:"):
+            codes.append([int(v) for v in line.split()[1:]])
+    return rows, codes
+
+
+def test_quantizer_golden_ties_floor_zero_row():
+    for row, code in zip(*_read_quant_golden()):
+        q, r = O.quantize_int8_rows(np.array([row], np.float32))
+        assert q[0].tolist() == code
+
+
+def test_quantizer_single_value_and_range():
+    u = np.zeros((2, 10), np.float32)
+    u[0, 3] = 0.37
+    u[1, 7] = -5.0
+    q, r = O.quantize_int8_rows(u)
+    assert q[0, 3] == 127 and q[1, 7] == -127 and np.count_nonzero(q) == 2
+    big = wl.random_matrix((50, 300), 5)
+    q, _ = O.quantize_int8_rows(big)
+    assert q.min() >= -127 and q.max() == 127
+
+
+def test_ternary_linear_integer_rows():
+    """A row whose absmax is 127 and whose values are integers quantises to
+    itself, so y = s_w * (u . w) exactly (catches a wrong dequant scale)."""
+    u = np.zeros((1, 8), np.float32)
+    u[0, :] = [127, -3, 5, 0, 2, -127, 1, 1]
+    w = wl.random_ternary((3, 8), 4)
+    y = O.ternary_linear(u, w, np.float32(0.5))
+    np.testing.assert_allclose(y, 0.5 * (u.astype(np.float64) @ w.T.astype(np.float64)), rtol=1e-15)
+
+
+# --- denormalise -------------------------------------------------------------------------
+
+def test_denormalize_identity_and_affine():
+    a = _rng(15).standard_normal((4, 3))
+    assert np.array_equal(O.denormalize(a), a)
+    np.testing.assert_allclose(O.denormalize(a, np.ones(3), 2 * np.ones(3)), 2 * a + 1, rtol=1e-15)
+
+
+# --- whole-expert special cases ------------------------------------------------------
+
+def _tiny_setup(cfg=TINY, B=1):
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, B)
+    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+    return W, inp, cache
+
+
+def test_prefix_kv_build_bruteforce_entries():
+    """cache[c][0|1][b][g][p][:] is head g's slice of X_p W^T (catches a
+    transposed projection or a wrong head split)."""
+    cfg = TINY.with_(n_kv_heads=2, n_heads=2)
+    W, inp, cache = _tiny_setup(cfg, B=2)
+    for c, l in enumerate([l for l in range(cfg.n_layers) if cfg.has_prefix(l)]):
+        for b, g, p in itertools.product(range(2), range(2), range(cfg.prefix_len)):
+            for kv, name in ((0, "W_kc"), (1, "W_vc")):
+                Wm = W[f"L{l}.{name}"]
+                rows = Wm[g * cfg.head_dim:(g + 1) * cfg.head_dim]
+                bf = bf_linear([inp["prefix"][b, p]], rows)[0]
+                np.testing.assert_allclose(cache[c, kv, b, g, p], bf, rtol=1e-12)
+
+
+def test_zero_velocity_end_to_end():
+    """W_out = 0, b_out = 0: the expert's velocity vanishes, output = noise."""
+    W, inp, cache = _tiny_setup()
+    W["W_out"] = np.zeros_like(W["W_out"])
+    W["b_out"] = np.zeros_like(W["b_out"])
+    tau = wl.uniform_schedule(TINY.n_steps)
+    out = O.denoise(TINY, W, cache, inp["noise"], inp["state"], tau)
+    assert np.array_equal(out, inp["noise"].astype(np.float64))
+
+
+def test_constant_velocity_end_to_end():
+    """W_out = 0, b_out = c: exact Euler endpoint noise + (tau_T - tau_0) c,
+    then denormalised."""
+    W, inp, cache = _tiny_setup()
+    c = np.array([0.3, -1.1])
+    W["W_out"] = np.zeros_like(W["W_out"])
+    W["b_out"] = c.astype(np.float32)
+    tau = np.array([1.0, 0.6, 0.25, 0.0], np.float32)
+    mean, std = np.array([1.0, -2.0]), np.array([0.5, 3.0])
+    out = O.denoise(TINY, W, cache, inp["noise"], inp["state"], tau, mean, std)
+    expect = (inp["noise"][0] + (0.0 - 1.0) * c.astype(np.float32).astype(np.float64)) * std + mean
+    np.testing.assert_allclose(out[0], expect, rtol=1e-14)
+
+
+def test_regression_head_is_single_pass():
+    """head_regression: the output is the head's value, not a + dt v."""
+    cfg = TINY.with_(head_regression=True, n_steps=1)
+    W, inp, cache = _tiny_setup(cfg)
+    W["W_out"] = np.zeros_like(W["W_out"])
+    W["b_out"] = np.array([0.25, -0.5], np.float32)
+    out = O.denoise(cfg, W, cache, inp["noise"], inp["state"], wl.uniform_schedule(1))
+    assert np.array_equal(out[0], np.tile([0.25, -0.5], (cfg.n_action, 1)))
+
+
+@pytest.mark.parametrize("pattern", ["self_cross", "joint", "alt"])
+def test_zero_gates_equal_zero_layers(pattern):
+    """All residual gates alpha = 0: every layer is skipped, so the forward
+    equals the same expert with no layers (catches an ungated residual)."""
+    cfg = TINY.with_(pattern=pattern, mlp="swiglu")
+    W, inp, cache = _tiny_setup(cfg)
+    d, ns = cfg.d_model, cfg.n_sub
+    for l in range(cfg.n_layers):
+        for j in range(ns):
+            W[f"L{l}.W_mod"][(3 * j + 2) * d:(3 * j + 3) * d] = 0
+            W[f"L{l}.b_mod"][(3 * j + 2) * d:(3 * j + 3) * d] = 0
+    a = inp["noise"][0].astype(np.float64)
+    cb = cache[:, :, 0]
+    full = O.expert_forward(cfg, W, cb, a, inp["state"][0], 0.4)
+    empty = O.expert_forward(cfg.with_(n_layers=0), W, None, a, inp["state"][0], 0.4)
+    np.testing.assert_allclose(full, empty, rtol=1e-13)
+
+
+@pytest.mark.parametrize("pattern", ["self_cross", "joint", "alt"])
+def test_cache_reuse_equals_recompute(pattern):
+    """The cached cross K/V and K/V recomputed at every solver step agree
+    bitwise in fp64."""
+    cfg = TINY.with_(pattern=pattern)
+    W, inp, cache = _tiny_setup(cfg, B=2)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    a = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+    b = O.denoise(cfg, W, None, inp["noise"], inp["state"], tau, prefix_hidden=inp["prefix"])
+    assert np.array_equal(a, b)
+
+
+def test_prefix_row_permutation_invariance():
+    """The expert attends to every prefix row without a mask or positions,
+    so permuting prefix rows leaves the chunk unchanged."""
+    cfg = TINY.with_(pattern="joint")
+    W, inp, cache = _tiny_setup(cfg)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    perm = _rng(16).permutation(cfg.prefix_len)
+    cache_p = O.prefix_kv_build(cfg, W, inp["prefix"][:, perm])
+    a = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+    b = O.denoise(cfg, W, cache_p, inp["noise"], inp["state"], tau)
+    np.testing.assert_allclose(a, b, rtol=1e-12, atol=1e-14)
+
+
+def test_batch_requests_independent():
+    W, inp, cache = _tiny_setup(B=3)
+    tau = wl.uniform_schedule(TINY.n_steps)
+    allb = O.denoise(TINY, W, cache, inp["noise"], inp["state"], tau)
+    one = O.denoise(TINY, W, cache, inp["noise"], inp["state"], tau, requests=[1])
+    assert np.array_equal(allb[1], one[0])
+    assert not np.allclose(allb[0], allb[1])
+
+
+def test_ternary_expert_runs_and_uses_w2a8():
+    """Ternary matrices go through the W2A8 linear: scaling every ternary
+    scale by 2 scales every projection by 2 exactly."""
+    cfg = TINY.with_(wtype="ternary", head_regression=True, n_steps=1, mlp="relu2glu", pattern="joint")
+    W, inp, cache = _tiny_setup(cfg)
+    u = wl.random_matrix((3, cfg.d_model), 9)
+    y1 = O._lin(cfg, W, "L0.W_q", u)
+    W2 = dict(W)
+    W2["L0.W_q.scale"] = np.float32(2 * W["L0.W_q.scale"])
+    np.testing.assert_allclose(O._lin(cfg, W2, "L0.W_q", u), 2 * y1, rtol=1e-15)
+    q, r = O.quantize_int8_rows(u)
+    acc = q.astype(np.int64) @ W["L0.W_q"].astype(np.int64).T
+    np.testing.assert_allclose(y1, acc * (float(W["L0.W_q.scale"]) * r[:, None].astype(np.float64) / 127),
+                               rtol=1e-15)
+
+
+def test_final_modulation_slot_order():
+    """(gamma_f, beta_f) = first and second half of W_fm SiLU(c) + b_fm: with
+    W_fm = 0, b_fm = [1...; 0.5...], gated-off layers and W_in = W_s = 0 the
+    velocity is (2 x0/rms(x0) + 0.5) W_out^T + b_out with x0 = b_in + b_s + E_pos."""
+    cfg = TINY
+    W, inp, cache = _tiny_setup(cfg)
+    d = cfg.d_model
+    W["W_fm"] = np.zeros_like(W["W_fm"])
+    W["b_fm"] = np.concatenate([np.ones(d), np.full(d, 0.5)]).astype(np.float32)
+    W["W_in"] = np.zeros_like(W["W_in"])
+    W["W_s"] = np.zeros_like(W["W_s"])
+    for l in range(cfg.n_layers):
+        for j in range(cfg.n_sub):
+            W[f"L{l}.W_mod"][(3 * j + 2) * d:(3 * j + 3) * d] = 0
+            W[f"L{l}.b_mod"][(3 * j + 2) * d:(3 * j + 3) * d] = 0
+    x0 = (W["b_in"].astype(np.float64) + W["b_s"] + W["E_pos"])
+    rms = np.sqrt(np.mean(x0 * x0, axis=-1, keepdims=True) + cfg.rms_eps)
+    expect = (2 * x0 / rms + 0.5) @ W["W_out"].T.astype(np.float64) + W["b_out"]
+    v = O.expert_forward(cfg, W, cache[:, :, 0], inp["noise"][0], inp["state"][0], 0.7)
+    np.testing.assert_allclose(v, expect, rtol=1e-13)
