@@ -1,0 +1,164 @@
+/*
+ * vla.h -- C ABI of the MI355X (gfx950) flow-matching action-expert library.
+ *
+ * The library runs the action stage of the VLA inference pattern (paper,
+ * Sec. 3.1 and Algorithm 1): a cached vision-language prefix is projected once
+ * into a per-layer cross-attention K/V cache (Appendix A.2, item 3), and a
+ * short action chunk is integrated over T solver steps by an action expert that
+ * cross-attends to that cache; the chunk is then denormalised (Sec. 3.3 item iv).
+ * A ternary-weight x int8-activation GEMM (Sec. 4.5, the W2A8 matmul of
+ * BitVLA) is exported on its own.
+ *
+ * Conventions for every call:
+ *  - Buffers are DEVICE pointers owned by the caller unless marked HOST.
+ *  - Work is enqueued asynchronously on `stream` (a hipStream_t; NULL = the
+ *    null stream); results are valid once the stream has synchronised.
+ *  - Every argument is validated on the host before any work is enqueued.  On
+ *    failure the call returns a non-zero vla_status, enqueues nothing, writes
+ *    nothing, and vla_last_error() describes the failure.  Nothing throws.
+ *  - Device pointers must be 16-byte aligned.
+ *  - A model is not safe for concurrent calls; use one model per stream.
+ */
+#ifndef VLA_H_
+#define VLA_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  VLA_OK = 0,
+  VLA_E_ARG = 1,          /* null pointer, misaligned pointer, bad enum value */
+  VLA_E_SHAPE = 2,        /* inconsistent or unsupported dimensions */
+  VLA_E_UNSUPPORTED = 3,  /* valid request this build does not implement */
+  VLA_E_NOMEM = 4,        /* device allocation failed */
+  VLA_E_DEVICE = 5,       /* a HIP call or kernel launch failed */
+  VLA_E_NONFINITE = 6     /* NaN/Inf in the output (VLA_CHECK_FINITE=1 only) */
+} vla_status;
+
+/* Weight element type of the dense matrices. */
+typedef enum { VLA_W_F32 = 0, VLA_W_BF16 = 1, VLA_W_TERNARY = 2 } vla_wtype;
+
+/* Sublayer pattern of each expert layer (execution order):
+ *   SELF_CROSS     : self-attention, cross-attention, MLP
+ *   JOINT          : joint attention (one softmax over [prefix ; chunk]), MLP
+ *   ALT_CROSS_SELF : even layers cross-attention + MLP, odd layers self-attention + MLP */
+typedef enum { VLA_PAT_SELF_CROSS = 0, VLA_PAT_JOINT = 1, VLA_PAT_ALT_CROSS_SELF = 2 } vla_pattern;
+
+/* MLP form: GELU(u W1^T) W2^T, or act(u Wg^T) * (u Wu^T) then Wd, with act
+ * GELU (tanh form) for GEGLU, SiLU for SWIGLU, relu^2 for RELU2GLU. */
+typedef enum { VLA_MLP_GELU = 0, VLA_MLP_GEGLU = 1, VLA_MLP_SWIGLU = 2, VLA_MLP_RELU2GLU = 3 } vla_mlp;
+
+typedef struct vla_config {
+  int32_t n_layers;        /* L */
+  int32_t d_model;         /* d (even) */
+  int32_t n_heads;         /* H query heads */
+  int32_t head_dim;        /* hd (multiple of 16, <= 256) */
+  int32_t n_kv_heads;      /* G (H % G == 0); head i reads K/V head floor(i*G/H) */
+  int32_t d_ff;            /* F (multiple of 16) */
+  int32_t d_prefix;        /* d_p, width of the prefix hidden states */
+  int32_t n_action;        /* n, action tokens per chunk */
+  int32_t d_action;        /* A */
+  int32_t d_state;         /* S, proprioceptive state width */
+  int32_t pattern;         /* vla_pattern */
+  int32_t mlp;             /* vla_mlp */
+  int32_t wtype;           /* vla_wtype */
+  int32_t head_regression; /* 1: single-pass regression head, no time input, n_steps must be 1 */
+  float rms_eps;           /* adaRMS epsilon (e.g. 1e-6) */
+} vla_config;
+
+typedef struct vla_model vla_model; /* opaque */
+
+/* Number of entries vla_model_create expects in its weight table. */
+int32_t vla_weight_count(const vla_config* cfg);
+
+/*
+ * Create a model from a table of device pointers (copied into library-owned,
+ * possibly re-tiled memory; the caller may free its buffers once this returns).
+ * Synchronous.  Table order and shapes ([out][in] row-major, y = x W^T):
+ *   globals: W_in [d][A], b_in [d], W_s [d][S], b_s [d], E_pos [n][d],
+ *            then W_t1 [d][d], b_t1 [d], W_t2 [d][d], b_t2 [d], W_fm [2d][d], b_fm [2d]
+ *            (regression head instead: mod_f [2d] fp32),
+ *            then W_out [A][d], b_out [A];
+ *   per layer: W_mod [3*n_sub*d][d], b_mod [3*n_sub*d] (regression: mod [3*n_sub*d] fp32),
+ *            then per attention sublayer W_q [H*hd][d], W_k, W_v [G*hd][d] (self/joint),
+ *            W_kc, W_vc [G*hd][d_p] (cross/joint), W_o [d][H*hd];
+ *            per MLP W1 [F][d], W2 [d][F] (GELU) or W_g, W_u [F][d], W_d [d][F].
+ * Dense matrices are fp32 (VLA_W_F32) or bf16 (VLA_W_BF16 and VLA_W_TERNARY);
+ * biases and modulation tables are fp32.  With VLA_W_TERNARY every attention
+ * and MLP matrix is packed 2-bit [N][K/4] bytes (code w+1 of w[n][4j+i] in bits
+ * 2i..2i+1 of byte j) and is followed in the table by a device pointer to its
+ * fp32 per-tensor scale.
+ * n_sub = 3 (SELF_CROSS) or 2.  Errors: VLA_E_ARG, VLA_E_SHAPE, VLA_E_NOMEM, VLA_E_DEVICE.
+ */
+vla_status vla_model_create(const vla_config* cfg, const void* const* weights, int32_t n_weights,
+                            vla_model** out);
+void vla_model_destroy(vla_model* model);
+
+/* Bytes of the cross-attention K/V cache for `batch` requests of `prefix_len`
+ * prefix tokens: Lc * 2 * batch * G * prefix_len * hd * elem, with Lc the number
+ * of layers that have a cross or joint sublayer and elem 4 (fp32 models) or 2.
+ * Returns 0 on invalid arguments. */
+size_t vla_kv_cache_bytes(const vla_model* model, int32_t batch, int32_t prefix_len);
+
+/*
+ * Project the prefix hidden states once into the cross-attention cache.
+ * prefix_hidden: [batch][prefix_len][d_p], fp32 for fp32 models, bf16 otherwise.
+ * kv_cache: [Lc][2][batch][G][prefix_len][hd] (K then V), same element type;
+ * kv_cache_bytes must equal vla_kv_cache_bytes(model, batch, prefix_len).
+ * The cache stays valid until the caller overwrites it (one denoising
+ * integration, Appendix A.2 item 3).
+ */
+vla_status vla_prefix_kv_build(vla_model* model, const void* prefix_hidden, int32_t batch,
+                               int32_t prefix_len, void* kv_cache, size_t kv_cache_bytes,
+                               void* stream);
+
+/*
+ * Integrate one action chunk per request (Algorithm 1, solver loop and
+ * denormalisation).  For k = 0..n_steps-1 the expert evaluates the velocity v
+ * at (a_k, tau_k) and a_{k+1} = a_k + (tau_{k+1} - tau_k) v; the regression
+ * head (n_steps == 1) returns its output directly.  Finally
+ * actions = a * act_std + act_mean.
+ *   kv_cache   : as built by vla_prefix_kv_build for (batch, prefix_len)
+ *   noise      : [batch][n][A] fp32 (a_0)
+ *   state      : [batch][S] fp32
+ *   t_schedule : HOST [n_steps+1] fp32, finite; copied before the call returns
+ *   n_steps    : 1..64
+ *   act_mean, act_std : [A] fp32 or NULL (identity)
+ *   actions_out: [batch][n][A] fp32; may alias noise
+ * Requests are independent; weights and the schedule are shared.
+ * With the environment variable VLA_CHECK_FINITE=1 the call synchronises the
+ * stream and returns VLA_E_NONFINITE if any output is NaN or Inf.
+ */
+vla_status vla_denoise(vla_model* model, const void* kv_cache, size_t kv_cache_bytes, int32_t batch,
+                       int32_t prefix_len, const float* noise, const float* state,
+                       const float* t_schedule, int32_t n_steps, const float* act_mean,
+                       const float* act_std, float* actions_out, void* stream);
+
+/*
+ * W2A8 GEMM (Sec. 4.5): acc[m][n] = sum_k x[m][k] * w[n][k], int32, exact.
+ *   x        : [M][K] int8, row-major
+ *   w_packed : [N][K/4] bytes in the 2-bit layout of vla_model_create
+ *   acc_out  : [M][N] int32
+ * K % 4 == 0, K <= 2^23 / 128 (so |acc| < 2^31 is guaranteed).  A code of 3 in
+ * w_packed is undefined input.  M, N >= 0; M*N == 0 enqueues nothing.
+ */
+vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
+                            int32_t* acc_out, void* stream);
+
+/* Loop driver of vla_denoise: 0 = one launch per phase on the stream,
+ * 1 = the same launches captured once in a HIP graph and replayed (default). */
+enum { VLA_OPT_LOOP_MODE = 0 };
+vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
+
+/* Thread-local message for the last non-OK status of this thread. */
+const char* vla_last_error(void);
+const char* vla_status_string(int32_t status);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_H_ */

@@ -1,0 +1,47 @@
+/*
+ * vla_test.h -- per-kernel entry points of libvla for parity tests.
+ *
+ * Not part of the product ABI.  Each call validates its arguments like the
+ * product calls, runs one kernel of the denoise loop on `stream`, synchronises
+ * the stream (test entries allocate and free scratch memory) and returns.
+ * All buffers are device pointers, 16-byte aligned.  elem: 0 = fp32, 1 = bf16.
+ */
+#ifndef VLA_TEST_H_
+#define VLA_TEST_H_
+
+#include "vla.h"
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+/* y[M][N] (fp32) = x[M][K] w[N][K]^T on the MFMA GEMM of the projections,
+ * with its split-K reduction.  K % 8 == 0 (bf16) or K % 4 == 0 (fp32).
+ * force_nsplit > 0 forces that many K-splits (0 = the runtime's choice). */
+vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
+                         int32_t force_nsplit, float* y, void* stream);
+
+/* Attention of B requests of n action tokens (paper Sec. 3.1: the action head
+ * cross-attends to the cached prefix).  mode 0 self (keys = the n tokens),
+ * 1 cross (keys = the P cached rows), 2 joint (one softmax over both).
+ *   q [B*n][H*hd]; k_self, v_self [B*n][G*hd]; k_cache, v_cache [B][G][P][hd];
+ *   o [B*n][H*hd]; all in elem.  kv_split = 0 lets the runtime choose. */
+vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const void* k_self,
+                              const void* v_self, const void* k_cache, const void* v_cache, int32_t B,
+                              int32_t n, int32_t P, int32_t H, int32_t G, int32_t hd, int32_t kv_split,
+                              void* o, void* stream);
+
+/* Per-token absmax int8 quantiser of the W2A8 path: x [M][K] fp32 ->
+ * q [M][K] int8, r [M] fp32. */
+vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q, float* r, void* stream);
+
+/* W2A8 linear: quantise x [M][K] fp32 per token, multiply by the packed
+ * ternary w [N][K/4] (K % 64 == 0) and dequantise with the per-tensor scale
+ * `scale`: y [M][N] fp32 = acc * scale * r_m / 127. */
+vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
+                                   float scale, float* y, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+#endif /* VLA_TEST_H_ */

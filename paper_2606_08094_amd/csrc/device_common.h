@@ -1,0 +1,132 @@
+// Device-side building blocks shared by the gfx950 kernels of the denoise loop.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+#include "vla_internal.h"
+
+typedef uint16_t bf16_t;  // bf16 storage
+typedef __bf16 bf16x8_t __attribute__((ext_vector_type(8)));
+typedef __bf16 bf16x2_t __attribute__((ext_vector_type(2)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef int i32x4 __attribute__((ext_vector_type(4)));
+
+#define VLA_DEV __device__ __forceinline__
+
+VLA_DEV float bf2f(bf16_t b) { return __uint_as_float(((uint32_t)b) << 16); }
+
+// float -> bf16, round to nearest even (hardware conversion on gfx950).
+VLA_DEV bf16_t f2bf(float f) {
+  __bf16 h = static_cast<__bf16>(f);
+  return __builtin_bit_cast(bf16_t, h);
+}
+
+VLA_DEV uint32_t pack_bf16x2(float lo, float hi) {
+  bf16x2_t v = {static_cast<__bf16>(lo), static_cast<__bf16>(hi)};
+  return __builtin_bit_cast(uint32_t, v);
+}
+
+// Elements per 16-byte vector and conversion helpers, per storage type.
+template <typename T> struct ElemTraits;
+template <> struct ElemTraits<float> {
+  static constexpr int E = 4;
+  static VLA_DEV float to_f(float v) { return v; }
+  static VLA_DEV float from_f(float v) { return v; }
+};
+template <> struct ElemTraits<bf16_t> {
+  static constexpr int E = 8;
+  static VLA_DEV float to_f(bf16_t v) { return bf2f(v); }
+  static VLA_DEV bf16_t from_f(float v) { return f2bf(v); }
+};
+
+// Pack 16 bytes worth of float values (E of them) into the storage type.
+VLA_DEV uint4 pack16(const float* v, float) {
+  return make_uint4(__float_as_uint(v[0]), __float_as_uint(v[1]), __float_as_uint(v[2]),
+                    __float_as_uint(v[3]));
+}
+VLA_DEV uint4 pack16(const float* v, bf16_t) {
+  return make_uint4(pack_bf16x2(v[0], v[1]), pack_bf16x2(v[2], v[3]), pack_bf16x2(v[4], v[5]),
+                    pack_bf16x2(v[6], v[7]));
+}
+VLA_DEV void unpack16(uint4 u, float* v, float) {
+  v[0] = __uint_as_float(u.x); v[1] = __uint_as_float(u.y);
+  v[2] = __uint_as_float(u.z); v[3] = __uint_as_float(u.w);
+}
+VLA_DEV void unpack16(uint4 u, float* v, bf16_t) {
+  const uint32_t w[4] = {u.x, u.y, u.z, u.w};
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    v[2 * i] = __uint_as_float(w[i] << 16);
+    v[2 * i + 1] = __uint_as_float(w[i] & 0xFFFF0000u);
+  }
+}
+
+// One 16-byte A fragment times one 16-byte B fragment into a 16x16 fp32 tile.
+// bf16: one v_mfma_f32_16x16x32_bf16 (8 k-values per lane).
+// fp32: four v_mfma_f32_16x16x4_f32 (one k-value per lane each).
+VLA_DEV void mma16(f32x4& acc, uint4 a, uint4 b, bf16_t) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, a),
+                                                __builtin_bit_cast(bf16x8_t, b), acc, 0, 0, 0);
+}
+VLA_DEV void mma16(f32x4& acc, uint4 a, uint4 b, float) {
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.x), __uint_as_float(b.x), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.y), __uint_as_float(b.y), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.z), __uint_as_float(b.z), acc, 0, 0, 0);
+  acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
+}
+
+VLA_DEV uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+VLA_DEV void stg16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
+
+// Activations (fp32).  GELU uses the tanh form.
+VLA_DEV float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+VLA_DEV float gelu_tanh_f(float x) {
+  const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
+  float inner = k0 * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.0f + tanhf(inner));
+}
+VLA_DEV float act_f(int act, float x) {
+  switch (act) {
+    case ACT_SILU: return silu_f(x);
+    case ACT_GELU: return gelu_tanh_f(x);
+    case ACT_RELU2: { float r = fmaxf(x, 0.0f); return r * r; }
+    default: return x;
+  }
+}
+
+// Sum over the 16 lanes that share lane/16 (the columns of one MFMA tile row group).
+VLA_DEV float sum16(float v) {
+  v += __shfl_xor(v, 1, 64);
+  v += __shfl_xor(v, 2, 64);
+  v += __shfl_xor(v, 4, 64);
+  v += __shfl_xor(v, 8, 64);
+  return v;
+}
+VLA_DEV float wave_sum(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+VLA_DEV float wave_max(float v) {
+#pragma unroll
+  for (int o = 32; o > 0; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
+  return v;
+}
+
+// Split-K arrival: every thread has stored its partials; returns true in all
+// threads of the last workgroup to arrive on `counter` (which it resets).
+VLA_DEV bool splitk_arrive_last(unsigned* counter, unsigned nsplit, int* lds_flag) {
+  __threadfence();
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    unsigned old = atomicAdd(counter, 1u);
+    bool last = (old == nsplit - 1);
+    if (last) atomicExch(counter, 0u);
+    *lds_flag = last ? 1 : 0;
+  }
+  __syncthreads();
+  bool last = *lds_flag != 0;
+  if (last) __threadfence();
+  return last;
+}

@@ -1,0 +1,258 @@
+// Ternary-weight x int8-activation GEMM (W2A8) on the int8 MFMA units.
+//
+// Weights arrive packed 2 bits each ([N][K/4] bytes, code w+1 of w[n][4j+i] in
+// bits 2i..2i+1 of byte j).  Each lane loads 16 packed bytes = 64 consecutive
+// weights of one W row and widens them in registers to the codes c = w + 1 in
+// {0,1,2} as int8 (byte-permute + masks, no lookup table).  The MFMA then forms
+// sum_k q*c, and sum_k q*w = sum_k q*c - sum_k q is recovered with the row sums
+// of the activation codes, which the workgroup accumulates while staging X in
+// LDS.  All arithmetic is int32 and exact, so split-K partials can be summed
+// in any order.
+#include "gemm_epilogue.h"
+
+namespace {
+
+// 16 2-bit codes (one packed dword, natural k order) -> 16 int8 codes.
+VLA_DEV i32x4 unpack_codes(uint32_t p) {
+  const uint32_t lo = p & 0x33333333u;         // fields 0 and 2 of each byte
+  const uint32_t hi = (p >> 2) & 0x33333333u;  // fields 1 and 3 of each byte
+  i32x4 r;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) {
+    const uint32_t sel = (uint32_t)b | ((uint32_t)(4 + b) << 8) | ((uint32_t)b << 16) | ((uint32_t)(4 + b) << 24);
+    const uint32_t t = __builtin_amdgcn_perm(hi, lo, sel);  // [lo_b, hi_b, lo_b, hi_b]
+    r[b] = (int)((t & 0x00000303u) | ((t >> 4) & 0x03030000u));
+  }
+  return r;
+}
+
+VLA_DEV int sum_i8x16(uint4 v) {
+  int s = 0;
+  s = __builtin_amdgcn_sdot4((int)v.x, 0x01010101, s, false);
+  s = __builtin_amdgcn_sdot4((int)v.y, 0x01010101, s, false);
+  s = __builtin_amdgcn_sdot4((int)v.z, 0x01010101, s, false);
+  s = __builtin_amdgcn_sdot4((int)v.w, 0x01010101, s, false);
+  return s;
+}
+
+// Requires K % 64 == 0 (16-byte aligned packed rows).
+template <int MS, int NSUB, int NC>
+__global__ __launch_bounds__(256) void tern_kernel(TernArgs a) {
+  constexpr int KC = 256;  // 4 lane groups x 64 k
+  constexpr int KS = NC * KC;
+  constexpr int MT = 16 * MS;
+  constexpr int NT = 64 * NSUB;
+  constexpr int PITCH = KS + 16;
+
+  extern __shared__ __align__(16) unsigned char smem[];
+  int8_t* xs = reinterpret_cast<int8_t*>(smem);
+  int* rsum_s = reinterpret_cast<int*>(smem + (size_t)MT * PITCH);
+  float* red_s = reinterpret_cast<float*>(rsum_s + MT);  // [4][MT]
+  int* flag_s = reinterpret_cast<int*>(red_s + 4 * MT);
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K;
+  const int KB = K / 4;
+
+  int unit = blockIdx.x;
+  const int split = unit % a.nsplit;
+  unit /= a.nsplit;
+  const int ntile = unit % a.n_tiles;
+  const int mtile = unit / a.n_tiles;
+  const int m0 = mtile * MT;
+  const int k0 = split * KS;
+  const int kend = min(K, k0 + KS);
+  const int nw0 = ntile * NT + wave * 16 * NSUB;
+
+  uint4 wreg[NSUB][NC];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    const int n = nw0 + s * 16 + r16;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const int k = k0 + c * KC + g4 * 64;
+      wreg[s][c] = (n < N && k < kend) ? ldg16(a.w + (size_t)n * KB + k / 4) : make_uint4(0, 0, 0, 0);
+    }
+  }
+
+  if (tid < MT) rsum_s[tid] = 0;
+  __syncthreads();
+  constexpr int VROW = KS / 16;
+  for (int i = tid; i < MT * VROW; i += 256) {
+    const int row = i / VROW, kv = i - row * VROW;
+    const int m = m0 + row, k = k0 + kv * 16;
+    uint4 v = make_uint4(0, 0, 0, 0);
+    if (m < M && k < kend) {
+      v = ldg16(a.x + (size_t)m * K + k);
+      atomicAdd(&rsum_s[row], sum_i8x16(v));
+    }
+    *reinterpret_cast<uint4*>(xs + (size_t)row * PITCH + kv * 16) = v;
+  }
+  __syncthreads();
+
+  i32x4 acc[MS][NSUB];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) acc[ms][s] = i32x4{0, 0, 0, 0};
+#pragma unroll
+  for (int c = 0; c < NC; ++c) {
+    if (k0 + c * KC >= kend) break;
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms) {
+      const int8_t* xrow = xs + (size_t)(ms * 16 + r16) * PITCH + c * KC + g4 * 64;
+      uint4 xf[4];
+#pragma unroll
+      for (int r = 0; r < 4; ++r) xf[r] = *reinterpret_cast<const uint4*>(xrow + 16 * r);
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        const uint32_t pw[4] = {wreg[s][c].x, wreg[s][c].y, wreg[s][c].z, wreg[s][c].w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          acc[ms][s] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[r]),
+                                                             unpack_codes(pw[r]), acc[ms][s], 0, 0, 0);
+      }
+    }
+  }
+  // sum q*w = sum q*c - sum q over this slice.
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rs = rsum_s[ms * 16 + g4 * 4 + i];
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) acc[ms][s][i] -= rs;
+    }
+
+  if (a.nsplit > 1 && a.rscale == nullptr) {
+    // Raw int32 output: integer adds are exact and order-free, so the splits
+    // accumulate straight into the (zero-filled) output.
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + ms * 16 + g4 * 4 + i;
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+          const int n = nw0 + s * 16 + r16;
+          if (m < M && n < N) atomicAdd(&a.acc_out[(size_t)m * N + n], acc[ms][s][i]);
+        }
+      }
+    return;
+  }
+  if (a.nsplit > 1) {
+    const int tile = mtile * a.n_tiles + ntile;
+    constexpr int PER = 4 * MS * NSUB * 64;
+    i32x4* wsp = reinterpret_cast<i32x4*>(a.ws) + ((size_t)tile * a.nsplit) * PER;
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s)
+        wsp[(size_t)split * PER + ((wave * MS + ms) * NSUB + s) * 64 + lane] = acc[ms][s];
+    if (!splitk_arrive_last(&a.cnt[tile], (unsigned)a.nsplit, flag_s)) return;
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        i32x4 t = i32x4{0, 0, 0, 0};
+        for (int sp = 0; sp < a.nsplit; ++sp) t += wsp[(size_t)sp * PER + ((wave * MS + ms) * NSUB + s) * 64 + lane];
+        acc[ms][s] = t;
+      }
+  }
+
+  if (a.rscale == nullptr) {
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + ms * 16 + g4 * 4 + i;
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+          const int n = nw0 + s * 16 + r16;
+          if (m < M && n < N) a.acc_out[(size_t)m * N + n] = acc[ms][s][i];
+        }
+      }
+    return;
+  }
+  // y = acc * (s_w * r_m / 127), with s_w the per-tensor scale of the
+  // matrix that W row n belongs to.
+  float sw[NSUB];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    const int n = nw0 + s * 16 + r16;
+    sw[s] = (n < N) ? a.wscale[n] : 0.0f;
+  }
+  f32x4 y[MS][NSUB];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + ms * 16 + g4 * 4 + i;
+      const float rm = (m < M) ? a.rscale[m] : 0.0f;
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) y[ms][s][i] = (float)acc[ms][s][i] * (sw[s] * rm / 127.0f);
+    }
+  gemm_epilogue<bf16_t, MS, NSUB>(a.e, y, m0, ntile, nw0, red_s);
+}
+
+// Any K % 4 == 0: one thread per output, byte-wise unpacking.
+__global__ __launch_bounds__(256) void tern_generic_kernel(const int8_t* x, const uint8_t* w, int M, int N, int K,
+                                                           int32_t* out) {
+  const long long idx = blockIdx.x * 256LL + threadIdx.x;
+  if (idx >= (long long)M * N) return;
+  const int m = (int)(idx / N), n = (int)(idx - (long long)m * N);
+  const uint8_t* wr = w + (size_t)n * (K / 4);
+  const int8_t* xr = x + (size_t)m * K;
+  int acc = 0;
+  for (int j = 0; j < K / 4; ++j) {
+    const uint32_t byte = wr[j];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) acc += (int)xr[4 * j + i] * ((int)((byte >> (2 * i)) & 3u) - 1);
+  }
+  out[idx] = acc;
+}
+
+template <int MS, int NSUB, int NC>
+hipError_t tern_launch(const TernArgs& a, int units, hipStream_t s) {
+  constexpr int MT = 16 * MS;
+  const size_t lds = (size_t)MT * (NC * 256 + 16) + (size_t)MT * 4 + 4 * MT * 4 + 16;
+  hipLaunchKernelGGL((tern_kernel<MS, NSUB, NC>), dim3(units), dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
+template <int MS, int NSUB>
+hipError_t tern_nc(int nc, const TernArgs& a, int units, hipStream_t s) {
+  switch (nc) {
+    case 1: return tern_launch<MS, NSUB, 1>(a, units, s);
+    case 2: return tern_launch<MS, NSUB, 2>(a, units, s);
+    case 4: return tern_launch<MS, NSUB, 4>(a, units, s);
+    case 8: return tern_launch<MS, NSUB, 8>(a, units, s);
+  }
+  return hipErrorInvalidValue;
+}
+
+}  // namespace
+
+// ms: m-subtiles (1, 2, 4); nsub 1 or 2 (GLU pairs); nc from a.ks / 256.
+hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.K % 64 != 0) {
+    if (a.rscale != nullptr) return hipErrorInvalidValue;
+    const long long total = (long long)a.M * a.N;
+    hipLaunchKernelGGL(tern_generic_kernel, dim3((unsigned)((total + 255) / 256)), dim3(256), 0, s, a.x, a.w, a.M,
+                       a.N, a.K, a.acc_out);
+    return hipGetLastError();
+  }
+  const int nc = a.ks / 256;
+  const int nsub = (a.rscale != nullptr && a.e.epi == EPI_GLU) ? 2 : 1;
+  switch (ms * 10 + nsub) {
+    case 11: return tern_nc<1, 1>(nc, a, units, s);
+    case 12: return tern_nc<1, 2>(nc, a, units, s);
+    case 21: return tern_nc<2, 1>(nc, a, units, s);
+    case 22: return tern_nc<2, 2>(nc, a, units, s);
+    case 41: return tern_nc<4, 1>(nc, a, units, s);
+    case 42: return tern_nc<4, 2>(nc, a, units, s);
+  }
+  return hipErrorInvalidValue;
+}

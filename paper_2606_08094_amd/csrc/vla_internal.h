@@ -1,0 +1,152 @@
+// Internal interfaces between the host runtime (vla_api.hip) and the kernels.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#define VLA_MAX_STEPS 64
+
+enum ElemType { ET_F32 = 0, ET_BF16 = 1 };
+enum Act { ACT_NONE = 0, ACT_SILU = 1, ACT_GELU = 2, ACT_RELU2 = 3 };
+
+// Per-call values of vla_denoise, written to device memory by a tiny kernel
+// before the (possibly graph-replayed) launch sequence so that the sequence
+// itself never changes between calls.
+struct CallParams {
+  const void* kv_cache;
+  const float* noise;
+  const float* state;
+  float* actions_out;
+  const float* act_mean;
+  const float* act_std;
+  float tau[VLA_MAX_STEPS + 1];
+};
+
+// GEMM prologues: how the activation operand X reaches LDS.
+enum GemmPro {
+  PRO_PLAIN = 0,   // X already in the element type, [M][ldx]
+  PRO_ADARMS = 1,  // X is the fp32 residual; u = x * rstd * (1 + gamma) + beta
+};
+
+// GEMM epilogues, applied to y = X W^T after the split-K reduction.
+enum GemmEpi {
+  EPI_STORE = 0,    // out[m][n] = act(y + bias[n]) in the element type or fp32
+  EPI_RESID = 1,    // x[m][n] += alpha[n] * y; per-64-column partial sums of x^2
+  EPI_GLU = 2,      // W rows interleaved gate/up in blocks of 16: h = act(g) * u
+  EPI_EULER = 3,    // v = y + bias; a += dt v (or a = v); last step: denormalised output
+  EPI_KVCACHE = 4,  // scatter [rows of one request][K|V][G][hd] into the cache layout
+};
+
+struct GemmArgs {
+  // problem
+  int M, N, K;
+  const void* X;
+  int ldx;
+  const void* W;           // [N][K] row-major in the element type
+  // adaRMS prologue
+  const float* rowss;      // [rowss_np][M] partial sums of squares of X rows
+  int rowss_np;
+  const float* gamma;
+  const float* beta;
+  float eps;
+  // split-K
+  int ks;                  // K-slice per split (multiple of the chunk)
+  int nsplit;
+  int n_tiles;             // tiles along N
+  float* ws;
+  unsigned* cnt;
+  // epilogue
+  int epi;
+  int act;
+  const float* bias;
+  void* out;               // EPI_STORE / EPI_GLU destination
+  int ldo;
+  int out_f32;             // EPI_STORE: 1 = fp32 output, 0 = element type
+  float* xres;             // EPI_RESID residual [M][ldxr]
+  int ldxr;
+  const float* alpha;
+  float* rowss_out;        // EPI_RESID [n_tiles][M]
+  // EPI_EULER
+  float* a;                // [M][N]
+  const CallParams* cp;
+  int step;
+  int regression;
+  int last;
+  // EPI_KVCACHE: row m = b*P + p, column n = kv*d_kv + g*hd + c
+  void* cache;             // layer base: [2][B][G][P][hd]
+  int P, hd, d_kv, B;
+};
+
+struct AttnArgs {
+  int mode;                // 0 self, 1 cross, 2 joint
+  int B, n, P;             // requests, action tokens, prefix rows
+  int H, G, hd;
+  const void* q;           // [B*n][ldq], head h at column h*hd
+  int ldq;
+  const void* ks;          // self keys   [B*n][ldkv], head g at column g*hd
+  const void* vs;          // self values
+  int ldkv;
+  const void* kc;          // cache K of this layer: [B][G][P][hd]; NULL -> from cp
+  const void* vc;
+  const CallParams* cp;    // kv_cache base when kc == NULL
+  size_t layer_off;        // element offset of this layer's K block in the cache
+  void* o;                 // [B*n][ldo]
+  int ldo;
+  float scale;
+  int kv_split;            // key splits
+  int key_chunk;           // keys per split (multiple of 32)
+  float* ws;               // partial O and stats
+  unsigned* cnt;
+};
+
+struct QuantArgs {
+  int M, K;
+  const void* x;           // fp32 residual (adarms) or element type / fp32 plain
+  int ldx;
+  int src_type;            // 0 fp32, 1 bf16
+  int adarms;
+  const float* rowss;
+  int rowss_np;
+  const float* gamma;
+  const float* beta;
+  float eps;
+  int8_t* q;               // [M][K]
+  float* r;                // [M]
+};
+
+struct TernArgs {
+  int M, N, K;
+  const int8_t* x;         // [M][K]
+  const uint8_t* w;        // [N][K/4] packed
+  const float* rscale;     // [M] absmax per row (dequant) or NULL for raw acc
+  const float* wscale;     // [N] per W-row scale (the per-tensor scale of its matrix)
+  int32_t* acc_out;        // raw int32 output (when rscale == NULL); zero-filled if nsplit > 1
+  int ks, nsplit, n_tiles;
+  int* ws;
+  unsigned* cnt;
+  // dequantised epilogue (same meaning as GemmArgs)
+  GemmArgs e;
+};
+
+// ---- launchers (each enqueues on `s`, returns hipError_t) ----
+hipError_t launch_gemm(int et, int ms, int nsub, int nc, const GemmArgs& a, int units, hipStream_t s);
+int gemm_chunk_k(int et);  // K covered by one chunk (all 4 lane groups)
+size_t gemm_lds_bytes(int et, int ms, int nc);
+size_t gemm_ws_floats_per_unit(int ms, int nsub);
+
+hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s);
+size_t attention_ws_floats(const AttnArgs& a);
+
+hipError_t launch_set_params(CallParams* dst, const CallParams& src, hipStream_t s);
+hipError_t launch_init_chunk(int et, const CallParams* cp, float* a, float* xs, const void* W_s,
+                             const float* b_s, const float* b_in, int B, int n, int A, int S, int d,
+                             hipStream_t s);
+hipError_t launch_embed(int et, const float* a, const void* W_in, const float* xs, const void* E_pos,
+                        float* x, float* rowss, int B, int n, int A, int d, hipStream_t s);
+hipError_t launch_time_embed(int et, const CallParams* cp, void* e, int T, int Tpad, int d, hipStream_t s);
+hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
+hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
+hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s);
+hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
+hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);

@@ -1,0 +1,218 @@
+"""ctypes binding of libvla (include/vla.h, include/vla_test.h).
+
+Argument marshalling only: every step of the denoise loop runs in the HIP
+library.  Device buffers are passed as torch tensors (their data pointers) or
+as raw integer addresses; streams as torch.cuda.Stream, an integer handle, or
+None for torch's current stream.  If libvla.so is missing or fails to load,
+every call raises: there is no fallback.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Dict, List, Optional, Sequence
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libvla.so")
+
+PATTERNS = {"self_cross": 0, "joint": 1, "alt": 2}
+MLPS = {"gelu": 0, "geglu": 1, "swiglu": 2, "relu2glu": 3}
+WTYPES = {"f32": 0, "bf16": 1, "ternary": 2}
+STATUS = {0: "VLA_OK", 1: "VLA_E_ARG", 2: "VLA_E_SHAPE", 3: "VLA_E_UNSUPPORTED", 4: "VLA_E_NOMEM",
+          5: "VLA_E_DEVICE", 6: "VLA_E_NONFINITE"}
+VLA_OPT_LOOP_MODE = 0
+
+# Every symbol the headers declare.
+EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_cache_bytes",
+           "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
+           "vla_last_error", "vla_status_string",
+           "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear"]
+
+
+class VlaError(RuntimeError):
+    def __init__(self, status: int, msg: str):
+        super().__init__(f"{STATUS.get(status, status)}: {msg}")
+        self.status = status
+
+
+class VlaConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "d_model", "n_heads", "head_dim", "n_kv_heads", "d_ff", "d_prefix",
+        "n_action", "d_action", "d_state", "pattern", "mlp", "wtype", "head_regression")] + [
+        ("rms_eps", ctypes.c_float)]
+
+
+_lib = None
+
+
+def lib():
+    """Load libvla.so once; raise if it is absent."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise RuntimeError(f"{LIB_PATH} is missing: build it with python -m paper_2606_08094_amd.build")
+    L = ctypes.CDLL(LIB_PATH)
+    vp, i32, sz = ctypes.c_void_p, ctypes.c_int32, ctypes.c_size_t
+    sig = {
+        "vla_weight_count": (i32, [ctypes.POINTER(VlaConfig)]),
+        "vla_model_create": (i32, [ctypes.POINTER(VlaConfig), ctypes.POINTER(vp), i32, ctypes.POINTER(vp)]),
+        "vla_model_destroy": (None, [vp]),
+        "vla_kv_cache_bytes": (sz, [vp, i32, i32]),
+        "vla_prefix_kv_build": (i32, [vp, vp, i32, i32, vp, sz, vp]),
+        "vla_denoise": (i32, [vp, vp, sz, i32, i32, vp, vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp, vp]),
+        "vla_ternary_gemm": (i32, [vp, vp, i32, i32, i32, vp, vp]),
+        "vla_model_set_option": (i32, [vp, i32, i32]),
+        "vla_last_error": (ctypes.c_char_p, []),
+        "vla_status_string": (ctypes.c_char_p, [i32]),
+        "vla_test_gemm": (i32, [i32, vp, vp, i32, i32, i32, i32, vp, vp]),
+        "vla_test_attention": (i32, [i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]),
+        "vla_test_quantize_i8": (i32, [vp, i32, i32, vp, vp, vp]),
+        "vla_test_ternary_linear": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp]),
+    }
+    for name, (res, args) in sig.items():
+        f = getattr(L, name)
+        f.restype = res
+        f.argtypes = args
+    _lib = L
+    return L
+
+
+def _check(status: int):
+    if status != 0:
+        raise VlaError(status, lib().vla_last_error().decode())
+
+
+def _ptr(x) -> Optional[int]:
+    if x is None:
+        return None
+    if isinstance(x, int):
+        return x
+    return x.data_ptr()
+
+
+def _stream(s) -> Optional[int]:
+    if s is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(s, int):
+        return s
+    return s.cuda_stream
+
+
+def make_config(cfg) -> VlaConfig:
+    """vla_config from any object with the expert's attributes (string enums)."""
+    return VlaConfig(
+        n_layers=cfg.n_layers, d_model=cfg.d_model, n_heads=cfg.n_heads, head_dim=cfg.head_dim,
+        n_kv_heads=cfg.n_kv_heads, d_ff=cfg.d_ff, d_prefix=cfg.d_prefix, n_action=cfg.n_action,
+        d_action=cfg.d_action, d_state=cfg.d_state, pattern=PATTERNS[cfg.pattern], mlp=MLPS[cfg.mlp],
+        wtype=WTYPES[cfg.wtype], head_regression=int(bool(cfg.head_regression)), rms_eps=float(cfg.rms_eps))
+
+
+def weight_order(cfg) -> List[str]:
+    """Names of the weight-table entries in the order vla.h documents.
+    Ternary matrices are followed by '<name>.scale'."""
+    tern = cfg.wtype == "ternary"
+
+    def mat(name):
+        return [name, name + ".scale"] if tern else [name]
+
+    names = ["W_in", "b_in", "W_s", "b_s", "E_pos"]
+    names += ["mod_f"] if cfg.head_regression else ["W_t1", "b_t1", "W_t2", "b_t2", "W_fm", "b_fm"]
+    names += ["W_out", "b_out"]
+    for l in range(cfg.n_layers):
+        p = f"L{l}."
+        names += [p + "mod"] if cfg.head_regression else [p + "W_mod", p + "b_mod"]
+        if cfg.pattern == "self_cross":
+            kinds = ["self", "cross", "mlp"]
+        elif cfg.pattern == "joint":
+            kinds = ["joint", "mlp"]
+        else:
+            kinds = ["cross", "mlp"] if l % 2 == 0 else ["self", "mlp"]
+        for k in kinds:
+            if k == "mlp":
+                for w in (["W1", "W2"] if cfg.mlp == "gelu" else ["W_g", "W_u", "W_d"]):
+                    names += mat(p + w)
+            else:
+                names += mat(p + "W_q")
+                if k in ("self", "joint"):
+                    names += mat(p + "W_k") + mat(p + "W_v")
+                if k in ("cross", "joint"):
+                    names += mat(p + "W_kc") + mat(p + "W_vc")
+                names += mat(p + "W_o")
+    return names
+
+
+class Model:
+    """A vla_model created from device tensors keyed by weight-table name."""
+
+    def __init__(self, cfg, device_weights: Dict[str, object]):
+        self.cfg = cfg
+        self._c = make_config(cfg)
+        names = weight_order(cfg)
+        want = lib().vla_weight_count(ctypes.byref(self._c))
+        if want != len(names):
+            raise VlaError(1, f"weight table length mismatch ({want} vs {len(names)})")
+        table = (ctypes.c_void_p * len(names))(*[_ptr(device_weights[n]) for n in names])
+        h = ctypes.c_void_p()
+        _check(lib().vla_model_create(ctypes.byref(self._c), table, len(names), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().vla_model_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def kv_cache_bytes(self, batch: int, prefix_len: int) -> int:
+        return lib().vla_kv_cache_bytes(self.handle, batch, prefix_len)
+
+    def set_loop_mode(self, mode: int):
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_LOOP_MODE, mode))
+
+    def prefix_kv_build(self, prefix_hidden, batch: int, prefix_len: int, kv_cache, kv_cache_bytes: int,
+                        stream=None):
+        _check(lib().vla_prefix_kv_build(self.handle, _ptr(prefix_hidden), batch, prefix_len, _ptr(kv_cache),
+                                         kv_cache_bytes, _stream(stream)))
+
+    def denoise(self, kv_cache, kv_cache_bytes: int, batch: int, prefix_len: int, noise, state,
+                t_schedule: Sequence[float], act_mean=None, act_std=None, actions_out=None, stream=None):
+        n_steps = len(t_schedule) - 1
+        sched = (ctypes.c_float * len(t_schedule))(*[float(t) for t in t_schedule])
+        _check(lib().vla_denoise(self.handle, _ptr(kv_cache), kv_cache_bytes, batch, prefix_len, _ptr(noise),
+                                 _ptr(state), sched, n_steps, _ptr(act_mean), _ptr(act_std), _ptr(actions_out),
+                                 _stream(stream)))
+
+
+def weight_count(cfg) -> int:
+    c = make_config(cfg)
+    return lib().vla_weight_count(ctypes.byref(c))
+
+
+def ternary_gemm(x, w_packed, M: int, N: int, K: int, acc_out, stream=None):
+    _check(lib().vla_ternary_gemm(_ptr(x), _ptr(w_packed), M, N, K, _ptr(acc_out), _stream(stream)))
+
+
+# ---- test-only per-kernel entries (include/vla_test.h) ---------------------
+
+def test_gemm(elem: int, x, w, M: int, N: int, K: int, y, force_nsplit: int = 0, stream=None):
+    _check(lib().vla_test_gemm(elem, _ptr(x), _ptr(w), M, N, K, force_nsplit, _ptr(y), _stream(stream)))
+
+
+def test_attention(elem: int, mode: int, q, k_self, v_self, k_cache, v_cache, B: int, n: int, P: int, H: int,
+                   G: int, hd: int, o, kv_split: int = 0, stream=None):
+    _check(lib().vla_test_attention(elem, mode, _ptr(q), _ptr(k_self), _ptr(v_self), _ptr(k_cache),
+                                    _ptr(v_cache), B, n, P, H, G, hd, kv_split, _ptr(o), _stream(stream)))
+
+
+def test_quantize_i8(x, M: int, K: int, q, r, stream=None):
+    _check(lib().vla_test_quantize_i8(_ptr(x), M, K, _ptr(q), _ptr(r), _stream(stream)))
+
+
+def test_ternary_linear(x, w_packed, M: int, N: int, K: int, scale: float, y, stream=None):
+    _check(lib().vla_test_ternary_linear(_ptr(x), _ptr(w_packed), M, N, K, float(scale), _ptr(y), _stream(stream)))

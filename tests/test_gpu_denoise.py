@@ -1,0 +1,183 @@
+"""End-to-end parity of vla_prefix_kv_build + vla_denoise against the fp64
+oracle on the seeded workloads, plus the closed-form special cases run on the
+GPU (zero / constant velocity field), determinism, graph-vs-stream identity
+and batch independence.
+
+Tolerances on the final action chunk: max|d| <= 1e-4 for the fp32 workload,
+<= 2e-2 for bf16 and ternary workloads.
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import vla_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+TOL = {"f32": 1e-4, "bf16": 2e-2, "ternary": 2e-2}
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def _pipe(cfg, W, inp, loop_mode=1):
+    from vla_testlib import Pipeline
+    return Pipeline(cfg, W, inp, loop_mode)
+
+
+def _oracle(cfg, W, inp, tau, mean=None, std=None):
+    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+    return cache, O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau, mean, std)
+
+
+def _check_cache(pipe, cache_ref, cfg):
+    got = pipe.cache_array()
+    tol = 1e-5 if cfg.wtype == "f32" else 1e-2 * max(1.0, np.abs(cache_ref).max())
+    if cfg.wtype == "ternary":
+        tol = 3e-2 * np.abs(cache_ref).max()
+    err = np.abs(got - cache_ref).max()
+    assert err <= tol, f"cache max err {err} > {tol}"
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16", "ternary_w2a8"])
+def test_end_to_end(torch, name):
+    from vla_testlib import workload
+    cfg, W, inp = workload(name, 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    mean = np.linspace(-0.5, 0.5, cfg.d_action).astype(np.float32)
+    std = np.linspace(0.5, 2.0, cfg.d_action).astype(np.float32)
+    cache_ref, ref = _oracle(cfg, W, inp, tau, mean, std)
+    pipe = _pipe(cfg, W, inp)
+    try:
+        pipe.build_cache()
+        from vla_testlib import to_device
+        out = pipe.denoise(tau, to_device(mean), to_device(std))
+        torch.cuda.synchronize()
+        got = out.cpu().numpy().astype(np.float64)
+        _check_cache(pipe, cache_ref, cfg)
+        err = np.abs(got - ref).max()
+        print(f"{name}: max|d| = {err:.3e} (tol {TOL[cfg.wtype]})")
+        assert np.all(np.isfinite(got))
+        assert err <= TOL[cfg.wtype], f"{name}: max|d| {err}"
+    finally:
+        pipe.close()
+
+
+def test_tiny_nonuniform_schedule_and_batch(torch):
+    """fp32 workload, B = 3, a non-uniform schedule, stream and graph drivers."""
+    cfg = wl.TINY_F32
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 3)
+    tau = np.array([1.0, 0.8, 0.45, 0.3, 0.05, 0.0], np.float32)
+    _, ref = _oracle(cfg, W, inp, tau)
+    for mode in (0, 1):
+        pipe = _pipe(cfg, W, inp, loop_mode=mode)
+        try:
+            pipe.build_cache()
+            got = pipe.denoise(tau).cpu().numpy()
+            assert np.abs(got - ref).max() <= 1e-4
+        finally:
+            pipe.close()
+
+
+def test_zero_and_constant_velocity_on_gpu(torch):
+    """W_out = 0: b_out = 0 returns the noise bit-exactly; b_out = c gives the
+    Euler endpoint noise + (tau_T - tau_0) c."""
+    cfg = wl.SMOLVLA_BF16.with_(n_layers=2)
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 2)
+    W["W_out"] = np.zeros_like(W["W_out"])
+    W["b_out"] = np.zeros_like(W["b_out"])
+    tau = wl.uniform_schedule(cfg.n_steps)
+    pipe = _pipe(cfg, W, inp)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau).cpu().numpy()
+        assert np.array_equal(got, inp["noise"])
+    finally:
+        pipe.close()
+    c = np.linspace(-1, 1, cfg.d_action).astype(np.float32)
+    W["b_out"] = c
+    pipe = _pipe(cfg, W, inp)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau).cpu().numpy()
+        expect = inp["noise"] + (float(tau[-1]) - float(tau[0])) * c
+        np.testing.assert_allclose(got, expect, atol=2e-6)
+    finally:
+        pipe.close()
+
+
+def test_determinism_and_graph_equals_stream(torch):
+    from vla_testlib import workload
+    cfg, W, inp = workload("smolvla_bf16", 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    outs = []
+    for mode in (1, 0):
+        pipe = _pipe(cfg, W, inp, loop_mode=mode)
+        try:
+            pipe.build_cache()
+            a = pipe.denoise(tau).clone()
+            pipe.build_cache()       # rebuilt cache: same bits
+            b = pipe.denoise(tau).clone()
+            assert torch.equal(a, b)
+            outs.append(a)
+        finally:
+            pipe.close()
+    assert torch.equal(outs[0], outs[1])
+
+
+def test_stress_batch_independence_and_parity(torch):
+    """pi0-shaped stress workload (P = 2048, n = 100): B = 4 requests in one
+    call equal four B = 1 calls bitwise; request 0 matches the oracle over 2
+    solver steps."""
+    from vla_testlib import Pipeline
+    cfg = wl.STRESS_PI0.with_(n_steps=2)
+    W = wl.make_weights(cfg)
+    inp4 = wl.make_batch(cfg, 4)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    p4 = Pipeline(cfg, W, inp4)
+    try:
+        p4.build_cache()
+        out4 = p4.denoise(tau).cpu().numpy()
+    finally:
+        p4.close()
+    for r in (0, 3):
+        one = {k: v[r:r + 1] for k, v in inp4.items()}
+        p1 = Pipeline(cfg, W, one)
+        try:
+            p1.build_cache()
+            out1 = p1.denoise(tau).cpu().numpy()
+        finally:
+            p1.close()
+        assert np.array_equal(out1[0], out4[r]), f"request {r} differs between batch 4 and batch 1"
+        if r == 0:
+            _, ref = _oracle(cfg, W, one, tau)
+            err = np.abs(out1[0] - ref[0]).max()
+            assert err <= 2e-2, f"stress request 0 max|d| {err}"
+
+
+def test_cache_reuse_equals_rebuild_per_call(torch):
+    """The cached K/V serve every solver step: a T-step call equals the same
+    call after rebuilding the cache (bitwise)."""
+    cfg = wl.PI0_BF16.with_(n_layers=3, n_steps=4)
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    pipe = _pipe(cfg, W, inp)
+    try:
+        pipe.build_cache()
+        a = pipe.denoise(tau).clone()
+        b = pipe.denoise(tau).clone()
+        pipe.build_cache()
+        c = pipe.denoise(tau).clone()
+        assert torch.equal(a, b) and torch.equal(a, c)
+        _, ref = _oracle(cfg, W, inp, tau)
+        assert np.abs(a.cpu().numpy() - ref).max() <= 2e-2
+    finally:
+        pipe.close()

@@ -1,0 +1,167 @@
+"""Kernel-level parity of the HIP path against the fp64 oracle, through the
+C ABI (include/vla.h, include/vla_test.h), on seeded inputs at the
+workloads' real shapes plus ragged ones (M, N, K not multiples of the tiles)."""
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import vla_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def _vla():
+    from paper_2606_08094_amd import vla
+    return vla
+
+
+def _dev(torch, arr, bf16=False):
+    from vla_testlib import to_device
+    return to_device(arr, bf16)
+
+
+def _fp32_bound(x, w):
+    """Rigorous fp32-accumulation bound for x w^T: K * 2^-24 * |x| |w|^T (+ slack)."""
+    K = x.shape[1]
+    return (K * 2.0 ** -24 + 1e-7) * (np.abs(x) @ np.abs(w).T) + 1e-30
+
+
+GEMM_SHAPES = [
+    # (M, N, K)  pi0 / SmolVLA / tiny shapes, ragged edges, large M
+    (50, 2560, 1024), (50, 1024, 2048), (50, 1024, 4096), (50, 32, 1024),
+    (50, 1600, 720), (50, 720, 2048), (50, 6, 720),
+    (8, 384, 256), (8, 7, 256), (1, 5, 8), (17, 33, 136), (100, 2560, 1024),
+    (816, 512, 2048), (10, 6144, 1024),
+]
+
+
+@pytest.mark.parametrize("elem", [1, 0])
+@pytest.mark.parametrize("M,N,K", GEMM_SHAPES)
+def test_gemm_parity(torch, elem, M, N, K):
+    if elem == 0 and K % 4:
+        pytest.skip("fp32 needs K % 4 == 0")
+    bf = elem == 1
+    seed = 1000 * M + N + K
+    x = wl.random_matrix((M, K), seed, 1.0, bf16=bf)
+    w = wl.random_matrix((N, K), seed + 1, 0.05, bf16=bf)
+    ref = O.linear(x, w)
+    bound = _fp32_bound(x.astype(np.float64), w.astype(np.float64))
+    for split in (0, 1, 3):
+        y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        _vla().test_gemm(elem, _dev(torch, x, bf), _dev(torch, w, bf), M, N, K, y, force_nsplit=split)
+        got = y.cpu().numpy().astype(np.float64)
+        err = np.abs(got - ref)
+        assert np.all(err <= bound), f"split={split} max err {err.max()} worst ratio {(err / bound).max()}"
+
+
+ATTN_CASES = [
+    # (elem, mode, B, n, P, H, G, hd)
+    (1, 2, 1, 50, 816, 8, 1, 256),     # pi0 joint
+    (1, 1, 1, 50, 241, 15, 5, 64),     # SmolVLA cross
+    (1, 0, 1, 50, 0, 15, 5, 64),       # SmolVLA self
+    (1, 2, 1, 8, 512, 20, 5, 128),     # ternary workload joint
+    (1, 2, 2, 100, 300, 8, 1, 256),    # batched requests
+    (1, 1, 1, 3, 1, 4, 2, 64),         # single prefix key
+    (0, 0, 1, 8, 0, 4, 1, 64),         # tiny fp32 self
+    (0, 1, 1, 8, 64, 4, 1, 64),        # tiny fp32 cross
+    (0, 2, 2, 19, 45, 6, 3, 128),      # ragged fp32 joint
+]
+
+
+@pytest.mark.parametrize("case", ATTN_CASES, ids=[str(c) for c in ATTN_CASES])
+@pytest.mark.parametrize("kv_split", [0, 1, 3])
+def test_attention_parity(torch, case, kv_split):
+    elem, mode, B, n, P, H, G, hd = case
+    bf = elem == 1
+    s = 7 * n + P + H + hd + mode
+    q = wl.random_matrix((B * n, H * hd), s, 1.0, bf16=bf)
+    ks = wl.random_matrix((B * n, G * hd), s + 1, 1.0, bf16=bf)
+    vs = wl.random_matrix((B * n, G * hd), s + 2, 1.0, bf16=bf)
+    kc = wl.random_matrix((B, G, max(P, 1), hd), s + 3, 1.0, bf16=bf)
+    vc = wl.random_matrix((B, G, max(P, 1), hd), s + 4, 1.0, bf16=bf)
+    o = torch.full((B * n, H * hd), float("nan"), dtype=torch.bfloat16 if bf else torch.float32, device="cuda")
+    _vla().test_attention(elem, mode, _dev(torch, q, bf), _dev(torch, ks, bf), _dev(torch, vs, bf),
+                          _dev(torch, kc, bf), _dev(torch, vc, bf), B, n, P, H, G, hd, o, kv_split=kv_split)
+    got = o.float().cpu().numpy().astype(np.float64)
+    for b in range(B):
+        rows = slice(b * n, (b + 1) * n)
+        kself = ks[rows].reshape(n, G, hd).transpose(1, 0, 2)
+        vself = vs[rows].reshape(n, G, hd).transpose(1, 0, 2)
+        if mode == 0:
+            kk, vv = kself, vself
+        elif mode == 1:
+            kk, vv = kc[b], vc[b]
+        else:
+            kk, vv = np.concatenate([kc[b], kself], 1), np.concatenate([vc[b], vself], 1)
+        ref = O.attention(q[rows], kk, vv, H, G, hd)
+        # bf16: probabilities and the output are rounded to bf16 (relative 2^-8 each)
+        tol = 1.2e-2 * np.abs(vv).max() if bf else 2e-5
+        err = np.abs(got[rows] - ref).max()
+        assert err <= tol, f"request {b}: max err {err} > {tol}"
+
+
+def test_quantize_i8_bit_exact(torch):
+    rows, codes = [], []
+    import os
+    for line in open(os.path.join(os.path.dirname(__file__), "golden", "quantizer_ties.txt")):
+        if line.startswith("row:"):
+            rows.append([float(v) for v in line.split()[1:]])
+    K = 300
+    x = wl.random_matrix((37, K), 5, 3.0)
+    for i, r in enumerate(rows):
+        x[i, :] = 0
+        x[i, :len(r)] = r
+    x[len(rows), :] = 0.0
+    qd = torch.empty((37, K), dtype=torch.int8, device="cuda")
+    rd = torch.empty(37, dtype=torch.float32, device="cuda")
+    _vla().test_quantize_i8(_dev(torch, x), 37, K, qd, rd)
+    q_ref, r_ref = O.quantize_int8_rows(x)
+    assert np.array_equal(qd.cpu().numpy(), q_ref)
+    assert np.array_equal(rd.cpu().numpy(), r_ref)
+
+
+TERN_SHAPES = [(8, 3840, 2560), (8, 2560, 2560), (8, 13824, 2560), (8, 2560, 6912), (56, 2560, 6912),
+               (512, 1280, 2560), (3, 17, 64), (20, 100, 192), (5, 7, 68), (2, 3, 4)]
+
+
+@pytest.mark.parametrize("M,N,K", TERN_SHAPES)
+def test_ternary_gemm_bit_exact(torch, M, N, K):
+    x = wl.random_int8((M, K), M + N)
+    w = wl.random_ternary((N, K), K + N)
+    # include the extreme rows: all -128 and all 127
+    x[0, :] = -128
+    if M > 1:
+        x[1, :] = 127
+    packed = wl.pack_ternary(w)
+    out = torch.full((M, N), 12345, dtype=torch.int32, device="cuda")
+    _vla().ternary_gemm(torch.from_numpy(x).cuda(), torch.from_numpy(packed).cuda(), M, N, K, out)
+    assert np.array_equal(out.cpu().numpy().astype(np.int64), O.ternary_gemm(x, packed, K))
+
+
+def test_ternary_gemm_empty(torch):
+    out = torch.zeros(1, dtype=torch.int32, device="cuda")
+    x = torch.zeros(16, dtype=torch.int8, device="cuda")
+    w = torch.zeros(16, dtype=torch.uint8, device="cuda")
+    _vla().ternary_gemm(x, w, 0, 5, 64, out)
+    _vla().ternary_gemm(x, w, 3, 0, 64, out)
+    assert int(out.cpu()[0]) == 0
+
+
+@pytest.mark.parametrize("M,N,K", [(8, 3840, 2560), (8, 2560, 6912), (512, 1280, 2560), (13, 70, 128)])
+def test_ternary_linear(torch, M, N, K):
+    x = wl.random_matrix((M, K), 3 + M, 1.0)
+    w = wl.random_ternary((N, K), 4 + N)
+    scale = np.float32(0.0244)
+    y = torch.empty((M, N), dtype=torch.float32, device="cuda")
+    _vla().test_ternary_linear(_dev(torch, x), torch.from_numpy(wl.pack_ternary(w)).cuda(), M, N, K, float(scale), y)
+    ref = O.ternary_linear(x, w, scale)
+    # identical int8 codes and int32 sums; only the fp32 dequantisation rounds
+    np.testing.assert_allclose(y.cpu().numpy(), ref, rtol=1e-6, atol=1e-7)
