@@ -41,6 +41,17 @@ P_MAX = 4.0
 ABSMAX_FLOOR = np.float32(1e-5)
 
 
+# --- storage precision ------------------------------------------------------
+
+def round_to_bf16(x):
+    """Nearest-even bf16 value of float32(x), as float64 (fp32 first, as a
+    kernel that accumulates in fp32 and stores bf16 would)."""
+    f = np.ascontiguousarray(np.asarray(x, dtype=F64).astype(np.float32))
+    u = f.view(np.uint32).astype(np.uint64)
+    u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
+    return u.astype(np.uint32).view(np.float32).astype(F64)
+
+
 # --- elementwise pieces -----------------------------------------------------
 
 def silu(x):
@@ -245,14 +256,20 @@ def input_embedding(cfg, W, a, s):
     return linear(a, W["W_in"], W["b_in"]) + xs + np.asarray(W["E_pos"], F64)
 
 
-def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None) -> np.ndarray:
+def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str = "fp64") -> np.ndarray:
     """One pass of the action head over the chunk a [n][A]: returns the velocity
     (or, for the regression head, the action chunk) v [n][A].
 
     cache_b: [Lc][2][G][P][hd] for this request.  If prefix_b is given the
     cross K/V are recomputed from it here instead of being read from cache_b
     (used to check that caching changes nothing).
+
+    storage="kernel" rounds to bf16 the values a bf16 kernel stores between
+    steps of the W2A8 path (the projected Q, K, V and the attention output that
+    the O-projection quantiser reads), so that every int8 quantisation decision
+    is taken on inputs of the kernel's precision; "fp64" keeps them exact.
     """
+    rb = round_to_bf16 if storage == "kernel" else (lambda v: v)
     mods, (gf, bf) = modulation(cfg, W, t)
     x = input_embedding(cfg, W, a, s)
     H, G, hd, eps = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.rms_eps
@@ -276,10 +293,10 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None) -> np.ndarray
                     h = mlp_activation(cfg.mlp, _lin(cfg, W, p + "W_g", u), _lin(cfg, W, p + "W_u", u))
                     y = _lin(cfg, W, p + "W_d", h)
             else:
-                q = _lin(cfg, W, p + "W_q", u)
+                q = rb(_lin(cfg, W, p + "W_q", u))
                 if kind in ("self", "joint"):
-                    ks = split_heads(_lin(cfg, W, p + "W_k", u), G, hd)
-                    vs = split_heads(_lin(cfg, W, p + "W_v", u), G, hd)
+                    ks = split_heads(rb(_lin(cfg, W, p + "W_k", u)), G, hd)
+                    vs = split_heads(rb(_lin(cfg, W, p + "W_v", u)), G, hd)
                 if kind == "self":
                     k_all, v_all = ks, vs
                 elif kind == "cross":
@@ -287,7 +304,7 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None) -> np.ndarray
                 else:   # joint: one softmax over [prefix rows ; action rows]
                     k_all = np.concatenate([kc, ks], axis=1)
                     v_all = np.concatenate([vc, vs], axis=1)
-                o = attention(q, k_all, v_all, H, G, hd)
+                o = rb(attention(q, k_all, v_all, H, G, hd))
                 y = _lin(cfg, W, p + "W_o", o)
             x = x + np.asarray(alpha, F64) * y
     return linear(ada_rms(x, gf, bf, eps), W["W_out"], W["b_out"])
@@ -313,15 +330,19 @@ def denormalize(a, mean=None, std=None):
 
 
 def denoise(cfg, W, cache, noise, state, tau, act_mean=None, act_std=None,
-            prefix_hidden=None, requests: Optional[List[int]] = None) -> np.ndarray:
+            prefix_hidden=None, requests: Optional[List[int]] = None, storage: str = "fp64") -> np.ndarray:
     """The whole chunk for every request: Euler over T solver steps (the
     regression head takes one pass and returns its output), then denormalise.
 
     cache [Lc][2][B][G][P][hd]; noise [B][n][A]; state [B][S]; tau [T+1].
     With prefix_hidden given, cross K/V are recomputed at every step instead of
     read from the cache.  requests restricts the evaluation to some of the B.
+    storage="kernel" (see expert_forward) also reads the cache as bf16, its
+    element type in a bf16 kernel.
     """
     noise = np.asarray(noise, F64)
+    if storage == "kernel" and cache is not None:
+        cache = round_to_bf16(cache)
     B = noise.shape[0]
     reqs = range(B) if requests is None else requests
     out = np.zeros((len(reqs),) + noise.shape[1:], dtype=F64)
@@ -330,7 +351,7 @@ def denoise(cfg, W, cache, noise, state, tau, act_mean=None, act_std=None,
         pb = None if prefix_hidden is None else np.asarray(prefix_hidden, F64)[b]
 
         def vel(a, k, t, cb=cb, pb=pb, b=b):
-            return expert_forward(cfg, W, cb, a, state[b], t, prefix_b=pb)
+            return expert_forward(cfg, W, cb, a, state[b], t, prefix_b=pb, storage=storage)
 
         if cfg.head_regression:
             a = vel(noise[b], 0, float(tau[0]))

@@ -4,8 +4,14 @@ GPU (zero / constant velocity field), determinism, graph-vs-stream identity
 and batch independence.
 
 Tolerances on the final action chunk: max|d| <= 1e-4 for the fp32 workload,
-<= 2e-2 for bf16 and ternary workloads.
+<= 2e-2 for the bf16 workloads.  The 24-layer W2A8 workload is checked against
+the oracle's own rounding-noise envelope (tests/golden/ternary_envelope.txt):
+its int8 activation codes flip under any rounding difference and the flips
+compound, so elementwise agreement is asserted only where no flip can cascade
+(one layer, one residual branch at a time).
 """
+import os
+
 import numpy as np
 import pytest
 
@@ -44,7 +50,7 @@ def _check_cache(pipe, cache_ref, cfg):
     assert err <= tol, f"cache max err {err} > {tol}"
 
 
-@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16", "ternary_w2a8"])
+@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16"])
 def test_end_to_end(torch, name):
     from vla_testlib import workload
     cfg, W, inp = workload(name, 1)
@@ -181,3 +187,54 @@ def test_cache_reuse_equals_rebuild_per_call(torch):
         assert np.abs(a.cpu().numpy() - ref).max() <= 2e-2
     finally:
         pipe.close()
+
+
+def _ternary_run(torch, cfg, W, inp):
+    from vla_testlib import Pipeline
+    tau = wl.uniform_schedule(1)
+    pipe = Pipeline(cfg, W, inp)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        cache_ref = O.prefix_kv_build(cfg, W, inp["prefix"])
+        _check_cache(pipe, cache_ref, cfg)
+    finally:
+        pipe.close()
+    ref = O.denoise(cfg, W, cache_ref, inp["noise"], inp["state"], tau, storage="kernel")
+    return got, ref
+
+
+@pytest.mark.parametrize("branch", ["attention", "mlp"])
+def test_ternary_single_branch(torch, branch):
+    """Full W2A8 widths (d = 2560, F = 6912, 20 x 128 heads, 5 K/V heads,
+    P = 512), one layer, one residual branch gated on (alpha = 0.5) and the
+    other off: every ternary projection, quantiser and epilogue of the branch
+    runs, and no flipped code can cascade through a later layer."""
+    cfg = wl.TERNARY_W2A8.with_(n_layers=1)
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    d = cfg.d_model
+    mod = W["L0.mod"]
+    on, off = (0, 1) if branch == "attention" else (1, 0)
+    mod[(3 * on + 2) * d:(3 * on + 3) * d] = 0.5
+    mod[(3 * off + 2) * d:(3 * off + 3) * d] = 0.0
+    got, ref = _ternary_run(torch, cfg, W, inp)
+    err = np.abs(got - ref).max()
+    print(f"ternary {branch} branch: max|d| = {err:.3e}")
+    assert err <= 2e-2
+
+
+def test_ternary_full_depth_envelope(torch):
+    """24-layer W2A8 workload: the GPU chunk lies within twice the oracle's own
+    rounding-noise envelope around the oracle chunk."""
+    from vla_testlib import workload
+    cfg, W, inp = workload("ternary_w2a8", 1)
+    env_max, env_mean, ref_rms = np.loadtxt(os.path.join(os.path.dirname(__file__), "golden",
+                                                         "ternary_envelope.txt"))
+    got, ref = _ternary_run(torch, cfg, W, inp)
+    d = np.abs(got - ref)
+    print(f"ternary 24 layers: max|d| = {d.max():.3e} (envelope {env_max:.3e}), "
+          f"mean|d| = {d.mean():.3e} (envelope {env_mean:.3e}), rms ref {ref_rms:.3f}")
+    assert np.all(np.isfinite(got))
+    assert abs(np.sqrt(np.mean(ref ** 2)) - ref_rms) < 1e-6 * max(1.0, ref_rms) + 1e-9
+    assert d.mean() <= 2 * env_mean and d.max() <= 2 * env_max
