@@ -1,0 +1,204 @@
+#!/usr/bin/env python3
+"""Benchmark of the denoise loop on one MI355X.
+
+A bench step is one whole pass of the hot path for one observation: the
+prefix cross-K/V build plus the full solver loop (time conditioning, T Euler
+steps of the expert, denormalisation) for the pi0-shaped bf16 expert at
+batch 1 (18 layers, width 1024, 8 x 256 query heads, 1 K/V head, GeGLU 4096,
+816 prefix tokens of width 2048, chunk 50 x 32, T = 10).  Inputs are seeded,
+synthetic and resident in HBM before the timed region.
+
+Prints one JSON line: chunks/s as `value`, the per-solver-step latency from
+the linear fit chunk(T) = fixed + T * step over T in {1, 2, 5, 10}, the
+roofline of the dominant kernel (algorithmic bytes per launch over its mean
+launch time, both from a live per-launch HIP-event pass), and the CPU
+oracle timed on a bounded sample on this host.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+sys.path.insert(0, os.path.join(ROOT, "tests"))
+
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
+BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
+WORKLOAD = "pi0_bf16"
+
+
+def log(*a):
+    print(*a, file=sys.stderr, flush=True)
+
+
+def time_chunks(torch, pipe, tau, iters):
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(iters):
+        pipe.build_cache()
+        pipe.denoise(tau)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / iters
+
+
+def time_denoise(torch, pipe, tau, iters):
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(iters):
+        pipe.denoise(tau)
+    end.record()
+    torch.cuda.synchronize()
+    return start.elapsed_time(end) / iters
+
+
+def roofline_from_profile(ops, T):
+    """Dominant kernel = the (kind, shape) group with the largest total time."""
+    groups = {}
+    for o in ops:
+        key = (o["kind"], o["M"], o["N"], o["K"])
+        g = groups.setdefault(key, {"n": 0, "ms": 0.0, "bytes": 0.0, "flops": 0.0})
+        g["n"] += 1
+        g["ms"] += o["ms"]
+        g["bytes"] += o["bytes"]
+        g["flops"] += o["flops"]
+    breakdown = sorted(({"op": f"{k[0]} M={k[1]} N={k[2]} K={k[3]}", "launches": v["n"],
+                         "mean_us": round(1000.0 * v["ms"] / v["n"], 2),
+                         "GBps": round(v["bytes"] / (v["ms"] * 1e-3) / 1e9, 1),
+                         "share": 0.0, "ms": v["ms"]} for k, v in groups.items()),
+                       key=lambda r: -r["ms"])
+    tot = sum(r["ms"] for r in breakdown)
+    for r in breakdown:
+        r["share"] = round(r.pop("ms") / tot, 3)
+    (kind, M, N, K), g = max(groups.items(), key=lambda kv: kv[1]["ms"])
+    bytes_per = g["bytes"] / g["n"]
+    us_per = 1000.0 * g["ms"] / g["n"]
+    achieved = bytes_per / (us_per * 1e-6) / 1e9
+    total_ms = sum(o["ms"] for o in ops)
+    step_bytes = sum(o["bytes"] for o in ops) / T
+    return {
+        "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+        "kernel": f"{kind} M={M} N={N} K={K}", "launches_per_chunk": g["n"],
+        "bytes_per_launch": int(bytes_per), "launch_us": round(us_per, 3),
+        "flops_per_launch": int(g["flops"] / g["n"]),
+        "share_of_profiled_time": round(g["ms"] / total_ms, 3),
+        "alg_bytes_per_solver_step": int(step_bytes),
+        "breakdown": breakdown[:12],
+    }
+
+
+def cpu_baseline(cfg, W, inp, tau):
+    """The oracle as it stands, one full chunk (prefix K/V build + T Euler
+    steps) of the same workload on the host cores."""
+    from oracle import vla_oracle as O
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    t0 = time.perf_counter()
+    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+    O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+    dt = time.perf_counter() - t0
+    return {"value": round(1.0 / dt, 5), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
+            "sample": f"1 chunk of {cfg.name} (prefix K/V build + {cfg.n_steps} Euler steps, batch 1), "
+                      f"{dt:.1f} s, numpy fp64"}
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=30, help="timed chunks")
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this benchmark runs on exactly one GPU: the denoise loop of one "
+                                   "request batch is a single-GPU workload (requests shard across GPUs "
+                                   "with no exchange); run with --gpus 1"}))
+        sys.exit(2)
+
+    import numpy as np
+    import torch
+    import workloads as wl
+    from vla_testlib import Pipeline
+
+    cfg = wl.CONFIGS[WORKLOAD]
+    log("generating weights ...")
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    pipe = Pipeline(cfg, W, inp, loop_mode=1)
+    log("warmup ...")
+    for _ in range(args.warmup):
+        pipe.build_cache()
+        pipe.denoise(tau)
+    torch.cuda.synchronize()
+    log("timed region ...")
+    ms_chunk = time_chunks(torch, pipe, tau, args.steps)
+    log(f"chunk {ms_chunk * 1000:.1f} us")
+
+    # per-solver-step latency: linear fit of denoise time over T
+    Ts = [1, 2, 5, cfg.n_steps]
+    ms_T = []
+    for T in Ts:
+        tT = wl.uniform_schedule(T)
+        for _ in range(3):
+            pipe.denoise(tT)
+        ms_T.append(min(time_denoise(torch, pipe, tT, max(5, args.steps // 2)) for _ in range(2)))
+    slope, intercept = np.polyfit(np.array(Ts, float), np.array(ms_T), 1)
+    ms_build = time_chunks(torch, pipe, tau, 1) - ms_T[-1]
+
+    # live per-launch timings (launch-per-phase driver with HIP events)
+    pipe.model.set_profile(True)
+    pipe.denoise(tau)
+    pipe.denoise(tau)
+    torch.cuda.synchronize()
+    ops = pipe.model.profile_read()
+    pipe.model.set_profile(False)
+    roof = roofline_from_profile(ops, cfg.n_steps)
+    step_bytes = roof["alg_bytes_per_solver_step"]
+    step_us = slope * 1000.0
+    result = {
+        "metric": "denoise step latency (µs) + action chunks/sec @ batch 1; % MFMA/HBM roofline",
+        "value": round(1000.0 / ms_chunk, 2),
+        "unit": "chunks/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_chunk, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "pi0_bf16: 18 layers, width 1024, 8x256 query heads, 1 KV head, GeGLU 4096, "
+                               "prefix 816 (width 2048), chunk 50x32, 10 Euler steps",
+                   "batch": 1, "solver_steps": cfg.n_steps, "prefix_len": cfg.prefix_len, "chunk": cfg.n_action,
+                   "parallelism": "single GPU"},
+        "denoise_step_us": round(step_us, 2),
+        "chunk_fixed_us": round(intercept * 1000.0, 2),
+        "prefix_kv_build_us": round(ms_build * 1000.0, 2),
+        "denoise_T_us": {str(T): round(v * 1000.0, 2) for T, v in zip(Ts, ms_T)},
+        "step_hbm_frac": round(step_bytes / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "roofline": roof,
+    }
+    pipe.close()
+    if not args.no_cpu_baseline:
+        log("cpu baseline (oracle) ...")
+        result["cpu_baseline"] = cpu_baseline(cfg, W, inp, tau)
+    print(json.dumps(result), flush=True)
+
+
+if __name__ == "__main__":
+    main()

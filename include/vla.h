@@ -56,9 +56,9 @@ typedef struct vla_config {
   int32_t n_layers;        /* L */
   int32_t d_model;         /* d (even) */
   int32_t n_heads;         /* H query heads */
-  int32_t head_dim;        /* hd (multiple of 16, <= 256) */
+  int32_t head_dim;        /* hd: 64, 128 or 256 (fp32 models: 64 or 128) */
   int32_t n_kv_heads;      /* G (H % G == 0); head i reads K/V head floor(i*G/H) */
-  int32_t d_ff;            /* F (multiple of 16) */
+  int32_t d_ff;            /* F (multiple of 16; of 64 for ternary models) */
   int32_t d_prefix;        /* d_p, width of the prefix hidden states */
   int32_t n_action;        /* n, action tokens per chunk */
   int32_t d_action;        /* A */
@@ -149,10 +149,32 @@ vla_status vla_denoise(vla_model* model, const void* kv_cache, size_t kv_cache_b
 vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
                             int32_t* acc_out, void* stream);
 
-/* Loop driver of vla_denoise: 0 = one launch per phase on the stream,
- * 1 = the same launches captured once in a HIP graph and replayed (default). */
-enum { VLA_OPT_LOOP_MODE = 0 };
+/* Options:
+ *  VLA_OPT_LOOP_MODE: loop driver of vla_denoise, 0 = one launch per phase on
+ *    the stream, 1 = the same launches captured once in a HIP graph and
+ *    replayed (default).
+ *  VLA_OPT_PROFILE: 1 = time every launch of the following vla_denoise calls
+ *    with HIP events (launch-per-phase driver; read with vla_profile_read). */
+enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
+
+/* One timed launch of a profiled vla_denoise call. */
+enum { VLA_OP_GEMM = 0, VLA_OP_GEMM_GLU = 1, VLA_OP_ATTENTION = 2, VLA_OP_TERNARY = 3,
+       VLA_OP_QUANTIZE = 4, VLA_OP_SMALL = 5 };
+typedef struct vla_op_time {
+  int32_t kind;   /* VLA_OP_* */
+  int32_t M;      /* GEMM rows (tokens) / attention queries */
+  int32_t N;      /* GEMM output columns / attention keys */
+  int32_t K;      /* GEMM reduction length / attention head_dim */
+  double bytes;   /* algorithmic bytes: weights + cached K/V read once, activations in and out */
+  double flops;   /* algorithmic flops (integer ops for the W2A8 GEMM) */
+  float ms;       /* measured duration between HIP events around the launch */
+} vla_op_time;
+
+/* Copy the launch timings of the model's last profiled vla_denoise call into
+ * out[0 .. max_ops-1] (synchronising on its events).  Returns the number of
+ * launches of that call, or -1 if nothing was profiled. */
+int32_t vla_profile_read(vla_model* model, vla_op_time* out, int32_t max_ops);
 
 /* Thread-local message for the last non-OK status of this thread. */
 const char* vla_last_error(void);

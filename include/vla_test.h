@@ -15,11 +15,12 @@
 extern "C" {
 #endif
 
-/* y[M][N] (fp32) = x[M][K] w[N][K]^T on the MFMA GEMM of the projections,
- * with its split-K reduction.  K % 8 == 0 (bf16) or K % 4 == 0 (fp32).
- * force_nsplit > 0 forces that many K-splits (0 = the runtime's choice). */
+/* y[M][N] (fp32) = x[M][K] w[N][K]^T on the MFMA GEMMs of the projections.
+ * K % 8 == 0 (bf16) or K % 4 == 0 (fp32).  variant: 0 = the runtime's choice,
+ * 1 = the wide kernel, 2 = the skinny kernel (VLA_E_UNSUPPORTED if the shape
+ * does not fit it). */
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
-                         int32_t force_nsplit, float* y, void* stream);
+                         int32_t variant, float* y, void* stream);
 
 /* Attention of B requests of n action tokens (paper Sec. 3.1: the action head
  * cross-attends to the cached prefix).  mode 0 self (keys = the n tokens),

@@ -1,15 +1,16 @@
-// Fused epilogues of the expert's projections, shared by the dense MFMA GEMM
-// and the ternary W2A8 GEMM.  The caller passes the reduced fp32 tile of one
-// workgroup: lane holds rows 4*(lane/16)+i of each 16-row subtile ms and
-// column lane%16 of W-row subtile s, for W rows nw0 + 16*s + lane%16.
+// Fused epilogues of the expert's projections, shared by the dense MFMA GEMMs
+// and the ternary W2A8 GEMM.  One call handles the reduced fp32 tile of one
+// wave: lane holds rows 4*(lane/16)+i of each 16-row subtile ms (rows from m0)
+// and column lane%16 of each of the NSUB W-row subtiles starting at W row nb.
+// EPI_PARTIAL writes the raw fp32 tile of K-split `split` to
+// out + split * M * ldo (a later launch sums the splits).
 #pragma once
 #include "device_common.h"
 
 template <typename T, int MS, int NSUB>
-__device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x4 (&acc)[MS][NSUB], int m0, int ntile,
-                                              int nw0, float* red_s) {
-  constexpr int MT = 16 * MS;
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+__device__ __forceinline__ void wave_epilogue(const GemmArgs& a, const f32x4 (&acc)[MS][NSUB], int m0, int nb,
+                                              int split) {
+  const int lane = threadIdx.x & 63;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int M = a.M, N = a.N;
   switch (a.epi) {
@@ -21,7 +22,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x4 (&acc)[MS
           const int m = m0 + ms * 16 + g4 * 4 + i;
 #pragma unroll
           for (int s = 0; s < NSUB; ++s) {
-            const int n = nw0 + s * 16 + r16;
+            const int n = nb + s * 16 + r16;
             if (m < M && n < N) {
               float v = acc[ms][s][i] + (a.bias ? a.bias[n] : 0.0f);
               v = act_f(a.act, v);
@@ -43,7 +44,7 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x4 (&acc)[MS
           const int m = m0 + ms * 16 + g4 * 4 + i;
 #pragma unroll
           for (int s = 0; s < NSUB; ++s) {
-            const int n = nw0 + s * 16 + r16;
+            const int n = nb + s * 16 + r16;
             if (m < M && n < N) {
               const int b = m / a.P, p = m - b * a.P;
               const int kv = n / a.d_kv, rem = n - kv * a.d_kv;
@@ -56,8 +57,9 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x4 (&acc)[MS
       break;
     }
     case EPI_GLU: {
+      // W rows nb .. nb+15 are gate rows, nb+16 .. nb+31 the matching up rows.
       const int F = N / 2;
-      const int f = ntile * 64 + wave * 16 + r16;
+      const int f = (nb / 32) * 16 + r16;
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -73,36 +75,40 @@ __device__ __forceinline__ void gemm_epilogue(const GemmArgs& a, f32x4 (&acc)[MS
         }
       break;
     }
+    case EPI_PARTIAL: {
+      float* out = reinterpret_cast<float*>(a.out) + (size_t)split * M * a.ldo;
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int m = m0 + ms * 16 + g4 * 4 + i;
+#pragma unroll
+          for (int s = 0; s < NSUB; ++s) {
+            const int n = nb + s * 16 + r16;
+            if (m < M && n < N) out[(size_t)m * a.ldo + n] = acc[ms][s][i];
+          }
+        }
+      break;
+    }
     case EPI_RESID: {
-      const int n = nw0 + r16;  // NSUB == 1
+      const int n = nb + r16;  // NSUB == 1
       const float al = (n < N) ? a.alpha[n] : 0.0f;
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
-          const int row = ms * 16 + g4 * 4 + i;
-          const int m = m0 + row;
-          float sq = 0.0f;
+          const int m = m0 + ms * 16 + g4 * 4 + i;
           if (m < M && n < N) {
             float* xp = a.xres + (size_t)m * a.ldxr + n;
-            const float xv = *xp + al * acc[ms][0][i];
-            *xp = xv;
-            sq = xv * xv;
+            *xp = *xp + al * acc[ms][0][i];
           }
-          sq = sum16(sq);
-          if (r16 == 0) red_s[wave * MT + row] = sq;
         }
-      __syncthreads();
-      if (tid < MT && m0 + tid < M) {
-        const float t = red_s[tid] + red_s[MT + tid] + red_s[2 * MT + tid] + red_s[3 * MT + tid];
-        a.rowss_out[(size_t)ntile * M + m0 + tid] = t;
-      }
       break;
     }
     case EPI_EULER: {
       const CallParams* cp = a.cp;
       const float dt = cp->tau[a.step + 1] - cp->tau[a.step];
-      const int n = nw0 + r16;
+      const int n = nb + r16;
 #pragma unroll
       for (int ms = 0; ms < MS; ++ms)
 #pragma unroll

@@ -1,16 +1,24 @@
 // Attention of the action tokens over [cached prefix K/V ; action-token K/V].
 //
 // Self (keys = the chunk's own tokens), cross (keys = the cached prefix rows)
-// and joint (one softmax over both) share one kernel.  Head h reads K/V head
-// floor(h*G/H).  No mask: every key is visible to every query.
+// and joint (one softmax over both) share one kernel.  Query head h reads K/V
+// head floor(h*G/H).  No mask: every key is visible to every query.
 //
-// One wave handles (request b, head h, a tile of 16 queries, one key split).
-// Scores are computed transposed, S^T = K Q^T on MFMA, so that each lane's
-// column is one query: the running max and sum of the online softmax live in
-// the lane, and P^T comes out of the accumulator already in the B-operand
-// layout of O^T += V^T P^T.  V blocks of 32 keys are staged in LDS.  Key splits
-// write unnormalised partials plus (max, sum); the last wave to arrive merges
-// them in split order.
+// One workgroup handles (request b, 16-query tile, K/V head g, key split) with
+// one wave per query head of the group, so a K/V block of 32 keys is staged in
+// LDS once and serves every head that shares it.  Blocks are double-buffered:
+// the loads of block j+1 are in flight while block j is multiplied.  Prefix
+// blocks and action-token blocks never mix, so a block has a single source.
+//
+// Scores are computed transposed, S^T = K Q^T on MFMA, so each lane's column is
+// one query and the online-softmax statistics live in the lane.  Row rho of
+// score tile t holds key 8*(rho/4) + 4*t + rho%4 of the block; lane group q
+// (= lane/16) then holds keys 8q .. 8q+7 across the two tiles, exactly the k
+// slots of its B operand in O^T += V^T P^T, and V is stored transposed in LDS
+// ([dim][key]) so the A operand is one 16-byte read.
+//
+// With more than one key split each split writes its output normalised by its
+// own sum (bf16) plus its (max, sum); attn_merge combines them.
 #include "device_common.h"
 
 namespace {
@@ -18,29 +26,41 @@ namespace {
 constexpr float kLog2e = 1.4426950408889634f;
 
 template <typename T, int HD>
-__global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
-  constexpr int E = ElemTraits<T>::E;
+struct AttnLds {
+  static constexpr int E = ElemTraits<T>::E;
+  static constexpr int KP = HD + E;       // K row pitch (elements)
+  static constexpr int VP = 32 + E;       // V^T row pitch (elements)
+  static constexpr size_t KBYTES = 32 * KP * sizeof(T);
+  static constexpr size_t VBYTES = HD * VP * sizeof(T);
+  static constexpr size_t BUF = KBYTES + VBYTES;
+};
+
+template <typename T, int HD>
+__global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
+  using L = AttnLds<T, HD>;
+  constexpr int E = L::E;
   constexpr int NQV = HD / (4 * E);   // 16-byte vectors per lane along hd
   constexpr int DT = HD / 16;         // 16-wide dim tiles of O^T
-  __shared__ __align__(16) T vlds[32 * HD];
-  __shared__ int flag_s;
+  extern __shared__ __align__(16) unsigned char smem[];
 
-  const int lane = threadIdx.x, r16 = lane & 15, g4 = lane >> 4;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int nthr = blockDim.x;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int per = a.H / a.G;          // query heads per K/V head (= waves)
   const int QT = (a.n + 15) / 16;
   int u = blockIdx.x;
   const int split = u % a.kv_split;
   u /= a.kv_split;
+  const int g = u % a.G;
+  u /= a.G;
   const int qt = u % QT;
-  u /= QT;
-  const int h = u % a.H;
-  const int b = u / a.H;
-  const int g = (h * a.G) / a.H;
+  const int b = u / QT;
+  const int h = g * per + wave;
 
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
-  const int total = npre + nself;
-  const int kbeg = split * a.key_chunk;
-  const int kend = min(total, kbeg + a.key_chunk);
+  const int nbp = (npre + 31) / 32, nbs = (nself + 31) / 32;
+  const int jbeg = split * a.key_chunk, jend = min(nbp + nbs, jbeg + a.key_chunk);
 
   const T* kc = reinterpret_cast<const T*>(a.kc);
   const T* vc = reinterpret_cast<const T*>(a.vc);
@@ -48,14 +68,83 @@ __global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
     kc = reinterpret_cast<const T*>(a.cp->kv_cache) + a.layer_off;
     vc = kc + (size_t)a.B * a.G * a.P * HD;
   }
-  const T* ksf = reinterpret_cast<const T*>(a.ks);
-  const T* vsf = reinterpret_cast<const T*>(a.vs);
-  auto key_row = [&](const T* cache, const T* selfp, int key) -> const T* {
-    if (key < npre) return cache + (((size_t)b * a.G + g) * a.P + key) * HD;
-    return selfp + (size_t)(b * a.n + key - npre) * a.ldkv + g * HD;
+  kc += ((size_t)b * a.G + g) * a.P * HD;
+  vc += ((size_t)b * a.G + g) * a.P * HD;
+  const T* ksf = reinterpret_cast<const T*>(a.ks) + (size_t)b * a.n * a.ldkv + g * HD;
+  const T* vsf = reinterpret_cast<const T*>(a.vs) + (size_t)b * a.n * a.ldkv + g * HD;
+
+  // Staging of one K/V block: every thread owns items tid, tid + nthr, ...
+  // (16-byte vectors of a K row and of a V row).  The first SU items are
+  // loaded into registers by `fetch` (issued before the math on the previous
+  // block) and written to LDS by `store`; any further items are copied
+  // synchronously by `store`.
+  constexpr int ITEMS = 32 * (HD / E);
+  constexpr int SU = 4;
+  uint4 kreg[SU], vreg[SU];
+  auto src = [&](int j, int kr, const T*& kp, const T*& vp) -> bool {
+    const bool pre = j < nbp;
+    const int key0 = pre ? j * 32 : (j - nbp) * 32;
+    const int cnt = pre ? min(32, npre - key0) : min(32, nself - key0);
+    if (kr >= cnt) return false;
+    const int key = key0 + kr;
+    kp = pre ? kc + (size_t)key * HD : ksf + (size_t)key * a.ldkv;
+    vp = pre ? vc + (size_t)key * HD : vsf + (size_t)key * a.ldkv;
+    return true;
+  };
+  auto block_cnt = [&](int j) {
+    const bool pre = j < nbp;
+    const int key0 = pre ? j * 32 : (j - nbp) * 32;
+    return pre ? min(32, npre - key0) : min(32, nself - key0);
+  };
+  auto fetch = [&](int j) {
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int i = threadIdx.x + u * nthr;
+      const int kr = i / (HD / E), cv = i - kr * (HD / E);
+      const T *kp, *vp;
+      if (i < ITEMS && src(j, kr, kp, vp)) {
+        kreg[u] = ldg16(kp + cv * E);
+        vreg[u] = ldg16(vp + cv * E);
+      } else {
+        kreg[u] = make_uint4(0, 0, 0, 0);
+        vreg[u] = make_uint4(0, 0, 0, 0);
+      }
+    }
+  };
+  auto put = [&](int buf, int i, uint4 kv4, uint4 vv4) {
+    T* kl = reinterpret_cast<T*>(smem + buf * L::BUF);
+    T* vl = reinterpret_cast<T*>(smem + buf * L::BUF + L::KBYTES);
+    const int kr = i / (HD / E), cv = i - kr * (HD / E);
+    *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * E) = kv4;
+    const uint32_t w4[4] = {vv4.x, vv4.y, vv4.z, vv4.w};
+    if constexpr (E == 8) {
+#pragma unroll
+      for (int e = 0; e < 8; ++e)
+        reinterpret_cast<bf16_t*>(vl)[(cv * 8 + e) * L::VP + kr] = (bf16_t)(w4[e >> 1] >> (16 * (e & 1)));
+    } else {
+#pragma unroll
+      for (int e = 0; e < 4; ++e) reinterpret_cast<float*>(vl)[(cv * 4 + e) * L::VP + kr] = __uint_as_float(w4[e]);
+    }
+  };
+  auto store = [&](int j, int buf) {
+#pragma unroll
+    for (int u = 0; u < SU; ++u) {
+      const int i = threadIdx.x + u * nthr;
+      if (i < ITEMS) put(buf, i, kreg[u], vreg[u]);
+    }
+    for (int i = threadIdx.x + SU * nthr; i < ITEMS; i += nthr) {
+      const int kr = i / (HD / E), cv = i - kr * (HD / E);
+      const T *kp, *vp;
+      uint4 kv4 = make_uint4(0, 0, 0, 0), vv4 = make_uint4(0, 0, 0, 0);
+      if (src(j, kr, kp, vp)) {
+        kv4 = ldg16(kp + cv * E);
+        vv4 = ldg16(vp + cv * E);
+      }
+      put(buf, i, kv4, vv4);
+    }
   };
 
-  // Q fragments (B operand of S^T): lane holds query row r16, dims g4*HD/4 + c*E ...
+  // Q fragments (B operand of S^T): query row r16 of head h, dims g4*HD/4 + c*E ..
   const int qrow = qt * 16 + r16;
   const T* qp = reinterpret_cast<const T*>(a.q) + (size_t)(b * a.n + qrow) * a.ldq + h * HD + g4 * (HD / 4);
   uint4 qf[NQV];
@@ -68,39 +157,38 @@ __global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
   float mrun = -INFINITY, lrun = 0.0f;
   const float sc = a.scale * kLog2e;
 
-  for (int kb = kbeg; kb < kend; kb += 32) {
-    // Scores of 32 keys: two 16-key tiles, lane holds keys 16t + 4*g4 + i for query r16.
+  if (jbeg < jend) {
+    fetch(jbeg);
+    store(jbeg, 0);
+  }
+  for (int j = jbeg; j < jend; ++j) {
+    const int buf = (j - jbeg) & 1;
+    const int cnt = block_cnt(j);
+    __syncthreads();                   // block j staged; block j-1 fully read
+    if (j + 1 < jend) fetch(j + 1);    // global loads in flight during the math below
+    const T* kl = reinterpret_cast<const T*>(smem + buf * L::BUF);
+    const T* vl = reinterpret_cast<const T*>(smem + buf * L::BUF + L::KBYTES);
+
+    // scores: tile t, row rho = r16 -> key 8*(rho/4) + 4t + rho%4
     f32x4 s[2];
 #pragma unroll
     for (int t = 0; t < 2; ++t) {
       s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int key = kb + t * 16 + r16;
-      const bool kv_ok = key < kend;
-      const T* kp = kv_ok ? key_row(kc, ksf, key) + g4 * (HD / 4) : nullptr;
+      const int kr = 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+      const T* krow = kl + kr * L::KP + g4 * (HD / 4);
 #pragma unroll
-      for (int c = 0; c < NQV; ++c) {
-        const uint4 kf = kv_ok ? ldg16(kp + c * E) : make_uint4(0, 0, 0, 0);
-        mma16(s[t], kf, qf[c], T());
-      }
+      for (int c = 0; c < NQV; ++c) mma16(s[t], *reinterpret_cast<const uint4*>(krow + c * E), qf[c], T());
     }
-    // Stage V rows kb .. kb+31 in LDS (zeros past the end).
-    __syncthreads();
-    for (int i = lane; i < 32 * (HD / E); i += 64) {
-      const int kr = i / (HD / E), cv = i - kr * (HD / E);
-      const int key = kb + kr;
-      uint4 val = make_uint4(0, 0, 0, 0);
-      if (key < kend) val = ldg16(key_row(vc, vsf, key) + cv * E);
-      *reinterpret_cast<uint4*>(vlds + kr * HD + cv * E) = val;
-    }
-    // Online softmax update for query r16.
+    // lane holds keys 8*g4 + 4t + i for query r16
     float bmax = -INFINITY;
+    float p[8];
 #pragma unroll
     for (int t = 0; t < 2; ++t)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int key = kb + t * 16 + g4 * 4 + i;
-        const float v = (key < kend) ? s[t][i] * sc : -INFINITY;
-        s[t][i] = v;
+        const int kr = 8 * g4 + 4 * t + i;
+        const float v = (kr < cnt) ? s[t][i] * sc : -INFINITY;
+        p[4 * t + i] = v;
         bmax = fmaxf(bmax, v);
       }
     bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
@@ -108,24 +196,18 @@ __global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
     const float mnew = fmaxf(mrun, bmax);
     const float corr = exp2f(mrun - mnew);
     float psum = 0.0f;
-    float p[8];
 #pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const float pv = exp2f(s[t][i] - mnew);
-        p[t * 4 + i] = pv;
-        psum += pv;
-      }
+    for (int k = 0; k < 8; ++k) {
+      p[k] = exp2f(p[k] - mnew);
+      psum += p[k];
+    }
     psum += __shfl_xor(psum, 16, 64);
     psum += __shfl_xor(psum, 32, 64);
     lrun = lrun * corr + psum;
     mrun = mnew;
 #pragma unroll
     for (int d = 0; d < DT; ++d) o[d] *= corr;
-    __syncthreads();
-    // O^T += V^T P^T over these 32 keys.  k-slot j of lane group g4 is key
-    // 4*g4 + j (j < 4) or 16 + 4*g4 + (j - 4).
+    // O^T += V^T P^T: k slot k of lane group g4 is key 8*g4 + k.
     if constexpr (E == 8) {
       uint4 pb;
       pb.x = pack_bf16x2(p[0], p[1]);
@@ -134,92 +216,152 @@ __global__ __launch_bounds__(64) void attn_kernel(AttnArgs a) {
       pb.w = pack_bf16x2(p[6], p[7]);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const int dim = d * 16 + r16;
-        const bf16_t* vb = reinterpret_cast<const bf16_t*>(vlds) + dim;
-        uint32_t w[4];
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          const int k0 = (j < 2) ? (4 * g4 + 2 * j) : (16 + 4 * g4 + 2 * (j - 2));
-          w[j] = (uint32_t)vb[k0 * HD] | ((uint32_t)vb[(k0 + 1) * HD] << 16);
-        }
-        mma16(o[d], make_uint4(w[0], w[1], w[2], w[3]), pb, T());
+        const uint4 va = *reinterpret_cast<const uint4*>(vl + (d * 16 + r16) * L::VP + 8 * g4);
+        mma16(o[d], va, pb, T());
       }
     } else {
-      const float* vf = reinterpret_cast<const float*>(vlds);
 #pragma unroll
       for (int d = 0; d < DT; ++d) {
-        const int dim = d * 16 + r16;
+        const float* vrow = reinterpret_cast<const float*>(vl) + (d * 16 + r16) * L::VP + 8 * g4;
 #pragma unroll
-        for (int t = 0; t < 2; ++t)
-#pragma unroll
-          for (int i = 0; i < 4; ++i)
-            o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vf[(t * 16 + 4 * g4 + i) * HD + dim], p[t * 4 + i],
-                                                        o[d], 0, 0, 0);
+        for (int k = 0; k < 8; ++k) o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vrow[k], p[k], o[d], 0, 0, 0);
       }
     }
+    if (j + 1 < jend) store(j + 1, buf ^ 1);
   }
 
   // Lane holds O^T[dim = 16d + 4*g4 + i][query r16].
-  auto store = [&](const f32x4* ov, float inv) {
-    if (qrow >= a.n) return;
+  if (qrow >= a.n) return;
+  const float inv = lrun > 0.0f ? 1.0f / lrun : 0.0f;
+  if (a.kv_split == 1) {
     T* op = reinterpret_cast<T*>(a.o) + (size_t)(b * a.n + qrow) * a.ldo + h * HD;
 #pragma unroll
     for (int d = 0; d < DT; ++d)
 #pragma unroll
-      for (int i = 0; i < 4; ++i) op[d * 16 + 4 * g4 + i] = ElemTraits<T>::from_f(ov[d][i] * inv);
-  };
-
-  if (a.kv_split == 1) {
-    store(o, 1.0f / lrun);
+      for (int i = 0; i < 4; ++i) op[d * 16 + 4 * g4 + i] = ElemTraits<T>::from_f(o[d][i] * inv);
     return;
   }
-  const int tile = (b * a.H + h) * QT + qt;
-  constexpr int PER = DT * 64 * 4 + 2 * 64;  // floats per (tile, split)
-  float* wsp = a.ws + (size_t)tile * a.kv_split * PER;
-  {
-    float* mine = wsp + (size_t)split * PER;
-    f32x4* ov = reinterpret_cast<f32x4*>(mine);
+  // partial: normalised by its own sum, plus (max, sum)
+  const int rows = a.B * a.n, dq = a.H * HD;
+  T* pp = reinterpret_cast<T*>(a.part) + ((size_t)split * rows + b * a.n + qrow) * dq + h * HD;
 #pragma unroll
-    for (int d = 0; d < DT; ++d) ov[d * 64 + lane] = o[d];
-    mine[DT * 256 + lane] = mrun;
-    mine[DT * 256 + 64 + lane] = lrun;
+  for (int d = 0; d < DT; ++d)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) pp[d * 16 + 4 * g4 + i] = ElemTraits<T>::from_f(o[d][i] * inv);
+  if (g4 == 0) {
+    float* st = a.stats + (((size_t)split * rows + b * a.n + qrow) * a.H + h) * 2;
+    st[0] = mrun;
+    st[1] = lrun;
   }
-  if (!splitk_arrive_last(&a.cnt[tile], (unsigned)a.kv_split, &flag_s)) return;
-  float mmax = -INFINITY;
-  for (int sp = 0; sp < a.kv_split; ++sp) mmax = fmaxf(mmax, wsp[(size_t)sp * PER + DT * 256 + lane]);
-  float lsum = 0.0f;
-  f32x4 acc[DT];
-#pragma unroll
-  for (int d = 0; d < DT; ++d) acc[d] = f32x4{0.f, 0.f, 0.f, 0.f};
-  for (int sp = 0; sp < a.kv_split; ++sp) {
-    const float* part = wsp + (size_t)sp * PER;
-    const float f = exp2f(part[DT * 256 + lane] - mmax);
-    lsum += f * part[DT * 256 + 64 + lane];
-    const f32x4* ov = reinterpret_cast<const f32x4*>(part);
-#pragma unroll
-    for (int d = 0; d < DT; ++d) acc[d] += f * ov[d * 64 + lane];
+}
+
+// O[m][h] = sum_s w_s O_s / sum_s w_s with w_s = l_s * 2^(m_s - max_s m_s).
+// One thread per 16-byte vector of the output row; the splits' vectors are
+// loaded four at a time.
+template <typename T>
+__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+  constexpr int E = ElemTraits<T>::E;
+  const int m = blockIdx.x;
+  const int rows = a.B * a.n, dq = a.H * a.hd;
+  __shared__ float wgt[64 * 32];   // kv_split <= 64, H <= 32
+  for (int h = threadIdx.x; h < a.H; h += blockDim.x) {
+    float mx = -INFINITY;
+    for (int s = 0; s < a.kv_split; ++s) mx = fmaxf(mx, a.stats[(((size_t)s * rows + m) * a.H + h) * 2]);
+    float tot = 0.0f;
+    for (int s = 0; s < a.kv_split; ++s) {
+      const float* st = a.stats + (((size_t)s * rows + m) * a.H + h) * 2;
+      const float w = st[1] * exp2f(st[0] - mx);
+      wgt[s * a.H + h] = w;
+      tot += w;
+    }
+    for (int s = 0; s < a.kv_split; ++s) wgt[s * a.H + h] /= tot;
   }
-  store(acc, 1.0f / lsum);
+  __syncthreads();
+  const T* part = reinterpret_cast<const T*>(a.part);
+  T* op = reinterpret_cast<T*>(a.o) + (size_t)m * a.ldo;
+  for (int c = threadIdx.x * E; c < dq; c += blockDim.x * E) {
+    const int h = c / a.hd;
+    float acc[E];
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+    int s = 0;
+    for (; s + 4 <= a.kv_split; s += 4) {
+      uint4 v[4];
+#pragma unroll
+      for (int u = 0; u < 4; ++u) v[u] = ldg16(part + ((size_t)(s + u) * rows + m) * dq + c);
+#pragma unroll
+      for (int u = 0; u < 4; ++u) {
+        float f[E];
+        unpack16(v[u], f, T());
+        const float w = wgt[(s + u) * a.H + h];
+#pragma unroll
+        for (int e = 0; e < E; ++e) acc[e] += w * f[e];
+      }
+    }
+    for (; s < a.kv_split; ++s) {
+      float f[E];
+      unpack16(ldg16(part + ((size_t)s * rows + m) * dq + c), f, T());
+      const float w = wgt[s * a.H + h];
+#pragma unroll
+      for (int e = 0; e < E; ++e) acc[e] += w * f[e];
+    }
+    stg16(op + c, pack16(acc, T()));
+  }
 }
 
 template <typename T, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   const int QT = (a.n + 15) / 16;
-  const int units = a.B * a.H * QT * a.kv_split;
+  const int units = a.B * QT * a.G * a.kv_split;
   if (units <= 0) return hipSuccess;
-  hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(units), dim3(64), 0, s, a);
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, HD>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int threads = 64 * (a.H / a.G);
+  using L = AttnLds<T, HD>;
+  const size_t lds = 2 * L::BUF;
+  hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(units), dim3(threads), lds, s, a);
+  hipError_t e = hipGetLastError();
+  if (e != hipSuccess || a.kv_split == 1) return e;
+  hipLaunchKernelGGL(attn_merge_kernel<T>, dim3(a.B * a.n), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-size_t attention_ws_floats(const AttnArgs& a) {
+// Keys per split in 32-key blocks, the number of splits, and the workspace.
+void attention_split(AttnArgs& a, int want_splits) {
+  const int npre = (a.mode == 0) ? 0 : a.P;
+  const int nself = (a.mode == 1) ? 0 : a.n;
+  const int nblocks = (npre + 31) / 32 + (nself + 31) / 32;
   const int QT = (a.n + 15) / 16;
-  const size_t per = (size_t)(a.hd / 16) * 64 * 4 + 2 * 64;
-  return a.kv_split > 1 ? (size_t)a.B * a.H * QT * a.kv_split * per : 0;
+  int s = want_splits;
+  if (s <= 0) {
+    const int base = a.B * QT * a.G;
+    s = (96 + base - 1) / base;   // about 96 workgroups
+  }
+  s = s < 1 ? 1 : (s > nblocks ? nblocks : s);
+  s = s > 64 ? 64 : s;
+  a.key_chunk = (nblocks + s - 1) / s;
+  a.kv_split = (nblocks + a.key_chunk - 1) / a.key_chunk;
+}
+
+size_t attention_part_bytes(int et, const AttnArgs& a) {
+  if (a.kv_split <= 1) return 0;
+  return (size_t)a.kv_split * a.B * a.n * a.H * a.hd * (et == ET_BF16 ? 2 : 4);
+}
+
+size_t attention_stats_bytes(const AttnArgs& a) {
+  if (a.kv_split <= 1) return 0;
+  return (size_t)a.kv_split * a.B * a.n * a.H * 2 * sizeof(float);
 }
 
 hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s) {
+  if (a.H % a.G != 0 || a.H / a.G > 8 || a.H > 32 || a.kv_split > 64) return hipErrorInvalidValue;
   if (et == ET_BF16) {
     switch (a.hd) {
       case 64: return launch_hd<bf16_t, 64>(a, s);

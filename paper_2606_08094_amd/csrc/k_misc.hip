@@ -26,30 +26,115 @@ __global__ __launch_bounds__(256) void init_chunk_kernel(const CallParams* cp, f
   for (int i = threadIdx.x; i < n * A; i += 256) a[(size_t)b * n * A + i] = nz[i];
 }
 
-// x[m] = a[m] W_in^T + xs[b] + E_pos[token]; rowss[p][m] = sum of x^2 over
-// columns 64p .. 64p+63 (the same partition as the residual GEMM epilogue).
+// One workgroup per token row: finish the residual stream x (add the split-K
+// partials of a residual projection, or form the input embedding) and write
+// the next sublayer's adaRMS input u.  A thread owns the columns
+// 4*(tid + 256*i); all of its loads are issued before the row reduction.
 template <typename T>
-__global__ __launch_bounds__(256) void embed_kernel(const float* a, const T* W_in, const float* xs,
-                                                     const T* E_pos, float* x, float* rowss, int M, int n,
-                                                     int A, int d) {
+__global__ __launch_bounds__(256) void row_norm_kernel(RowNormArgs a) {
+  constexpr int CPT = 4;  // float4 groups per thread: d <= 4 * 256 * CPT
   const int m = blockIdx.x;
-  const int b = m / n, tok = m - b * n;
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  __shared__ float arow[64];
-  for (int i = threadIdx.x; i < A; i += 256) arow[i] = a[(size_t)m * A + i];
-  __syncthreads();
-  const int npart = (d + 63) / 64;
-  for (int j0 = 0; j0 < d; j0 += 256) {
-    const int j = j0 + threadIdx.x;
-    float v = 0.0f;
-    if (j < d) {
-      v = xs[(size_t)b * d + j] + ElemTraits<T>::to_f(E_pos[(size_t)tok * d + j]);
-      for (int k = 0; k < A; ++k) v += arow[k] * ElemTraits<T>::to_f(W_in[(size_t)j * A + k]);
-      x[(size_t)m * d + j] = v;
+  const int d = a.d;
+  const int t = threadIdx.x;
+  __shared__ float red[4];
+  float4 xv[CPT];
+  float ss = 0.0f;
+  if (a.mode == 0) {
+    const float* xr = a.x + (size_t)m * d;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = 4 * (t + 256 * i);
+      xv[i] = c < d ? *reinterpret_cast<const float4*>(xr + c) : make_float4(0.f, 0.f, 0.f, 0.f);
     }
-    const float ss = wave_sum(v * v);
-    const int p = j0 / 64 + wave;
-    if (lane == 0 && p < npart) rowss[(size_t)p * M + m] = ss;
+    if (a.alpha != nullptr) {
+      float4 ps[CPT], al[CPT];
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        const int c = 4 * (t + 256 * i);
+        ps[i] = make_float4(0.f, 0.f, 0.f, 0.f);
+        al[i] = c < d ? *reinterpret_cast<const float4*>(a.alpha + c) : make_float4(0.f, 0.f, 0.f, 0.f);
+      }
+      for (int s0 = 0; s0 < a.nsplit; s0 += 4) {
+        float4 pv[4][CPT];
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int i = 0; i < CPT; ++i) {
+            const int c = 4 * (t + 256 * i);
+            pv[u][i] = (s0 + u < a.nsplit && c < d)
+                           ? *reinterpret_cast<const float4*>(a.part + ((size_t)(s0 + u) * a.M + m) * d + c)
+                           : make_float4(0.f, 0.f, 0.f, 0.f);
+          }
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+#pragma unroll
+          for (int i = 0; i < CPT; ++i) {
+            ps[i].x += pv[u][i].x; ps[i].y += pv[u][i].y; ps[i].z += pv[u][i].z; ps[i].w += pv[u][i].w;
+          }
+      }
+#pragma unroll
+      for (int i = 0; i < CPT; ++i) {
+        xv[i].x += al[i].x * ps[i].x; xv[i].y += al[i].y * ps[i].y;
+        xv[i].z += al[i].z * ps[i].z; xv[i].w += al[i].w * ps[i].w;
+      }
+    }
+  } else {
+    const int b = m / a.n, tok = m - b * a.n;
+    __shared__ float arow[64];
+    if (t < a.A) arow[t] = a.a[(size_t)m * a.A + t];
+    __syncthreads();
+    const T* W = reinterpret_cast<const T*>(a.W_in);
+    const T* ep = reinterpret_cast<const T*>(a.E_pos) + (size_t)tok * d;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = 4 * (t + 256 * i);
+      float v[4] = {0.f, 0.f, 0.f, 0.f};
+      if (c < d) {
+        const float4 x4 = *reinterpret_cast<const float4*>(a.xs + (size_t)b * d + c);
+        v[0] = x4.x + ElemTraits<T>::to_f(ep[c]);
+        v[1] = x4.y + ElemTraits<T>::to_f(ep[c + 1]);
+        v[2] = x4.z + ElemTraits<T>::to_f(ep[c + 2]);
+        v[3] = x4.w + ElemTraits<T>::to_f(ep[c + 3]);
+        for (int k = 0; k < a.A; ++k) {
+          const float ak = arow[k];
+#pragma unroll
+          for (int e = 0; e < 4; ++e) v[e] += ak * ElemTraits<T>::to_f(W[(size_t)(c + e) * a.A + k]);
+        }
+      }
+      xv[i] = make_float4(v[0], v[1], v[2], v[3]);
+    }
+  }
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = 4 * (t + 256 * i);
+    if (c < d) {
+      *reinterpret_cast<float4*>(a.x + (size_t)m * d + c) = xv[i];
+      ss += xv[i].x * xv[i].x + xv[i].y * xv[i].y + xv[i].z * xv[i].z + xv[i].w * xv[i].w;
+    }
+  }
+  ss = wave_sum(ss);
+  if ((t & 63) == 0) red[t >> 6] = ss;
+  __syncthreads();
+  const float rstd = 1.0f / sqrtf((red[0] + red[1] + red[2] + red[3]) / (float)d + a.eps);
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = 4 * (t + 256 * i);
+    if (c >= d) continue;
+    const float4 g = *reinterpret_cast<const float4*>(a.gamma + c);
+    const float4 bb = *reinterpret_cast<const float4*>(a.beta + c);
+    const float u0 = xv[i].x * rstd * (1.0f + g.x) + bb.x;
+    const float u1 = xv[i].y * rstd * (1.0f + g.y) + bb.y;
+    const float u2 = xv[i].z * rstd * (1.0f + g.z) + bb.z;
+    const float u3 = xv[i].w * rstd * (1.0f + g.w) + bb.w;
+    if (a.u_f32) {
+      *reinterpret_cast<float4*>(reinterpret_cast<float*>(a.u) + (size_t)m * d + c) = make_float4(u0, u1, u2, u3);
+    } else {
+      T* up = reinterpret_cast<T*>(a.u) + (size_t)m * d + c;
+      up[0] = ElemTraits<T>::from_f(u0);
+      up[1] = ElemTraits<T>::from_f(u1);
+      up[2] = ElemTraits<T>::from_f(u2);
+      up[3] = ElemTraits<T>::from_f(u3);
+    }
   }
 }
 
@@ -88,17 +173,8 @@ __global__ void fill_u32_kernel(unsigned* p, unsigned v, size_t n) {
 __global__ __launch_bounds__(256) void quantize_kernel(QuantArgs a) {
   extern __shared__ float us[];
   __shared__ float red[4];
-  __shared__ float rstd_s;
   const int m = blockIdx.x;
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-  if (a.adarms) {
-    if (threadIdx.x == 0) {
-      float ss = 0.0f;
-      for (int p = 0; p < a.rowss_np; ++p) ss += a.rowss[(size_t)p * a.M + m];
-      rstd_s = 1.0f / sqrtf(ss / (float)a.K + a.eps);
-    }
-    __syncthreads();
-  }
   float amax = 0.0f;
   for (int k = threadIdx.x; k < a.K; k += 256) {
     float v;
@@ -106,7 +182,6 @@ __global__ __launch_bounds__(256) void quantize_kernel(QuantArgs a) {
       v = bf2f(reinterpret_cast<const bf16_t*>(a.x)[(size_t)m * a.ldx + k]);
     else
       v = reinterpret_cast<const float*>(a.x)[(size_t)m * a.ldx + k];
-    if (a.adarms) v = v * rstd_s * (1.0f + a.gamma[k]) + a.beta[k];
     us[k] = v;
     amax = fmaxf(amax, fabsf(v));
   }
@@ -146,15 +221,13 @@ hipError_t launch_init_chunk(int et, const CallParams* cp, float* a, float* xs, 
   return hipGetLastError();
 }
 
-hipError_t launch_embed(int et, const float* a, const void* W_in, const float* xs, const void* E_pos,
-                        float* x, float* rowss, int B, int n, int A, int d, hipStream_t s) {
-  const int M = B * n;
+hipError_t launch_row_norm(int et, const RowNormArgs& a, hipStream_t s) {
+  if (a.M <= 0) return hipSuccess;
+  if (a.d > 4 * 256 * 4 || a.d % 4 || (a.mode == 1 && a.A > 64)) return hipErrorInvalidValue;
   if (et == ET_BF16)
-    hipLaunchKernelGGL(embed_kernel<bf16_t>, dim3(M), dim3(256), 0, s, a, reinterpret_cast<const bf16_t*>(W_in),
-                       xs, reinterpret_cast<const bf16_t*>(E_pos), x, rowss, M, n, A, d);
+    hipLaunchKernelGGL(row_norm_kernel<bf16_t>, dim3(a.M), dim3(256), 0, s, a);
   else
-    hipLaunchKernelGGL(embed_kernel<float>, dim3(M), dim3(256), 0, s, a, reinterpret_cast<const float*>(W_in),
-                       xs, reinterpret_cast<const float*>(E_pos), x, rowss, M, n, A, d);
+    hipLaunchKernelGGL(row_norm_kernel<float>, dim3(a.M), dim3(256), 0, s, a);
   return hipGetLastError();
 }
 

@@ -6,8 +6,9 @@
 // {0,1,2} as int8 (byte-permute + masks, no lookup table).  The MFMA then forms
 // sum_k q*c, and sum_k q*w = sum_k q*c - sum_k q is recovered with the row sums
 // of the activation codes, which the workgroup accumulates while staging X in
-// LDS.  All arithmetic is int32 and exact, so split-K partials can be summed
-// in any order.
+// LDS.  All arithmetic is int32 and exact.  A workgroup walks the whole K
+// range (its K-slices one after another); only the raw int32 entry splits K
+// across workgroups, adding the exact partial sums atomically.
 #include "gemm_epilogue.h"
 
 namespace {
@@ -47,8 +48,6 @@ __global__ __launch_bounds__(256) void tern_kernel(TernArgs a) {
   extern __shared__ __align__(16) unsigned char smem[];
   int8_t* xs = reinterpret_cast<int8_t*>(smem);
   int* rsum_s = reinterpret_cast<int*>(smem + (size_t)MT * PITCH);
-  float* red_s = reinterpret_cast<float*>(rsum_s + MT);  // [4][MT]
-  int* flag_s = reinterpret_cast<int*>(red_s + 4 * MT);
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
@@ -65,57 +64,62 @@ __global__ __launch_bounds__(256) void tern_kernel(TernArgs a) {
   const int kend = min(K, k0 + KS);
   const int nw0 = ntile * NT + wave * 16 * NSUB;
 
-  uint4 wreg[NSUB][NC];
-#pragma unroll
-  for (int s = 0; s < NSUB; ++s) {
-    const int n = nw0 + s * 16 + r16;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const int k = k0 + c * KC + g4 * 64;
-      wreg[s][c] = (n < N && k < kend) ? ldg16(a.w + (size_t)n * KB + k / 4) : make_uint4(0, 0, 0, 0);
-    }
-  }
-
-  if (tid < MT) rsum_s[tid] = 0;
-  __syncthreads();
-  constexpr int VROW = KS / 16;
-  for (int i = tid; i < MT * VROW; i += 256) {
-    const int row = i / VROW, kv = i - row * VROW;
-    const int m = m0 + row, k = k0 + kv * 16;
-    uint4 v = make_uint4(0, 0, 0, 0);
-    if (m < M && k < kend) {
-      v = ldg16(a.x + (size_t)m * K + k);
-      atomicAdd(&rsum_s[row], sum_i8x16(v));
-    }
-    *reinterpret_cast<uint4*>(xs + (size_t)row * PITCH + kv * 16) = v;
-  }
-  __syncthreads();
-
   i32x4 acc[MS][NSUB];
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) acc[ms][s] = i32x4{0, 0, 0, 0};
+  if (tid < MT) rsum_s[tid] = 0;
+
+  // K-slices of this split, one after another inside the workgroup
+  const int kstop = (a.nsplit > 1) ? kend : K;
+  for (int ks0 = k0; ks0 < kstop; ks0 += KS) {
+    const int send = min(kstop, ks0 + KS);
+    uint4 wreg[NSUB][NC];
 #pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    if (k0 + c * KC >= kend) break;
+    for (int s = 0; s < NSUB; ++s) {
+      const int n = nw0 + s * 16 + r16;
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms) {
-      const int8_t* xrow = xs + (size_t)(ms * 16 + r16) * PITCH + c * KC + g4 * 64;
-      uint4 xf[4];
+      for (int c = 0; c < NC; ++c) {
+        const int k = ks0 + c * KC + g4 * 64;
+        wreg[s][c] = (n < N && k < send) ? ldg16(a.w + (size_t)n * KB + k / 4) : make_uint4(0, 0, 0, 0);
+      }
+    }
+    __syncthreads();  // rsum_s zeroed / previous slice's LDS reads done
+    constexpr int VROW = KS / 16;
+    for (int i = tid; i < MT * VROW; i += 256) {
+      const int row = i / VROW, kv = i - row * VROW;
+      const int m = m0 + row, k = ks0 + kv * 16;
+      uint4 v = make_uint4(0, 0, 0, 0);
+      if (m < M && k < send) {
+        v = ldg16(a.x + (size_t)m * K + k);
+        atomicAdd(&rsum_s[row], sum_i8x16(v));
+      }
+      *reinterpret_cast<uint4*>(xs + (size_t)row * PITCH + kv * 16) = v;
+    }
+    __syncthreads();
 #pragma unroll
-      for (int r = 0; r < 4; ++r) xf[r] = *reinterpret_cast<const uint4*>(xrow + 16 * r);
+    for (int c = 0; c < NC; ++c) {
+      if (ks0 + c * KC >= send) break;
 #pragma unroll
-      for (int s = 0; s < NSUB; ++s) {
-        const uint32_t pw[4] = {wreg[s][c].x, wreg[s][c].y, wreg[s][c].z, wreg[s][c].w};
+      for (int ms = 0; ms < MS; ++ms) {
+        const int8_t* xrow = xs + (size_t)(ms * 16 + r16) * PITCH + c * KC + g4 * 64;
+        uint4 xf[4];
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          acc[ms][s] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[r]),
-                                                             unpack_codes(pw[r]), acc[ms][s], 0, 0, 0);
+        for (int r = 0; r < 4; ++r) xf[r] = *reinterpret_cast<const uint4*>(xrow + 16 * r);
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s) {
+          const uint32_t pw[4] = {wreg[s][c].x, wreg[s][c].y, wreg[s][c].z, wreg[s][c].w};
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            acc[ms][s] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[r]),
+                                                               unpack_codes(pw[r]), acc[ms][s], 0, 0, 0);
+        }
       }
     }
   }
-  // sum q*w = sum q*c - sum q over this slice.
+  __syncthreads();
+  // sum q*w = sum q*c - sum q over the K range of this workgroup.
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
@@ -141,26 +145,6 @@ __global__ __launch_bounds__(256) void tern_kernel(TernArgs a) {
       }
     return;
   }
-  if (a.nsplit > 1) {
-    const int tile = mtile * a.n_tiles + ntile;
-    constexpr int PER = 4 * MS * NSUB * 64;
-    i32x4* wsp = reinterpret_cast<i32x4*>(a.ws) + ((size_t)tile * a.nsplit) * PER;
-#pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s)
-        wsp[(size_t)split * PER + ((wave * MS + ms) * NSUB + s) * 64 + lane] = acc[ms][s];
-    if (!splitk_arrive_last(&a.cnt[tile], (unsigned)a.nsplit, flag_s)) return;
-#pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) {
-        i32x4 t = i32x4{0, 0, 0, 0};
-        for (int sp = 0; sp < a.nsplit; ++sp) t += wsp[(size_t)sp * PER + ((wave * MS + ms) * NSUB + s) * 64 + lane];
-        acc[ms][s] = t;
-      }
-  }
-
   if (a.rscale == nullptr) {
 #pragma unroll
     for (int ms = 0; ms < MS; ++ms)
@@ -193,7 +177,7 @@ __global__ __launch_bounds__(256) void tern_kernel(TernArgs a) {
 #pragma unroll
       for (int s = 0; s < NSUB; ++s) y[ms][s][i] = (float)acc[ms][s][i] * (sw[s] * rm / 127.0f);
     }
-  gemm_epilogue<bf16_t, MS, NSUB>(a.e, y, m0, ntile, nw0, red_s);
+  wave_epilogue<bf16_t, MS, NSUB>(a.e, y, m0, nw0, 0);
 }
 
 // Any K % 4 == 0: one thread per output, byte-wise unpacking.
@@ -216,7 +200,7 @@ __global__ __launch_bounds__(256) void tern_generic_kernel(const int8_t* x, cons
 template <int MS, int NSUB, int NC>
 hipError_t tern_launch(const TernArgs& a, int units, hipStream_t s) {
   constexpr int MT = 16 * MS;
-  const size_t lds = (size_t)MT * (NC * 256 + 16) + (size_t)MT * 4 + 4 * MT * 4 + 16;
+  const size_t lds = (size_t)MT * (NC * 256 + 16) + (size_t)MT * 4;
   hipLaunchKernelGGL((tern_kernel<MS, NSUB, NC>), dim3(units), dim3(256), lds, s, a);
   return hipGetLastError();
 }

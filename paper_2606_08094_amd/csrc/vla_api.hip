@@ -89,6 +89,8 @@ vla_status validate_config(const vla_config* c) {
       return fail(VLA_E_SHAPE, "ternary weights need every K (d, d_p, H*hd, F) to be a multiple of 64");
   }
   if (c->d_action > 64) return fail(VLA_E_UNSUPPORTED, "d_action > 64");
+  if (c->n_heads / c->n_kv_heads > 8 || c->n_heads > 32)
+    return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head or more than 32 heads");
   if (c->head_regression != 0 && c->head_regression != 1) return fail(VLA_E_ARG, "head_regression must be 0/1");
   if (!(c->rms_eps > 0.0f) || !std::isfinite(c->rms_eps)) return fail(VLA_E_ARG, "rms_eps must be finite and > 0");
   if (c->n_action > 4096 || c->d_model > 16384 || c->d_ff > 65536)
@@ -133,6 +135,8 @@ struct vla_model {
   std::map<std::tuple<int, int, int>, std::unique_ptr<Plan>> plans;
   std::map<std::pair<int, int>, std::unique_ptr<PrefixWs>> prefix_ws;
   int loop_mode = 1;
+  int profile = 0;
+  void* last_profiled = nullptr;  // Plan* of the last profiled call
   hipStream_t cap_stream = nullptr;
   ~vla_model();
 };
@@ -175,22 +179,40 @@ struct TableReader {
 
 namespace {
 
-using Op = std::function<hipError_t(hipStream_t)>;
+struct Op {
+  std::function<hipError_t(hipStream_t)> fn;
+  vla_op_time info;
+  hipError_t operator()(hipStream_t s) const { return fn(s); }
+};
+
+vla_op_time op_info(int kind, int M, int N, int K, double bytes, double flops) {
+  vla_op_time t{};
+  t.kind = kind;
+  t.M = M;
+  t.N = N;
+  t.K = K;
+  t.bytes = bytes;
+  t.flops = flops;
+  return t;
+}
 
 struct Plan {
   int B = 0, P = 0, T = 0;
   std::vector<void*> allocs;
   CallParams* cp = nullptr;
-  float *a = nullptr, *xs = nullptr, *x = nullptr, *rowss = nullptr, *mods = nullptr, *modf = nullptr;
+  float *a = nullptr, *xs = nullptr, *x = nullptr, *mods = nullptr, *modf = nullptr;
+  void* u = nullptr;          // adaRMS output, input of the next projection
+  float* part = nullptr;      // split-K partials of the residual projections
   void *e = nullptr, *h1 = nullptr, *sc = nullptr, *qkv = nullptr, *o = nullptr, *h = nullptr;
   int8_t* q8 = nullptr;
   float* r8 = nullptr;
-  float* ws = nullptr;
-  unsigned* cnt = nullptr;
-  size_t ws_floats = 0, n_cnt = 0;
+  void* apart = nullptr;      // attention key-split partials
+  float* astats = nullptr;
   std::vector<Op> ops;
   hipGraphExec_t exec = nullptr;
+  std::vector<hipEvent_t> events;  // 2 per op when profiled
   ~Plan() {
+    for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (exec) (void)hipGraphExecDestroy(exec);
     for (void* p : allocs) (void)hipFree(p);
   }
@@ -198,9 +220,6 @@ struct Plan {
 
 struct PrefixWs {
   std::vector<void*> allocs;
-  float* ws = nullptr;
-  unsigned* cnt = nullptr;
-  size_t ws_floats = 0, n_cnt = 0;
   int8_t* q8 = nullptr;
   float* r8 = nullptr;
   ~PrefixWs() {
@@ -212,120 +231,117 @@ struct Tiling {
   int ms, nsub, nc, nsplit, n_tiles, m_tiles, units;
 };
 
-Tiling gemm_tiling(int et, int M, int N, int K, int nsub, int force_nsplit = 0) {
-  Tiling t{};
-  t.ms = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  t.nsub = nsub;
-  t.m_tiles = cdiv(M, 16 * t.ms);
-  t.n_tiles = cdiv(N, 64 * nsub);
-  const int KC = gemm_chunk_k(et);
-  const int base = t.m_tiles * t.n_tiles;
-  t.nc = 1;
-  for (int nc : {4, 2, 1}) {
-    const int nsplit = cdiv(K, nc * KC);
-    // Largest K-slice that still yields one workgroup per CU (or the split
-    // count a test asks for).
-    const bool ok = force_nsplit > 0 ? nsplit >= force_nsplit : base * nsplit >= 256;
-    if (ok) {
-      t.nc = nc;
-      break;
-    }
-  }
-  t.nsplit = cdiv(K, t.nc * KC);
-  t.units = base * t.nsplit;
-  return t;
-}
-
+// W2A8 GEMM: 64*nsub W rows per workgroup over the whole K (K-slices of
+// 256*nc looped inside the workgroup).
 Tiling tern_tiling(int M, int N, int K, int nsub) {
   Tiling t{};
   t.ms = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   t.nsub = nsub;
   t.m_tiles = cdiv(M, 16 * t.ms);
   t.n_tiles = cdiv(N, 64 * nsub);
-  const int base = t.m_tiles * t.n_tiles;
-  for (int nc : {8, 4, 2, 1}) {
-    const int nsplit = cdiv(K, nc * 256);
-    if (base * nsplit >= 256 || nc == 1) {
-      t.nc = nc;
-      t.nsplit = nsplit;
-      break;
-    }
-  }
-  t.units = base * t.nsplit;
+  t.nc = K <= 256 ? 1 : K <= 512 ? 2 : K <= 1024 ? 4 : 8;
+  t.nsplit = 1;
+  t.units = t.m_tiles * t.n_tiles;
   return t;
+}
+
+// Dense GEMM launch: the skinny kernel when the shape allows, else the wide one.
+struct DenseLaunch {
+  bool skinny;
+  SkinnyShape sk;
+  WideShape wd;
+  int units() const { return skinny ? sk.units : wd.units; }
+};
+
+// variant: 0 = skinny when it fits (split-K only for EPI_PARTIAL), 1 = wide.
+DenseLaunch dense_launch(int et, const GemmArgs& a, int nsub, int variant = 0) {
+  DenseLaunch d{};
+  d.skinny = variant != 1 && skinny_plan(et, a.M, a.N, a.K, nsub, a.epi == EPI_PARTIAL, &d.sk);
+  if (!d.skinny) wide_plan(et, a.M, a.N, a.K, nsub, &d.wd);
+  return d;
+}
+
+hipError_t launch_dense(int et, const DenseLaunch& d, const GemmArgs& a, hipStream_t s) {
+  return d.skinny ? launch_gemm_skinny(et, d.sk, a, s) : launch_gemm_wide(et, d.wd, a, s);
 }
 
 // Collects the launches of a plan and the workspace they need.
 struct Builder {
   vla_model* m;
   std::vector<Op>* ops;
-  float** ws;
-  unsigned** cnt;
-  size_t ws_need = 0, cnt_need = 0;
+  void** apart;
+  float** astats;
+  size_t part_need = 0, stats_need = 0;
 
-  void gemm(GemmArgs a, int nsub, int force_nsplit = 0) {
+  void gemm(GemmArgs a, int nsub) {
     const int et = m->et;
-    const Tiling t = gemm_tiling(et, a.M, a.N, a.K, nsub, force_nsplit);
-    a.ks = t.nc * gemm_chunk_k(et);
-    a.nsplit = t.nsplit;
-    a.n_tiles = t.n_tiles;
-    if (t.nsplit > 1) {
-      ws_need = std::max(ws_need, (size_t)t.m_tiles * t.n_tiles * t.nsplit * gemm_ws_floats_per_unit(t.ms, nsub));
-      cnt_need = std::max(cnt_need, (size_t)t.m_tiles * t.n_tiles);
-    }
-    float** wsp = ws;
-    unsigned** cntp = cnt;
-    ops->push_back([=](hipStream_t s) {
-      GemmArgs g = a;
-      g.ws = *wsp;
-      g.cnt = *cntp;
-      return launch_gemm(et, t.ms, nsub, t.nc, g, t.units, s);
-    });
+    const DenseLaunch dl = dense_launch(et, a, nsub);
+    const double es = esize(et);
+    const double xb = es;
+    double ob = a.out_f32 ? 4.0 : es;
+    if (a.epi == EPI_PARTIAL) ob = 4.0 * (dl.skinny ? dl.sk.nsplit : 1);
+    if (a.epi == EPI_RESID) ob = 8.0;                           // residual read + write
+    if (a.epi == EPI_GLU) ob = es * 0.5;                        // one output per gate/up pair
+    const double bytes = (double)a.N * a.K * es + (double)a.M * a.K * xb + (double)a.M * a.N * ob;
+    ops->push_back(Op{[=](hipStream_t s) { return launch_dense(et, dl, a, s); },
+                      op_info(nsub == 2 ? VLA_OP_GEMM_GLU : VLA_OP_GEMM, a.M, a.N, a.K, bytes,
+                              2.0 * a.M * a.N * a.K)});
   }
 
   void tern(TernArgs a, int nsub) {
     const Tiling t = tern_tiling(a.M, a.N, a.K, nsub);
     a.ks = t.nc * 256;
-    a.nsplit = t.nsplit;
+    a.nsplit = 1;
     a.n_tiles = t.n_tiles;
-    if (t.nsplit > 1) {
-      ws_need = std::max(ws_need, (size_t)t.m_tiles * t.n_tiles * t.nsplit * gemm_ws_floats_per_unit(t.ms, nsub));
-      cnt_need = std::max(cnt_need, (size_t)t.m_tiles * t.n_tiles);
-    }
-    float** wsp = ws;
-    unsigned** cntp = cnt;
-    ops->push_back([=](hipStream_t s) {
-      TernArgs g = a;
-      g.ws = reinterpret_cast<int*>(*wsp);
-      g.cnt = *cntp;
-      return launch_ternary_gemm(g, t.ms, t.units, s);
-    });
+    double ob = a.e.out_f32 ? 4.0 : 2.0;
+    if (a.e.epi == EPI_RESID) ob = 8.0;
+    if (a.e.epi == EPI_GLU) ob = 2.0;
+    const double bytes = (double)a.N * a.K / 4.0 + (double)a.M * a.K + (double)a.M * a.N * ob;
+    ops->push_back(Op{[=](hipStream_t s) { return launch_ternary_gemm(a, t.ms, t.units, s); },
+                      op_info(VLA_OP_TERNARY, a.M, a.N, a.K, bytes, 2.0 * a.M * a.N * a.K)});
   }
 
   void attn(AttnArgs a) {
     const int QT = cdiv(a.n, 16);
     const int total = (a.mode == 0 ? 0 : a.P) + (a.mode == 1 ? 0 : a.n);
-    const int base = a.B * a.H * QT;
-    int split = std::max(1, std::min(cdiv(256, base), cdiv(total, 32)));
-    a.key_chunk = cdiv(cdiv(total, split), 32) * 32;
-    a.kv_split = cdiv(total, a.key_chunk);
-    if (a.kv_split > 1) {
-      ws_need = std::max(ws_need, attention_ws_floats(a));
-      cnt_need = std::max(cnt_need, (size_t)base);
-    }
+    (void)QT;
+    attention_split(a, 0);
     const int et = m->et;
-    float** wsp = ws;
-    unsigned** cntp = cnt;
-    ops->push_back([=](hipStream_t s) {
-      AttnArgs g = a;
-      g.ws = *wsp;
-      g.cnt = *cntp;
-      return launch_attention(et, g, s);
-    });
+    part_need = std::max(part_need, attention_part_bytes(et, a));
+    stats_need = std::max(stats_need, attention_stats_bytes(a));
+    void** pp = apart;
+    float** sp = astats;
+    const double es = esize(et);
+    const double keys = total;
+    const double bytes = (double)a.B * a.G * (a.mode == 0 ? 0 : a.P) * a.hd * 2 * es +  // cached K/V
+                         (double)a.B * a.n * (2.0 * a.H * a.hd + (a.mode == 1 ? 0 : 2.0 * a.G * a.hd)) * es;
+    ops->push_back(Op{[=](hipStream_t s) {
+                        AttnArgs g = a;
+                        g.part = *pp;
+                        g.stats = *sp;
+                        return launch_attention(et, g, s);
+                      },
+                      op_info(VLA_OP_ATTENTION, a.B * a.n, (int)keys, a.hd, bytes,
+                              4.0 * a.B * a.n * a.H * a.hd * keys)});
+  }
+
+  void row_norm(RowNormArgs r) {
+    const int et = m->et;
+    const double es = esize(et);
+    const double bytes = (double)r.M * r.d * (8.0 + 4.0 * r.nsplit + (r.u_f32 ? 4.0 : es)) +
+                         (r.mode == 1 ? (double)r.d * (r.A + r.n) * es : 0.0);
+    ops->push_back(Op{[=](hipStream_t s) { return launch_row_norm(et, r, s); },
+                      op_info(VLA_OP_SMALL, r.M, r.d, r.nsplit, bytes, 0.0)});
   }
 
   void quant(QuantArgs q) {
-    ops->push_back([=](hipStream_t s) { return launch_quantize(q, s); });
+    const double bytes = (double)q.M * q.K * ((q.src_type == 1 ? 2.0 : 4.0) + 1.0);
+    ops->push_back(Op{[=](hipStream_t s) { return launch_quantize(q, s); },
+                      op_info(VLA_OP_QUANTIZE, q.M, 0, q.K, bytes, 0.0)});
+  }
+
+  void small(std::function<hipError_t(hipStream_t)> f, int M, int N, int K, double bytes) {
+    ops->push_back(Op{std::move(f), op_info(VLA_OP_SMALL, M, N, K, bytes, 0.0)});
   }
 };
 
@@ -337,15 +353,8 @@ GemmArgs gemm_base(const vla_model* m, int M, int N, int K, const void* X, int l
   a.X = X;
   a.ldx = ldx;
   a.W = W;
-  a.eps = m->cfg.rms_eps;
+  (void)m;
   return a;
-}
-
-void set_adarms(GemmArgs& a, const float* rowss, int np, const float* gamma, const float* beta) {
-  a.rowss = rowss;
-  a.rowss_np = np;
-  a.gamma = gamma;
-  a.beta = beta;
 }
 
 int mlp_act(int mlp) {
@@ -364,14 +373,14 @@ vla_status build_plan(vla_model* m, Plan* p) {
   const int M = B * n, L = c.n_layers, ns = m->ns, dq = m->dq, dkv = m->dkv, hd = c.head_dim;
   const int et = m->et;
   const size_t es = esize(et);
-  const int np = cdiv(d, 64);
+  const bool u32 = m->tern || et == ET_F32;   // W2A8 quantiser input and fp32 models keep u in fp32
   const size_t modrow = (size_t)L * 3 * ns * d;
   Alloc al{p->allocs};
   VLA_TRY(al((void**)&p->cp, sizeof(CallParams)));
   VLA_TRY(al((void**)&p->a, (size_t)M * A * 4));
   VLA_TRY(al((void**)&p->xs, (size_t)B * d * 4));
   VLA_TRY(al((void**)&p->x, (size_t)M * d * 4));
-  VLA_TRY(al((void**)&p->rowss, (size_t)np * M * 4));
+  VLA_TRY(al(&p->u, (size_t)M * d * (u32 ? 4 : es)));
   int ldqkv = 0;
   for (auto& lay : m->layers)
     for (auto& sw : lay) ldqkv = std::max(ldqkv, sw.n_qkv);
@@ -390,15 +399,16 @@ vla_status build_plan(vla_model* m, Plan* p) {
     VLA_TRY(al((void**)&p->r8, (size_t)M * 4));
   }
 
-  Builder bld{m, &p->ops, &p->ws, &p->cnt};
-  std::vector<Op>& ops = p->ops;
+  Builder bld{m, &p->ops, &p->apart, &p->astats};
   CallParams* cp = p->cp;
+  size_t part_need = 0;
 
-  ops.push_back([=](hipStream_t s) {
+  bld.small([=](hipStream_t s) {
     return launch_init_chunk(et, cp, p->a, p->xs, m->W_s, m->b_s, m->b_in, B, n, A, S, d, s);
-  });
+  }, B, d, S, (double)d * S * es + (double)B * (S + d) * 4 + (double)M * A * 8);
   if (!c.head_regression) {
-    ops.push_back([=](hipStream_t s) { return launch_time_embed(et, cp, p->e, T, T, d, s); });
+    bld.small([=](hipStream_t s) { return launch_time_embed(et, cp, p->e, T, T, d, s); }, T, d, 0,
+              (double)T * d * es);
     GemmArgs g = gemm_base(m, T, d, d, p->e, d, m->W_t1);
     g.epi = EPI_STORE;
     g.bias = m->b_t1;
@@ -429,43 +439,94 @@ vla_status build_plan(vla_model* m, Plan* p) {
     bld.gemm(g, 1);
   }
 
+  // Residual projection (O or down) of a dense model: split-K partials summed
+  // by the following row kernel (skinny), or the residual update in the
+  // epilogue (wide).  Returns the partial count the row kernel must add.
+  auto resid_gemm = [&](GemmArgs g, const float* alp, RowNormArgs& rn) {
+    DenseLaunch dl;
+    g.epi = EPI_PARTIAL;
+    dl = dense_launch(et, g, 1);
+    if (dl.skinny) {
+      g.out = nullptr;  // set at run time from the plan's partial buffer
+      g.ldo = d;
+      part_need = std::max(part_need, (size_t)dl.sk.nsplit * M * d);
+      GemmArgs gg = g;
+      float** partp = &p->part;
+      const double bytes = (double)g.N * g.K * es + (double)g.M * g.K * es + 4.0 * dl.sk.nsplit * g.M * g.N;
+      bld.ops->push_back(Op{[=](hipStream_t s) {
+                              GemmArgs q = gg;
+                              q.out = *partp;
+                              return launch_dense(et, dl, q, s);
+                            },
+                            op_info(VLA_OP_GEMM, g.M, g.N, g.K, bytes, 2.0 * g.M * g.N * g.K)});
+      rn.nsplit = dl.sk.nsplit;
+      rn.alpha = alp;
+    } else {
+      g.epi = EPI_RESID;
+      g.xres = p->x;
+      g.ldxr = d;
+      g.alpha = alp;
+      bld.gemm(g, 1);
+      rn.nsplit = 0;
+      rn.alpha = nullptr;
+    }
+  };
+
   const size_t layer_block = (size_t)2 * B * c.n_kv_heads * P * hd;  // elements per cache layer
   for (int k = 0; k < T; ++k) {
     const float* modk = c.head_regression ? m->mod_static : p->mods + (size_t)k * modrow;
     const float* modfk = c.head_regression ? m->modf_static : p->modf + (size_t)k * 2 * d;
-    ops.push_back([=](hipStream_t s) {
-      return launch_embed(et, p->a, m->W_in, p->xs, m->E_pos, p->x, p->rowss, B, n, A, d, s);
-    });
+    // (gamma, beta) of the sublayer after (l, j); the final pair after the last one
+    auto next_gb = [&](int l, int j, const float** gam, const float** bet) {
+      int nl = l, nj = j + 1;
+      if (nj >= (int)m->layers[l].size()) {
+        nl = l + 1;
+        nj = 0;
+      }
+      if (nl >= L) {
+        *gam = modfk;
+        *bet = modfk + d;
+      } else {
+        *gam = modk + ((size_t)nl * ns + nj) * 3 * d;
+        *bet = *gam + d;
+      }
+    };
+    RowNormArgs rn{};
+    rn.mode = 1; rn.M = M; rn.d = d; rn.x = p->x; rn.a = p->a; rn.W_in = m->W_in; rn.xs = p->xs;
+    rn.E_pos = m->E_pos; rn.n = n; rn.A = A; rn.eps = c.rms_eps; rn.u = p->u; rn.u_f32 = u32;
+    if (L > 0) {
+      rn.gamma = modk;
+      rn.beta = modk + d;
+    } else {
+      rn.gamma = modfk;
+      rn.beta = modfk + d;
+      rn.u_f32 = et == ET_F32;
+    }
+    bld.row_norm(rn);
     for (int l = 0; l < L; ++l) {
       const std::vector<SubW>& subs = m->layers[l];
       for (int j = 0; j < (int)subs.size(); ++j) {
         const SubW& sw = subs[j];
-        const float* gam = modk + ((size_t)l * ns + j) * 3 * d;
-        const float* bet = gam + d;
-        const float* alp = gam + 2 * d;
+        const float* alp = modk + ((size_t)l * ns + j) * 3 * d + 2 * d;
+        RowNormArgs nr{};
+        nr.mode = 0; nr.M = M; nr.d = d; nr.x = p->x; nr.eps = c.rms_eps; nr.u = p->u; nr.u_f32 = u32;
+        next_gb(l, j, &nr.gamma, &nr.beta);
+        // the head projection is dense: it reads u in the element type
+        if (l == L - 1 && j == (int)subs.size() - 1) nr.u_f32 = et == ET_F32;
         if (sw.kind == K_MLP) {
           const bool glu = c.mlp != VLA_MLP_GELU;
           const int ngu = glu ? 2 * F : F;
           if (!m->tern) {
-            GemmArgs g = gemm_base(m, M, ngu, d, p->x, d, sw.gu);
-            set_adarms(g, p->rowss, np, gam, bet);
+            GemmArgs g = gemm_base(m, M, ngu, d, p->u, d, sw.gu);
             g.epi = glu ? EPI_GLU : EPI_STORE;
             g.act = mlp_act(c.mlp);
             g.out = p->h;
             g.ldo = F;
             bld.gemm(g, glu ? 2 : 1);
-            g = gemm_base(m, M, d, F, p->h, F, sw.dn);
-            g.epi = EPI_RESID;
-            g.xres = p->x;
-            g.ldxr = d;
-            g.alpha = alp;
-            g.rowss_out = p->rowss;
-            bld.gemm(g, 1);
+            resid_gemm(gemm_base(m, M, d, F, p->h, F, sw.dn), alp, nr);
           } else {
             QuantArgs q{};
-            q.M = M; q.K = d; q.x = p->x; q.ldx = d; q.src_type = 0; q.adarms = 1;
-            q.rowss = p->rowss; q.rowss_np = np; q.gamma = gam; q.beta = bet; q.eps = c.rms_eps;
-            q.q = p->q8; q.r = p->r8;
+            q.M = M; q.K = d; q.x = p->u; q.ldx = d; q.src_type = 0; q.q = p->q8; q.r = p->r8;
             bld.quant(q);
             TernArgs t{};
             t.M = M; t.N = ngu; t.K = d; t.x = p->q8; t.w = (const uint8_t*)sw.gu; t.rscale = p->r8; t.wscale = sw.s_gu;
@@ -477,7 +538,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
             t.e.out_f32 = 1;
             bld.tern(t, glu ? 2 : 1);
             q = QuantArgs{};
-            q.M = M; q.K = F; q.x = p->h; q.ldx = F; q.src_type = 0; q.adarms = 0; q.q = p->q8; q.r = p->r8;
+            q.M = M; q.K = F; q.x = p->h; q.ldx = F; q.src_type = 0; q.q = p->q8; q.r = p->r8;
             bld.quant(q);
             t = TernArgs{};
             t.M = M; t.N = d; t.K = F; t.x = p->q8; t.w = (const uint8_t*)sw.dn; t.rscale = p->r8; t.wscale = sw.s_dn;
@@ -486,23 +547,18 @@ vla_status build_plan(vla_model* m, Plan* p) {
             t.e.xres = p->x;
             t.e.ldxr = d;
             t.e.alpha = alp;
-            t.e.rowss_out = p->rowss;
             bld.tern(t, 1);
           }
         } else {
-          // Q (and self K, V) projection
           if (!m->tern) {
-            GemmArgs g = gemm_base(m, M, sw.n_qkv, d, p->x, d, sw.qkv);
-            set_adarms(g, p->rowss, np, gam, bet);
+            GemmArgs g = gemm_base(m, M, sw.n_qkv, d, p->u, d, sw.qkv);
             g.epi = EPI_STORE;
             g.out = p->qkv;
             g.ldo = ldqkv;
             bld.gemm(g, 1);
           } else {
             QuantArgs q{};
-            q.M = M; q.K = d; q.x = p->x; q.ldx = d; q.src_type = 0; q.adarms = 1;
-            q.rowss = p->rowss; q.rowss_np = np; q.gamma = gam; q.beta = bet; q.eps = c.rms_eps;
-            q.q = p->q8; q.r = p->r8;
+            q.M = M; q.K = d; q.x = p->u; q.ldx = d; q.src_type = 0; q.q = p->q8; q.r = p->r8;
             bld.quant(q);
             TernArgs t{};
             t.M = M; t.N = sw.n_qkv; t.K = d; t.x = p->q8; t.w = (const uint8_t*)sw.qkv; t.rscale = p->r8;
@@ -529,16 +585,10 @@ vla_status build_plan(vla_model* m, Plan* p) {
           at.scale = 1.0f / std::sqrt((float)hd);
           bld.attn(at);
           if (!m->tern) {
-            GemmArgs g = gemm_base(m, M, d, dq, p->o, dq, sw.o);
-            g.epi = EPI_RESID;
-            g.xres = p->x;
-            g.ldxr = d;
-            g.alpha = alp;
-            g.rowss_out = p->rowss;
-            bld.gemm(g, 1);
+            resid_gemm(gemm_base(m, M, d, dq, p->o, dq, sw.o), alp, nr);
           } else {
             QuantArgs q{};
-            q.M = M; q.K = dq; q.x = p->o; q.ldx = dq; q.src_type = 1; q.adarms = 0; q.q = p->q8; q.r = p->r8;
+            q.M = M; q.K = dq; q.x = p->o; q.ldx = dq; q.src_type = 1; q.q = p->q8; q.r = p->r8;
             bld.quant(q);
             TernArgs t{};
             t.M = M; t.N = d; t.K = dq; t.x = p->q8; t.w = (const uint8_t*)sw.o; t.rscale = p->r8; t.wscale = sw.s_o;
@@ -547,15 +597,22 @@ vla_status build_plan(vla_model* m, Plan* p) {
             t.e.xres = p->x;
             t.e.ldxr = d;
             t.e.alpha = alp;
-            t.e.rowss_out = p->rowss;
             bld.tern(t, 1);
           }
         }
+        // finish the residual stream and normalise for the next sublayer
+        float** partp = &p->part;
+        const double bytes = (double)M * d * (8.0 + 4.0 * nr.nsplit + (u32 ? 4.0 : es));
+        bld.ops->push_back(Op{[=](hipStream_t s) {
+                                RowNormArgs r = nr;
+                                r.part = *partp;
+                                return launch_row_norm(et, r, s);
+                              },
+                              op_info(VLA_OP_SMALL, M, d, nr.nsplit, bytes, 0.0)});
       }
     }
-    // head: final adaRMS, out-projection and the Euler update
-    GemmArgs g = gemm_base(m, M, A, d, p->x, d, m->W_out);
-    set_adarms(g, p->rowss, np, modfk, modfk + d);
+    // head: out-projection of the finally-normalised stream and the Euler update
+    GemmArgs g = gemm_base(m, M, A, d, p->u, d, m->W_out);
     g.epi = EPI_EULER;
     g.bias = m->b_out;
     g.a = p->a;
@@ -566,19 +623,30 @@ vla_status build_plan(vla_model* m, Plan* p) {
     bld.gemm(g, 1);
   }
 
-  if (bld.ws_need) VLA_TRY(al((void**)&p->ws, bld.ws_need * 4));
-  if (bld.cnt_need) {
-    VLA_TRY(al((void**)&p->cnt, bld.cnt_need * 4));
-    HIP_TRY(hipMemset(p->cnt, 0, bld.cnt_need * 4));
-  }
-  p->ws_floats = bld.ws_need;
-  p->n_cnt = bld.cnt_need;
+  if (part_need) VLA_TRY(al((void**)&p->part, part_need * 4));
+  if (bld.part_need) VLA_TRY(al(&p->apart, bld.part_need));
+  if (bld.stats_need) VLA_TRY(al((void**)&p->astats, bld.stats_need));
   HIP_TRY(hipDeviceSynchronize());
   return VLA_OK;
 }
 
 vla_status run_ops(const std::vector<Op>& ops, hipStream_t s) {
   for (const Op& op : ops) HIP_TRY(op(s));
+  return VLA_OK;
+}
+
+// Launch-per-phase with a HIP event pair around every launch.
+vla_status run_ops_profiled(Plan* p, hipStream_t s) {
+  if (p->events.size() != 2 * p->ops.size()) {
+    for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
+    p->events.assign(2 * p->ops.size(), nullptr);
+    for (auto& e : p->events) HIP_TRY(hipEventCreate(&e));
+  }
+  for (size_t i = 0; i < p->ops.size(); ++i) {
+    HIP_TRY(hipEventRecord(p->events[2 * i], s));
+    HIP_TRY(p->ops[i](s));
+    HIP_TRY(hipEventRecord(p->events[2 * i + 1], s));
+  }
   return VLA_OK;
 }
 
@@ -636,6 +704,11 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
   if (option == VLA_OPT_LOOP_MODE) {
     if (value < 0 || value > 1) return fail(VLA_E_ARG, "loop mode %d out of range", value);
     m->loop_mode = value;
+    return VLA_OK;
+  }
+  if (option == VLA_OPT_PROFILE) {
+    if (value < 0 || value > 1) return fail(VLA_E_ARG, "profile flag %d out of range", value);
+    m->profile = value;
     return VLA_OK;
   }
   return fail(VLA_E_ARG, "unknown option %d", option);
@@ -859,33 +932,13 @@ vla_status get_prefix_ws(vla_model* m, int B, int P, PrefixWs** out) {
     return VLA_OK;
   }
   std::unique_ptr<PrefixWs> w(new PrefixWs());
-  const int M = B * P;
-  size_t ws_need = 0, cnt_need = 0;
-  const int N = 2 * m->dkv, K = m->cfg.d_prefix;
   if (m->tern) {
-    const Tiling t = tern_tiling(M, N, K, 1);
-    if (t.nsplit > 1) {
-      ws_need = (size_t)t.m_tiles * t.n_tiles * t.nsplit * gemm_ws_floats_per_unit(t.ms, 1);
-      cnt_need = (size_t)t.m_tiles * t.n_tiles;
-    }
-  } else {
-    const Tiling t = gemm_tiling(m->et, M, N, K, 1);
-    if (t.nsplit > 1) {
-      ws_need = (size_t)t.m_tiles * t.n_tiles * t.nsplit * gemm_ws_floats_per_unit(t.ms, 1);
-      cnt_need = (size_t)t.m_tiles * t.n_tiles;
-    }
+    Alloc al{w->allocs};
+    const size_t M = (size_t)B * P;
+    VLA_TRY(al((void**)&w->q8, M * m->cfg.d_prefix));
+    VLA_TRY(al((void**)&w->r8, M * 4));
+    HIP_TRY(hipDeviceSynchronize());
   }
-  Alloc al{w->allocs};
-  if (ws_need) VLA_TRY(al((void**)&w->ws, ws_need * 4));
-  if (cnt_need) {
-    VLA_TRY(al((void**)&w->cnt, cnt_need * 4));
-    HIP_TRY(hipMemset(w->cnt, 0, cnt_need * 4));
-  }
-  if (m->tern) {
-    VLA_TRY(al((void**)&w->q8, (size_t)M * K));
-    VLA_TRY(al((void**)&w->r8, (size_t)M * 4));
-  }
-  HIP_TRY(hipDeviceSynchronize());
   *out = w.get();
   m->prefix_ws[key] = std::move(w);
   return VLA_OK;
@@ -940,16 +993,12 @@ vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t 
       g.cache = (char*)kv_cache + (size_t)sw.cache_idx * layer_block * es;
       g.P = prefix_len; g.hd = hd; g.d_kv = m->dkv; g.B = batch;
       if (!m->tern) {
-        const Tiling t = gemm_tiling(m->et, M, N, K, 1);
-        g.ks = t.nc * gemm_chunk_k(m->et); g.nsplit = t.nsplit; g.n_tiles = t.n_tiles;
-        g.ws = w->ws; g.cnt = w->cnt;
-        HIP_TRY(launch_gemm(m->et, t.ms, 1, t.nc, g, t.units, s));
+        HIP_TRY(launch_dense(m->et, dense_launch(m->et, g, 1), g, s));
       } else {
         TernArgs ta{};
         const Tiling t = tern_tiling(M, N, K, 1);
         ta.M = M; ta.N = N; ta.K = K; ta.x = w->q8; ta.w = (const uint8_t*)sw.kvc; ta.rscale = w->r8;
-        ta.wscale = sw.s_kvc; ta.ks = t.nc * 256; ta.nsplit = t.nsplit; ta.n_tiles = t.n_tiles;
-        ta.ws = reinterpret_cast<int*>(w->ws); ta.cnt = w->cnt; ta.e = g;
+        ta.wscale = sw.s_kvc; ta.ks = t.nc * 256; ta.nsplit = 1; ta.n_tiles = t.n_tiles; ta.e = g;
         HIP_TRY(launch_ternary_gemm(ta, t.ms, t.units, s));
       }
     }
@@ -989,7 +1038,10 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
   auto it = m->plans.find(key);
   Plan* p;
   if (it == m->plans.end()) {
-    if (m->plans.size() >= 8) m->plans.erase(m->plans.begin());
+    if (m->plans.size() >= 8) {
+      if (m->last_profiled == m->plans.begin()->second.get()) m->last_profiled = nullptr;
+      m->plans.erase(m->plans.begin());
+    }
     std::unique_ptr<Plan> np(new Plan());
     np->B = batch;
     np->P = prefix_len;
@@ -1002,7 +1054,10 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(launch_set_params(p->cp, cpv, s));
-  if (m->loop_mode == 0) {
+  if (m->profile) {
+    VLA_TRY(run_ops_profiled(p, s));
+    m->last_profiled = p;
+  } else if (m->loop_mode == 0) {
     VLA_TRY(run_ops(p->ops, s));
   } else {
     if (!p->exec) {
@@ -1058,38 +1113,52 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
   a.M = M; a.N = N; a.K = K; a.x = x; a.w = w_packed; a.acc_out = acc_out;
   Tiling t = tern_tiling(M, N, K, 1);
   if (K % 64 != 0) t = Tiling{1, 1, 1, 1, 1, 1, 1};
+  // Few output tiles: split K across workgroups; the int32 partial sums are
+  // exact and are added atomically into the zero-filled output.
+  if (K % 64 == 0 && t.units < 256 && K > 256) {
+    t.nc = 1;
+    t.nsplit = std::min(cdiv(K, 256), cdiv(256, t.units));
+    while ((long long)t.nc * 256 * t.nsplit < K) ++t.nsplit;
+    t.units *= t.nsplit;
+  }
   a.ks = t.nc * 256; a.nsplit = t.nsplit; a.n_tiles = t.n_tiles;
   if (a.nsplit > 1) HIP_TRY(launch_fill_u32(reinterpret_cast<unsigned*>(acc_out), 0u, (size_t)M * N, s));
   HIP_TRY(launch_ternary_gemm(a, t.ms, t.units, s));
   return VLA_OK;
 }
 
+int32_t vla_profile_read(vla_model* m, vla_op_time* out, int32_t max_ops) {
+  if (!m || !m->last_profiled) return -1;
+  Plan* p = static_cast<Plan*>(m->last_profiled);
+  const int32_t n = (int32_t)p->ops.size();
+  for (int32_t i = 0; i < n && i < max_ops && out; ++i) {
+    out[i] = p->ops[i].info;
+    float ms = -1.0f;
+    if (hipEventSynchronize(p->events[2 * i + 1]) == hipSuccess &&
+        hipEventElapsedTime(&ms, p->events[2 * i], p->events[2 * i + 1]) != hipSuccess)
+      ms = -1.0f;
+    out[i].ms = ms;
+  }
+  return n;
+}
+
 // ---- test entries ----------------------------------------------------------
 
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
-                         int32_t force_nsplit, float* y, void* stream) {
+                         int32_t variant, float* y, void* stream) {
   if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
+  if (variant < 0 || variant > 2) return fail(VLA_E_ARG, "variant must be 0, 1 or 2");
   if (!x || !w || !y || !al16(x) || !al16(w) || !al16(y)) return fail(VLA_E_ARG, "bad buffer");
   if (M < 1 || N < 1 || K < 1 || K % (elem ? 8 : 4)) return fail(VLA_E_SHAPE, "bad GEMM shape");
   const int et = elem ? ET_BF16 : ET_F32;
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  const Tiling t = gemm_tiling(et, M, N, K, 1, force_nsplit);
   GemmArgs g{};
   g.M = M; g.N = N; g.K = K; g.X = x; g.ldx = K; g.W = w;
-  g.ks = t.nc * gemm_chunk_k(et); g.nsplit = t.nsplit; g.n_tiles = t.n_tiles;
   g.epi = EPI_STORE; g.out = y; g.ldo = N; g.out_f32 = 1;
-  float* ws = nullptr;
-  unsigned* cnt = nullptr;
-  if (t.nsplit > 1) {
-    HIP_TRY(hipMalloc(&ws, (size_t)t.m_tiles * t.n_tiles * t.nsplit * gemm_ws_floats_per_unit(t.ms, 1) * 4));
-    HIP_TRY(hipMalloc(&cnt, (size_t)t.m_tiles * t.n_tiles * 4));
-    HIP_TRY(hipMemset(cnt, 0, (size_t)t.m_tiles * t.n_tiles * 4));
-  }
-  g.ws = ws; g.cnt = cnt;
-  hipError_t e = launch_gemm(et, t.ms, 1, t.nc, g, t.units, s);
+  DenseLaunch d = dense_launch(et, g, 1, variant);
+  if (variant == 2 && !d.skinny) return fail(VLA_E_UNSUPPORTED, "shape not supported by the skinny GEMM");
+  hipError_t e = launch_dense(et, d, g, s);
   hipError_t e2 = hipStreamSynchronize(s);
-  (void)hipFree(ws);
-  (void)hipFree(cnt);
   if (e != hipSuccess || e2 != hipSuccess)
     return fail(VLA_E_DEVICE, "gemm: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   return VLA_OK;
@@ -1109,23 +1178,21 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
   a.mode = mode; a.B = B; a.n = n; a.P = mode == 0 ? 0 : P; a.H = H; a.G = G; a.hd = hd;
   a.q = q; a.ldq = H * hd; a.ks = k_self; a.vs = v_self; a.ldkv = G * hd;
   a.kc = k_cache; a.vc = v_cache; a.o = o; a.ldo = H * hd; a.scale = 1.0f / std::sqrt((float)hd);
-  const int total = (mode == 0 ? 0 : P) + (mode == 1 ? 0 : n);
-  const int QT = cdiv(n, 16);
-  int split = kv_split > 0 ? kv_split : std::max(1, std::min(cdiv(256, B * H * QT), cdiv(total, 32)));
-  a.key_chunk = cdiv(cdiv(total, split), 32) * 32;
-  a.kv_split = cdiv(total, a.key_chunk);
-  float* ws = nullptr;
-  unsigned* cnt = nullptr;
+  if (H / G > 8 || H > 32) return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head");
+  attention_split(a, kv_split);
+  const int et = elem ? ET_BF16 : ET_F32;
+  void* part = nullptr;
+  float* stats = nullptr;
   if (a.kv_split > 1) {
-    HIP_TRY(hipMalloc(&ws, attention_ws_floats(a) * 4));
-    HIP_TRY(hipMalloc(&cnt, (size_t)B * H * QT * 4));
-    HIP_TRY(hipMemset(cnt, 0, (size_t)B * H * QT * 4));
+    HIP_TRY(hipMalloc(&part, attention_part_bytes(et, a)));
+    HIP_TRY(hipMalloc(&stats, attention_stats_bytes(a)));
   }
-  a.ws = ws; a.cnt = cnt;
-  hipError_t e = launch_attention(elem ? ET_BF16 : ET_F32, a, s);
+  a.part = part;
+  a.stats = stats;
+  hipError_t e = launch_attention(et, a, s);
   hipError_t e2 = hipStreamSynchronize(s);
-  (void)hipFree(ws);
-  (void)hipFree(cnt);
+  (void)hipFree(part);
+  (void)hipFree(stats);
   if (e != hipSuccess || e2 != hipSuccess)
     return fail(VLA_E_DEVICE, "attention: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   return VLA_OK;
@@ -1151,29 +1218,22 @@ vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int3
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   const Tiling t = tern_tiling(M, N, K, 1);
   int8_t* q8 = nullptr;
-  float *r8 = nullptr, *sc = nullptr, *ws = nullptr;
-  unsigned* cnt = nullptr;
+  float *r8 = nullptr, *sc = nullptr;
   HIP_TRY(hipMalloc(&q8, (size_t)M * K));
   HIP_TRY(hipMalloc(&r8, (size_t)M * 4));
   HIP_TRY(hipMalloc(&sc, (size_t)N * 4));
   std::vector<float> hs(N, scale);
   HIP_TRY(hipMemcpy(sc, hs.data(), (size_t)N * 4, hipMemcpyHostToDevice));
-  if (t.nsplit > 1) {
-    HIP_TRY(hipMalloc(&ws, (size_t)t.m_tiles * t.n_tiles * t.nsplit * gemm_ws_floats_per_unit(t.ms, 1) * 4));
-    HIP_TRY(hipMalloc(&cnt, (size_t)t.m_tiles * t.n_tiles * 4));
-    HIP_TRY(hipMemset(cnt, 0, (size_t)t.m_tiles * t.n_tiles * 4));
-  }
   QuantArgs qa{};
   qa.M = M; qa.K = K; qa.x = x; qa.ldx = K; qa.src_type = 0; qa.q = q8; qa.r = r8;
   TernArgs a{};
   a.M = M; a.N = N; a.K = K; a.x = q8; a.w = w_packed; a.rscale = r8; a.wscale = sc;
-  a.ks = t.nc * 256; a.nsplit = t.nsplit; a.n_tiles = t.n_tiles;
-  a.ws = reinterpret_cast<int*>(ws); a.cnt = cnt;
+  a.ks = t.nc * 256; a.nsplit = 1; a.n_tiles = t.n_tiles;
   a.e.M = M; a.e.N = N; a.e.K = K; a.e.epi = EPI_STORE; a.e.out = y; a.e.ldo = N; a.e.out_f32 = 1;
   hipError_t e = launch_quantize(qa, s);
   if (e == hipSuccess) e = launch_ternary_gemm(a, t.ms, t.units, s);
   hipError_t e2 = hipStreamSynchronize(s);
-  (void)hipFree(q8); (void)hipFree(r8); (void)hipFree(sc); (void)hipFree(ws); (void)hipFree(cnt);
+  (void)hipFree(q8); (void)hipFree(r8); (void)hipFree(sc);
   if (e != hipSuccess || e2 != hipSuccess)
     return fail(VLA_E_DEVICE, "ternary linear: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   return VLA_OK;

@@ -23,19 +23,14 @@ struct CallParams {
   float tau[VLA_MAX_STEPS + 1];
 };
 
-// GEMM prologues: how the activation operand X reaches LDS.
-enum GemmPro {
-  PRO_PLAIN = 0,   // X already in the element type, [M][ldx]
-  PRO_ADARMS = 1,  // X is the fp32 residual; u = x * rstd * (1 + gamma) + beta
-};
-
 // GEMM epilogues, applied to y = X W^T after the split-K reduction.
 enum GemmEpi {
   EPI_STORE = 0,    // out[m][n] = act(y + bias[n]) in the element type or fp32
-  EPI_RESID = 1,    // x[m][n] += alpha[n] * y; per-64-column partial sums of x^2
+  EPI_RESID = 1,    // x[m][n] += alpha[n] * y
   EPI_GLU = 2,      // W rows interleaved gate/up in blocks of 16: h = act(g) * u
   EPI_EULER = 3,    // v = y + bias; a += dt v (or a = v); last step: denormalised output
   EPI_KVCACHE = 4,  // scatter [rows of one request][K|V][G][hd] into the cache layout
+  EPI_PARTIAL = 5,  // raw fp32 split-K partial: out[split][m][n]
 };
 
 struct GemmArgs {
@@ -44,18 +39,8 @@ struct GemmArgs {
   const void* X;
   int ldx;
   const void* W;           // [N][K] row-major in the element type
-  // adaRMS prologue
-  const float* rowss;      // [rowss_np][M] partial sums of squares of X rows
-  int rowss_np;
-  const float* gamma;
-  const float* beta;
-  float eps;
-  // split-K
-  int ks;                  // K-slice per split (multiple of the chunk)
-  int nsplit;
-  int n_tiles;             // tiles along N
-  float* ws;
-  unsigned* cnt;
+  int n_tiles;             // tiles along N (set by the launcher)
+  int nsplit;              // K-splits (set by the launcher; > 1 only with EPI_PARTIAL)
   // epilogue
   int epi;
   int act;
@@ -66,7 +51,6 @@ struct GemmArgs {
   float* xres;             // EPI_RESID residual [M][ldxr]
   int ldxr;
   const float* alpha;
-  float* rowss_out;        // EPI_RESID [n_tiles][M]
   // EPI_EULER
   float* a;                // [M][N]
   const CallParams* cp;
@@ -95,24 +79,41 @@ struct AttnArgs {
   int ldo;
   float scale;
   int kv_split;            // key splits
-  int key_chunk;           // keys per split (multiple of 32)
-  float* ws;               // partial O and stats
-  unsigned* cnt;
+  int key_chunk;           // 32-key blocks per split
+  void* part;              // [kv_split][B*n][H*hd] per-split output (kv_split > 1)
+  float* stats;            // [kv_split][B*n][H][2] per-split (max, sum)
 };
 
 struct QuantArgs {
   int M, K;
-  const void* x;           // fp32 residual (adarms) or element type / fp32 plain
+  const void* x;           // [M][ldx] fp32 or bf16
   int ldx;
   int src_type;            // 0 fp32, 1 bf16
-  int adarms;
-  const float* rowss;
-  int rowss_np;
+  int8_t* q;               // [M][K]
+  float* r;                // [M]
+};
+
+// Per-row residual finish + adaRMS of the next sublayer:
+//   x[m] = x[m] + alpha * sum_s part[s][m]      (mode 0; nsplit may be 0)
+//   x[m] = a[m] W_in^T + xs[b] + E_pos[token]    (mode 1, the input embedding)
+//   u[m] = x[m] / sqrt(mean(x[m]^2) + eps) * (1 + gamma) + beta
+struct RowNormArgs {
+  int mode;
+  int M, d;
+  float* x;                // [M][d]
+  const float* part;       // [nsplit][M][d]
+  int nsplit;
+  const float* alpha;      // [d] or NULL (no residual update)
+  const float* a;          // mode 1: [M][A]
+  const void* W_in;        // [d][A]
+  const float* xs;         // [B][d]
+  const void* E_pos;       // [n][d]
+  int n, A;
   const float* gamma;
   const float* beta;
   float eps;
-  int8_t* q;               // [M][K]
-  float* r;                // [M]
+  void* u;                 // [M][d] element type (u_f32 = 0) or fp32
+  int u_f32;
 };
 
 struct TernArgs {
@@ -122,28 +123,38 @@ struct TernArgs {
   const float* rscale;     // [M] absmax per row (dequant) or NULL for raw acc
   const float* wscale;     // [N] per W-row scale (the per-tensor scale of its matrix)
   int32_t* acc_out;        // raw int32 output (when rscale == NULL); zero-filled if nsplit > 1
-  int ks, nsplit, n_tiles;
-  int* ws;
-  unsigned* cnt;
+  int ks, nsplit, n_tiles;  // nsplit > 1 only for the raw int32 output (atomic accumulation)
   // dequantised epilogue (same meaning as GemmArgs)
   GemmArgs e;
 };
 
-// ---- launchers (each enqueues on `s`, returns hipError_t) ----
-hipError_t launch_gemm(int et, int ms, int nsub, int nc, const GemmArgs& a, int units, hipStream_t s);
-int gemm_chunk_k(int et);  // K covered by one chunk (all 4 lane groups)
-size_t gemm_lds_bytes(int et, int ms, int nc);
-size_t gemm_ws_floats_per_unit(int ms, int nsub);
+// Launch shapes of the two dense GEMM kernels (chosen on the host).
+struct SkinnyShape {
+  int ms, nsub, cpw, nsplit, n_tiles, m_tiles, units;
+  size_t lds;
+};
+struct WideShape {
+  int ms, nsub, nc, n_tiles, m_tiles, units;
+  size_t lds;
+};
 
-hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s);
-size_t attention_ws_floats(const AttnArgs& a);
+// ---- launchers (each enqueues on `s`, returns hipError_t) ----
+int gemm_chunk_k(int et);  // K covered by one chunk (all 4 lane groups of a wave)
+bool skinny_plan(int et, int M, int N, int K, int nsub, bool allow_split, SkinnyShape* sh);
+void wide_plan(int et, int M, int N, int K, int nsub, WideShape* sh);
+hipError_t launch_gemm_skinny(int et, const SkinnyShape& sh, GemmArgs a, hipStream_t s);
+hipError_t launch_gemm_wide(int et, const WideShape& sh, GemmArgs a, hipStream_t s);
+
+hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s);  // + merge when kv_split > 1
+void attention_split(AttnArgs& a, int want_splits);                      // 0 = about 96 workgroups
+size_t attention_part_bytes(int et, const AttnArgs& a);
+size_t attention_stats_bytes(const AttnArgs& a);
 
 hipError_t launch_set_params(CallParams* dst, const CallParams& src, hipStream_t s);
 hipError_t launch_init_chunk(int et, const CallParams* cp, float* a, float* xs, const void* W_s,
                              const float* b_s, const float* b_in, int B, int n, int A, int S, int d,
                              hipStream_t s);
-hipError_t launch_embed(int et, const float* a, const void* W_in, const float* xs, const void* E_pos,
-                        float* x, float* rowss, int B, int n, int A, int d, hipStream_t s);
+hipError_t launch_row_norm(int et, const RowNormArgs& a, hipStream_t s);
 hipError_t launch_time_embed(int et, const CallParams* cp, void* e, int T, int Tpad, int d, hipStream_t s);
 hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);

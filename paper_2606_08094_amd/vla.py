@@ -21,11 +21,13 @@ WTYPES = {"f32": 0, "bf16": 1, "ternary": 2}
 STATUS = {0: "VLA_OK", 1: "VLA_E_ARG", 2: "VLA_E_SHAPE", 3: "VLA_E_UNSUPPORTED", 4: "VLA_E_NOMEM",
           5: "VLA_E_DEVICE", 6: "VLA_E_NONFINITE"}
 VLA_OPT_LOOP_MODE = 0
+VLA_OPT_PROFILE = 1
+OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small"}
 
 # Every symbol the headers declare.
 EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_cache_bytes",
            "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
-           "vla_last_error", "vla_status_string",
+           "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear"]
 
 
@@ -40,6 +42,11 @@ class VlaConfig(ctypes.Structure):
         "n_layers", "d_model", "n_heads", "head_dim", "n_kv_heads", "d_ff", "d_prefix",
         "n_action", "d_action", "d_state", "pattern", "mlp", "wtype", "head_regression")] + [
         ("rms_eps", ctypes.c_float)]
+
+
+class VlaOpTime(ctypes.Structure):
+    _fields_ = [("kind", ctypes.c_int32), ("M", ctypes.c_int32), ("N", ctypes.c_int32), ("K", ctypes.c_int32),
+                ("bytes", ctypes.c_double), ("flops", ctypes.c_double), ("ms", ctypes.c_float)]
 
 
 _lib = None
@@ -65,6 +72,7 @@ def lib():
         "vla_model_set_option": (i32, [vp, i32, i32]),
         "vla_last_error": (ctypes.c_char_p, []),
         "vla_status_string": (ctypes.c_char_p, [i32]),
+        "vla_profile_read": (i32, [vp, ctypes.POINTER(VlaOpTime), i32]),
         "vla_test_gemm": (i32, [i32, vp, vp, i32, i32, i32, i32, vp, vp]),
         "vla_test_attention": (i32, [i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]),
         "vla_test_quantize_i8": (i32, [vp, i32, i32, vp, vp, vp]),
@@ -175,6 +183,19 @@ class Model:
     def set_loop_mode(self, mode: int):
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_LOOP_MODE, mode))
 
+    def set_profile(self, on: bool):
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_PROFILE, int(bool(on))))
+
+    def profile_read(self) -> List[dict]:
+        """Per-launch timings of the last profiled denoise call."""
+        n = lib().vla_profile_read(self.handle, None, 0)
+        if n < 0:
+            return []
+        buf = (VlaOpTime * n)()
+        lib().vla_profile_read(self.handle, buf, n)
+        return [dict(kind=OP_KINDS.get(o.kind, str(o.kind)), M=o.M, N=o.N, K=o.K, bytes=o.bytes,
+                     flops=o.flops, ms=o.ms) for o in buf]
+
     def prefix_kv_build(self, prefix_hidden, batch: int, prefix_len: int, kv_cache, kv_cache_bytes: int,
                         stream=None):
         _check(lib().vla_prefix_kv_build(self.handle, _ptr(prefix_hidden), batch, prefix_len, _ptr(kv_cache),
@@ -200,8 +221,8 @@ def ternary_gemm(x, w_packed, M: int, N: int, K: int, acc_out, stream=None):
 
 # ---- test-only per-kernel entries (include/vla_test.h) ---------------------
 
-def test_gemm(elem: int, x, w, M: int, N: int, K: int, y, force_nsplit: int = 0, stream=None):
-    _check(lib().vla_test_gemm(elem, _ptr(x), _ptr(w), M, N, K, force_nsplit, _ptr(y), _stream(stream)))
+def test_gemm(elem: int, x, w, M: int, N: int, K: int, y, variant: int = 0, stream=None):
+    _check(lib().vla_test_gemm(elem, _ptr(x), _ptr(w), M, N, K, variant, _ptr(y), _stream(stream)))
 
 
 def test_attention(elem: int, mode: int, q, k_self, v_self, k_cache, v_cache, B: int, n: int, P: int, H: int,

@@ -100,6 +100,7 @@ def test_call_validation_without_device():
     assert L.vla_status_string(6) == b"VLA_E_NONFINITE"
     # test entries validate too
     assert vla.STATUS[L.vla_test_gemm(2, 16, 16, 1, 1, 8, 0, 16, None)] == "VLA_E_ARG"
+    assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 3, 16, None)] == "VLA_E_ARG"
     assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 7, 0, 16, None)] == "VLA_E_SHAPE"
     assert vla.STATUS[L.vla_test_attention(1, 2, 16, 16, 16, 16, 16, 1, 4, 4, 6, 4, 64, 0, 16, None)] == "VLA_E_SHAPE"
 
