@@ -29,6 +29,7 @@ sys.path.insert(0, os.path.join(ROOT, "tests"))
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 WORKLOAD = "pi0_bf16"
+PROFILE_REPS = 20              # back-to-back repetitions per timed launch
 
 
 def log(*a):
@@ -159,13 +160,13 @@ def main():
     slope, intercept = np.polyfit(np.array(Ts, float), np.array(ms_T), 1)
     ms_build = time_chunks(torch, pipe, tau, 1) - ms_T[-1]
 
-    # live per-launch timings (launch-per-phase driver with HIP events)
-    pipe.model.set_profile(True)
-    pipe.denoise(tau)
+    # live per-launch timings: launch-per-phase driver, every launch repeated
+    # PROFILE_REPS times between one HIP event pair on the plan's stream
+    pipe.model.set_profile(PROFILE_REPS)
     pipe.denoise(tau)
     torch.cuda.synchronize()
     ops = pipe.model.profile_read()
-    pipe.model.set_profile(False)
+    pipe.model.set_profile(0)
     roof = roofline_from_profile(ops, cfg.n_steps)
     step_bytes = roof["alg_bytes_per_solver_step"]
     step_us = slope * 1000.0

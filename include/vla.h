@@ -153,14 +153,18 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *  VLA_OPT_LOOP_MODE: loop driver of vla_denoise, 0 = one launch per phase on
  *    the stream, 1 = the same launches captured once in a HIP graph and
  *    replayed (default).
- *  VLA_OPT_PROFILE: 1 = time every launch of the following vla_denoise calls
- *    with HIP events (launch-per-phase driver; read with vla_profile_read). */
+ *  VLA_OPT_PROFILE: R in 1..1000 = time every launch of the following
+ *    vla_denoise calls with HIP events (launch-per-phase driver; read with
+ *    vla_profile_read).  Each launch runs R times back to back between its
+ *    event pair and the reported time is the mean; with R > 1 the in-place
+ *    updates repeat, so such a call is for timing only and its outputs are
+ *    not the integration's.  0 = off. */
 enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
 
 /* One timed launch of a profiled vla_denoise call. */
 enum { VLA_OP_GEMM = 0, VLA_OP_GEMM_GLU = 1, VLA_OP_ATTENTION = 2, VLA_OP_TERNARY = 3,
-       VLA_OP_QUANTIZE = 4, VLA_OP_SMALL = 5 };
+       VLA_OP_QUANTIZE = 4, VLA_OP_SMALL = 5, VLA_OP_ATTN_MERGE = 6 };
 typedef struct vla_op_time {
   int32_t kind;   /* VLA_OP_* */
   int32_t M;      /* GEMM rows (tokens) / attention queries */
@@ -168,7 +172,7 @@ typedef struct vla_op_time {
   int32_t K;      /* GEMM reduction length / attention head_dim */
   double bytes;   /* algorithmic bytes: weights + cached K/V read once, activations in and out */
   double flops;   /* algorithmic flops (integer ops for the W2A8 GEMM) */
-  float ms;       /* measured duration between HIP events around the launch */
+  float ms;       /* mean duration of the launch (HIP events, see VLA_OPT_PROFILE) */
 } vla_op_time;
 
 /* Copy the launch timings of the model's last profiled vla_denoise call into

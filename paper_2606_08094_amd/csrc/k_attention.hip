@@ -310,7 +310,7 @@ __global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
 }
 
 template <typename T, int HD>
-hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
+hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
   const int QT = (a.n + 15) / 16;
   const int units = a.B * QT * a.G * a.kv_split;
   if (units <= 0) return hipSuccess;
@@ -324,9 +324,12 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s) {
   const int threads = 64 * (a.H / a.G);
   using L = AttnLds<T, HD>;
   const size_t lds = 2 * L::BUF;
-  hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(units), dim3(threads), lds, s, a);
-  hipError_t e = hipGetLastError();
-  if (e != hipSuccess || a.kv_split == 1) return e;
+  if (which != 2) {
+    hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(units), dim3(threads), lds, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (which == 1 || a.kv_split == 1) return hipSuccess;
   hipLaunchKernelGGL(attn_merge_kernel<T>, dim3(a.B * a.n), dim3(256), 0, s, a);
   return hipGetLastError();
 }
@@ -360,18 +363,18 @@ size_t attention_stats_bytes(const AttnArgs& a) {
   return (size_t)a.kv_split * a.B * a.n * a.H * 2 * sizeof(float);
 }
 
-hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s) {
+hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which) {
   if (a.H % a.G != 0 || a.H / a.G > 8 || a.H > 32 || a.kv_split > 64) return hipErrorInvalidValue;
   if (et == ET_BF16) {
     switch (a.hd) {
-      case 64: return launch_hd<bf16_t, 64>(a, s);
-      case 128: return launch_hd<bf16_t, 128>(a, s);
-      case 256: return launch_hd<bf16_t, 256>(a, s);
+      case 64: return launch_hd<bf16_t, 64>(a, s, which);
+      case 128: return launch_hd<bf16_t, 128>(a, s, which);
+      case 256: return launch_hd<bf16_t, 256>(a, s, which);
     }
   } else {
     switch (a.hd) {
-      case 64: return launch_hd<float, 64>(a, s);
-      case 128: return launch_hd<float, 128>(a, s);
+      case 64: return launch_hd<float, 64>(a, s, which);
+      case 128: return launch_hd<float, 128>(a, s, which);
     }
   }
   return hipErrorInvalidValue;

@@ -211,6 +211,7 @@ struct Plan {
   std::vector<Op> ops;
   hipGraphExec_t exec = nullptr;
   std::vector<hipEvent_t> events;  // 2 per op when profiled
+  int prof_reps = 1;
   ~Plan() {
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (exec) (void)hipGraphExecDestroy(exec);
@@ -315,14 +316,27 @@ struct Builder {
     const double keys = total;
     const double bytes = (double)a.B * a.G * (a.mode == 0 ? 0 : a.P) * a.hd * 2 * es +  // cached K/V
                          (double)a.B * a.n * (2.0 * a.H * a.hd + (a.mode == 1 ? 0 : 2.0 * a.G * a.hd)) * es;
+    const bool split = a.kv_split > 1;
+    // Key-split partials (element type) plus (m, l) per split: traffic of this
+    // implementation, not of the method, so only the merge reports them.
+    const double pbytes = split ? (double)a.kv_split * a.B * a.n * a.H * (a.hd * es + 8.0) : 0.0;
     ops->push_back(Op{[=](hipStream_t s) {
                         AttnArgs g = a;
                         g.part = *pp;
                         g.stats = *sp;
-                        return launch_attention(et, g, s);
+                        return launch_attention(et, g, s, 1);
                       },
                       op_info(VLA_OP_ATTENTION, a.B * a.n, (int)keys, a.hd, bytes,
                               4.0 * a.B * a.n * a.H * a.hd * keys)});
+    if (split)
+      ops->push_back(Op{[=](hipStream_t s) {
+                          AttnArgs g = a;
+                          g.part = *pp;
+                          g.stats = *sp;
+                          return launch_attention(et, g, s, 2);
+                        },
+                        op_info(VLA_OP_ATTN_MERGE, a.B * a.n, a.kv_split, a.hd,
+                                pbytes + (double)a.B * a.n * a.H * a.hd * es, 0.0)});
   }
 
   void row_norm(RowNormArgs r) {
@@ -635,8 +649,11 @@ vla_status run_ops(const std::vector<Op>& ops, hipStream_t s) {
   return VLA_OK;
 }
 
-// Launch-per-phase with a HIP event pair around every launch.
-vla_status run_ops_profiled(Plan* p, hipStream_t s) {
+// Launch-per-phase with a HIP event pair around every launch, each launch
+// repeated `reps` times between its two events (the mean is elapsed / reps, so
+// the cost of recording the events is amortised).  Repeated launches redo
+// in-place updates, so a profiled call with reps > 1 is for timing only.
+vla_status run_ops_profiled(Plan* p, hipStream_t s, int reps) {
   if (p->events.size() != 2 * p->ops.size()) {
     for (hipEvent_t e : p->events) (void)hipEventDestroy(e);
     p->events.assign(2 * p->ops.size(), nullptr);
@@ -644,7 +661,7 @@ vla_status run_ops_profiled(Plan* p, hipStream_t s) {
   }
   for (size_t i = 0; i < p->ops.size(); ++i) {
     HIP_TRY(hipEventRecord(p->events[2 * i], s));
-    HIP_TRY(p->ops[i](s));
+    for (int r = 0; r < reps; ++r) HIP_TRY(p->ops[i](s));
     HIP_TRY(hipEventRecord(p->events[2 * i + 1], s));
   }
   return VLA_OK;
@@ -707,7 +724,7 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
     return VLA_OK;
   }
   if (option == VLA_OPT_PROFILE) {
-    if (value < 0 || value > 1) return fail(VLA_E_ARG, "profile flag %d out of range", value);
+    if (value < 0 || value > 1000) return fail(VLA_E_ARG, "profile repetitions %d out of range", value);
     m->profile = value;
     return VLA_OK;
   }
@@ -1055,8 +1072,9 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(launch_set_params(p->cp, cpv, s));
   if (m->profile) {
-    VLA_TRY(run_ops_profiled(p, s));
+    VLA_TRY(run_ops_profiled(p, s, m->profile));
     m->last_profiled = p;
+    p->prof_reps = m->profile;
   } else if (m->loop_mode == 0) {
     VLA_TRY(run_ops(p->ops, s));
   } else {
@@ -1137,7 +1155,7 @@ int32_t vla_profile_read(vla_model* m, vla_op_time* out, int32_t max_ops) {
     if (hipEventSynchronize(p->events[2 * i + 1]) == hipSuccess &&
         hipEventElapsedTime(&ms, p->events[2 * i], p->events[2 * i + 1]) != hipSuccess)
       ms = -1.0f;
-    out[i].ms = ms;
+    out[i].ms = ms < 0.0f ? ms : ms / (float)p->prof_reps;
   }
   return n;
 }

@@ -145,7 +145,9 @@ void wide_plan(int et, int M, int N, int K, int nsub, WideShape* sh);
 hipError_t launch_gemm_skinny(int et, const SkinnyShape& sh, GemmArgs a, hipStream_t s);
 hipError_t launch_gemm_wide(int et, const WideShape& sh, GemmArgs a, hipStream_t s);
 
-hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s);  // + merge when kv_split > 1
+// which: 0 = key-split kernel and (when kv_split > 1) the merge, 1 = the
+// key-split kernel only, 2 = the merge only.
+hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which = 0);
 void attention_split(AttnArgs& a, int want_splits);                      // 0 = about 96 workgroups
 size_t attention_part_bytes(int et, const AttnArgs& a);
 size_t attention_stats_bytes(const AttnArgs& a);

@@ -22,7 +22,8 @@ STATUS = {0: "VLA_OK", 1: "VLA_E_ARG", 2: "VLA_E_SHAPE", 3: "VLA_E_UNSUPPORTED",
           5: "VLA_E_DEVICE", 6: "VLA_E_NONFINITE"}
 VLA_OPT_LOOP_MODE = 0
 VLA_OPT_PROFILE = 1
-OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small"}
+OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
+            6: "attn_merge"}
 
 # Every symbol the headers declare.
 EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_cache_bytes",
@@ -183,8 +184,10 @@ class Model:
     def set_loop_mode(self, mode: int):
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_LOOP_MODE, mode))
 
-    def set_profile(self, on: bool):
-        _check(lib().vla_model_set_option(self.handle, VLA_OPT_PROFILE, int(bool(on))))
+    def set_profile(self, reps: int):
+        """0 = off; R >= 1 = time each launch of the next denoise calls as the
+        mean of R back-to-back repetitions (R > 1 is for timing only)."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_PROFILE, int(reps)))
 
     def profile_read(self) -> List[dict]:
         """Per-launch timings of the last profiled denoise call."""
