@@ -151,20 +151,25 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
 
 /* Options:
  *  VLA_OPT_LOOP_MODE: loop driver of vla_denoise, 0 = one launch per phase on
- *    the stream, 1 = the same launches captured once in a HIP graph and
- *    replayed (default).
+ *    the stream, 1 (default) = the same launches captured once in a HIP graph
+ *    and replayed, 2 = one persistent cooperative kernel for the whole step
+ *    loop where the model supports it (batch 1, bf16, joint attention,
+ *    H % 8 == 0 and the shape limits of the team layout), else as 1.
  *  VLA_OPT_PROFILE: R in 1..1000 = time every launch of the following
  *    vla_denoise calls with HIP events (launch-per-phase driver; read with
  *    vla_profile_read).  Each launch runs R times back to back between its
  *    event pair and the reported time is the mean; with R > 1 the in-place
  *    updates repeat, so such a call is for timing only and its outputs are
- *    not the integration's.  0 = off. */
-enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1 };
+ *    not the integration's.  0 = off.
+ *  VLA_OPT_TRACE: 1 = the persistent kernel records a phase timeline (the
+ *    100 MHz device clock before and after every barrier, one workgroup per
+ *    team); read it with vla_test_persist_trace (vla_test.h). */
+enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
 
 /* One timed launch of a profiled vla_denoise call. */
 enum { VLA_OP_GEMM = 0, VLA_OP_GEMM_GLU = 1, VLA_OP_ATTENTION = 2, VLA_OP_TERNARY = 3,
-       VLA_OP_QUANTIZE = 4, VLA_OP_SMALL = 5, VLA_OP_ATTN_MERGE = 6 };
+       VLA_OP_QUANTIZE = 4, VLA_OP_SMALL = 5, VLA_OP_ATTN_MERGE = 6, VLA_OP_PERSIST = 7 };
 typedef struct vla_op_time {
   int32_t kind;   /* VLA_OP_* */
   int32_t M;      /* GEMM rows (tokens) / attention queries */

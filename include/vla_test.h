@@ -42,6 +42,13 @@ vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q,
 vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
                                    float scale, float* y, void* stream);
 
+/* Phase timeline of the model's last persistent vla_denoise call made with
+ * VLA_OPT_TRACE = 1: for each of the 8 teams, max_per_team 100 MHz clock
+ * values (before and after every barrier, in order; unused entries hold
+ * stale data) copied to out [8][max_per_team] (host).  Synchronises the
+ * device.  Returns the entries copied per team, or -1 if nothing was traced. */
+int32_t vla_test_persist_trace(struct vla_model* model, uint64_t* out, int32_t max_per_team);
+
 #ifdef __cplusplus
 }
 #endif

@@ -18,7 +18,7 @@ INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(PKG, "_build")
 LIB = os.path.join(PKG, "libvla.so")
 
-SOURCES = ["k_gemm.hip", "k_attention.hip", "k_misc.hip", "k_ternary.hip", "vla_api.hip"]
+SOURCES = ["k_gemm.hip", "k_attention.hip", "k_misc.hip", "k_ternary.hip", "k_persist.hip", "vla_api.hip"]
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
 FLAGS = [

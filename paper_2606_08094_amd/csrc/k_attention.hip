@@ -5,20 +5,23 @@
 // head floor(h*G/H).  No mask: every key is visible to every query.
 //
 // One workgroup handles (request b, 16-query tile, K/V head g, key split) with
-// one wave per query head of the group, so a K/V block of 32 keys is staged in
-// LDS once and serves every head that shares it.  Blocks are double-buffered:
-// the loads of block j+1 are in flight while block j is multiplied.  Prefix
-// blocks and action-token blocks never mix, so a block has a single source.
+// one wave per query head of the group, so the split's K/V blocks (32 keys
+// each, up to KB of them) are staged in LDS once and serve every head that
+// shares them.  All global loads of the workgroup -- the Q fragments of every
+// wave and the K/V of every block of the split -- are issued before the first
+// LDS store, so the workgroup pays one memory latency, then runs the blocks
+// from LDS.  Prefix blocks and action-token blocks never mix, so a block has a
+// single source.
 //
 // Scores are computed transposed, S^T = K Q^T on MFMA, so each lane's column is
 // one query and the online-softmax statistics live in the lane.  Row rho of
 // score tile t holds key 8*(rho/4) + 4*t + rho%4 of the block; lane group q
 // (= lane/16) then holds keys 8q .. 8q+7 across the two tiles, exactly the k
 // slots of its B operand in O^T += V^T P^T, and V is stored transposed in LDS
-// ([dim][key]) so the A operand is one 16-byte read.
+// ([dim][key], written as key pairs) so the A operand is one 16-byte read.
 //
 // With more than one key split each split writes its output normalised by its
-// own sum (bf16) plus its (max, sum); attn_merge combines them.
+// own sum (element type) plus its (max, sum); attn_merge combines them.
 #include "device_common.h"
 
 namespace {
@@ -32,8 +35,14 @@ struct AttnLds {
   static constexpr int VP = 32 + E;       // V^T row pitch (elements)
   static constexpr size_t KBYTES = 32 * KP * sizeof(T);
   static constexpr size_t VBYTES = HD * VP * sizeof(T);
-  static constexpr size_t BUF = KBYTES + VBYTES;
+  static constexpr size_t BUF = KBYTES + VBYTES;  // one 32-key block
 };
+
+// Most 32-key blocks one workgroup stages in LDS (KB_MAX * BUF <= 160 KB for
+// every supported element type and head_dim).
+constexpr int KB_MAX = 4;
+static_assert(KB_MAX * AttnLds<bf16_t, 256>::BUF <= 160 * 1024, "LDS");
+static_assert(KB_MAX * AttnLds<float, 128>::BUF <= 160 * 1024, "LDS");
 
 template <typename T, int HD>
 __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
@@ -41,6 +50,8 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   constexpr int E = L::E;
   constexpr int NQV = HD / (4 * E);   // 16-byte vectors per lane along hd
   constexpr int DT = HD / 16;         // 16-wide dim tiles of O^T
+  constexpr int VPR = HD / E;         // 16-byte vectors per K/V row
+  constexpr int UB = 4;               // items per thread per load round
   extern __shared__ __align__(16) unsigned char smem[];
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -60,7 +71,8 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
   const int nbp = (npre + 31) / 32, nbs = (nself + 31) / 32;
-  const int jbeg = split * a.key_chunk, jend = min(nbp + nbs, jbeg + a.key_chunk);
+  const int jbeg = split * a.key_chunk;
+  const int nblk = min(nbp + nbs, jbeg + a.key_chunk) - jbeg;
 
   const T* kc = reinterpret_cast<const T*>(a.kc);
   const T* vc = reinterpret_cast<const T*>(a.vc);
@@ -73,75 +85,15 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   const T* ksf = reinterpret_cast<const T*>(a.ks) + (size_t)b * a.n * a.ldkv + g * HD;
   const T* vsf = reinterpret_cast<const T*>(a.vs) + (size_t)b * a.n * a.ldkv + g * HD;
 
-  // Staging of one K/V block: every thread owns items tid, tid + nthr, ...
-  // (16-byte vectors of a K row and of a V row).  The first SU items are
-  // loaded into registers by `fetch` (issued before the math on the previous
-  // block) and written to LDS by `store`; any further items are copied
-  // synchronously by `store`.
-  constexpr int ITEMS = 32 * (HD / E);
-  constexpr int SU = 4;
-  uint4 kreg[SU], vreg[SU];
-  auto src = [&](int j, int kr, const T*& kp, const T*& vp) -> bool {
+  // key `kr` of block jb of this split: source row pointers, false if past the end
+  auto src = [&](int jb, int kr, const T*& kp, const T*& vp) -> bool {
+    const int j = jbeg + jb;
     const bool pre = j < nbp;
-    const int key0 = pre ? j * 32 : (j - nbp) * 32;
-    const int cnt = pre ? min(32, npre - key0) : min(32, nself - key0);
-    if (kr >= cnt) return false;
-    const int key = key0 + kr;
+    const int key = (pre ? j : j - nbp) * 32 + kr;
+    if (key >= (pre ? npre : nself)) return false;
     kp = pre ? kc + (size_t)key * HD : ksf + (size_t)key * a.ldkv;
     vp = pre ? vc + (size_t)key * HD : vsf + (size_t)key * a.ldkv;
     return true;
-  };
-  auto block_cnt = [&](int j) {
-    const bool pre = j < nbp;
-    const int key0 = pre ? j * 32 : (j - nbp) * 32;
-    return pre ? min(32, npre - key0) : min(32, nself - key0);
-  };
-  auto fetch = [&](int j) {
-#pragma unroll
-    for (int u = 0; u < SU; ++u) {
-      const int i = threadIdx.x + u * nthr;
-      const int kr = i / (HD / E), cv = i - kr * (HD / E);
-      const T *kp, *vp;
-      if (i < ITEMS && src(j, kr, kp, vp)) {
-        kreg[u] = ldg16(kp + cv * E);
-        vreg[u] = ldg16(vp + cv * E);
-      } else {
-        kreg[u] = make_uint4(0, 0, 0, 0);
-        vreg[u] = make_uint4(0, 0, 0, 0);
-      }
-    }
-  };
-  auto put = [&](int buf, int i, uint4 kv4, uint4 vv4) {
-    T* kl = reinterpret_cast<T*>(smem + buf * L::BUF);
-    T* vl = reinterpret_cast<T*>(smem + buf * L::BUF + L::KBYTES);
-    const int kr = i / (HD / E), cv = i - kr * (HD / E);
-    *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * E) = kv4;
-    const uint32_t w4[4] = {vv4.x, vv4.y, vv4.z, vv4.w};
-    if constexpr (E == 8) {
-#pragma unroll
-      for (int e = 0; e < 8; ++e)
-        reinterpret_cast<bf16_t*>(vl)[(cv * 8 + e) * L::VP + kr] = (bf16_t)(w4[e >> 1] >> (16 * (e & 1)));
-    } else {
-#pragma unroll
-      for (int e = 0; e < 4; ++e) reinterpret_cast<float*>(vl)[(cv * 4 + e) * L::VP + kr] = __uint_as_float(w4[e]);
-    }
-  };
-  auto store = [&](int j, int buf) {
-#pragma unroll
-    for (int u = 0; u < SU; ++u) {
-      const int i = threadIdx.x + u * nthr;
-      if (i < ITEMS) put(buf, i, kreg[u], vreg[u]);
-    }
-    for (int i = threadIdx.x + SU * nthr; i < ITEMS; i += nthr) {
-      const int kr = i / (HD / E), cv = i - kr * (HD / E);
-      const T *kp, *vp;
-      uint4 kv4 = make_uint4(0, 0, 0, 0), vv4 = make_uint4(0, 0, 0, 0);
-      if (src(j, kr, kp, vp)) {
-        kv4 = ldg16(kp + cv * E);
-        vv4 = ldg16(vp + cv * E);
-      }
-      put(buf, i, kv4, vv4);
-    }
   };
 
   // Q fragments (B operand of S^T): query row r16 of head h, dims g4*HD/4 + c*E ..
@@ -151,23 +103,75 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < NQV; ++c) qf[c] = (qrow < a.n) ? ldg16(qp + c * E) : make_uint4(0, 0, 0, 0);
 
+  // Stage every block of the split.  K item i: vector i % VPR of key row
+  // (i / VPR) % 32 of block i / (32 VPR).  V item i: vector i / 16 % VPR of the
+  // key pair i % 16, block i / (16 VPR); a pair is written as one 2-element
+  // column of V^T.  Keys past the end are zero (no NaN from unwritten LDS).
+  const int nk = nblk * 32 * VPR, nv = nblk * 16 * VPR;
+  for (int base = threadIdx.x; base < nk; base += UB * nthr) {
+    uint4 kr4[UB], v0[UB], v1[UB];
+#pragma unroll
+    for (int q = 0; q < UB; ++q) {
+      const int i = base + q * nthr;
+      kr4[q] = make_uint4(0, 0, 0, 0);
+      v0[q] = make_uint4(0, 0, 0, 0);
+      v1[q] = make_uint4(0, 0, 0, 0);
+      const T *kp, *vp;
+      if (i < nk) {
+        const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
+        const int kr = r / VPR, cv = r - kr * VPR;
+        if (src(jb, kr, kp, vp)) kr4[q] = ldg16(kp + cv * E);
+      }
+      if (i < nv) {
+        const int jb = i / (16 * VPR), r = i - jb * 16 * VPR;
+        const int kp2 = r & 15, cv = r >> 4;
+        if (src(jb, 2 * kp2, kp, vp)) v0[q] = ldg16(vp + cv * E);
+        if (src(jb, 2 * kp2 + 1, kp, vp)) v1[q] = ldg16(vp + cv * E);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < UB; ++q) {
+      const int i = base + q * nthr;
+      if (i < nk) {
+        const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
+        const int kr = r / VPR, cv = r - kr * VPR;
+        T* kl = reinterpret_cast<T*>(smem + jb * L::BUF);
+        *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * E) = kr4[q];
+      }
+      if (i < nv) {
+        const int jb = i / (16 * VPR), r = i - jb * 16 * VPR;
+        const int kp2 = r & 15, cv = r >> 4;
+        T* vl = reinterpret_cast<T*>(smem + jb * L::BUF + L::KBYTES);
+        const uint32_t a4[4] = {v0[q].x, v0[q].y, v0[q].z, v0[q].w};
+        const uint32_t b4[4] = {v1[q].x, v1[q].y, v1[q].z, v1[q].w};
+        if constexpr (E == 8) {
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+            const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+            *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
+          }
+        } else {
+#pragma unroll
+          for (int e = 0; e < 4; ++e)
+            *reinterpret_cast<uint2*>(vl + (cv * 4 + e) * L::VP + 2 * kp2) = make_uint2(a4[e], b4[e]);
+        }
+      }
+    }
+  }
+  __syncthreads();
+
   f32x4 o[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.0f;
   const float sc = a.scale * kLog2e;
 
-  if (jbeg < jend) {
-    fetch(jbeg);
-    store(jbeg, 0);
-  }
-  for (int j = jbeg; j < jend; ++j) {
-    const int buf = (j - jbeg) & 1;
-    const int cnt = block_cnt(j);
-    __syncthreads();                   // block j staged; block j-1 fully read
-    if (j + 1 < jend) fetch(j + 1);    // global loads in flight during the math below
-    const T* kl = reinterpret_cast<const T*>(smem + buf * L::BUF);
-    const T* vl = reinterpret_cast<const T*>(smem + buf * L::BUF + L::KBYTES);
+  for (int jb = 0; jb < nblk; ++jb) {
+    const int j = jbeg + jb;
+    const int cnt = j < nbp ? min(32, npre - j * 32) : min(32, nself - (j - nbp) * 32);
+    const T* kl = reinterpret_cast<const T*>(smem + jb * L::BUF);
+    const T* vl = reinterpret_cast<const T*>(smem + jb * L::BUF + L::KBYTES);
 
     // scores: tile t, row rho = r16 -> key 8*(rho/4) + 4t + rho%4
     f32x4 s[2];
@@ -227,7 +231,6 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
         for (int k = 0; k < 8; ++k) o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vrow[k], p[k], o[d], 0, 0, 0);
       }
     }
-    if (j + 1 < jend) store(j + 1, buf ^ 1);
   }
 
   // Lane holds O^T[dim = 16d + 4*g4 + i][query r16].
@@ -256,57 +259,54 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
 }
 
 // O[m][h] = sum_s w_s O_s / sum_s w_s with w_s = l_s * 2^(m_s - max_s m_s).
-// One thread per 16-byte vector of the output row; the splits' vectors are
-// loaded four at a time.
+// One wave per (output row, 64 16-byte vectors of the row); each lane merges
+// one vector in a single online pass (running max, rescaled sums) with the
+// (max, sum) and the partial vectors of SB splits loaded at once.
+constexpr int MERGE_SB = 16;
+
 template <typename T>
-__global__ __launch_bounds__(256) void attn_merge_kernel(AttnArgs a) {
+__global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
   constexpr int E = ElemTraits<T>::E;
-  const int m = blockIdx.x;
   const int rows = a.B * a.n, dq = a.H * a.hd;
-  __shared__ float wgt[64 * 32];   // kv_split <= 64, H <= 32
-  for (int h = threadIdx.x; h < a.H; h += blockDim.x) {
-    float mx = -INFINITY;
-    for (int s = 0; s < a.kv_split; ++s) mx = fmaxf(mx, a.stats[(((size_t)s * rows + m) * a.H + h) * 2]);
-    float tot = 0.0f;
-    for (int s = 0; s < a.kv_split; ++s) {
-      const float* st = a.stats + (((size_t)s * rows + m) * a.H + h) * 2;
-      const float w = st[1] * exp2f(st[0] - mx);
-      wgt[s * a.H + h] = w;
-      tot += w;
-    }
-    for (int s = 0; s < a.kv_split; ++s) wgt[s * a.H + h] /= tot;
-  }
-  __syncthreads();
+  const int cblocks = (dq + 64 * E - 1) / (64 * E);
+  const int m = blockIdx.x / cblocks;
+  const int c = ((blockIdx.x - m * cblocks) * 64 + threadIdx.x) * E;
+  if (c >= dq) return;
+  const int h = c / a.hd;
+  const int S = a.kv_split, H = a.H;
   const T* part = reinterpret_cast<const T*>(a.part);
-  T* op = reinterpret_cast<T*>(a.o) + (size_t)m * a.ldo;
-  for (int c = threadIdx.x * E; c < dq; c += blockDim.x * E) {
-    const int h = c / a.hd;
-    float acc[E];
+  float acc[E];
 #pragma unroll
-    for (int e = 0; e < E; ++e) acc[e] = 0.0f;
-    int s = 0;
-    for (; s + 4 <= a.kv_split; s += 4) {
-      uint4 v[4];
+  for (int e = 0; e < E; ++e) acc[e] = 0.0f;
+  float mx = -INFINITY, tot = 0.0f;
+  for (int s0 = 0; s0 < S; s0 += MERGE_SB) {
+    uint4 v[MERGE_SB];
+    float2 st[MERGE_SB];
 #pragma unroll
-      for (int u = 0; u < 4; ++u) v[u] = ldg16(part + ((size_t)(s + u) * rows + m) * dq + c);
-#pragma unroll
-      for (int u = 0; u < 4; ++u) {
-        float f[E];
-        unpack16(v[u], f, T());
-        const float w = wgt[(s + u) * a.H + h];
-#pragma unroll
-        for (int e = 0; e < E; ++e) acc[e] += w * f[e];
-      }
+    for (int q = 0; q < MERGE_SB; ++q) {
+      const bool ok = s0 + q < S;
+      st[q] = ok ? *reinterpret_cast<const float2*>(a.stats + (((size_t)(s0 + q) * rows + m) * H + h) * 2)
+                 : make_float2(-INFINITY, 0.0f);
+      v[q] = ok ? ldg16(part + ((size_t)(s0 + q) * rows + m) * dq + c) : make_uint4(0, 0, 0, 0);
     }
-    for (; s < a.kv_split; ++s) {
+#pragma unroll
+    for (int q = 0; q < MERGE_SB; ++q) {
+      if (s0 + q >= S || st[q].y <= 0.0f) continue;
+      const float mnew = fmaxf(mx, st[q].x);
+      const float corr = exp2f(mx - mnew);
+      const float w = st[q].y * exp2f(st[q].x - mnew);
       float f[E];
-      unpack16(ldg16(part + ((size_t)s * rows + m) * dq + c), f, T());
-      const float w = wgt[s * a.H + h];
+      unpack16(v[q], f, T());
 #pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] += w * f[e];
+      for (int e = 0; e < E; ++e) acc[e] = acc[e] * corr + w * f[e];
+      tot = tot * corr + w;
+      mx = mnew;
     }
-    stg16(op + c, pack16(acc, T()));
   }
+  const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
+#pragma unroll
+  for (int e = 0; e < E; ++e) acc[e] *= inv;
+  stg16(reinterpret_cast<T*>(a.o) + (size_t)m * a.ldo + c, pack16(acc, T()));
 }
 
 template <typename T, int HD>
@@ -323,20 +323,24 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
   }
   const int threads = 64 * (a.H / a.G);
   using L = AttnLds<T, HD>;
-  const size_t lds = 2 * L::BUF;
+  if (a.key_chunk < 1 || a.key_chunk > KB_MAX) return hipErrorInvalidValue;
+  const size_t lds = (size_t)a.key_chunk * L::BUF;
   if (which != 2) {
     hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(units), dim3(threads), lds, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
   if (which == 1 || a.kv_split == 1) return hipSuccess;
-  hipLaunchKernelGGL(attn_merge_kernel<T>, dim3(a.B * a.n), dim3(256), 0, s, a);
+  constexpr int E = ElemTraits<T>::E;
+  const int cblocks = (a.H * HD + 64 * E - 1) / (64 * E);
+  hipLaunchKernelGGL(attn_merge_kernel<T>, dim3(a.B * a.n * cblocks), dim3(64), 0, s, a);
   return hipGetLastError();
 }
 
 }  // namespace
 
-// Keys per split in 32-key blocks, the number of splits, and the workspace.
+// Keys per split in 32-key blocks (at most KB_MAX), the number of splits, and
+// the workspace.  By default the splits target about 112 workgroups.
 void attention_split(AttnArgs& a, int want_splits) {
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
@@ -345,13 +349,17 @@ void attention_split(AttnArgs& a, int want_splits) {
   int s = want_splits;
   if (s <= 0) {
     const int base = a.B * QT * a.G;
-    s = (96 + base - 1) / base;   // about 96 workgroups
+    s = (112 + base - 1) / base;
   }
   s = s < 1 ? 1 : (s > nblocks ? nblocks : s);
-  s = s > 64 ? 64 : s;
-  a.key_chunk = (nblocks + s - 1) / s;
-  a.kv_split = (nblocks + a.key_chunk - 1) / a.key_chunk;
+  int kc = (nblocks + s - 1) / s;
+  kc = kc < (nblocks + 63) / 64 ? (nblocks + 63) / 64 : kc;  // at most 64 splits
+  if (kc > KB_MAX) kc = KB_MAX;
+  a.key_chunk = kc;
+  a.kv_split = (nblocks + kc - 1) / kc;
 }
+
+int attention_max_blocks() { return 64 * KB_MAX; }
 
 size_t attention_part_bytes(int et, const AttnArgs& a) {
   if (a.kv_split <= 1) return 0;
@@ -364,7 +372,7 @@ size_t attention_stats_bytes(const AttnArgs& a) {
 }
 
 hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which) {
-  if (a.H % a.G != 0 || a.H / a.G > 8 || a.H > 32 || a.kv_split > 64) return hipErrorInvalidValue;
+  if (a.H % a.G != 0 || a.H / a.G > 8 || a.H > 32 || a.kv_split > 64 || a.kv_split < 1) return hipErrorInvalidValue;
   if (et == ET_BF16) {
     switch (a.hd) {
       case 64: return launch_hd<bf16_t, 64>(a, s, which);

@@ -6,21 +6,24 @@
 //
 // gemm_skinny -- the per-step projections, M <= 128 token rows.
 //   A workgroup of 8 waves owns 16*NSUB rows of W (NSUB = 2: a gate/up pair
-//   of interleaved 16-row blocks) and a K-range of up to 8*CPW chunks of
-//   KC = 4*VPL*E k-values (split-K across workgroups when K is longer).  Every
-//   wave first issues the loads of its W chunks (the HBM stream), then the
-//   workgroup stages the [MT][K-range] X tile in LDS with all of a thread's
-//   loads in flight at once; wave w multiplies chunks w, w+8, ...  The eight
-//   partial tiles are summed in wave order through LDS and wave 0 runs the
-//   epilogue.
+//   of interleaved 16-row blocks), up to 16*MS token rows and one K-range
+//   (split-K across workgroups when the grid would otherwise not fill the
+//   chip).  The K-range is cut into chunks of KC k-values; wave w takes
+//   chunks w, w+8, ... (CPW per round).  Every operand goes straight from
+//   global memory into MFMA-layout registers: a round issues all W and X
+//   loads of the wave before the first MFMA, so a workgroup pays one memory
+//   latency per round instead of one per staging step.  The eight partial
+//   tiles are summed in wave order through LDS and waves 0..MS-1 run the
+//   epilogue of one 16-row subtile each.
 //
-// gemm_wide -- large M or very large N (prefix K/V build, modulation tables,
-//   batched requests).  Four waves along N (NT = 64*NSUB), X staged per K-slice
-//   in LDS and shared by the four waves, K-slices looped inside the workgroup.
+// gemm_wide -- large M (prefix K/V build, batched requests).  Four waves along
+//   N (NT = 64*NSUB), X staged per K-slice in LDS and shared by the four
+//   waves, K-slices looped inside the workgroup.
 //
-// In both, lane l of a wave loads 64 contiguous bytes of W row (l % 16) at
-// k-offset (l / 16) * KCL of a chunk, and reads X with the same k mapping, so
-// the MFMA's k order is a permutation common to both operands.
+// Operand layout: in a chunk, lane l of a wave reads 16-byte vector v of row
+// (l % 16) at k-offset v*4*E + (l/16)*E, for W and X alike, so the MFMA's k
+// order is a permutation common to both operands and every load instruction
+// of a wave reads 64 contiguous bytes per row.
 #include "gemm_epilogue.h"
 
 namespace {
@@ -63,88 +66,87 @@ VLA_DEV void stage_x(const GemmArgs& a, T* xs, int pitch, int m0, int k0, int KW
 template <typename T, int MS, int NSUB, int CPW>
 __global__ __launch_bounds__(64 * WKS) void gemm_skinny(GemmArgs a) {
   constexpr int E = ElemTraits<T>::E;
-  constexpr int KCL = VPL * E;
-  constexpr int KC = 4 * KCL;
-  constexpr int MT = 16 * MS;
+  constexpr int KC = 4 * VPL * E;
   extern __shared__ __align__(16) unsigned char smem[];
-  T* xs = reinterpret_cast<T*>(smem);               // [MT][pitch]
-  f32x4* red = reinterpret_cast<f32x4*>(smem);      // reuses the X tile after the MFMA loop
+  f32x4* red = reinterpret_cast<f32x4*>(smem);  // [WKS][MS][NSUB][64]
 
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int N = a.N, K = a.K;
+  const int M = a.M, N = a.N, K = a.K;
   int bid = blockIdx.x;
   const int split = bid % a.nsplit;
   bid /= a.nsplit;
   const int ntile = bid % a.n_tiles, mtile = bid / a.n_tiles;
-  const int m0 = mtile * MT;
+  const int m0 = mtile * 16 * MS;
   const int nb = ntile * 16 * NSUB;
-  const int k0 = split * (WKS * CPW * KC);
-  const int k1 = min(K, k0 + WKS * CPW * KC);
+  const int k0 = split * a.kper;
+  const int k1 = min(K, k0 + a.kper);
   const int nck = (k1 - k0 + KC - 1) / KC;
-  const int pitch = nck * KC + E;
-
-  // 1. W chunks of this wave -> registers
   const T* W = reinterpret_cast<const T*>(a.W);
-  uint4 wreg[CPW][NSUB][VPL];
-#pragma unroll
-  for (int j = 0; j < CPW; ++j) {
-    const int kc = k0 + (wave + j * WKS) * KC + g4 * KCL;
-#pragma unroll
-    for (int s = 0; s < NSUB; ++s) {
-      const int n = nb + s * 16 + r16;
-#pragma unroll
-      for (int v = 0; v < VPL; ++v) {
-        const int k = kc + v * E;
-        wreg[j][s][v] = (n < N && k < k1) ? ldg16(W + (size_t)n * K + k) : make_uint4(0, 0, 0, 0);
-      }
-    }
-  }
+  const T* X = reinterpret_cast<const T*>(a.X);
 
-  // 2. the X tile of this K-range in LDS
-  stage_x<T, MT>(a, xs, pitch, m0, k0, nck * KC);
-  __syncthreads();
-
-  // 3. MFMA over this wave's chunks
   f32x4 acc[MS][NSUB];
 #pragma unroll
   for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
     for (int s = 0; s < NSUB; ++s) acc[ms][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  for (int c0 = 0; c0 < nck; c0 += WKS * CPW) {
+    uint4 wreg[CPW][NSUB][VPL];
+    uint4 xreg[CPW][MS][VPL];
 #pragma unroll
-  for (int j = 0; j < CPW; ++j) {
-    const int c = wave + j * WKS;
-    if (c >= nck) break;
+    for (int j = 0; j < CPW; ++j) {
+      const int c = c0 + wave + j * WKS;
+      const int kc = k0 + c * KC + g4 * E;
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms) {
-      const T* xrow = xs + (size_t)(ms * 16 + r16) * pitch + c * KC + g4 * KCL;
-      uint4 xf[VPL];
+      for (int s = 0; s < NSUB; ++s) {
+        const int n = nb + s * 16 + r16;
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) xf[v] = *reinterpret_cast<const uint4*>(xrow + v * E);
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s)
-#pragma unroll
-        for (int v = 0; v < VPL; ++v) mma16(acc[ms][s], xf[v], wreg[j][s][v], T());
+        for (int v = 0; v < VPL; ++v) {
+          const int k = kc + v * 4 * E;
+          wreg[j][s][v] = (c < nck && n < N && k < k1) ? ldg16(W + (size_t)n * K + k) : make_uint4(0, 0, 0, 0);
+        }
+      }
     }
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      const int c = c0 + wave + j * WKS;
+      const int kc = k0 + c * KC + g4 * E;
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) {
+        const int m = m0 + ms * 16 + r16;
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) {
+          const int k = kc + v * 4 * E;
+          xreg[j][ms][v] = (c < nck && m < M && k < k1) ? ldg16(X + (size_t)m * a.ldx + k) : make_uint4(0, 0, 0, 0);
+        }
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+        for (int s = 0; s < NSUB; ++s)
+#pragma unroll
+          for (int v = 0; v < VPL; ++v) mma16(acc[ms][s], xreg[j][ms][v], wreg[j][s][v], T());
   }
 
-  // 4. sum the eight partial tiles in wave order; epilogue on wave 0
-  __syncthreads();  // every wave is done reading the X tile
-  if (wave > 0) {
+  // sum the eight partial tiles in wave order; wave ms < MS finishes subtile ms
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
+  for (int ms = 0; ms < MS; ++ms)
 #pragma unroll
-      for (int s = 0; s < NSUB; ++s) red[(((wave - 1) * MS + ms) * NSUB + s) * 64 + lane] = acc[ms][s];
-  }
+    for (int s = 0; s < NSUB; ++s) red[((wave * MS + ms) * NSUB + s) * 64 + lane] = acc[ms][s];
   __syncthreads();
-  if (wave != 0) return;
+  if (wave >= MS) return;
+  f32x4 r[1][NSUB];
 #pragma unroll
-  for (int w = 1; w < WKS; ++w)
+  for (int s = 0; s < NSUB; ++s) {
+    r[0][s] = red[((0 * MS + wave) * NSUB + s) * 64 + lane];
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-      for (int s = 0; s < NSUB; ++s) acc[ms][s] += red[(((w - 1) * MS + ms) * NSUB + s) * 64 + lane];
-  wave_epilogue<T, MS, NSUB>(a, acc, m0, nb, split);
+    for (int w = 1; w < WKS; ++w) r[0][s] += red[((w * MS + wave) * NSUB + s) * 64 + lane];
+  }
+  wave_epilogue<T, 1, NSUB>(a, r, m0 + wave * 16, nb, split);
 }
 
 // ---------------------------------------------------------------------------
@@ -286,26 +288,25 @@ int cdiv_i(int a, int b) { return (a + b - 1) / b; }
 int gemm_chunk_k(int et) { return et == ET_BF16 ? 128 : 64; }
 
 bool skinny_plan(int et, int M, int N, int K, int nsub, bool allow_split, SkinnyShape* sh) {
-  const int es = et == ET_BF16 ? 2 : 4;
-  const int E = 16 / es;
   const int KC = gemm_chunk_k(et);
   if (M > 128) return false;
   sh->ms = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
-  const int MT = 16 * sh->ms;
   sh->nsub = nsub;
-  // K-range per workgroup: 8 or 16 chunks, as long as the X tile fits in LDS
-  sh->cpw = ((size_t)MT * (2 * WKS * KC + E) * es <= 136 * 1024) ? 2 : 1;
-  const int krange = WKS * sh->cpw * KC;
-  sh->nsplit = cdiv_i(K, krange);
-  if (sh->nsplit > 1 && !allow_split) return false;
-  if (sh->nsplit == 1 && sh->cpw == 2 && K <= WKS * KC) sh->cpw = 1;
   sh->n_tiles = cdiv_i(N, 16 * nsub);
-  sh->m_tiles = cdiv_i(M, MT);
-  sh->units = sh->n_tiles * sh->m_tiles * sh->nsplit;
-  const int kr = std::min(K, WKS * sh->cpw * KC);
-  const size_t tile = (size_t)MT * (cdiv_i(kr, KC) * KC + E) * es;
-  const size_t red = (size_t)(WKS - 1) * sh->ms * nsub * 64 * 16;
-  sh->lds = std::max(tile, red);
+  sh->m_tiles = cdiv_i(M, 16 * sh->ms);
+  const int chunks = cdiv_i(K, KC);
+  const int base = sh->n_tiles * sh->m_tiles;
+  // Split K only where the epilogue allows it, as far as keeps the grid in one
+  // pass over the 256 compute units.
+  int nsplit = 1;
+  if (allow_split) nsplit = std::max(1, std::min(chunks, 256 / std::max(1, base)));
+  const int cps = cdiv_i(chunks, nsplit);  // chunks per split
+  sh->nsplit = cdiv_i(chunks, cps);
+  sh->kper = cps * KC;
+  // two chunks per wave and round when the registers allow it
+  sh->cpw = (cps > WKS && (sh->ms + nsub) * 2 * 16 + sh->ms * nsub * 4 <= 200) ? 2 : 1;
+  sh->units = base * sh->nsplit;
+  sh->lds = (size_t)WKS * sh->ms * nsub * 64 * 16;
   return true;
 }
 
@@ -328,6 +329,7 @@ hipError_t launch_gemm_skinny(int et, const SkinnyShape& sh, GemmArgs a, hipStre
   if (sh.units <= 0) return hipSuccess;
   a.n_tiles = sh.n_tiles;
   a.nsplit = sh.nsplit;
+  a.kper = sh.kper;
   return et == ET_BF16 ? skinny_t<bf16_t>(sh, a, s) : skinny_t<float>(sh, a, s);
 }
 

@@ -1,0 +1,988 @@
+// Persistent tensor-parallel denoise loop for the batch-1 bf16 expert with
+// joint attention: one cooperative launch runs every solver step, layer and
+// sublayer of vla_denoise (Algorithm 1's loop), with no kernel boundary inside.
+//
+// The 256 workgroups (4 waves each: one wave per SIMD, so a wave may hold up to
+// 512 registers of prefetched operands) form 8 teams of 32 (team = blockIdx %
+// 8; the dispatcher places those on one XCD each, so a team's traffic stays in
+// that XCD's L2).  Team x owns query heads [x*HT, (x+1)*HT) and MLP columns
+// [x*F/8, (x+1)*F/8); it recomputes the K/V head its queries share.  Per layer:
+//   Q  team GEMM u -> [q of the team's heads | k | v]          team barrier
+//   A  attention over [prefix ; chunk] in key splits           team barrier
+//   M  merge the splits -> o_team (each rank 1/8 of a tile)     team barrier
+//   O  o_team W_o[:, team cols]^T -> delta0                     grid barrier
+//   R  x += alpha * (sum of the 8 teams' delta0); adaRMS -> u   team barrier
+//   G  team GEMM u -> act(gate) * up (or act(W1 u)) -> h_team   team barrier
+//   D  h_team W_d[:, team cols]^T -> delta1                     grid barrier
+//   R  x += alpha * sum delta1; adaRMS of the next sublayer     team barrier
+// Every team keeps its own copy of the residual stream x, held in registers by
+// the workgroup that owns each row (rank r: rows r and r + 32), so R is local
+// to a workgroup.  After the last layer R also runs the head, the Euler update
+// and the next step's input embedding.  Weights and cached prefix K/V do not
+// depend on the step's activations: a workgroup issues their loads before it
+// waits at the barrier that precedes the phase using them.
+//
+// Memory model: data that one workgroup writes and another reads moves through
+// device-coherent (sc1) buffer stores and loads, so no L2 write-back or
+// invalidate is needed and correctness does not depend on where workgroups are
+// placed.  Barriers are relaxed agent-scope counters; every wait is bounded,
+// and a timeout sets *err, writes NaN into the chunk and makes every
+// workgroup leave.
+#include "device_common.h"
+
+namespace {
+
+typedef unsigned u32x4_t __attribute__((ext_vector_type(4)));
+typedef unsigned u32x2_t __attribute__((ext_vector_type(2)));
+typedef __amdgpu_buffer_rsrc_t rsrc_t;
+
+constexpr int NTEAM = 8, TSIZE = 32, NWG = NTEAM * TSIZE;
+constexpr int NW = 4, NTHR = 64 * NW;    // waves and threads of a workgroup
+constexpr int SC1 = 16;                  // buffer cache policy: device-coherent
+constexpr int KBA_MAX = 2;               // 32-key blocks per attention split
+constexpr long SPIN_LIMIT = 1L << 21;
+constexpr float kLog2e = 1.4426950408889634f;
+
+// Buffer resource over [base, base + bytes): loads past the end read zero,
+// stores past the end are dropped.
+VLA_DEV rsrc_t mkr(const void* base, size_t bytes) {
+  return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
+}
+VLA_DEV uint4 ldc16(rsrc_t r, unsigned off) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, SC1);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+VLA_DEV uint4 bld16(rsrc_t r, unsigned voff, unsigned soff, int coherent) {
+  const u32x4_t v = coherent ? __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, SC1)
+                             : __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
+VLA_DEV float2 ldc8f(rsrc_t r, unsigned off) {
+  const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, SC1);
+  return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
+}
+VLA_DEV void stc8(rsrc_t r, unsigned off, unsigned lo, unsigned hi) {
+  __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{lo, hi}, r, (int)off, 0, SC1);
+}
+VLA_DEV void stc4(rsrc_t r, unsigned off, unsigned v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, SC1); }
+VLA_DEV void stc2(rsrc_t r, unsigned off, unsigned short v) {
+  __builtin_amdgcn_raw_buffer_store_b16(v, r, (int)off, 0, SC1);
+}
+
+// ---------------------------------------------------------------------------
+// Barriers.  Counters only grow; the k-th team barrier waits for 32 k
+// arrivals on the team counter, the k-th grid barrier for 8 k team arrivals on
+// the global counter (the last workgroup of a team to arrive forwards it).
+struct Sync {
+  unsigned* tcnt;   // [8][32], one counter per team at [team * 32]
+  unsigned* xcnt;   // [8][32]
+  unsigned* glob;   // [64], counter at [0]
+  int* err;
+  unsigned tk, gk;  // barriers passed by this workgroup
+};
+
+VLA_DEV bool spin_until(unsigned* c, unsigned target, int* err) {
+  long it = 0;
+  while (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+    if (++it > SPIN_LIMIT) {
+      __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+      return false;
+    }
+    if ((it & 255) == 0 && __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
+    __builtin_amdgcn_s_sleep(1);
+  }
+  return true;
+}
+
+// A barrier is split into arrive and wait so that loads independent of the
+// other workgroups (the next phase's weights) can be issued in between: the
+// arrival has to wait for this workgroup's stores (one vmcnt covers loads and
+// stores), loads issued after it do not delay it.
+VLA_DEV void team_arrive(Sync& s, int team) {
+  __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
+  __syncthreads();
+  ++s.tk;
+  if (threadIdx.x == 0) __hip_atomic_fetch_add(s.tcnt + team * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+// Returns false (in every thread) if the run must stop.
+VLA_DEV bool team_wait(Sync& s, int team, int* lds_flag) {
+  if (threadIdx.x == 0) *lds_flag = spin_until(s.tcnt + team * 32, s.tk * TSIZE, s.err) ? 1 : 0;
+  __syncthreads();
+  return *lds_flag != 0;
+}
+
+VLA_DEV void grid_arrive(Sync& s, int team) {
+  __builtin_amdgcn_s_waitcnt(0);
+  __syncthreads();
+  ++s.gk;
+  if (threadIdx.x == 0) {
+    const unsigned old = __hip_atomic_fetch_add(s.xcnt + team * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    if (old == s.gk * TSIZE - 1) __hip_atomic_fetch_add(s.glob, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+}
+
+VLA_DEV bool grid_wait(Sync& s, int* lds_flag) {
+  if (threadIdx.x == 0) *lds_flag = spin_until(s.glob, s.gk * NTEAM, s.err) ? 1 : 0;
+  __syncthreads();
+  return *lds_flag != 0;
+}
+
+// ---------------------------------------------------------------------------
+// Team GEMM tile: rows [0, M) (M <= 64, four 16-row subtiles), NS 16-row W
+// tiles, K <= 1024 in chunks of 128; wave w takes chunks w and w + 4.  Lane
+// (r16, g4) holds k = 128 c + 32 v + 8 g4 .. + 8 of row r16 (chunk c), for X
+// and W alike.  Operands come through buffer loads whose lane offset is one
+// register plus an immediate and whose row-block offset is uniform; X is a
+// buffer of exactly M rows of length K, so rows past M read zero.
+constexpr int VPL = 4;
+constexpr int CPW = 2;
+
+template <int NS>
+struct WTile {
+  uint4 w[CPW][NS][VPL];
+};
+
+// W: [rows][ldw] bf16 (rsrc over the matrix), columns kofs + k; wrow[s] < 0: tile s absent.
+template <int NS>
+VLA_DEV void prefetch_w(WTile<NS>& t, rsrc_t W, int ldw, int kofs, int K, const int (&wrow)[NS]) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    const int kc = 128 * (wave + NW * j);
+    const unsigned vb = (unsigned)(r16 * ldw + kofs + kc + 8 * g4) * 2u;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      const bool on = kc < K && wrow[s] >= 0;
+      const unsigned sb = on ? (unsigned)wrow[s] * (unsigned)ldw * 2u : 0u;
+#pragma unroll
+      for (int v = 0; v < VPL; ++v) t.w[j][s][v] = on ? bld16(W, vb + 64u * v, sb, 0) : make_uint4(0, 0, 0, 0);
+    }
+  }
+}
+
+// acc[ms][s] over this wave's chunks; X = [M][K] bf16 through sc1 loads.
+template <int NS>
+VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, rsrc_t X, int K) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  uint4 xr[CPW][4][VPL];
+#pragma unroll
+  for (int j = 0; j < CPW; ++j) {
+    const int kc = 128 * (wave + NW * j);
+    const unsigned vb = (unsigned)(r16 * K + kc + 8 * g4) * 2u;
+#pragma unroll
+    for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+      for (int v = 0; v < VPL; ++v)
+        xr[j][ms][v] = kc < K ? bld16(X, vb + 64u * v, (unsigned)(16 * ms * K) * 2u, 1) : make_uint4(0, 0, 0, 0);
+  }
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      acc[ms][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int j = 0; j < CPW; ++j)
+#pragma unroll
+        for (int v = 0; v < VPL; ++v) mma16(acc[ms][s], xr[j][ms][v], t.w[j][s][v], bf16_t());
+    }
+}
+
+// Sum the 4 waves' tiles through LDS (red: 4 * 4 * NS * 64 f32x4); afterwards
+// wave w holds the full 16-row subtile w in acc[0][s].
+template <int NS>
+VLA_DEV void tile_reduce(f32x4 (&acc)[4][NS], f32x4* red) {
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+    for (int s = 0; s < NS; ++s) red[((wave * 4 + ms) * NS + s) * 64 + lane] = acc[ms][s];
+  __syncthreads();
+#pragma unroll
+  for (int s = 0; s < NS; ++s) {
+    f32x4 r = red[((0 * 4 + wave) * NS + s) * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < NW; ++w) r += red[((w * 4 + wave) * NS + s) * 64 + lane];
+    acc[0][s] = r;
+  }
+}
+
+// ---------------------------------------------------------------------------
+template <int HD>
+struct PLds {
+  static constexpr int KP = HD + 8;    // K row pitch (bf16)
+  static constexpr int VP = 32 + 8;    // V^T row pitch (bf16)
+  static constexpr size_t KBYTES = 32 * KP * 2;
+  static constexpr size_t BUF = KBYTES + (size_t)HD * VP * 2;
+};
+
+size_t lds_main(int hd) {
+  const size_t att = KBA_MAX * (hd == 256 ? PLds<256>::BUF : hd == 128 ? PLds<128>::BUF : PLds<64>::BUF);
+  const size_t red2 = (size_t)NW * 4 * 2 * 64 * 16;
+  return att > red2 ? att : red2;
+}
+
+template <int HD, int DPT>
+__global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
+  using L = PLds<HD>;
+  constexpr int VPR = HD / 8;              // 16-byte vectors per K/V row
+  constexpr int NQV = HD / 32;             // Q fragments per lane
+  constexpr int DTL = HD / 16;             // dim tiles of O^T
+  constexpr int NKI = (KBA_MAX * 32 * VPR + NTHR - 1) / NTHR;  // K items per thread
+  constexpr int NVI = (KBA_MAX * 16 * VPR + NTHR - 1) / NTHR;  // V key-pair items per thread
+  constexpr int OKS = 8;                   // O-projection k-steps of 32 (K = HT * hd <= 256)
+  constexpr int OTW = 2;                   // O-projection 16-column tiles per rank
+  extern __shared__ __align__(16) unsigned char smem[];
+  __shared__ int flag;
+  __shared__ float red_s[2][NW];
+  __shared__ float sa[2][32];              // a of this workgroup's rows (broadcast copy)
+  __shared__ float hv[2][NW][32];          // head partial sums per wave
+  __shared__ PLayer lt[PERSIST_MAX_LAYERS];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int team = blockIdx.x % NTEAM, rank = blockIdx.x / NTEAM;
+  const int n = a.n, d = a.d, HT = a.HT, A = a.A;
+  const int HTD = HT * HD, QW = (HT + 2) * HD, F8 = a.F / 8, S = a.nsplit;
+  const int QT = (n + 15) / 16;
+  const int dq = a.H * HD, dkv = a.G * HD;
+  const int gteam = (team * HT * a.G) / a.H;        // K/V head of the team's queries
+  f32x4* red = reinterpret_cast<f32x4*>(smem);
+  for (int i = tid; i < a.L; i += NTHR) lt[i] = a.layers[i];
+  const bf16_t* kvbase = reinterpret_cast<const bf16_t*>(a.cp->kv_cache);
+
+  Sync sy{a.sync, a.sync + 8 * 32, a.sync + 16 * 32, a.err, 0u, 0u};
+  unsigned long long* trace = (a.trace && rank == 0) ? a.trace + (size_t)team * PERSIST_TRACE_MAX : nullptr;
+  int tev = 0;
+  auto mark = [&]() {
+    if (trace && tid == 0 && tev < PERSIST_TRACE_MAX) trace[tev] = __builtin_amdgcn_s_memrealtime();
+    ++tev;
+  };
+  // A barrier timed out: leave, marking the chunk as failed (NaN).
+  auto bail = [&]() {
+    for (int i = tid; i < n * a.A; i += NTHR) a.cp->actions_out[i] = __int_as_float(0x7fc00000);
+  };
+
+  // team-local workspace
+  const rsrc_t Ur = mkr((const bf16_t*)a.u + (size_t)team * n * d, (size_t)n * d * 2);
+  const rsrc_t Qr = mkr((const bf16_t*)a.qkv + (size_t)team * n * QW, (size_t)n * QW * 2);
+  const rsrc_t APr = mkr((const bf16_t*)a.apart + (size_t)team * S * n * HTD, (size_t)S * n * HTD * 2);
+  const rsrc_t ASr = mkr(a.astat + (size_t)team * S * n * HT * 2, (size_t)S * n * HT * 8);
+  const rsrc_t Hr = mkr((const bf16_t*)a.hbuf + (size_t)team * n * F8, (size_t)n * F8 * 2);
+  const rsrc_t OMr = mkr((const bf16_t*)a.omerged + (size_t)team * n * HTD, (size_t)n * HTD * 2);
+  const rsrc_t Dr = mkr(a.delta, (size_t)2 * NTEAM * n * d * 4);   // [buf][team][n][d]
+
+  // rows of this workgroup and their residual stream (columns tid*DPT + e)
+  const int mrow[2] = {rank, rank + TSIZE};
+  const bool mok[2] = {rank < n, rank + TSIZE < n};
+  float xr[2][DPT];
+  float areg[2] = {0.f, 0.f};              // thread j < A: a[mrow][j]
+  for (int r = 0; r < 2; ++r)
+    if (mok[r] && tid < A) areg[r] = a.a0[(size_t)mrow[r] * A + tid];
+
+  const size_t modstep = (size_t)a.L * 2 * 3 * d;
+  auto gam = [&](int k, int l, int j) { return a.mods + k * modstep + ((size_t)l * 2 + j) * 3 * d; };
+
+  // ---- row-phase pieces ----------------------------------------------------
+  // block sums of v0 (row 0) and v1 (row 1)
+  auto sum2 = [&](float v0, float v1, float& s0, float& s1) {
+    v0 = wave_sum(v0);
+    v1 = wave_sum(v1);
+    if (lane == 0) {
+      red_s[0][wave] = v0;
+      red_s[1][wave] = v1;
+    }
+    __syncthreads();
+    s0 = 0.f;
+    s1 = 0.f;
+#pragma unroll
+    for (int w = 0; w < NW; ++w) {
+      s0 += red_s[0][w];
+      s1 += red_s[1][w];
+    }
+    __syncthreads();
+  };
+  // adaRMS of both rows with (g, b); u (bf16) to the team's U
+  auto norm_store = [&](const float* g, const float* b) {
+    float ss[2] = {0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) ss[r] += xr[r][e] * xr[r][e];
+    const int c = tid * DPT;
+    float gg[DPT], bb[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+      gg[e] = g[c + e];
+      bb[e] = b[c + e];
+    }
+    float t0, t1;
+    sum2(ss[0], ss[1], t0, t1);
+    const float rs[2] = {1.0f / sqrtf(t0 / (float)d + a.eps), 1.0f / sqrtf(t1 / (float)d + a.eps)};
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      if (!mok[r]) continue;
+      float u[DPT];
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) u[e] = xr[r][e] * rs[r] * (1.0f + gg[e]) + bb[e];
+      const unsigned off = (unsigned)(mrow[r] * d + c) * 2u;
+      if constexpr (DPT == 4) stc8(Ur, off, pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]));
+      else stc4(Ur, off, pack_bf16x2(u[0], u[1]));
+    }
+  };
+  // x += alpha * (sum over teams of delta[buf]), summed in team order
+  auto resid = [&](int buf, const float* alpha) {
+    const int c = tid * DPT;
+    float al[DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) al[e] = alpha[c + e];
+    float dv[2][NTEAM][DPT];
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int y = 0; y < NTEAM; ++y) {
+        const unsigned off = (unsigned)((((size_t)buf * NTEAM + y) * n + mrow[r]) * d + c) * 4u;
+        if constexpr (DPT == 4) {
+          const uint4 v = mok[r] ? ldc16(Dr, off) : make_uint4(0, 0, 0, 0);
+          dv[r][y][0] = __uint_as_float(v.x);
+          dv[r][y][1] = __uint_as_float(v.y);
+          dv[r][y][2] = __uint_as_float(v.z);
+          dv[r][y][3] = __uint_as_float(v.w);
+        } else {
+          const float2 v = mok[r] ? ldc8f(Dr, off) : make_float2(0.f, 0.f);
+          dv[r][y][0] = v.x;
+          dv[r][y][1] = v.y;
+        }
+      }
+#pragma unroll
+    for (int r = 0; r < 2; ++r) {
+      if (!mok[r]) continue;
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) {
+        float sum = 0.f;
+#pragma unroll
+        for (int y = 0; y < NTEAM; ++y) sum += dv[r][y][e];
+        xr[r][e] += al[e] * sum;
+      }
+    }
+  };
+  // x = a W_in^T + xs + E_pos (input embedding of the chunk tokens); the
+  // thread's W_in rows, E_pos and xs values are loaded first.
+  auto embed = [&]() {
+    if (tid < 32) {
+      sa[0][tid] = tid < A ? areg[0] : 0.f;
+      sa[1][tid] = tid < A ? areg[1] : 0.f;
+    }
+    const bf16_t* Win = reinterpret_cast<const bf16_t*>(a.w_in);
+    const bf16_t* Ep = reinterpret_cast<const bf16_t*>(a.e_pos);
+    constexpr int AV = 32 / 8;           // 16-byte vectors of a W_in row (A <= 32)
+    uint4 wv[DPT][AV];
+    float base[DPT], ep[2][DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+      const int c = tid * DPT + e;
+#pragma unroll
+      for (int q = 0; q < AV; ++q) wv[e][q] = (8 * q < A) ? ldg16(Win + (size_t)c * A + 8 * q) : make_uint4(0, 0, 0, 0);
+      base[e] = a.xs[c];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) ep[r][e] = mok[r] ? bf2f(Ep[(size_t)mrow[r] * d + c]) : 0.f;
+    }
+    __syncthreads();
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        float v = 0.f;
+        if (mok[r]) {
+          v = base[e] + ep[r][e];
+#pragma unroll
+          for (int q = 0; q < AV; ++q) {
+            if (8 * q >= A) break;
+            float f[8];
+            unpack16(wv[e][q], f, bf16_t());
+#pragma unroll
+            for (int t = 0; t < 8; ++t)
+              if (8 * q + t < A) v += sa[r][8 * q + t] * f[t];
+          }
+        }
+        xr[r][e] = v;
+      }
+    }
+    __syncthreads();
+  };
+  // head v = u_f W_out^T + b_out on the final adaRMS (fp32), then the Euler
+  // update of a (threads j < A); writes the chunk on the last step.
+  auto head = [&](int k) {
+    const float* g = a.modf + (size_t)k * 2 * d;
+    const float* b = g + d;
+    const bf16_t* Wo = reinterpret_cast<const bf16_t*>(a.w_out);
+    // this thread's W_out columns, all A rows, loaded first
+    float wo_[32][DPT];
+#pragma unroll
+    for (int j = 0; j < 32; ++j)
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) wo_[j][e] = j < A ? bf2f(Wo[(size_t)j * d + tid * DPT + e]) : 0.f;
+    float ss[2] = {0.f, 0.f};
+#pragma unroll
+    for (int r = 0; r < 2; ++r)
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) ss[r] += xr[r][e] * xr[r][e];
+    float t0, t1;
+    sum2(ss[0], ss[1], t0, t1);
+    const float rs[2] = {1.0f / sqrtf(t0 / (float)d + a.eps), 1.0f / sqrtf(t1 / (float)d + a.eps)};
+    float uf[2][DPT];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e) {
+      const int c = tid * DPT + e;
+      const float gg = g[c], bb = b[c];
+#pragma unroll
+      for (int r = 0; r < 2; ++r) uf[r][e] = xr[r][e] * rs[r] * (1.0f + gg) + bb;
+    }
+#pragma unroll
+    for (int j = 0; j < 32; ++j) {
+      if (j >= A) break;
+      float p0 = 0.f, p1 = 0.f;
+#pragma unroll
+      for (int e = 0; e < DPT; ++e) {
+        p0 += uf[0][e] * wo_[j][e];
+        p1 += uf[1][e] * wo_[j][e];
+      }
+      p0 = wave_sum(p0);
+      p1 = wave_sum(p1);
+      if (lane == 0) {
+        hv[0][wave][j] = p0;
+        hv[1][wave][j] = p1;
+      }
+    }
+    __syncthreads();
+    const CallParams* cp = a.cp;
+    const float dt = cp->tau[k + 1] - cp->tau[k];
+    if (tid < A) {
+#pragma unroll
+      for (int r = 0; r < 2; ++r) {
+        float v = a.b_out[tid];
+#pragma unroll
+        for (int w = 0; w < NW; ++w) v += hv[r][w][tid];
+        areg[r] += dt * v;
+      }
+      if (k == a.T - 1 && team == 0) {
+#pragma unroll
+        for (int r = 0; r < 2; ++r) {
+          if (!mok[r]) continue;
+          float o = areg[r];
+          if (cp->act_std) o *= cp->act_std[tid];
+          if (cp->act_mean) o += cp->act_mean[tid];
+          cp->actions_out[(size_t)mrow[r] * A + tid] = o;
+        }
+      }
+    }
+    __syncthreads();
+  };
+
+  // ---- phase pieces ----------------------------------------------------------
+  const int NTQ = QW / 16;                 // QKV tiles of the team
+  auto qkv_rows = [&](int (&wrow)[2], int (&ocol)[2]) {
+#pragma unroll
+    for (int s = 0; s < 2; ++s) {
+      const int t = rank + TSIZE * s;
+      wrow[s] = -1;
+      ocol[s] = -1;
+      if (t >= NTQ) continue;
+      const int c = 16 * t;                // local column
+      if (c < HTD) wrow[s] = team * HTD + c;
+      else if (c < HTD + HD) wrow[s] = dq + gteam * HD + (c - HTD);
+      else wrow[s] = dq + dkv + gteam * HD + (c - HTD - HD);
+      ocol[s] = c;
+    }
+  };
+  const int npairs = F8 / 16;              // 16-column groups of h per team (one per rank)
+  auto gu_rows = [&](int (&wrow)[2]) {
+    const int p = rank;
+    if (p >= npairs) {
+      wrow[0] = wrow[1] = -1;
+    } else if (a.glu) {
+      wrow[0] = team * 2 * F8 + 32 * p;
+      wrow[1] = wrow[0] + 16;
+    } else {
+      wrow[0] = team * F8 + 16 * p;
+      wrow[1] = -1;
+    }
+  };
+  const int DCOL = d / TSIZE;             // down-projection columns per rank (16 or 32)
+  auto dn_rows = [&](int (&wrow)[2]) {
+    wrow[0] = rank * DCOL;
+    wrow[1] = DCOL > 16 ? rank * DCOL + 16 : -1;
+  };
+
+  // attention split of this rank
+  const int npre = a.P, nself = n;
+  const int nbp = (npre + 31) / 32, nbs = (nself + 31) / 32;
+  const bool att_on = rank < S;
+  const int jbeg = rank * a.kba;
+  const int nblk = att_on ? min(nbp + nbs, jbeg + a.kba) - jbeg : 0;
+  uint4 kpre[NKI], vp0[NVI], vp1[NVI];
+  auto prefetch_kv = [&](int l) {
+    const bf16_t* kc = kvbase + lt[l].cache_off + (size_t)gteam * npre * HD;
+    const bf16_t* vc = kc + (size_t)a.G * npre * HD;
+#pragma unroll
+    for (int q = 0; q < NKI; ++q) {
+      const int i = tid + q * NTHR;
+      kpre[q] = make_uint4(0, 0, 0, 0);
+      if (i < nblk * 32 * VPR) {
+        const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
+        const int kr = rr / VPR, cv = rr - kr * VPR;
+        const int j = jbeg + jb, key = j * 32 + kr;
+        if (j < nbp && key < npre) kpre[q] = ldg16(kc + (size_t)key * HD + cv * 8);
+      }
+    }
+#pragma unroll
+    for (int q = 0; q < NVI; ++q) {
+      const int i = tid + q * NTHR;
+      vp0[q] = make_uint4(0, 0, 0, 0);
+      vp1[q] = make_uint4(0, 0, 0, 0);
+      if (i < nblk * 16 * VPR) {
+        const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
+        const int kp2 = rr & 15, cv = rr >> 4;
+        const int j = jbeg + jb, key = j * 32 + 2 * kp2;
+        if (j < nbp && key < npre) vp0[q] = ldg16(vc + (size_t)key * HD + cv * 8);
+        if (j < nbp && key + 1 < npre) vp1[q] = ldg16(vc + (size_t)(key + 1) * HD + cv * 8);
+      }
+    }
+  };
+
+  WTile<2> wq, wg, wd;
+  uint4 wo[OTW][OKS];                      // O: this wave's W_o rows (OTW tiles of 16) over K = HT * hd
+  const int CW = d / TSIZE;                // O-projection columns per rank (16 or 32)
+  const int ot = rank / 8, ocb = rank % 8; // merge: query tile and column eighth of this rank
+  auto prefetch_wo = [&](int l) {
+    const rsrc_t W = mkr(lt[l].wo, (size_t)d * dq * 2);
+    const unsigned vb = (unsigned)(r16 * dq + team * HTD + 8 * g4) * 2u;
+#pragma unroll
+    for (int t = 0; t < OTW; ++t) {
+      const int cl = 16 * t;
+      const bool on = wave < QT && cl < CW;
+      const unsigned sb = on ? (unsigned)(rank * CW + cl) * (unsigned)dq * 2u : 0u;
+#pragma unroll
+      for (int ks = 0; ks < OKS; ++ks)
+        wo[t][ks] = (on && 32 * ks < HTD) ? bld16(W, vb + 64u * ks, sb, 0) : make_uint4(0, 0, 0, 0);
+    }
+  };
+
+  __syncthreads();
+  mark();
+  {
+    int wr[2], oc[2];
+    qkv_rows(wr, oc);
+    prefetch_w<2>(wq, mkr(lt[0].wqkv, (size_t)(dq + 2 * dkv) * d * 2), d, 0, d, wr);
+  }
+  embed();
+  norm_store(gam(0, 0, 0), gam(0, 0, 0) + d);
+  mark();
+  team_arrive(sy, team);
+      if (!team_wait(sy, team, &flag)) return bail();
+  mark();
+
+  for (int k = 0; k < a.T; ++k) {
+    for (int l = 0; l < a.L; ++l) {
+      const PLayer& ly = lt[l];
+      // ---- Q: u -> [q | k | v] of the team -----------------------------------
+      {
+        int wr[2], oc[2];
+        qkv_rows(wr, oc);
+        f32x4 acc[4][2];
+        tile_mma<2>(acc, wq, Ur, d);
+        tile_reduce<2>(acc, red);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          if (oc[s] < 0) continue;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int m = 16 * wave + 4 * g4 + i;
+            if (m < n) stc2(Qr, (unsigned)(m * QW + oc[s] + r16) * 2u, f2bf(acc[0][s][i]));
+          }
+        }
+      }
+      mark();
+      team_arrive(sy, team);
+      prefetch_kv(l);
+      if (!team_wait(sy, team, &flag)) return bail();
+      mark();
+
+      // ---- A: attention partials of key split `rank` ---------------------------
+      if (att_on) {
+        // Stage the split's blocks: prefix keys from the prefetched registers,
+        // then this step's k, v of the chunk tokens (rows past the end read zero).
+        auto put_k = [&](int i, uint4 v) {
+          const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
+          const int kr = rr / VPR, cv = rr - kr * VPR;
+          bf16_t* kl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF);
+          *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * 8) = v;
+        };
+        auto put_v = [&](int i, uint4 v0, uint4 v1) {
+          const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
+          const int kp2 = rr & 15, cv = rr >> 4;
+          bf16_t* vl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF + L::KBYTES);
+          const uint32_t a4[4] = {v0.x, v0.y, v0.z, v0.w};
+          const uint32_t b4[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+          for (int e = 0; e < 8; ++e) {
+            const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+            const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+            *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
+          }
+        };
+        // Q fragments of wave (hh, qs): issued first, used after staging
+        const int hh = wave / QT, qs = wave - hh * QT;
+        const bool qwave = hh < HT;
+        const int qrow = 16 * qs + r16;
+        uint4 qf[NQV];
+        const unsigned qb = (unsigned)(qrow * QW + hh * HD + g4 * (HD / 4)) * 2u;
+#pragma unroll
+        for (int c = 0; c < NQV; ++c) qf[c] = qwave ? ldc16(Qr, qb + 16u * c) : make_uint4(0, 0, 0, 0);
+#pragma unroll
+        for (int q = 0; q < NKI; ++q) {
+          const int i = tid + q * NTHR;
+          if (i < nblk * 32 * VPR) put_k(i, kpre[q]);
+        }
+#pragma unroll
+        for (int q = 0; q < NVI; ++q) {
+          const int i = tid + q * NTHR;
+          if (i < nblk * 16 * VPR) put_v(i, vp0[q], vp1[q]);
+        }
+        if (jbeg + nblk > nbp) {   // the split holds chunk-token keys
+#pragma unroll
+          for (int q = 0; q < NKI; ++q) {
+            const int i = tid + q * NTHR;
+            if (i < nblk * 32 * VPR) {
+              const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
+              const int kr = rr / VPR, cv = rr - kr * VPR;
+              const int j = jbeg + jb, key = (j - nbp) * 32 + kr;
+              if (j >= nbp) put_k(i, ldc16(Qr, (unsigned)(key * QW + HTD + cv * 8) * 2u));
+            }
+          }
+#pragma unroll
+          for (int q = 0; q < NVI; ++q) {
+            const int i = tid + q * NTHR;
+            if (i < nblk * 16 * VPR) {
+              const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
+              const int kp2 = rr & 15, cv = rr >> 4;
+              const int j = jbeg + jb, key = (j - nbp) * 32 + 2 * kp2;
+              if (j >= nbp)
+                put_v(i, ldc16(Qr, (unsigned)(key * QW + HTD + HD + cv * 8) * 2u),
+                      ldc16(Qr, (unsigned)((key + 1) * QW + HTD + HD + cv * 8) * 2u));
+            }
+          }
+        }
+        __syncthreads();
+        if (qwave) {
+          f32x4 o[DTL];
+#pragma unroll
+          for (int dd = 0; dd < DTL; ++dd) o[dd] = f32x4{0.f, 0.f, 0.f, 0.f};
+          float mrun = -INFINITY, lrun = 0.0f;
+          const float sc = a.scale * kLog2e;
+          for (int jb = 0; jb < nblk; ++jb) {
+            const int j = jbeg + jb;
+            const int cnt = j < nbp ? min(32, npre - j * 32) : min(32, nself - (j - nbp) * 32);
+            const bf16_t* kl = reinterpret_cast<const bf16_t*>(smem + jb * L::BUF);
+            const bf16_t* vl = reinterpret_cast<const bf16_t*>(smem + jb * L::BUF + L::KBYTES);
+            f32x4 sv[2];
+#pragma unroll
+            for (int t = 0; t < 2; ++t) {
+              sv[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+              const int kr = 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+              const bf16_t* krow = kl + kr * L::KP + g4 * (HD / 4);
+#pragma unroll
+              for (int c = 0; c < NQV; ++c) mma16(sv[t], *reinterpret_cast<const uint4*>(krow + c * 8), qf[c], bf16_t());
+            }
+            float bmax = -INFINITY;
+            float p[8];
+#pragma unroll
+            for (int t = 0; t < 2; ++t)
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int kr = 8 * g4 + 4 * t + i;
+                const float v = (kr < cnt) ? sv[t][i] * sc : -INFINITY;
+                p[4 * t + i] = v;
+                bmax = fmaxf(bmax, v);
+              }
+            bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+            bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+            const float mnew = fmaxf(mrun, bmax);
+            const float corr = exp2f(mrun - mnew);
+            float psum = 0.0f;
+#pragma unroll
+            for (int kk = 0; kk < 8; ++kk) {
+              p[kk] = exp2f(p[kk] - mnew);
+              psum += p[kk];
+            }
+            psum += __shfl_xor(psum, 16, 64);
+            psum += __shfl_xor(psum, 32, 64);
+            lrun = lrun * corr + psum;
+            mrun = mnew;
+#pragma unroll
+            for (int dd = 0; dd < DTL; ++dd) o[dd] *= corr;
+            uint4 pb;
+            pb.x = pack_bf16x2(p[0], p[1]);
+            pb.y = pack_bf16x2(p[2], p[3]);
+            pb.z = pack_bf16x2(p[4], p[5]);
+            pb.w = pack_bf16x2(p[6], p[7]);
+#pragma unroll
+            for (int dd = 0; dd < DTL; ++dd) {
+              const uint4 va = *reinterpret_cast<const uint4*>(vl + (dd * 16 + r16) * L::VP + 8 * g4);
+              mma16(o[dd], va, pb, bf16_t());
+            }
+          }
+          // lane holds O^T[dim 16 dd + 4 g4 + i][query r16]
+          if (qrow < n) {
+            const float inv = lrun > 0.0f ? 1.0f / lrun : 0.0f;
+            const unsigned rowoff = (unsigned)((rank * n + qrow) * HTD + hh * HD);
+#pragma unroll
+            for (int dd = 0; dd < DTL; ++dd)
+              stc8(APr, (rowoff + 16 * dd + 4 * g4) * 2u, pack_bf16x2(o[dd][0] * inv, o[dd][1] * inv),
+                   pack_bf16x2(o[dd][2] * inv, o[dd][3] * inv));
+            if (g4 == 0)
+              stc8(ASr, (unsigned)(((rank * n + qrow) * HT + hh) * 2) * 4u, __float_as_uint(mrun),
+                   __float_as_uint(lrun));
+          }
+        }
+      }
+      mark();
+      team_arrive(sy, team);
+      prefetch_wo(l);
+      if (!team_wait(sy, team, &flag)) return bail();
+      mark();
+
+      // ---- M: merge the key splits; rank (t, cb) merges query tile t, columns
+      // [cb * HTD / 8, (cb + 1) * HTD / 8) of the team's heads into o_team -------
+      if (ot < QT) {
+        const int cw8 = HTD / 8;                          // merged columns per rank (8 .. 32)
+        const int nv = 16 * (cw8 / 8);                    // 16-byte vectors
+        for (int i = tid; i < nv; i += NTHR) {
+          const int rr = i / (cw8 / 8), cv = ocb * (cw8 / 8) + (i - rr * (cw8 / 8));
+          const int m = 16 * ot + rr;
+          const int hh = (cv * 8) / HD;
+          float acc8[8];
+#pragma unroll
+          for (int e = 0; e < 8; ++e) acc8[e] = 0.f;
+          if (m < n) {
+            float mx = -INFINITY, tot = 0.f;
+            for (int s0 = 0; s0 < S; s0 += 16) {
+              uint4 v[16];
+              float2 st[16];
+#pragma unroll
+              for (int q = 0; q < 16; ++q) {
+                const bool ok = s0 + q < S;
+                st[q] = ok ? ldc8f(ASr, (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u) : make_float2(-INFINITY, 0.f);
+                v[q] = ok ? ldc16(APr, (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u) : make_uint4(0, 0, 0, 0);
+              }
+#pragma unroll
+              for (int q = 0; q < 16; ++q) {
+                if (s0 + q >= S || st[q].y <= 0.f) continue;
+                const float mnew = fmaxf(mx, st[q].x);
+                const float corr = exp2f(mx - mnew);
+                const float w = st[q].y * exp2f(st[q].x - mnew);
+                float f[8];
+                unpack16(v[q], f, bf16_t());
+#pragma unroll
+                for (int e = 0; e < 8; ++e) acc8[e] = acc8[e] * corr + w * f[e];
+                tot = tot * corr + w;
+                mx = mnew;
+              }
+            }
+            const float inv = tot > 0.f ? 1.0f / tot : 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc8[e] *= inv;
+            const uint4 pk = pack16(acc8, bf16_t());
+            stc8(OMr, (unsigned)(m * HTD + cv * 8) * 2u, pk.x, pk.y);
+            stc8(OMr, (unsigned)(m * HTD + cv * 8 + 4) * 2u, pk.z, pk.w);
+          }
+        }
+      }
+      mark();
+      team_arrive(sy, team);
+      if (!team_wait(sy, team, &flag)) return bail();
+      mark();
+
+      // ---- O: o_team (all rows) times W_o[rank's CW columns][team heads]^T;
+      // wave w takes query tile w --------------------------------------------------
+      {
+        bf16_t* otile = reinterpret_cast<bf16_t*>(smem);   // [64][HTD + 8]
+        const int OP = HTD + 8;
+        const int nv = 64 * (HTD / 8);
+        for (int i = tid; i < nv; i += NTHR) {
+          const int rr = i / (HTD / 8), cv = i - rr * (HTD / 8);
+          *reinterpret_cast<uint4*>(otile + rr * OP + cv * 8) = ldc16(OMr, (unsigned)(rr * HTD + cv * 8) * 2u);
+        }
+        __syncthreads();
+        if (wave < QT) {
+#pragma unroll
+          for (int t = 0; t < OTW; ++t) {
+            const int cl = 16 * t;
+            if (cl >= CW) break;
+            f32x4 acc = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int ks = 0; ks < OKS; ++ks) {
+              if (32 * ks >= HTD) break;
+              const uint4 av = *reinterpret_cast<const uint4*>(otile + (16 * wave + r16) * OP + 32 * ks + 8 * g4);
+              mma16(acc, av, wo[t][ks], bf16_t());
+            }
+            const int col = rank * CW + cl + r16;
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+              const int m = 16 * wave + 4 * g4 + i;
+              if (m < n) stc4(Dr, (unsigned)((((size_t)0 * NTEAM + team) * n + m) * d + col) * 4u, __float_as_uint(acc[i]));
+            }
+          }
+        }
+      }
+      mark();
+      grid_arrive(sy, team);
+      {
+        int wr[2];
+        gu_rows(wr);
+        prefetch_w<2>(wg, mkr(ly.wgu, (size_t)(a.glu ? 2 : 1) * a.F * d * 2), d, 0, d, wr);
+      }
+      if (!grid_wait(sy, &flag)) return bail();
+      mark();
+
+      // ---- R: attention residual, adaRMS of the MLP sublayer --------------------
+      resid(0, gam(k, l, 0) + 2 * d);
+      norm_store(gam(k, l, 1), gam(k, l, 1) + d);
+      mark();
+      team_arrive(sy, team);
+      if (!team_wait(sy, team, &flag)) return bail();
+      mark();
+
+      // ---- G: u -> h of the team's MLP columns ------------------------------------
+      {
+        f32x4 acc[4][2];
+        tile_mma<2>(acc, wg, Ur, d);
+        tile_reduce<2>(acc, red);
+        if (rank < npairs) {
+          const int f = 16 * rank + r16;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int m = 16 * wave + 4 * g4 + i;
+            if (m >= n) continue;
+            const float h = a.glu ? act_f(a.act, acc[0][0][i]) * acc[0][1][i] : act_f(a.act, acc[0][0][i]);
+            stc2(Hr, (unsigned)(m * F8 + f) * 2u, f2bf(h));
+          }
+        }
+      }
+      mark();
+      team_arrive(sy, team);
+      {
+        int wr[2];
+        dn_rows(wr);
+        prefetch_w<2>(wd, mkr(ly.wd, (size_t)d * a.F * 2), a.F, team * F8, F8, wr);
+      }
+      if (!team_wait(sy, team, &flag)) return bail();
+      mark();
+
+      // ---- D: h_team W_d[:, team cols]^T -> delta1 -----------------------------------
+      {
+        int wr[2];
+        dn_rows(wr);
+        f32x4 acc[4][2];
+        tile_mma<2>(acc, wd, Hr, F8);
+        tile_reduce<2>(acc, red);
+#pragma unroll
+        for (int s = 0; s < 2; ++s) {
+          if (wr[s] < 0) continue;
+          const int col = wr[s] + r16;
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int m = 16 * wave + 4 * g4 + i;
+            if (m < n) stc4(Dr, (unsigned)((((size_t)1 * NTEAM + team) * n + m) * d + col) * 4u, __float_as_uint(acc[0][s][i]));
+          }
+        }
+      }
+      const bool last_layer = l == a.L - 1;
+      const bool last = last_layer && k == a.T - 1;
+      mark();
+      grid_arrive(sy, team);
+      {
+        int wr[2], oc[2];
+        qkv_rows(wr, oc);
+        const int nl = last_layer ? 0 : l + 1;
+        prefetch_w<2>(wq, mkr(lt[nl].wqkv, (size_t)(dq + 2 * dkv) * d * 2), d, 0, d, wr);
+      }
+      if (!grid_wait(sy, &flag)) return bail();
+      mark();
+
+      // ---- R: MLP residual; next sublayer's adaRMS (or head, Euler, embedding) ---
+      resid(1, gam(k, l, 1) + 2 * d);
+      if (!last_layer) {
+        norm_store(gam(k, l + 1, 0), gam(k, l + 1, 0) + d);
+      } else {
+        head(k);
+        if (k + 1 < a.T) {
+          embed();
+          norm_store(gam(k + 1, 0, 0), gam(k + 1, 0, 0) + d);
+        }
+      }
+      if (!last) {
+        mark();
+        team_arrive(sy, team);
+      if (!team_wait(sy, team, &flag)) return bail();
+        mark();
+      }
+    }
+  }
+  mark();
+}
+
+}  // namespace
+
+bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, int glu, int* kba, int* nsplit) {
+  if (!(d == 512 || d == 1024)) return false;   // R: d / 256 columns per thread; O: d / 8 columns per rank
+  if (!(hd == 64 || hd == 128 || hd == 256)) return false;
+  if (H % NTEAM != 0 || G < 1 || H % G != 0) return false;
+  const int HT = H / NTEAM;
+  // all heads of a team share one K/V head
+  for (int t = 0; t < NTEAM; ++t)
+    if ((t * HT * G) / H != ((t * HT + HT - 1) * G) / H) return false;
+  if (HT * hd > 256) return false;           // O-projection K and the attention Q registers
+  if (n < 1 || n > 2 * TSIZE) return false;  // two rows per rank, four 16-row subtiles
+  const int QT = (n + 15) / 16;
+  if (HT * QT > NW) return false;            // attention: one wave per (head, query tile)
+  if ((HT + 2) * hd / 16 > 2 * TSIZE) return false;  // QKV tiles: two per rank
+  if (F % 128 != 0 || F / 8 > 1024 || F / 128 > TSIZE) return false;  // h groups: one per rank
+  (void)glu;
+  if (A < 1 || A > 32) return false;         // head and embedding registers
+  const int nblocks = (P + 31) / 32 + (n + 31) / 32;
+  int k = 1;
+  while ((nblocks + k - 1) / k > TSIZE) ++k;
+  if (k < 2 && nblocks > 16) k = 2;          // fewer, larger splits: less merge traffic
+  if (k > KBA_MAX) return false;
+  *kba = k;
+  *nsplit = (nblocks + k - 1) / k;
+  return true;
+}
+
+size_t persist_lds_bytes(int hd, int HT) {
+  const size_t otile = (size_t)64 * (HT * hd + 8) * 2;
+  const size_t mainb = lds_main(hd);
+  return mainb > otile ? mainb : otile;
+}
+
+hipError_t launch_persist(const PersistArgs& a, hipStream_t s) {
+  const size_t lds = persist_lds_bytes(a.hd, a.HT);
+  void* args[] = {const_cast<PersistArgs*>(&a)};
+  const void* fn = nullptr;
+  const int dpt = a.d / NTHR;
+  switch (a.hd * 10 + dpt) {
+    case 2564: fn = reinterpret_cast<const void*>(&persist_kernel<256, 4>); break;
+    case 2562: fn = reinterpret_cast<const void*>(&persist_kernel<256, 2>); break;
+    case 1284: fn = reinterpret_cast<const void*>(&persist_kernel<128, 4>); break;
+    case 1282: fn = reinterpret_cast<const void*>(&persist_kernel<128, 2>); break;
+    case 644: fn = reinterpret_cast<const void*>(&persist_kernel<64, 4>); break;
+    case 642: fn = reinterpret_cast<const void*>(&persist_kernel<64, 2>); break;
+    default: return hipErrorInvalidValue;
+  }
+  hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
+  if (e != hipSuccess) return e;
+  return hipLaunchCooperativeKernel(fn, dim3(NWG), dim3(NTHR), args, (unsigned)lds, s);
+}

@@ -132,11 +132,13 @@ struct vla_model {
   float *b_t1 = nullptr, *b_t2 = nullptr, *b_fm = nullptr, *b_mod = nullptr;
   float *mod_static = nullptr, *modf_static = nullptr;
   std::vector<std::vector<SubW>> layers;
-  std::map<std::tuple<int, int, int>, std::unique_ptr<Plan>> plans;
+  std::map<std::tuple<int, int, int, int>, std::unique_ptr<Plan>> plans;
   std::map<std::pair<int, int>, std::unique_ptr<PrefixWs>> prefix_ws;
   int loop_mode = 1;
   int profile = 0;
+  int trace = 0;                  // record the persistent kernel's phase timeline
   void* last_profiled = nullptr;  // Plan* of the last profiled call
+  void* last_traced = nullptr;    // Plan* of the last traced call
   hipStream_t cap_stream = nullptr;
   ~vla_model();
 };
@@ -198,6 +200,7 @@ vla_op_time op_info(int kind, int M, int N, int K, double bytes, double flops) {
 
 struct Plan {
   int B = 0, P = 0, T = 0;
+  bool persist = false;       // one cooperative launch runs the whole step loop
   std::vector<void*> allocs;
   CallParams* cp = nullptr;
   float *a = nullptr, *xs = nullptr, *x = nullptr, *mods = nullptr, *modf = nullptr;
@@ -212,6 +215,8 @@ struct Plan {
   hipGraphExec_t exec = nullptr;
   std::vector<hipEvent_t> events;  // 2 per op when profiled
   int prof_reps = 1;
+  int* persist_err = nullptr;       // persistent kernel: set if a barrier timed out
+  unsigned long long* trace = nullptr;  // persistent kernel: phase timeline (8 x PERSIST_TRACE_MAX)
   ~Plan() {
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (exec) (void)hipGraphExecDestroy(exec);
@@ -380,6 +385,17 @@ int mlp_act(int mlp) {
   }
 }
 
+// The persistent step kernel covers the batch-1 bf16 dense expert with joint
+// attention whose shape fits its team layout (see persist_supported).
+bool persist_eligible(const vla_model* m, int B, int P, int T) {
+  const vla_config& c = m->cfg;
+  int kba = 0, nsplit = 0;
+  return !m->tern && m->et == ET_BF16 && c.pattern == VLA_PAT_JOINT && !c.head_regression && B == 1 &&
+         T >= 1 && c.n_layers >= 1 && c.n_layers <= PERSIST_MAX_LAYERS &&
+         persist_supported(m->d, c.head_dim, c.n_heads, c.n_kv_heads, c.d_ff, c.n_action, P, c.d_action,
+                           c.mlp != VLA_MLP_GELU, &kba, &nsplit);
+}
+
 vla_status build_plan(vla_model* m, Plan* p) {
   const vla_config& c = m->cfg;
   const int B = p->B, P = p->P, T = p->T;
@@ -451,6 +467,80 @@ vla_status build_plan(vla_model* m, Plan* p) {
     g.ldo = 2 * d;
     g.out_f32 = 1;
     bld.gemm(g, 1);
+  }
+
+  if (p->persist) {
+    PersistArgs pa{};
+    pa.L = L; pa.d = d; pa.H = c.n_heads; pa.G = c.n_kv_heads; pa.hd = hd; pa.F = F; pa.n = n; pa.P = P;
+    pa.A = A; pa.T = T;
+    pa.glu = c.mlp != VLA_MLP_GELU;
+    pa.act = mlp_act(c.mlp);
+    pa.HT = c.n_heads / 8;
+    if (!persist_supported(d, hd, c.n_heads, c.n_kv_heads, F, n, P, A, pa.glu, &pa.kba, &pa.nsplit))
+      return fail(VLA_E_UNSUPPORTED, "persistent kernel: unsupported shape");
+    pa.eps = c.rms_eps;
+    pa.scale = 1.0f / std::sqrt((float)hd);
+    const size_t layer_block = (size_t)2 * B * c.n_kv_heads * P * hd;
+    std::vector<PLayer> hl(L);
+    for (int l = 0; l < L; ++l) {
+      const std::vector<SubW>& subs = m->layers[l];
+      if (subs.size() != 2 || subs[0].kind != K_JOINT || subs[1].kind != K_MLP)
+        return fail(VLA_E_UNSUPPORTED, "persistent kernel: layer %d is not joint attention + MLP", l);
+      hl[l].wqkv = subs[0].qkv;
+      hl[l].wo = subs[0].o;
+      hl[l].wgu = subs[1].gu;
+      hl[l].wd = subs[1].dn;
+      hl[l].cache_off = (size_t)subs[0].cache_idx * layer_block;
+    }
+    PLayer* dl = nullptr;
+    VLA_TRY(al((void**)&dl, sizeof(PLayer) * L));
+    HIP_TRY(hipMemcpy(dl, hl.data(), sizeof(PLayer) * L, hipMemcpyHostToDevice));
+    pa.layers = dl;
+    pa.cp = cp;
+    pa.mods = p->mods;
+    pa.modf = p->modf;
+    pa.w_in = m->W_in;
+    pa.xs = p->xs;
+    pa.e_pos = m->E_pos;
+    pa.w_out = m->W_out;
+    pa.b_out = m->b_out;
+    pa.a0 = p->a;
+    const int HT = pa.HT;
+    VLA_TRY(al(&pa.u, (size_t)8 * n * d * 2));
+    VLA_TRY(al(&pa.qkv, (size_t)8 * n * (HT + 2) * hd * 2));
+    VLA_TRY(al(&pa.apart, (size_t)8 * pa.nsplit * n * HT * hd * 2));
+    VLA_TRY(al((void**)&pa.astat, (size_t)8 * pa.nsplit * n * HT * 2 * 4));
+    VLA_TRY(al(&pa.omerged, (size_t)8 * n * HT * hd * 2));
+    VLA_TRY(al(&pa.hbuf, (size_t)8 * n * (F / 8) * 2));
+    VLA_TRY(al((void**)&pa.delta, (size_t)2 * 8 * n * d * 4));
+    VLA_TRY(al((void**)&pa.sync, (size_t)PERSIST_SYNC_WORDS * 4));
+    VLA_TRY(al((void**)&pa.err, 16));
+    HIP_TRY(hipMemset(pa.err, 0, 16));
+    p->persist_err = pa.err;
+    VLA_TRY(al((void**)&p->trace, (size_t)8 * PERSIST_TRACE_MAX * 8));
+    pa.trace = nullptr;
+    const int* tracing = &m->trace;
+    unsigned long long* tbuf = p->trace;
+    // Per step and layer: the weights once, the cache once (algorithmic bytes).
+    double wbytes = 0.0;
+    for (int l = 0; l < L; ++l) {
+      const SubW& at = m->layers[l][0];
+      const SubW& ml = m->layers[l][1];
+      wbytes += ((double)at.n_qkv * d + (double)d * dq + (double)(pa.glu ? 2 : 1) * F * d + (double)d * F) * es;
+      (void)ml;
+    }
+    const double cbytes = (double)L * 2 * c.n_kv_heads * P * hd * es;
+    const double gflop = (double)T * (2.0 * n * wbytes / es + 4.0 * n * c.n_heads * hd * (P + n) * L);
+    bld.ops->push_back(Op{[=](hipStream_t s) {
+                            hipError_t e = launch_fill_u32(pa.sync, 0u, PERSIST_SYNC_WORDS, s);
+                            if (e != hipSuccess) return e;
+                            PersistArgs q = pa;
+                            q.trace = *tracing ? tbuf : nullptr;
+                            return launch_persist(q, s);
+                          },
+                          op_info(VLA_OP_PERSIST, n, L, T, (double)T * (wbytes + cbytes), gflop)});
+    HIP_TRY(hipDeviceSynchronize());
+    return VLA_OK;
   }
 
   // Residual projection (O or down) of a dense model: split-K partials summed
@@ -719,8 +809,13 @@ int32_t vla_weight_count(const vla_config* c) {
 vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
   if (!m) return fail(VLA_E_ARG, "model is NULL");
   if (option == VLA_OPT_LOOP_MODE) {
-    if (value < 0 || value > 1) return fail(VLA_E_ARG, "loop mode %d out of range", value);
+    if (value < 0 || value > 2) return fail(VLA_E_ARG, "loop mode %d out of range", value);
     m->loop_mode = value;
+    return VLA_OK;
+  }
+  if (option == VLA_OPT_TRACE) {
+    if (value < 0 || value > 1) return fail(VLA_E_ARG, "trace flag %d out of range", value);
+    m->trace = value;
     return VLA_OK;
   }
   if (option == VLA_OPT_PROFILE) {
@@ -1034,6 +1129,8 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
     if (q && !al16(q)) return fail(VLA_E_ARG, "device buffers must be 16-byte aligned");
   if (batch < 1 || prefix_len < 1) return fail(VLA_E_SHAPE, "batch and prefix_len must be >= 1");
   if ((long long)batch * c.n_action > 65536) return fail(VLA_E_UNSUPPORTED, "batch * n_action too large");
+  if ((prefix_len + 31) / 32 + (c.n_action + 31) / 32 > attention_max_blocks())
+    return fail(VLA_E_UNSUPPORTED, "prefix_len + n_action beyond %d keys", 32 * attention_max_blocks() - 32);
   if (n_steps < 1 || n_steps > VLA_MAX_STEPS) return fail(VLA_E_SHAPE, "n_steps %d not in 1..%d", n_steps, VLA_MAX_STEPS);
   if (c.head_regression && n_steps != 1) return fail(VLA_E_SHAPE, "the regression head takes n_steps == 1");
   if (kv_cache_bytes != vla_kv_cache_bytes(m, batch, prefix_len))
@@ -1051,18 +1148,21 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
   cpv.act_mean = act_mean;
   cpv.act_std = act_std;
 
-  auto key = std::make_tuple(batch, prefix_len, n_steps);
+  const bool persist = m->loop_mode == 2 && persist_eligible(m, batch, prefix_len, n_steps);
+  auto key = std::make_tuple(batch, prefix_len, n_steps, (int)persist);
   auto it = m->plans.find(key);
   Plan* p;
   if (it == m->plans.end()) {
     if (m->plans.size() >= 8) {
       if (m->last_profiled == m->plans.begin()->second.get()) m->last_profiled = nullptr;
+      if (m->last_traced == m->plans.begin()->second.get()) m->last_traced = nullptr;
       m->plans.erase(m->plans.begin());
     }
     std::unique_ptr<Plan> np(new Plan());
     np->B = batch;
     np->P = prefix_len;
     np->T = n_steps;
+    np->persist = persist;
     VLA_TRY(build_plan(m, np.get()));
     p = np.get();
     m->plans[key] = std::move(np);
@@ -1071,11 +1171,12 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
   }
   hipStream_t s = reinterpret_cast<hipStream_t>(stream);
   HIP_TRY(launch_set_params(p->cp, cpv, s));
+  if (p->persist && m->trace) m->last_traced = p;
   if (m->profile) {
     VLA_TRY(run_ops_profiled(p, s, m->profile));
     m->last_profiled = p;
     p->prof_reps = m->profile;
-  } else if (m->loop_mode == 0) {
+  } else if (m->loop_mode == 0 || p->persist) {
     VLA_TRY(run_ops(p->ops, s));
   } else {
     if (!p->exec) {
@@ -1108,6 +1209,11 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
     (void)hipFree(flag);
     if (e != hipSuccess) return fail(VLA_E_DEVICE, "hipStreamSynchronize: %s", hipGetErrorString(e));
     if (h) return fail(VLA_E_NONFINITE, "non-finite value in the action chunk");
+    if (p->persist_err) {
+      int perr = 0;
+      if (hipMemcpy(&perr, p->persist_err, 4, hipMemcpyDeviceToHost) == hipSuccess && perr)
+        return fail(VLA_E_DEVICE, "persistent kernel: a barrier timed out");
+    }
   }
   return VLA_OK;
 }
@@ -1162,6 +1268,20 @@ int32_t vla_profile_read(vla_model* m, vla_op_time* out, int32_t max_ops) {
 
 // ---- test entries ----------------------------------------------------------
 
+int32_t vla_test_persist_trace(vla_model* m, uint64_t* out, int32_t max_per_team) {
+  if (!m || !m->last_traced) return -1;
+  Plan* p = static_cast<Plan*>(m->last_traced);
+  if (!p->trace || max_per_team < 0) return -1;
+  if (hipDeviceSynchronize() != hipSuccess) return -1;
+  const int n = std::min(max_per_team, PERSIST_TRACE_MAX);
+  if (out)
+    for (int t = 0; t < 8; ++t)
+      if (hipMemcpy(out + (size_t)t * n, p->trace + (size_t)t * PERSIST_TRACE_MAX, (size_t)n * 8,
+                    hipMemcpyDeviceToHost) != hipSuccess)
+        return -1;
+  return n;
+}
+
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                          int32_t variant, float* y, void* stream) {
   if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
@@ -1197,6 +1317,8 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
   a.q = q; a.ldq = H * hd; a.ks = k_self; a.vs = v_self; a.ldkv = G * hd;
   a.kc = k_cache; a.vc = v_cache; a.o = o; a.ldo = H * hd; a.scale = 1.0f / std::sqrt((float)hd);
   if (H / G > 8 || H > 32) return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head");
+  if ((a.P + 31) / 32 + (mode == 1 ? 0 : (n + 31) / 32) > attention_max_blocks())
+    return fail(VLA_E_UNSUPPORTED, "too many keys");
   attention_split(a, kv_split);
   const int et = elem ? ET_BF16 : ET_F32;
   void* part = nullptr;

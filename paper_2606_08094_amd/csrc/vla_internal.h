@@ -41,6 +41,7 @@ struct GemmArgs {
   const void* W;           // [N][K] row-major in the element type
   int n_tiles;             // tiles along N (set by the launcher)
   int nsplit;              // K-splits (set by the launcher; > 1 only with EPI_PARTIAL)
+  int kper;                // K-range of one split (skinny kernel; set by the launcher)
   // epilogue
   int epi;
   int act;
@@ -130,13 +131,57 @@ struct TernArgs {
 
 // Launch shapes of the two dense GEMM kernels (chosen on the host).
 struct SkinnyShape {
-  int ms, nsub, cpw, nsplit, n_tiles, m_tiles, units;
+  int ms, nsub, cpw, nsplit, kper, n_tiles, m_tiles, units;
   size_t lds;
 };
 struct WideShape {
   int ms, nsub, nc, n_tiles, m_tiles, units;
   size_t lds;
 };
+
+// Persistent tensor-parallel denoise loop (bf16, joint attention, batch 1):
+// weights of one layer, library-owned.
+struct PLayer {
+  const void* wqkv;          // [d_q + 2 d_kv][d]
+  const void* wo;            // [d][d_q]
+  const void* wgu;           // GLU: gate/up interleaved in 16-row blocks [2F][d]; GELU: W1 [F][d]
+  const void* wd;            // [d][F]
+  size_t cache_off;          // element offset of this layer's K block in the cache
+};
+
+struct PersistArgs {
+  int L, d, H, G, hd, F, n, P, A, T;
+  int glu, act;              // MLP form: gate/up pair (1) or single W1 (0); activation
+  int HT;                    // query heads per team (H / 8)
+  int kba, nsplit;           // attention: 32-key blocks per split, key splits
+  float eps, scale;
+  const PLayer* layers;      // [L] (device)
+  const CallParams* cp;
+  const float* mods;         // [T][L * 2 * 3 * d]: per sublayer gamma, beta, alpha
+  const float* modf;         // [T][2 d]: final gamma, beta
+  const void* w_in;          // [d][A]
+  const float* xs;           // [d]: b_in + b_s + state W_s^T
+  const void* e_pos;         // [n][d]
+  const void* w_out;         // [A][d]
+  const float* b_out;        // [A]
+  const float* a0;           // [n][A]: the noise chunk a_0
+  // team-replicated workspace (team = one of 8 groups of 32 workgroups)
+  void* u;                   // [8][n][d]
+  void* qkv;                 // [8][n][(HT + 2) hd]: team heads' Q, the team's K, V
+  void* apart;               // [8][nsplit][n][HT hd]
+  float* astat;              // [8][nsplit][n][HT][2]
+  void* omerged;             // [8][n][HT hd]: merged attention output of the team's heads
+  void* hbuf;                // [8][n][F / 8]
+  float* delta;              // [2][8][n][d]: per-team partial residual updates
+  unsigned* sync;            // PERSIST_SYNC_WORDS counters, zero at launch
+  int* err;                  // set when a barrier times out
+  // optional phase timeline: workgroup 0 of each team records the 100 MHz
+  // clock before and after every barrier, PERSIST_TRACE_MAX entries per team
+  unsigned long long* trace;
+};
+constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 8 * 32 + 64;
+constexpr int PERSIST_TRACE_MAX = 8192;
+constexpr int PERSIST_MAX_LAYERS = 64;
 
 // ---- launchers (each enqueues on `s`, returns hipError_t) ----
 int gemm_chunk_k(int et);  // K covered by one chunk (all 4 lane groups of a wave)
@@ -148,7 +193,8 @@ hipError_t launch_gemm_wide(int et, const WideShape& sh, GemmArgs a, hipStream_t
 // which: 0 = key-split kernel and (when kv_split > 1) the merge, 1 = the
 // key-split kernel only, 2 = the merge only.
 hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which = 0);
-void attention_split(AttnArgs& a, int want_splits);                      // 0 = about 96 workgroups
+void attention_split(AttnArgs& a, int want_splits);  // want_splits 0 = about 112 workgroups
+int attention_max_blocks();  // most 32-key blocks (prefix blocks + action blocks) one call handles
 size_t attention_part_bytes(int et, const AttnArgs& a);
 size_t attention_stats_bytes(const AttnArgs& a);
 
@@ -163,3 +209,8 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s);
 hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
 hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);
+// Persistent kernel: whether a shape is supported, the dynamic LDS it needs,
+// and the cooperative launch (256 workgroups of 512 threads).
+bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, int glu, int* kba, int* nsplit);
+size_t persist_lds_bytes(int hd, int HT);
+hipError_t launch_persist(const PersistArgs& a, hipStream_t s);

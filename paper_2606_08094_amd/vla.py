@@ -22,14 +22,17 @@ STATUS = {0: "VLA_OK", 1: "VLA_E_ARG", 2: "VLA_E_SHAPE", 3: "VLA_E_UNSUPPORTED",
           5: "VLA_E_DEVICE", 6: "VLA_E_NONFINITE"}
 VLA_OPT_LOOP_MODE = 0
 VLA_OPT_PROFILE = 1
+VLA_OPT_TRACE = 2
+PERSIST_TRACE_MAX = 8192
 OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
-            6: "attn_merge"}
+            6: "attn_merge", 7: "persist"}
 
 # Every symbol the headers declare.
 EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_cache_bytes",
            "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
-           "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear"]
+           "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
+           "vla_test_persist_trace"]
 
 
 class VlaError(RuntimeError):
@@ -78,6 +81,7 @@ def lib():
         "vla_test_attention": (i32, [i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]),
         "vla_test_quantize_i8": (i32, [vp, i32, i32, vp, vp, vp]),
         "vla_test_ternary_linear": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp]),
+        "vla_test_persist_trace": (i32, [vp, ctypes.POINTER(ctypes.c_uint64), i32]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -188,6 +192,19 @@ class Model:
         """0 = off; R >= 1 = time each launch of the next denoise calls as the
         mean of R back-to-back repetitions (R > 1 is for timing only)."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_PROFILE, int(reps)))
+
+    def set_trace(self, on: bool):
+        """Record the persistent kernel's phase timeline on the next calls."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_TRACE, int(bool(on))))
+
+    def trace_read(self):
+        """[8][PERSIST_TRACE_MAX] uint64 clock values (100 MHz) of the last
+        traced persistent call, or None."""
+        import numpy as np
+        out = np.zeros((8, PERSIST_TRACE_MAX), np.uint64)
+        n = lib().vla_test_persist_trace(self.handle, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
+                                         PERSIST_TRACE_MAX)
+        return None if n < 0 else out
 
     def profile_read(self) -> List[dict]:
         """Per-launch timings of the last profiled denoise call."""

@@ -1,0 +1,109 @@
+"""Parity of the persistent step-loop driver (loop mode 2: one cooperative
+kernel runs every solver step) against the fp64 oracle, against the
+launch-per-phase graph driver, and run-to-run determinism.
+
+The driver covers batch-1 bf16 experts with joint attention whose shape fits
+its team layout (8 teams of 32 workgroups: query heads and MLP columns split
+over the teams).  Cases span one and two heads per team, grouped K/V heads,
+GeGLU / SwiGLU / GELU MLPs, ragged prefix and chunk lengths (prefix blocks and
+chunk blocks with partial 32-key tails, 16-row query tiles with a ragged last
+tile) and T = 1 .. 10.  Tolerance on the final chunk: max|d| <= 2e-2 (bf16).
+"""
+import numpy as np
+import pytest
+
+import workloads as wl
+from oracle import vla_oracle as O
+
+pytestmark = pytest.mark.gpu
+
+TOL = 2e-2
+
+SMALL = wl.PI0_BF16.with_(name="pi0_small", n_layers=2, d_model=512, head_dim=64, d_ff=2048, d_prefix=512,
+                          prefix_len=100, n_steps=3, seed_base=6000)
+
+CASES = {
+    "small_geglu": SMALL,
+    "small_gelu_ragged": SMALL.with_(name="small_gelu", mlp="gelu", n_action=20, prefix_len=37, n_steps=4,
+                                     seed_base=6100),
+    "two_heads_per_team_swiglu": SMALL.with_(name="h16", n_heads=16, n_kv_heads=2, mlp="swiglu", n_action=9,
+                                             prefix_len=70, d_action=7, d_state=7, n_steps=2, seed_base=6200),
+    "d1024_hd128_t1": SMALL.with_(name="d1024", d_model=1024, head_dim=128, d_ff=4096, d_prefix=1024,
+                                  n_action=33, prefix_len=129, n_steps=1, seed_base=6300),
+}
+
+
+@pytest.fixture(scope="module")
+def torch():
+    import torch as t
+    if not t.cuda.is_available():
+        pytest.skip("no GPU")
+    return t
+
+
+def _run(cfg, W, inp, tau, loop_mode, reps=1):
+    from vla_testlib import Pipeline
+    pipe = Pipeline(cfg, W, inp, loop_mode)
+    import torch
+    try:
+        pipe.build_cache()
+        outs = []
+        for _ in range(reps):
+            out = pipe.denoise(tau)
+            torch.cuda.synchronize()
+            outs.append(out.cpu().numpy().astype(np.float64).copy())
+        return outs
+    finally:
+        pipe.close()
+
+
+@pytest.mark.parametrize("case", sorted(CASES))
+def test_persist_matches_oracle_and_graph(torch, case):
+    cfg = CASES[case]
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+    ref = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+    got = _run(cfg, W, inp, tau, loop_mode=2, reps=2)
+    graph = _run(cfg, W, inp, tau, loop_mode=1)[0]
+    err = np.abs(got[0] - ref).max()
+    dg = np.abs(got[0] - graph).max()
+    print(f"{case}: persistent vs oracle max|d| = {err:.3e}, vs graph driver {dg:.3e}")
+    assert np.all(np.isfinite(got[0]))
+    assert err <= TOL, f"{case}: max|d| {err}"
+    assert dg <= TOL
+    assert np.array_equal(got[0], got[1]), "persistent driver is not deterministic"
+
+
+def test_persist_pi0_full(torch):
+    """The full pi0-shaped workload (18 layers, 816 prefix rows, T = 10) with
+    denormalisation statistics."""
+    from vla_testlib import Pipeline, to_device, workload
+    cfg, W, inp = workload("pi0_bf16", 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    mean = np.linspace(-0.5, 0.5, cfg.d_action).astype(np.float32)
+    std = np.linspace(0.5, 2.0, cfg.d_action).astype(np.float32)
+    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+    ref = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau, mean, std)
+    pipe = Pipeline(cfg, W, inp, loop_mode=2)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau, to_device(mean), to_device(std)).cpu().numpy().astype(np.float64)
+    finally:
+        pipe.close()
+    err = np.abs(got - ref).max()
+    print(f"pi0_bf16 persistent: max|d| = {err:.3e}")
+    assert err <= TOL
+
+
+def test_ineligible_model_falls_back(torch):
+    """Loop mode 2 on a model the persistent kernel does not cover (fp32,
+    self + cross attention) runs the graph driver: identical output."""
+    cfg = wl.TINY_F32
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 2)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    a = _run(cfg, W, inp, tau, loop_mode=2)[0]
+    b = _run(cfg, W, inp, tau, loop_mode=1)[0]
+    assert np.array_equal(a, b)
