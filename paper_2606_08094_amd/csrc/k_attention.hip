@@ -57,16 +57,19 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int nthr = blockDim.x;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int per = a.H / a.G;          // query heads per K/V head (= waves)
+  const int per = a.H / a.G;          // query heads per K/V head
+  const int hpw = per / a.hsplit;     // of them in this workgroup (= waves)
   const int QT = (a.n + 15) / 16;
   int u = blockIdx.x;
   const int split = u % a.kv_split;
   u /= a.kv_split;
+  const int hs = u % a.hsplit;
+  u /= a.hsplit;
   const int g = u % a.G;
   u /= a.G;
   const int qt = u % QT;
   const int b = u / QT;
-  const int h = g * per + wave;
+  const int h = g * per + hs * hpw + wave;
 
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
@@ -236,21 +239,25 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   // Lane holds O^T[dim = 16d + 4*g4 + i][query r16].
   if (qrow >= a.n) return;
   const float inv = lrun > 0.0f ? 1.0f / lrun : 0.0f;
+  // the lane's 4 consecutive dims of each 16-dim tile go out as one store
+  auto put4 = [&](T* dst, const f32x4& v) {
+    if constexpr (E == 8) {
+      *reinterpret_cast<uint2*>(dst) = make_uint2(pack_bf16x2(v[0] * inv, v[1] * inv), pack_bf16x2(v[2] * inv, v[3] * inv));
+    } else {
+      *reinterpret_cast<float4*>(dst) = make_float4(v[0] * inv, v[1] * inv, v[2] * inv, v[3] * inv);
+    }
+  };
   if (a.kv_split == 1) {
     T* op = reinterpret_cast<T*>(a.o) + (size_t)(b * a.n + qrow) * a.ldo + h * HD;
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) op[d * 16 + 4 * g4 + i] = ElemTraits<T>::from_f(o[d][i] * inv);
+    for (int d = 0; d < DT; ++d) put4(op + d * 16 + 4 * g4, o[d]);
     return;
   }
   // partial: normalised by its own sum, plus (max, sum)
   const int rows = a.B * a.n, dq = a.H * HD;
   T* pp = reinterpret_cast<T*>(a.part) + ((size_t)split * rows + b * a.n + qrow) * dq + h * HD;
 #pragma unroll
-  for (int d = 0; d < DT; ++d)
-#pragma unroll
-    for (int i = 0; i < 4; ++i) pp[d * 16 + 4 * g4 + i] = ElemTraits<T>::from_f(o[d][i] * inv);
+  for (int d = 0; d < DT; ++d) put4(pp + d * 16 + 4 * g4, o[d]);
   if (g4 == 0) {
     float* st = a.stats + (((size_t)split * rows + b * a.n + qrow) * a.H + h) * 2;
     st[0] = mrun;
@@ -312,7 +319,7 @@ __global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
 template <typename T, int HD>
 hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
   const int QT = (a.n + 15) / 16;
-  const int units = a.B * QT * a.G * a.kv_split;
+  const int units = a.B * QT * a.G * a.hsplit * a.kv_split;
   if (units <= 0) return hipSuccess;
   static bool attr = false;
   if (!attr) {
@@ -321,7 +328,8 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
     if (e != hipSuccess) return e;
     attr = true;
   }
-  const int threads = 64 * (a.H / a.G);
+  if (a.hsplit < 1 || (a.H / a.G) % a.hsplit) return hipErrorInvalidValue;
+  const int threads = 64 * (a.H / a.G / a.hsplit);
   using L = AttnLds<T, HD>;
   if (a.key_chunk < 1 || a.key_chunk > KB_MAX) return hipErrorInvalidValue;
   const size_t lds = (size_t)a.key_chunk * L::BUF;
@@ -341,14 +349,28 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
 
 // Keys per split in 32-key blocks (at most KB_MAX), the number of splits, and
 // the workspace.  By default the splits target about 112 workgroups.
-void attention_split(AttnArgs& a, int want_splits) {
+void attention_split(AttnArgs& a, int want_splits, int want_hsplit) {
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
   const int nblocks = (npre + 31) / 32 + (nself + 31) / 32;
   const int QT = (a.n + 15) / 16;
+  const int per = a.H / a.G;
+  // Heads per workgroup: each workgroup reads Q and writes O of its heads for
+  // its query tile once per key split, so large groups are split until each
+  // workgroup holds at most 4 heads.
+  int hs = want_hsplit;
+  if (hs <= 0) {
+    hs = 1;
+    while (per / hs > 4 && per % (2 * hs) == 0) hs *= 2;
+  }
+  if (hs < 1 || per % hs) hs = 1;
+  a.hsplit = hs;
   int s = want_splits;
   if (s <= 0) {
-    const int base = a.B * QT * a.G;
+    // About 112 workgroups: the merge reads every split's partial output, so
+    // past half the chip more splits cost the merge more than they save in
+    // the key loop (pi0 shape: 14 splits beat 28 by 0.5 us per layer).
+    const int base = a.B * QT * a.G * hs;
     s = (112 + base - 1) / base;
   }
   s = s < 1 ? 1 : (s > nblocks ? nblocks : s);

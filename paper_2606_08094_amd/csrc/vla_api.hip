@@ -137,6 +137,7 @@ struct vla_model {
   int loop_mode = 1;
   int profile = 0;
   int trace = 0;                  // record the persistent kernel's phase timeline
+  int attn_splits = 0;            // key splits of the launch-per-phase attention (0 = automatic)
   void* last_profiled = nullptr;  // Plan* of the last profiled call
   void* last_traced = nullptr;    // Plan* of the last traced call
   hipStream_t cap_stream = nullptr;
@@ -311,7 +312,7 @@ struct Builder {
     const int QT = cdiv(a.n, 16);
     const int total = (a.mode == 0 ? 0 : a.P) + (a.mode == 1 ? 0 : a.n);
     (void)QT;
-    attention_split(a, 0);
+    attention_split(a, m->attn_splits % 100, m->attn_splits / 100);
     const int et = m->et;
     part_need = std::max(part_need, attention_part_bytes(et, a));
     stats_need = std::max(stats_need, attention_stats_bytes(a));
@@ -811,6 +812,17 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
   if (option == VLA_OPT_LOOP_MODE) {
     if (value < 0 || value > 2) return fail(VLA_E_ARG, "loop mode %d out of range", value);
     m->loop_mode = value;
+    return VLA_OK;
+  }
+  if (option == VLA_OPT_ATTN_SPLITS) {
+    if (value < 0 || value % 100 > 64 || value / 100 > 8)
+      return fail(VLA_E_ARG, "attention splits %d out of range", value);
+    if (value != m->attn_splits) {
+      m->plans.clear();            // plans bake the split count in
+      m->last_profiled = nullptr;
+      m->last_traced = nullptr;
+    }
+    m->attn_splits = value;
     return VLA_OK;
   }
   if (option == VLA_OPT_TRACE) {
@@ -1319,7 +1331,7 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
   if (H / G > 8 || H > 32) return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head");
   if ((a.P + 31) / 32 + (mode == 1 ? 0 : (n + 31) / 32) > attention_max_blocks())
     return fail(VLA_E_UNSUPPORTED, "too many keys");
-  attention_split(a, kv_split);
+  attention_split(a, kv_split % 100, kv_split / 100);
   const int et = elem ? ET_BF16 : ET_F32;
   void* part = nullptr;
   float* stats = nullptr;

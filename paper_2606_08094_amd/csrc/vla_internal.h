@@ -80,6 +80,7 @@ struct AttnArgs {
   int ldo;
   float scale;
   int kv_split;            // key splits
+  int hsplit;              // groups of query heads per K/V head (workgroups per group)
   int key_chunk;           // 32-key blocks per split
   void* part;              // [kv_split][B*n][H*hd] per-split output (kv_split > 1)
   float* stats;            // [kv_split][B*n][H][2] per-split (max, sum)
@@ -193,7 +194,9 @@ hipError_t launch_gemm_wide(int et, const WideShape& sh, GemmArgs a, hipStream_t
 // which: 0 = key-split kernel and (when kv_split > 1) the merge, 1 = the
 // key-split kernel only, 2 = the merge only.
 hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which = 0);
-void attention_split(AttnArgs& a, int want_splits);  // want_splits 0 = about 112 workgroups
+// want_splits / want_hsplit 0 = automatic (at most 4 heads per workgroup,
+// about 224 workgroups)
+void attention_split(AttnArgs& a, int want_splits, int want_hsplit = 0);
 int attention_max_blocks();  // most 32-key blocks (prefix blocks + action blocks) one call handles
 size_t attention_part_bytes(int et, const AttnArgs& a);
 size_t attention_stats_bytes(const AttnArgs& a);

@@ -23,6 +23,7 @@ STATUS = {0: "VLA_OK", 1: "VLA_E_ARG", 2: "VLA_E_SHAPE", 3: "VLA_E_UNSUPPORTED",
 VLA_OPT_LOOP_MODE = 0
 VLA_OPT_PROFILE = 1
 VLA_OPT_TRACE = 2
+VLA_OPT_ATTN_SPLITS = 3
 PERSIST_TRACE_MAX = 8192
 OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
             6: "attn_merge", 7: "persist"}
@@ -192,6 +193,10 @@ class Model:
         """0 = off; R >= 1 = time each launch of the next denoise calls as the
         mean of R back-to-back repetitions (R > 1 is for timing only)."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_PROFILE, int(reps)))
+
+    def set_attn_splits(self, splits: int):
+        """Key splits of the launch-per-phase attention (0 = automatic)."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_ATTN_SPLITS, int(splits)))
 
     def set_trace(self, on: bool):
         """Record the persistent kernel's phase timeline on the next calls."""

@@ -82,9 +82,12 @@ ATTN_CASES = [
 
 
 @pytest.mark.parametrize("case", ATTN_CASES, ids=[str(c) for c in ATTN_CASES])
-@pytest.mark.parametrize("kv_split", [0, 1, 3])
+@pytest.mark.parametrize("kv_split", [0, 1, 3, 201, 403, 800])
 def test_attention_parity(torch, case, kv_split):
+    """kv_split: key splits (% 100) and query-head groups per K/V head (// 100)."""
     elem, mode, B, n, P, H, G, hd = case
+    if kv_split // 100 and (H // G) % (kv_split // 100):
+        pytest.skip("head groups must divide the heads per K/V head")
     bf = elem == 1
     s = 7 * n + P + H + hd + mode
     q = wl.random_matrix((B * n, H * hd), s, 1.0, bf16=bf)
