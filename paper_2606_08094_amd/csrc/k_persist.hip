@@ -3,9 +3,10 @@
 // sublayer of vla_denoise (Algorithm 1's loop), with no kernel boundary inside.
 //
 // The 256 workgroups (4 waves each: one wave per SIMD, so a wave may hold up to
-// 512 registers of prefetched operands) form 8 teams of 32 (team = blockIdx %
-// 8; the dispatcher places those on one XCD each, so a team's traffic stays in
-// that XCD's L2).  Team x owns query heads [x*HT, (x+1)*HT) and MLP columns
+// 512 registers of prefetched operands) form 8 teams of 32: a team is the set
+// of workgroups running on one XCD (read from the hardware XCC id at start, so
+// the grouping does not rely on the dispatch order) and its traffic stays in
+// that XCD's L2.  Team x owns query heads [x*HT, (x+1)*HT) and MLP columns
 // [x*F/8, (x+1)*F/8); it recomputes the K/V head its queries share.  Per layer:
 //   Q  team GEMM u -> [q of the team's heads | k | v]          team barrier
 //   A  attention over [prefix ; chunk] in key splits           team barrier
@@ -22,12 +23,12 @@
 // depend on the step's activations: a workgroup issues their loads before it
 // waits at the barrier that precedes the phase using them.
 //
-// Memory model: data that one workgroup writes and another reads moves through
-// device-coherent (sc1) buffer stores and loads, so no L2 write-back or
-// invalidate is needed and correctness does not depend on where workgroups are
-// placed.  Barriers are relaxed agent-scope counters; every wait is bounded,
-// and a timeout sets *err, writes NaN into the chunk and makes every
-// workgroup leave.
+// Memory model: data that one workgroup writes and another reads is stored
+// with plain (write-through) stores and read with device-coherent (sc1) buffer
+// loads; the residual deltas, which cross XCDs, are also stored with sc1.  No
+// L2 write-back or invalidate is needed.  Barriers are relaxed agent-scope
+// counters; every wait is bounded, and a timeout sets *err, writes NaN into
+// the chunk and makes every workgroup leave.
 #include "device_common.h"
 
 namespace {
@@ -38,7 +39,9 @@ typedef __amdgpu_buffer_rsrc_t rsrc_t;
 
 constexpr int NTEAM = 8, TSIZE = 32, NWG = NTEAM * TSIZE;
 constexpr int NW = 4, NTHR = 64 * NW;    // waves and threads of a workgroup
-constexpr int SC1 = 16;                  // buffer cache policy: device-coherent
+constexpr int LDX = 16;                  // loads of exchanged data: device-coherent (sc1)
+constexpr int STL = 0;                   // stores of exchanged data: plain (write through to L2)
+constexpr int SC1 = 16;                  // device-coherent policy of the cross-team deltas
 constexpr int KBA_MAX = 2;               // 32-key blocks per attention split
 constexpr long SPIN_LIMIT = 1L << 21;
 constexpr float kLog2e = 1.4426950408889634f;
@@ -48,25 +51,40 @@ constexpr float kLog2e = 1.4426950408889634f;
 VLA_DEV rsrc_t mkr(const void* base, size_t bytes) {
   return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, (int)bytes, 0x00020000);
 }
-VLA_DEV uint4 ldc16(rsrc_t r, unsigned off) {
-  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, SC1);
+// Cache policies of exchanged data.  Stores are plain: the L1 writes through,
+// so after a store completes its data is in the writer XCD's L2.  Loads of
+// data another workgroup wrote are device-coherent (sc1): they miss the CU's
+// L1, which may hold a stale copy from an earlier layer.  (L2-coherent sc0
+// loads still hit stale L1 lines here, even after an L1 invalidate.)  The
+// residual deltas cross XCDs and are written with sc1 stores.
+template <int POL>
+VLA_DEV uint4 ld16(rsrc_t r, unsigned off) {
+  const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(r, (int)off, 0, POL);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
 VLA_DEV uint4 bld16(rsrc_t r, unsigned voff, unsigned soff, int coherent) {
-  const u32x4_t v = coherent ? __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, SC1)
+  const u32x4_t v = coherent ? __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, LDX)
                              : __builtin_amdgcn_raw_buffer_load_b128(r, (int)voff, (int)soff, 0);
   return make_uint4(v.x, v.y, v.z, v.w);
 }
-VLA_DEV float2 ldc8f(rsrc_t r, unsigned off) {
-  const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, SC1);
+template <int POL>
+VLA_DEV float2 ld8f(rsrc_t r, unsigned off) {
+  const u32x2_t v = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, POL);
   return make_float2(__uint_as_float(v.x), __uint_as_float(v.y));
 }
-VLA_DEV void stc8(rsrc_t r, unsigned off, unsigned lo, unsigned hi) {
-  __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{lo, hi}, r, (int)off, 0, SC1);
+template <int POL>
+VLA_DEV void st8(rsrc_t r, unsigned off, unsigned lo, unsigned hi) {
+  __builtin_amdgcn_raw_buffer_store_b64(u32x2_t{lo, hi}, r, (int)off, 0, POL);
 }
-VLA_DEV void stc4(rsrc_t r, unsigned off, unsigned v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, SC1); }
-VLA_DEV void stc2(rsrc_t r, unsigned off, unsigned short v) {
-  __builtin_amdgcn_raw_buffer_store_b16(v, r, (int)off, 0, SC1);
+template <int POL>
+VLA_DEV void st4(rsrc_t r, unsigned off, unsigned v) { __builtin_amdgcn_raw_buffer_store_b32(v, r, (int)off, 0, POL); }
+VLA_DEV void st2(rsrc_t r, unsigned off, unsigned short v) { __builtin_amdgcn_raw_buffer_store_b16(v, r, (int)off, 0, STL); }
+
+// Hardware id of the XCD (accelerator complex die) this wave runs on.
+VLA_DEV unsigned xcc_id() {
+  unsigned v;
+  asm volatile("s_getreg_b32 %0, hwreg(HW_REG_XCC_ID)" : "=s"(v));
+  return v & 0xfu;
 }
 
 // ---------------------------------------------------------------------------
@@ -105,9 +123,22 @@ VLA_DEV void team_arrive(Sync& s, int team) {
   if (threadIdx.x == 0) __hip_atomic_fetch_add(s.tcnt + team * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
+// First poll of a barrier counter, issued right after the arrival and before
+// the next phase's prefetch loads: the wait for its value does not also wait
+// for those loads (loads complete in order).
+VLA_DEV unsigned team_peek(const Sync& s, int team) {
+  return threadIdx.x == 0 ? __hip_atomic_load(s.tcnt + team * 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+}
+VLA_DEV unsigned grid_peek(const Sync& s) {
+  return threadIdx.x == 0 ? __hip_atomic_load(s.glob, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+}
+
 // Returns false (in every thread) if the run must stop.
-VLA_DEV bool team_wait(Sync& s, int team, int* lds_flag) {
-  if (threadIdx.x == 0) *lds_flag = spin_until(s.tcnt + team * 32, s.tk * TSIZE, s.err) ? 1 : 0;
+VLA_DEV bool team_wait(Sync& s, int team, int* lds_flag, unsigned peek = 0u) {
+  if (threadIdx.x == 0) {
+    const unsigned target = s.tk * TSIZE;
+    *lds_flag = (peek >= target || spin_until(s.tcnt + team * 32, target, s.err)) ? 1 : 0;
+  }
   __syncthreads();
   return *lds_flag != 0;
 }
@@ -122,8 +153,11 @@ VLA_DEV void grid_arrive(Sync& s, int team) {
   }
 }
 
-VLA_DEV bool grid_wait(Sync& s, int* lds_flag) {
-  if (threadIdx.x == 0) *lds_flag = spin_until(s.glob, s.gk * NTEAM, s.err) ? 1 : 0;
+VLA_DEV bool grid_wait(Sync& s, int* lds_flag, unsigned peek = 0u) {
+  if (threadIdx.x == 0) {
+    const unsigned target = s.gk * NTEAM;
+    *lds_flag = (peek >= target || spin_until(s.glob, target, s.err)) ? 1 : 0;
+  }
   __syncthreads();
   return *lds_flag != 0;
 }
@@ -243,7 +277,22 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int team = blockIdx.x % NTEAM, rank = blockIdx.x / NTEAM;
+  // Team = the XCD this workgroup runs on, rank = its arrival order there, so
+  // the team-local exchange through the XCD's L2 is coherent whatever order
+  // the dispatcher used.  A team with more than 32 members (a part or mode
+  // without 8 XCDs of 32 CUs) stops the run through the error flag.
+  __shared__ int s_team, s_rank;
+  if (tid == 0) {
+    const unsigned x = xcc_id();
+    s_team = (int)(x % NTEAM);
+    s_rank = (int)__hip_atomic_fetch_add(a.sync + PERSIST_RANK_OFF + (x % NTEAM), 1u, __ATOMIC_RELAXED,
+                                         __HIP_MEMORY_SCOPE_AGENT);
+    if (s_rank >= TSIZE || x >= (unsigned)NTEAM)
+      __hip_atomic_fetch_or(a.err, 2, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  }
+  __syncthreads();
+  if (s_rank >= TSIZE) return;
+  const int team = s_team, rank = s_rank;
   const int n = a.n, d = a.d, HT = a.HT, A = a.A;
   const int HTD = HT * HD, QW = (HT + 2) * HD, F8 = a.F / 8, S = a.nsplit;
   const int QT = (n + 15) / 16;
@@ -304,110 +353,116 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
     }
     __syncthreads();
   };
+  // Row-phase loads are branch-free: an absent row gets an offset past the
+  // end of its buffer resource (the load returns zero), so every load of a
+  // helper is issued before the first wait.
+  const int c0 = tid * DPT;                // this thread's residual columns
+  constexpr unsigned OOB = 0x7ffffff0u;
+  auto ldf = [&](float (&v)[DPT], const float* src) {   // DPT contiguous fp32
+    if constexpr (DPT == 4) {
+      const float4 t = *reinterpret_cast<const float4*>(src);
+      v[0] = t.x; v[1] = t.y; v[2] = t.z; v[3] = t.w;
+    } else {
+      const float2 t = *reinterpret_cast<const float2*>(src);
+      v[0] = t.x; v[1] = t.y;
+    }
+  };
+  auto ldbf = [&](float (&v)[DPT], rsrc_t r, unsigned off) {   // DPT contiguous bf16
+    if constexpr (DPT == 4) {
+      const u32x2_t t = __builtin_amdgcn_raw_buffer_load_b64(r, (int)off, 0, 0);
+      v[0] = __uint_as_float(t.x << 16); v[1] = __uint_as_float(t.x & 0xffff0000u);
+      v[2] = __uint_as_float(t.y << 16); v[3] = __uint_as_float(t.y & 0xffff0000u);
+    } else {
+      const unsigned t = __builtin_amdgcn_raw_buffer_load_b32(r, (int)off, 0, 0);
+      v[0] = __uint_as_float(t << 16); v[1] = __uint_as_float(t & 0xffff0000u);
+    }
+  };
   // adaRMS of both rows with (g, b); u (bf16) to the team's U
   auto norm_store = [&](const float* g, const float* b) {
+    float gg[DPT], bb[DPT];
+    ldf(gg, g + c0);
+    ldf(bb, b + c0);
     float ss[2] = {0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < 2; ++r)
 #pragma unroll
       for (int e = 0; e < DPT; ++e) ss[r] += xr[r][e] * xr[r][e];
-    const int c = tid * DPT;
-    float gg[DPT], bb[DPT];
-#pragma unroll
-    for (int e = 0; e < DPT; ++e) {
-      gg[e] = g[c + e];
-      bb[e] = b[c + e];
-    }
     float t0, t1;
     sum2(ss[0], ss[1], t0, t1);
     const float rs[2] = {1.0f / sqrtf(t0 / (float)d + a.eps), 1.0f / sqrtf(t1 / (float)d + a.eps)};
 #pragma unroll
     for (int r = 0; r < 2; ++r) {
-      if (!mok[r]) continue;
       float u[DPT];
 #pragma unroll
       for (int e = 0; e < DPT; ++e) u[e] = xr[r][e] * rs[r] * (1.0f + gg[e]) + bb[e];
-      const unsigned off = (unsigned)(mrow[r] * d + c) * 2u;
-      if constexpr (DPT == 4) stc8(Ur, off, pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]));
-      else stc4(Ur, off, pack_bf16x2(u[0], u[1]));
+      const unsigned off = mok[r] ? (unsigned)(mrow[r] * d + c0) * 2u : OOB;
+      if constexpr (DPT == 4) st8<STL>(Ur, off, pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]));
+      else st4<STL>(Ur, off, pack_bf16x2(u[0], u[1]));
     }
   };
   // x += alpha * (sum over teams of delta[buf]), summed in team order
   auto resid = [&](int buf, const float* alpha) {
-    const int c = tid * DPT;
     float al[DPT];
-#pragma unroll
-    for (int e = 0; e < DPT; ++e) al[e] = alpha[c + e];
+    ldf(al, alpha + c0);
     float dv[2][NTEAM][DPT];
 #pragma unroll
     for (int r = 0; r < 2; ++r)
 #pragma unroll
       for (int y = 0; y < NTEAM; ++y) {
-        const unsigned off = (unsigned)((((size_t)buf * NTEAM + y) * n + mrow[r]) * d + c) * 4u;
+        const unsigned off = mok[r] ? (unsigned)((((size_t)buf * NTEAM + y) * n + mrow[r]) * d + c0) * 4u : OOB;
         if constexpr (DPT == 4) {
-          const uint4 v = mok[r] ? ldc16(Dr, off) : make_uint4(0, 0, 0, 0);
+          const uint4 v = ld16<SC1>(Dr, off);
           dv[r][y][0] = __uint_as_float(v.x);
           dv[r][y][1] = __uint_as_float(v.y);
           dv[r][y][2] = __uint_as_float(v.z);
           dv[r][y][3] = __uint_as_float(v.w);
         } else {
-          const float2 v = mok[r] ? ldc8f(Dr, off) : make_float2(0.f, 0.f);
+          const float2 v = ld8f<SC1>(Dr, off);
           dv[r][y][0] = v.x;
           dv[r][y][1] = v.y;
         }
       }
 #pragma unroll
-    for (int r = 0; r < 2; ++r) {
-      if (!mok[r]) continue;
+    for (int r = 0; r < 2; ++r)
 #pragma unroll
       for (int e = 0; e < DPT; ++e) {
         float sum = 0.f;
 #pragma unroll
         for (int y = 0; y < NTEAM; ++y) sum += dv[r][y][e];
-        xr[r][e] += al[e] * sum;
+        xr[r][e] += al[e] * sum;   // absent rows: xr stays 0 (their deltas read as 0)
       }
-    }
   };
-  // x = a W_in^T + xs + E_pos (input embedding of the chunk tokens); the
-  // thread's W_in rows, E_pos and xs values are loaded first.
+  // x = a W_in^T + xs + E_pos (input embedding of the chunk tokens).  W_in is
+  // the zero-padded [d][32] copy; sa holds a with zeros past A.
+  const rsrc_t WIr = mkr(a.w_in, (size_t)d * 32 * 2);
+  const rsrc_t EPr = mkr(a.e_pos, (size_t)n * d * 2);
+  const rsrc_t WOr = mkr(a.w_out, (size_t)A * d * 2);
   auto embed = [&]() {
     if (tid < 32) {
       sa[0][tid] = tid < A ? areg[0] : 0.f;
       sa[1][tid] = tid < A ? areg[1] : 0.f;
     }
-    const bf16_t* Win = reinterpret_cast<const bf16_t*>(a.w_in);
-    const bf16_t* Ep = reinterpret_cast<const bf16_t*>(a.e_pos);
-    constexpr int AV = 32 / 8;           // 16-byte vectors of a W_in row (A <= 32)
-    uint4 wv[DPT][AV];
+    uint4 wv[DPT][4];
+#pragma unroll
+    for (int e = 0; e < DPT; ++e)
+#pragma unroll
+      for (int q = 0; q < 4; ++q) wv[e][q] = ld16<0>(WIr, (unsigned)((c0 + e) * 32 + 8 * q) * 2u);
     float base[DPT], ep[2][DPT];
+    ldf(base, a.xs + c0);
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) {
-      const int c = tid * DPT + e;
-#pragma unroll
-      for (int q = 0; q < AV; ++q) wv[e][q] = (8 * q < A) ? ldg16(Win + (size_t)c * A + 8 * q) : make_uint4(0, 0, 0, 0);
-      base[e] = a.xs[c];
-#pragma unroll
-      for (int r = 0; r < 2; ++r) ep[r][e] = mok[r] ? bf2f(Ep[(size_t)mrow[r] * d + c]) : 0.f;
-    }
+    for (int r = 0; r < 2; ++r) ldbf(ep[r], EPr, mok[r] ? (unsigned)(mrow[r] * d + c0) * 2u : OOB);
     __syncthreads();
 #pragma unroll
     for (int e = 0; e < DPT; ++e) {
+      float f[32];
+#pragma unroll
+      for (int q = 0; q < 4; ++q) unpack16(wv[e][q], f + 8 * q, bf16_t());
 #pragma unroll
       for (int r = 0; r < 2; ++r) {
-        float v = 0.f;
-        if (mok[r]) {
-          v = base[e] + ep[r][e];
+        float v = base[e] + ep[r][e];
 #pragma unroll
-          for (int q = 0; q < AV; ++q) {
-            if (8 * q >= A) break;
-            float f[8];
-            unpack16(wv[e][q], f, bf16_t());
-#pragma unroll
-            for (int t = 0; t < 8; ++t)
-              if (8 * q + t < A) v += sa[r][8 * q + t] * f[t];
-          }
-        }
-        xr[r][e] = v;
+        for (int t = 0; t < 32; ++t) v += sa[r][t] * f[t];
+        xr[r][e] = mok[r] ? v : 0.f;
       }
     }
     __syncthreads();
@@ -417,13 +472,12 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   auto head = [&](int k) {
     const float* g = a.modf + (size_t)k * 2 * d;
     const float* b = g + d;
-    const bf16_t* Wo = reinterpret_cast<const bf16_t*>(a.w_out);
-    // this thread's W_out columns, all A rows, loaded first
-    float wo_[32][DPT];
+    float wo_[32][DPT];                    // W_out[j][c0 ..]; rows j >= A read zero
 #pragma unroll
-    for (int j = 0; j < 32; ++j)
-#pragma unroll
-      for (int e = 0; e < DPT; ++e) wo_[j][e] = j < A ? bf2f(Wo[(size_t)j * d + tid * DPT + e]) : 0.f;
+    for (int j = 0; j < 32; ++j) ldbf(wo_[j], WOr, j < A ? (unsigned)(j * d + c0) * 2u : OOB);
+    float gg[DPT], bb[DPT];
+    ldf(gg, g + c0);
+    ldf(bb, b + c0);
     float ss[2] = {0.f, 0.f};
 #pragma unroll
     for (int r = 0; r < 2; ++r)
@@ -434,15 +488,11 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
     const float rs[2] = {1.0f / sqrtf(t0 / (float)d + a.eps), 1.0f / sqrtf(t1 / (float)d + a.eps)};
     float uf[2][DPT];
 #pragma unroll
-    for (int e = 0; e < DPT; ++e) {
-      const int c = tid * DPT + e;
-      const float gg = g[c], bb = b[c];
+    for (int e = 0; e < DPT; ++e)
 #pragma unroll
-      for (int r = 0; r < 2; ++r) uf[r][e] = xr[r][e] * rs[r] * (1.0f + gg) + bb;
-    }
+      for (int r = 0; r < 2; ++r) uf[r][e] = xr[r][e] * rs[r] * (1.0f + gg[e]) + bb[e];
 #pragma unroll
     for (int j = 0; j < 32; ++j) {
-      if (j >= A) break;
       float p0 = 0.f, p1 = 0.f;
 #pragma unroll
       for (int e = 0; e < DPT; ++e) {
@@ -600,14 +650,15 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int m = 16 * wave + 4 * g4 + i;
-            if (m < n) stc2(Qr, (unsigned)(m * QW + oc[s] + r16) * 2u, f2bf(acc[0][s][i]));
+            if (m < n) st2(Qr, (unsigned)(m * QW + oc[s] + r16) * 2u, f2bf(acc[0][s][i]));
           }
         }
       }
       mark();
       team_arrive(sy, team);
+      const unsigned pk1 = team_peek(sy, team);
       prefetch_kv(l);
-      if (!team_wait(sy, team, &flag)) return bail();
+      if (!team_wait(sy, team, &flag, pk1)) return bail();
       mark();
 
       // ---- A: attention partials of key split `rank` ---------------------------
@@ -640,7 +691,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         uint4 qf[NQV];
         const unsigned qb = (unsigned)(qrow * QW + hh * HD + g4 * (HD / 4)) * 2u;
 #pragma unroll
-        for (int c = 0; c < NQV; ++c) qf[c] = qwave ? ldc16(Qr, qb + 16u * c) : make_uint4(0, 0, 0, 0);
+        for (int c = 0; c < NQV; ++c) qf[c] = qwave ? ld16<LDX>(Qr, qb + 16u * c) : make_uint4(0, 0, 0, 0);
 #pragma unroll
         for (int q = 0; q < NKI; ++q) {
           const int i = tid + q * NTHR;
@@ -659,7 +710,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
               const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
               const int kr = rr / VPR, cv = rr - kr * VPR;
               const int j = jbeg + jb, key = (j - nbp) * 32 + kr;
-              if (j >= nbp) put_k(i, ldc16(Qr, (unsigned)(key * QW + HTD + cv * 8) * 2u));
+              if (j >= nbp) put_k(i, ld16<LDX>(Qr, (unsigned)(key * QW + HTD + cv * 8) * 2u));
             }
           }
 #pragma unroll
@@ -670,8 +721,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
               const int kp2 = rr & 15, cv = rr >> 4;
               const int j = jbeg + jb, key = (j - nbp) * 32 + 2 * kp2;
               if (j >= nbp)
-                put_v(i, ldc16(Qr, (unsigned)(key * QW + HTD + HD + cv * 8) * 2u),
-                      ldc16(Qr, (unsigned)((key + 1) * QW + HTD + HD + cv * 8) * 2u));
+                put_v(i, ld16<LDX>(Qr, (unsigned)(key * QW + HTD + HD + cv * 8) * 2u),
+                      ld16<LDX>(Qr, (unsigned)((key + 1) * QW + HTD + HD + cv * 8) * 2u));
             }
           }
         }
@@ -740,18 +791,19 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
             const unsigned rowoff = (unsigned)((rank * n + qrow) * HTD + hh * HD);
 #pragma unroll
             for (int dd = 0; dd < DTL; ++dd)
-              stc8(APr, (rowoff + 16 * dd + 4 * g4) * 2u, pack_bf16x2(o[dd][0] * inv, o[dd][1] * inv),
+              st8<STL>(APr, (rowoff + 16 * dd + 4 * g4) * 2u, pack_bf16x2(o[dd][0] * inv, o[dd][1] * inv),
                    pack_bf16x2(o[dd][2] * inv, o[dd][3] * inv));
             if (g4 == 0)
-              stc8(ASr, (unsigned)(((rank * n + qrow) * HT + hh) * 2) * 4u, __float_as_uint(mrun),
+              st8<STL>(ASr, (unsigned)(((rank * n + qrow) * HT + hh) * 2) * 4u, __float_as_uint(mrun),
                    __float_as_uint(lrun));
           }
         }
       }
       mark();
       team_arrive(sy, team);
+      const unsigned pk2 = team_peek(sy, team);
       prefetch_wo(l);
-      if (!team_wait(sy, team, &flag)) return bail();
+      if (!team_wait(sy, team, &flag, pk2)) return bail();
       mark();
 
       // ---- M: merge the key splits; rank (t, cb) merges query tile t, columns
@@ -774,8 +826,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
               for (int q = 0; q < 16; ++q) {
                 const bool ok = s0 + q < S;
-                st[q] = ok ? ldc8f(ASr, (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u) : make_float2(-INFINITY, 0.f);
-                v[q] = ok ? ldc16(APr, (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u) : make_uint4(0, 0, 0, 0);
+                st[q] = ok ? ld8f<LDX>(ASr, (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u) : make_float2(-INFINITY, 0.f);
+                v[q] = ok ? ld16<LDX>(APr, (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u) : make_uint4(0, 0, 0, 0);
               }
 #pragma unroll
               for (int q = 0; q < 16; ++q) {
@@ -795,8 +847,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc8[e] *= inv;
             const uint4 pk = pack16(acc8, bf16_t());
-            stc8(OMr, (unsigned)(m * HTD + cv * 8) * 2u, pk.x, pk.y);
-            stc8(OMr, (unsigned)(m * HTD + cv * 8 + 4) * 2u, pk.z, pk.w);
+            st8<STL>(OMr, (unsigned)(m * HTD + cv * 8) * 2u, pk.x, pk.y);
+            st8<STL>(OMr, (unsigned)(m * HTD + cv * 8 + 4) * 2u, pk.z, pk.w);
           }
         }
       }
@@ -813,7 +865,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         const int nv = 64 * (HTD / 8);
         for (int i = tid; i < nv; i += NTHR) {
           const int rr = i / (HTD / 8), cv = i - rr * (HTD / 8);
-          *reinterpret_cast<uint4*>(otile + rr * OP + cv * 8) = ldc16(OMr, (unsigned)(rr * HTD + cv * 8) * 2u);
+          *reinterpret_cast<uint4*>(otile + rr * OP + cv * 8) = ld16<LDX>(OMr, (unsigned)(rr * HTD + cv * 8) * 2u);
         }
         __syncthreads();
         if (wave < QT) {
@@ -832,19 +884,20 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
               const int m = 16 * wave + 4 * g4 + i;
-              if (m < n) stc4(Dr, (unsigned)((((size_t)0 * NTEAM + team) * n + m) * d + col) * 4u, __float_as_uint(acc[i]));
+              if (m < n) st4<SC1>(Dr, (unsigned)((((size_t)0 * NTEAM + team) * n + m) * d + col) * 4u, __float_as_uint(acc[i]));
             }
           }
         }
       }
       mark();
       grid_arrive(sy, team);
+      const unsigned pk3 = grid_peek(sy);
       {
         int wr[2];
         gu_rows(wr);
         prefetch_w<2>(wg, mkr(ly.wgu, (size_t)(a.glu ? 2 : 1) * a.F * d * 2), d, 0, d, wr);
       }
-      if (!grid_wait(sy, &flag)) return bail();
+      if (!grid_wait(sy, &flag, pk3)) return bail();
       mark();
 
       // ---- R: attention residual, adaRMS of the MLP sublayer --------------------
@@ -867,18 +920,19 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
             const int m = 16 * wave + 4 * g4 + i;
             if (m >= n) continue;
             const float h = a.glu ? act_f(a.act, acc[0][0][i]) * acc[0][1][i] : act_f(a.act, acc[0][0][i]);
-            stc2(Hr, (unsigned)(m * F8 + f) * 2u, f2bf(h));
+            st2(Hr, (unsigned)(m * F8 + f) * 2u, f2bf(h));
           }
         }
       }
       mark();
       team_arrive(sy, team);
+      const unsigned pk4 = team_peek(sy, team);
       {
         int wr[2];
         dn_rows(wr);
         prefetch_w<2>(wd, mkr(ly.wd, (size_t)d * a.F * 2), a.F, team * F8, F8, wr);
       }
-      if (!team_wait(sy, team, &flag)) return bail();
+      if (!team_wait(sy, team, &flag, pk4)) return bail();
       mark();
 
       // ---- D: h_team W_d[:, team cols]^T -> delta1 -----------------------------------
@@ -895,7 +949,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int m = 16 * wave + 4 * g4 + i;
-            if (m < n) stc4(Dr, (unsigned)((((size_t)1 * NTEAM + team) * n + m) * d + col) * 4u, __float_as_uint(acc[0][s][i]));
+            if (m < n) st4<SC1>(Dr, (unsigned)((((size_t)1 * NTEAM + team) * n + m) * d + col) * 4u, __float_as_uint(acc[0][s][i]));
           }
         }
       }
@@ -903,13 +957,14 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       const bool last = last_layer && k == a.T - 1;
       mark();
       grid_arrive(sy, team);
+      const unsigned pk5 = grid_peek(sy);
       {
         int wr[2], oc[2];
         qkv_rows(wr, oc);
         const int nl = last_layer ? 0 : l + 1;
         prefetch_w<2>(wq, mkr(lt[nl].wqkv, (size_t)(dq + 2 * dkv) * d * 2), d, 0, d, wr);
       }
-      if (!grid_wait(sy, &flag)) return bail();
+      if (!grid_wait(sy, &flag, pk5)) return bail();
       mark();
 
       // ---- R: MLP residual; next sublayer's adaRMS (or head, Euler, embedding) ---

@@ -500,7 +500,13 @@ vla_status build_plan(vla_model* m, Plan* p) {
     pa.cp = cp;
     pa.mods = p->mods;
     pa.modf = p->modf;
-    pa.w_in = m->W_in;
+    // W_in zero-padded to [d][32] so the kernel's embedding reads aligned,
+    // fixed-length rows
+    void* win_pad = nullptr;
+    VLA_TRY(al(&win_pad, (size_t)d * 32 * 2));
+    HIP_TRY(hipMemset(win_pad, 0, (size_t)d * 32 * 2));
+    HIP_TRY(hipMemcpy2D(win_pad, 32 * 2, m->W_in, (size_t)A * 2, (size_t)A * 2, d, hipMemcpyDeviceToDevice));
+    pa.w_in = win_pad;
     pa.xs = p->xs;
     pa.e_pos = m->E_pos;
     pa.w_out = m->W_out;

@@ -181,6 +181,7 @@ struct PersistArgs {
   unsigned long long* trace;
 };
 constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 8 * 32 + 64;
+constexpr int PERSIST_RANK_OFF = 8 * 32 + 8 * 32 + 32;  // 8 per-XCD arrival counters (team ranks)
 constexpr int PERSIST_TRACE_MAX = 8192;
 constexpr int PERSIST_MAX_LAYERS = 64;
 
