@@ -88,75 +88,65 @@ VLA_DEV unsigned xcc_id() {
 }
 
 // ---------------------------------------------------------------------------
-// Barriers.  Counters only grow; the k-th team barrier waits for 32 k
-// arrivals on the team counter, the k-th grid barrier for 8 k team arrivals on
-// the global counter (the last workgroup of a team to arrive forwards it).
+// Barriers, without atomics.  Every workgroup owns one flag word holding the
+// number of barriers (team and grid alike) it has arrived at; the flags of a
+// team are one 128-byte line, flag[team * 32 + rank].  Arriving = waiting
+// until this workgroup's stores have completed, then a device-coherent store
+// of the new count.  A team barrier waits until the team's 32 flags reach the
+// count (one load per lane of the first wave), a grid barrier until all 256 do
+// (lane l reads flags 4l .. 4l+3).  Flags only grow, so a workgroup that is
+// already past the barrier also satisfies it.
 struct Sync {
-  unsigned* tcnt;   // [8][32], one counter per team at [team * 32]
-  unsigned* xcnt;   // [8][32]
-  unsigned* glob;   // [64], counter at [0]
+  unsigned* flag;   // [8][32]
   int* err;
-  unsigned tk, gk;  // barriers passed by this workgroup
+  unsigned bk;      // barriers this workgroup has arrived at
 };
 
-VLA_DEV bool spin_until(unsigned* c, unsigned target, int* err) {
-  long it = 0;
-  while (__hip_atomic_load(c, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
-    if (++it > SPIN_LIMIT) {
-      __hip_atomic_fetch_or(err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-      return false;
-    }
-    if ((it & 255) == 0 && __hip_atomic_load(err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) return false;
-    __builtin_amdgcn_s_sleep(1);
-  }
-  return true;
-}
-
-// A barrier is split into arrive and wait so that loads independent of the
-// other workgroups (the next phase's weights) can be issued in between: the
-// arrival has to wait for this workgroup's stores (one vmcnt covers loads and
-// stores), loads issued after it do not delay it.
-VLA_DEV void team_arrive(Sync& s, int team) {
+VLA_DEV void arrive(Sync& s, int team, int rank) {
   __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
   __syncthreads();
-  ++s.tk;
-  if (threadIdx.x == 0) __hip_atomic_fetch_add(s.tcnt + team * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  ++s.bk;
+  if (threadIdx.x == 0) __hip_atomic_store(s.flag + team * 32 + rank, s.bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
-// First poll of a barrier counter, issued right after the arrival and before
-// the next phase's prefetch loads: the wait for its value does not also wait
-// for those loads (loads complete in order).
-VLA_DEV unsigned team_peek(const Sync& s, int team) {
-  return threadIdx.x == 0 ? __hip_atomic_load(s.tcnt + team * 32, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
-}
-VLA_DEV unsigned grid_peek(const Sync& s) {
-  return threadIdx.x == 0 ? __hip_atomic_load(s.glob, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0u;
+// Smallest flag this lane of the first wave watches (team: lane < 32 reads
+// its teammate's flag; grid: four flags per lane); other threads return ~0.
+template <bool GRID>
+VLA_DEV unsigned flag_peek(const Sync& s, int team) {
+  const int t = threadIdx.x;
+  if (t >= 64) return 0xffffffffu;
+  if (GRID) {
+    unsigned v[4];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) v[i] = __hip_atomic_load(s.flag + 4 * t + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    return min(min(v[0], v[1]), min(v[2], v[3]));
+  }
+  return t < TSIZE ? __hip_atomic_load(s.flag + team * 32 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0xffffffffu;
 }
 
 // Returns false (in every thread) if the run must stop.
-VLA_DEV bool team_wait(Sync& s, int team, int* lds_flag, unsigned peek = 0u) {
-  if (threadIdx.x == 0) {
-    const unsigned target = s.tk * TSIZE;
-    *lds_flag = (peek >= target || spin_until(s.tcnt + team * 32, target, s.err)) ? 1 : 0;
-  }
-  __syncthreads();
-  return *lds_flag != 0;
-}
-
-VLA_DEV void grid_arrive(Sync& s, int team) {
-  __builtin_amdgcn_s_waitcnt(0);
-  __syncthreads();
-  ++s.gk;
-  if (threadIdx.x == 0) {
-    const unsigned old = __hip_atomic_fetch_add(s.xcnt + team * 32, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    if (old == s.gk * TSIZE - 1) __hip_atomic_fetch_add(s.glob, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-  }
-}
-
-VLA_DEV bool grid_wait(Sync& s, int* lds_flag, unsigned peek = 0u) {
-  if (threadIdx.x == 0) {
-    const unsigned target = s.gk * NTEAM;
-    *lds_flag = (peek >= target || spin_until(s.glob, target, s.err)) ? 1 : 0;
+template <bool GRID>
+VLA_DEV bool wait_flags(Sync& s, int team, int* lds_flag, unsigned peek) {
+  if (threadIdx.x < 64) {
+    const unsigned target = s.bk;
+    bool ok = true;
+    if (!__all(peek >= target)) {
+      long it = 0;
+      while (true) {
+        __builtin_amdgcn_s_sleep(1);
+        if (__all(flag_peek<GRID>(s, team) >= target)) break;
+        if (++it > SPIN_LIMIT) {
+          if (threadIdx.x == 0) __hip_atomic_fetch_or(s.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+          ok = false;
+          break;
+        }
+        if ((it & 255) == 0 && __hip_atomic_load(s.err, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT)) {
+          ok = false;
+          break;
+        }
+      }
+    }
+    if (threadIdx.x == 0) *lds_flag = ok ? 1 : 0;
   }
   __syncthreads();
   return *lds_flag != 0;
@@ -196,21 +186,33 @@ VLA_DEV void prefetch_w(WTile<NS>& t, rsrc_t W, int ldw, int kofs, int K, const 
   }
 }
 
-// acc[ms][s] over this wave's chunks; X = [M][K] bf16 through sc1 loads.
+// acc[ms][s] over this wave's chunks.  X is an exchanged activation in the
+// tiled layout [K/32][M][32] bf16 (so one load instruction of a wave reads 16
+// rows x 64 contiguous bytes = 1 KB); rows past M read zero.
+VLA_DEV unsigned xtile_off(int m, int k, int M) { return (unsigned)(((k >> 5) * M + m) * 64 + (k & 31) * 2); }
+
 template <int NS>
-VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, rsrc_t X, int K) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, rsrc_t X, int K, int M) {
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g4 = lane >> 4;
+  // offset = lane part (row r16 of subtile ms, 16-byte group g4) + a
+  // wave-uniform part (32-column block, subtile); absent rows and chunks
+  // past K get offsets beyond the buffer
+  unsigned vo[4];
+#pragma unroll
+  for (int ms = 0; ms < 4; ++ms) vo[ms] = (16 * ms + r16 < M) ? (unsigned)(r16 * 64 + g4 * 16) : 0x7ffffff0u;
   uint4 xr[CPW][4][VPL];
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
     const int kc = 128 * (wave + NW * j);
-    const unsigned vb = (unsigned)(r16 * K + kc + 8 * g4) * 2u;
 #pragma unroll
     for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
-      for (int v = 0; v < VPL; ++v)
-        xr[j][ms][v] = kc < K ? bld16(X, vb + 64u * v, (unsigned)(16 * ms * K) * 2u, 1) : make_uint4(0, 0, 0, 0);
+      for (int v = 0; v < VPL; ++v) {
+        const unsigned so = kc < K ? (unsigned)(((kc >> 5) + v) * M * 64 + ms * 16 * 64) : 0x7ffffff0u;
+        const u32x4_t x = __builtin_amdgcn_raw_buffer_load_b128(X, (int)vo[ms], (int)so, LDX);
+        xr[j][ms][v] = make_uint4(x.x, x.y, x.z, x.w);
+      }
   }
 #pragma unroll
   for (int ms = 0; ms < 4; ++ms)
@@ -302,7 +304,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   for (int i = tid; i < a.L; i += NTHR) lt[i] = a.layers[i];
   const bf16_t* kvbase = reinterpret_cast<const bf16_t*>(a.cp->kv_cache);
 
-  Sync sy{a.sync, a.sync + 8 * 32, a.sync + 16 * 32, a.err, 0u, 0u};
+  Sync sy{a.sync, a.err, 0u};
   unsigned long long* trace = (a.trace && rank == 0) ? a.trace + (size_t)team * PERSIST_TRACE_MAX : nullptr;
   int tev = 0;
   auto mark = [&]() {
@@ -395,7 +397,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       float u[DPT];
 #pragma unroll
       for (int e = 0; e < DPT; ++e) u[e] = xr[r][e] * rs[r] * (1.0f + gg[e]) + bb[e];
-      const unsigned off = mok[r] ? (unsigned)(mrow[r] * d + c0) * 2u : OOB;
+      const unsigned off = mok[r] ? xtile_off(mrow[r], c0, n) : OOB;   // tiled [d/32][n][32]
       if constexpr (DPT == 4) st8<STL>(Ur, off, pack_bf16x2(u[0], u[1]), pack_bf16x2(u[2], u[3]));
       else st4<STL>(Ur, off, pack_bf16x2(u[0], u[1]));
     }
@@ -576,29 +578,61 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   auto prefetch_kv = [&](int l) {
     const bf16_t* kc = kvbase + lt[l].cache_off + (size_t)gteam * npre * HD;
     const bf16_t* vc = kc + (size_t)a.G * npre * HD;
+    const rsrc_t KR = mkr(kc, (size_t)npre * HD * 2), VR = mkr(vc, (size_t)npre * HD * 2);
 #pragma unroll
     for (int q = 0; q < NKI; ++q) {
       const int i = tid + q * NTHR;
-      kpre[q] = make_uint4(0, 0, 0, 0);
-      if (i < nblk * 32 * VPR) {
-        const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
-        const int kr = rr / VPR, cv = rr - kr * VPR;
-        const int j = jbeg + jb, key = j * 32 + kr;
-        if (j < nbp && key < npre) kpre[q] = ldg16(kc + (size_t)key * HD + cv * 8);
-      }
+      const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
+      const int kr = rr / VPR, cv = rr - kr * VPR;
+      const int j = jbeg + jb, key = j * 32 + kr;
+      const bool ok = i < nblk * 32 * VPR && j < nbp;   // keys past the prefix read zero
+      kpre[q] = ld16<0>(KR, ok ? (unsigned)(key * HD + cv * 8) * 2u : OOB);
     }
 #pragma unroll
     for (int q = 0; q < NVI; ++q) {
       const int i = tid + q * NTHR;
-      vp0[q] = make_uint4(0, 0, 0, 0);
-      vp1[q] = make_uint4(0, 0, 0, 0);
-      if (i < nblk * 16 * VPR) {
-        const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
-        const int kp2 = rr & 15, cv = rr >> 4;
-        const int j = jbeg + jb, key = j * 32 + 2 * kp2;
-        if (j < nbp && key < npre) vp0[q] = ldg16(vc + (size_t)key * HD + cv * 8);
-        if (j < nbp && key + 1 < npre) vp1[q] = ldg16(vc + (size_t)(key + 1) * HD + cv * 8);
-      }
+      const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
+      const int kp2 = rr & 15, cv = rr >> 4;
+      const int j = jbeg + jb, key = j * 32 + 2 * kp2;
+      const bool ok = i < nblk * 16 * VPR && j < nbp;
+      vp0[q] = ld16<0>(VR, ok ? (unsigned)(key * HD + cv * 8) * 2u : OOB);
+      vp1[q] = ld16<0>(VR, ok ? (unsigned)((key + 1) * HD + cv * 8) * 2u : OOB);
+    }
+  };
+
+  // LDS staging of one attention split's blocks: K rows as they are, V transposed
+  // (dims x keys) for the O^T = V^T P^T products.
+  auto put_k = [&](int i, uint4 v) {
+    const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
+    const int kr = rr / VPR, cv = rr - kr * VPR;
+    bf16_t* kl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF);
+    *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * 8) = v;
+  };
+  auto put_v = [&](int i, uint4 v0, uint4 v1) {
+    const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
+    const int kp2 = rr & 15, cv = rr >> 4;
+    bf16_t* vl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF + L::KBYTES);
+    const uint32_t a4[4] = {v0.x, v0.y, v0.z, v0.w};
+    const uint32_t b4[4] = {v1.x, v1.y, v1.z, v1.w};
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+      const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+      const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+      *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
+    }
+  };
+  // Prefix K / V of the split, from the prefetched registers (chunk blocks get
+  // zeros here and their keys after the barrier).
+  auto stage_prefix = [&]() {
+#pragma unroll
+    for (int q = 0; q < NKI; ++q) {
+      const int i = tid + q * NTHR;
+      if (i < nblk * 32 * VPR) put_k(i, kpre[q]);
+    }
+#pragma unroll
+    for (int q = 0; q < NVI; ++q) {
+      const int i = tid + q * NTHR;
+      if (i < nblk * 16 * VPR) put_v(i, vp0[q], vp1[q]);
     }
   };
 
@@ -630,8 +664,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   embed();
   norm_store(gam(0, 0, 0), gam(0, 0, 0) + d);
   mark();
-  team_arrive(sy, team);
-      if (!team_wait(sy, team, &flag)) return bail();
+  arrive(sy, team, rank);
+      if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
   mark();
 
   for (int k = 0; k < a.T; ++k) {
@@ -642,7 +676,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         int wr[2], oc[2];
         qkv_rows(wr, oc);
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wq, Ur, d);
+        tile_mma<2>(acc, wq, Ur, d, n);
         tile_reduce<2>(acc, red);
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
@@ -655,75 +689,55 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      team_arrive(sy, team);
-      const unsigned pk1 = team_peek(sy, team);
+      arrive(sy, team, rank);
+      const unsigned pk1 = flag_peek<false>(sy, team);
       prefetch_kv(l);
-      if (!team_wait(sy, team, &flag, pk1)) return bail();
+      if (att_on) stage_prefix();   // independent of this step: done while the team arrives
+      if (!wait_flags<false>(sy, team, &flag, pk1)) return bail();
       mark();
 
       // ---- A: attention partials of key split `rank` ---------------------------
       if (att_on) {
-        // Stage the split's blocks: prefix keys from the prefetched registers,
-        // then this step's k, v of the chunk tokens (rows past the end read zero).
-        auto put_k = [&](int i, uint4 v) {
-          const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
-          const int kr = rr / VPR, cv = rr - kr * VPR;
-          bf16_t* kl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF);
-          *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * 8) = v;
-        };
-        auto put_v = [&](int i, uint4 v0, uint4 v1) {
-          const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
-          const int kp2 = rr & 15, cv = rr >> 4;
-          bf16_t* vl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF + L::KBYTES);
-          const uint32_t a4[4] = {v0.x, v0.y, v0.z, v0.w};
-          const uint32_t b4[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
-          }
-        };
-        // Q fragments of wave (hh, qs): issued first, used after staging
+        // Q fragments of wave (hh, qs) and this step's k, v of the chunk tokens
+        // that fall in the split's blocks: all issued at once, branch-free
+        // (prefix blocks and rows past the chunk read zero).
         const int hh = wave / QT, qs = wave - hh * QT;
         const bool qwave = hh < HT;
         const int qrow = 16 * qs + r16;
         uint4 qf[NQV];
         const unsigned qb = (unsigned)(qrow * QW + hh * HD + g4 * (HD / 4)) * 2u;
 #pragma unroll
-        for (int c = 0; c < NQV; ++c) qf[c] = qwave ? ld16<LDX>(Qr, qb + 16u * c) : make_uint4(0, 0, 0, 0);
+        for (int c = 0; c < NQV; ++c) qf[c] = ld16<LDX>(Qr, qwave ? qb + 16u * c : OOB);
+        uint4 kch[NKI], vc0[NVI], vc1[NVI];
 #pragma unroll
         for (int q = 0; q < NKI; ++q) {
           const int i = tid + q * NTHR;
-          if (i < nblk * 32 * VPR) put_k(i, kpre[q]);
+          const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
+          const int kr = rr / VPR, cv = rr - kr * VPR;
+          const int j = jbeg + jb, key = (j - nbp) * 32 + kr;
+          const bool ok = i < nblk * 32 * VPR && j >= nbp;
+          kch[q] = ld16<LDX>(Qr, ok ? (unsigned)(key * QW + HTD + cv * 8) * 2u : OOB);
         }
 #pragma unroll
         for (int q = 0; q < NVI; ++q) {
           const int i = tid + q * NTHR;
-          if (i < nblk * 16 * VPR) put_v(i, vp0[q], vp1[q]);
+          const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
+          const int kp2 = rr & 15, cv = rr >> 4;
+          const int j = jbeg + jb, key = (j - nbp) * 32 + 2 * kp2;
+          const bool ok = i < nblk * 16 * VPR && j >= nbp;
+          vc0[q] = ld16<LDX>(Qr, ok ? (unsigned)(key * QW + HTD + HD + cv * 8) * 2u : OOB);
+          vc1[q] = ld16<LDX>(Qr, ok ? (unsigned)((key + 1) * QW + HTD + HD + cv * 8) * 2u : OOB);
         }
         if (jbeg + nblk > nbp) {   // the split holds chunk-token keys
 #pragma unroll
           for (int q = 0; q < NKI; ++q) {
             const int i = tid + q * NTHR;
-            if (i < nblk * 32 * VPR) {
-              const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
-              const int kr = rr / VPR, cv = rr - kr * VPR;
-              const int j = jbeg + jb, key = (j - nbp) * 32 + kr;
-              if (j >= nbp) put_k(i, ld16<LDX>(Qr, (unsigned)(key * QW + HTD + cv * 8) * 2u));
-            }
+            if (i < nblk * 32 * VPR && jbeg + i / (32 * VPR) >= nbp) put_k(i, kch[q]);
           }
 #pragma unroll
           for (int q = 0; q < NVI; ++q) {
             const int i = tid + q * NTHR;
-            if (i < nblk * 16 * VPR) {
-              const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
-              const int kp2 = rr & 15, cv = rr >> 4;
-              const int j = jbeg + jb, key = (j - nbp) * 32 + 2 * kp2;
-              if (j >= nbp)
-                put_v(i, ld16<LDX>(Qr, (unsigned)(key * QW + HTD + HD + cv * 8) * 2u),
-                      ld16<LDX>(Qr, (unsigned)((key + 1) * QW + HTD + HD + cv * 8) * 2u));
-            }
+            if (i < nblk * 16 * VPR && jbeg + i / (16 * VPR) >= nbp) put_v(i, vc0[q], vc1[q]);
           }
         }
         __syncthreads();
@@ -800,10 +814,10 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      team_arrive(sy, team);
-      const unsigned pk2 = team_peek(sy, team);
+      arrive(sy, team, rank);
+      const unsigned pk2 = flag_peek<false>(sy, team);
       prefetch_wo(l);
-      if (!team_wait(sy, team, &flag, pk2)) return bail();
+      if (!wait_flags<false>(sy, team, &flag, pk2)) return bail();
       mark();
 
       // ---- M: merge the key splits; rank (t, cb) merges query tile t, columns
@@ -825,9 +839,9 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
               float2 st[16];
 #pragma unroll
               for (int q = 0; q < 16; ++q) {
-                const bool ok = s0 + q < S;
-                st[q] = ok ? ld8f<LDX>(ASr, (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u) : make_float2(-INFINITY, 0.f);
-                v[q] = ok ? ld16<LDX>(APr, (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u) : make_uint4(0, 0, 0, 0);
+                const bool ok = s0 + q < S;   // absent splits read (0, 0): skipped below
+                st[q] = ld8f<LDX>(ASr, ok ? (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u : OOB);
+                v[q] = ld16<LDX>(APr, ok ? (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u : OOB);
               }
 #pragma unroll
               for (int q = 0; q < 16; ++q) {
@@ -853,8 +867,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      team_arrive(sy, team);
-      if (!team_wait(sy, team, &flag)) return bail();
+      arrive(sy, team, rank);
+      if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
       mark();
 
       // ---- O: o_team (all rows) times W_o[rank's CW columns][team heads]^T;
@@ -862,10 +876,19 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       {
         bf16_t* otile = reinterpret_cast<bf16_t*>(smem);   // [64][HTD + 8]
         const int OP = HTD + 8;
-        const int nv = 64 * (HTD / 8);
-        for (int i = tid; i < nv; i += NTHR) {
+        const int nv = 64 * (HTD / 8);      // <= 8 vectors per thread (HTD <= 256)
+        uint4 ov[8];
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int i = tid + q * NTHR;
           const int rr = i / (HTD / 8), cv = i - rr * (HTD / 8);
-          *reinterpret_cast<uint4*>(otile + rr * OP + cv * 8) = ld16<LDX>(OMr, (unsigned)(rr * HTD + cv * 8) * 2u);
+          ov[q] = ld16<LDX>(OMr, i < nv ? (unsigned)(rr * HTD + cv * 8) * 2u : OOB);   // rows past n read zero
+        }
+#pragma unroll
+        for (int q = 0; q < 8; ++q) {
+          const int i = tid + q * NTHR;
+          const int rr = i / (HTD / 8), cv = i - rr * (HTD / 8);
+          if (i < nv) *reinterpret_cast<uint4*>(otile + rr * OP + cv * 8) = ov[q];
         }
         __syncthreads();
         if (wave < QT) {
@@ -890,28 +913,28 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      grid_arrive(sy, team);
-      const unsigned pk3 = grid_peek(sy);
+      arrive(sy, team, rank);
+      const unsigned pk3 = flag_peek<true>(sy, team);
       {
         int wr[2];
         gu_rows(wr);
         prefetch_w<2>(wg, mkr(ly.wgu, (size_t)(a.glu ? 2 : 1) * a.F * d * 2), d, 0, d, wr);
       }
-      if (!grid_wait(sy, &flag, pk3)) return bail();
+      if (!wait_flags<true>(sy, team, &flag, pk3)) return bail();
       mark();
 
       // ---- R: attention residual, adaRMS of the MLP sublayer --------------------
       resid(0, gam(k, l, 0) + 2 * d);
       norm_store(gam(k, l, 1), gam(k, l, 1) + d);
       mark();
-      team_arrive(sy, team);
-      if (!team_wait(sy, team, &flag)) return bail();
+      arrive(sy, team, rank);
+      if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
       mark();
 
       // ---- G: u -> h of the team's MLP columns ------------------------------------
       {
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wg, Ur, d);
+        tile_mma<2>(acc, wg, Ur, d, n);
         tile_reduce<2>(acc, red);
         if (rank < npairs) {
           const int f = 16 * rank + r16;
@@ -920,19 +943,19 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
             const int m = 16 * wave + 4 * g4 + i;
             if (m >= n) continue;
             const float h = a.glu ? act_f(a.act, acc[0][0][i]) * acc[0][1][i] : act_f(a.act, acc[0][0][i]);
-            st2(Hr, (unsigned)(m * F8 + f) * 2u, f2bf(h));
+            st2(Hr, xtile_off(m, f, n), f2bf(h));   // tiled [F8/32][n][32]
           }
         }
       }
       mark();
-      team_arrive(sy, team);
-      const unsigned pk4 = team_peek(sy, team);
+      arrive(sy, team, rank);
+      const unsigned pk4 = flag_peek<false>(sy, team);
       {
         int wr[2];
         dn_rows(wr);
         prefetch_w<2>(wd, mkr(ly.wd, (size_t)d * a.F * 2), a.F, team * F8, F8, wr);
       }
-      if (!team_wait(sy, team, &flag, pk4)) return bail();
+      if (!wait_flags<false>(sy, team, &flag, pk4)) return bail();
       mark();
 
       // ---- D: h_team W_d[:, team cols]^T -> delta1 -----------------------------------
@@ -940,7 +963,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         int wr[2];
         dn_rows(wr);
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wd, Hr, F8);
+        tile_mma<2>(acc, wd, Hr, F8, n);
         tile_reduce<2>(acc, red);
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
@@ -956,15 +979,15 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       const bool last_layer = l == a.L - 1;
       const bool last = last_layer && k == a.T - 1;
       mark();
-      grid_arrive(sy, team);
-      const unsigned pk5 = grid_peek(sy);
+      arrive(sy, team, rank);
+      const unsigned pk5 = flag_peek<true>(sy, team);
       {
         int wr[2], oc[2];
         qkv_rows(wr, oc);
         const int nl = last_layer ? 0 : l + 1;
         prefetch_w<2>(wq, mkr(lt[nl].wqkv, (size_t)(dq + 2 * dkv) * d * 2), d, 0, d, wr);
       }
-      if (!grid_wait(sy, &flag, pk5)) return bail();
+      if (!wait_flags<true>(sy, team, &flag, pk5)) return bail();
       mark();
 
       // ---- R: MLP residual; next sublayer's adaRMS (or head, Euler, embedding) ---
@@ -980,8 +1003,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       }
       if (!last) {
         mark();
-        team_arrive(sy, team);
-      if (!team_wait(sy, team, &flag)) return bail();
+        arrive(sy, team, rank);
+      if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
         mark();
       }
     }
@@ -1010,7 +1033,10 @@ bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, 
   const int nblocks = (P + 31) / 32 + (n + 31) / 32;
   int k = 1;
   while ((nblocks + k - 1) / k > TSIZE) ++k;
-  if (k < 2 && nblocks > 16) k = 2;          // fewer, larger splits: less merge traffic
+#ifndef VLA_PERSIST_KBA_MIN
+#define VLA_PERSIST_KBA_MIN 2
+#endif
+  if (k < VLA_PERSIST_KBA_MIN && nblocks > 16) k = VLA_PERSIST_KBA_MIN;  // fewer, larger splits: less merge traffic
   if (k > KBA_MAX) return false;
   *kba = k;
   *nsplit = (nblocks + k - 1) / k;

@@ -174,14 +174,14 @@ struct PersistArgs {
   void* omerged;             // [8][n][HT hd]: merged attention output of the team's heads
   void* hbuf;                // [8][n][F / 8]
   float* delta;              // [2][8][n][d]: per-team partial residual updates
-  unsigned* sync;            // PERSIST_SYNC_WORDS counters, zero at launch
+  unsigned* sync;            // PERSIST_SYNC_WORDS words (barrier flags, rank counters), zero at launch
   int* err;                  // set when a barrier times out
   // optional phase timeline: workgroup 0 of each team records the 100 MHz
   // clock before and after every barrier, PERSIST_TRACE_MAX entries per team
   unsigned long long* trace;
 };
-constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 8 * 32 + 64;
-constexpr int PERSIST_RANK_OFF = 8 * 32 + 8 * 32 + 32;  // 8 per-XCD arrival counters (team ranks)
+constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 32;  // barrier flags [8][32], then the per-XCD rank counters
+constexpr int PERSIST_RANK_OFF = 8 * 32;          // 8 per-XCD arrival counters (team ranks)
 constexpr int PERSIST_TRACE_MAX = 8192;
 constexpr int PERSIST_MAX_LAYERS = 64;
 
