@@ -30,6 +30,7 @@ HBM_PEAK_GBS = 8000.0          # MI355X HBM3E
 BF16_PEAK_TFLOPS = 2500.0      # dense bf16 MFMA
 WORKLOAD = "pi0_bf16"
 PROFILE_REPS = 20              # back-to-back repetitions per timed launch
+LOOP_MODE = 2                  # persistent step kernel (the library's default driver)
 
 
 def log(*a):
@@ -87,7 +88,7 @@ def roofline_from_profile(ops, T):
     step_bytes = sum(o["bytes"] for o in ops) / T
     return {
         "bound": "hbm", "achieved": round(achieved, 1), "peak": HBM_PEAK_GBS, "unit": "GB/s",
-        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": None,
+        "frac": round(achieved / HBM_PEAK_GBS, 4), "traffic": measured_traffic(kind),
         "kernel": f"{kind} M={M} N={N} K={K}", "launches_per_chunk": g["n"],
         "bytes_per_launch": int(bytes_per), "launch_us": round(us_per, 3),
         "flops_per_launch": int(g["flops"] / g["n"]),
@@ -95,6 +96,24 @@ def roofline_from_profile(ops, T):
         "alg_bytes_per_solver_step": int(step_bytes),
         "breakdown": breakdown[:12],
     }
+
+
+def measured_traffic(kernel_kind):
+    """HBM-side bytes per launch of the dominant kernel from the committed
+    rocprofv3 FETCH_SIZE / WRITE_SIZE record, scaled by a plain copy of known
+    size; None when there is no record or the kernel source changed since."""
+    if kernel_kind != "persist":
+        return None
+    import hashlib
+    rec_path = os.path.join(ROOT, "profiles", "persist_kernel_pi0_bf16_traffic.json")
+    try:
+        with open(rec_path) as f:
+            rec = json.load(f)
+        with open(os.path.join(ROOT, rec["source"]), "rb") as f:
+            sha = hashlib.sha256(f.read()).hexdigest()
+    except (OSError, KeyError, ValueError):
+        return None
+    return int(rec["traffic_bytes_per_launch"]) if sha == rec.get("source_sha256") else None
 
 
 def cpu_baseline(cfg, W, inp, tau):
@@ -121,7 +140,23 @@ def main():
     ap.add_argument("--steps", type=int, default=30, help="timed chunks")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-sweep", action="store_true",
+                    help="skip the T-sweep fit (every launch then runs the workload's T, so profiler "
+                         "averages compare directly with the roofline launch time)")
+    ap.add_argument("--copy-mb", type=int, default=0,
+                    help="only run 5 plain device-to-device copies of this many MiB (calibrates the "
+                         "rocprofv3 FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
     args = ap.parse_args()
+    if args.copy_mb > 0:
+        import torch
+        n = args.copy_mb << 18   # fp32 elements
+        src = torch.ones(n, dtype=torch.float32, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(5):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_mib": args.copy_mb, "copies": 5}))
+        return
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(json.dumps({"error": "this benchmark runs on exactly one GPU: the denoise loop of one "
@@ -139,7 +174,7 @@ def main():
     W = wl.make_weights(cfg)
     inp = wl.make_batch(cfg, 1)
     tau = wl.uniform_schedule(cfg.n_steps)
-    pipe = Pipeline(cfg, W, inp, loop_mode=1)
+    pipe = Pipeline(cfg, W, inp, loop_mode=LOOP_MODE)
     log("warmup ...")
     for _ in range(args.warmup):
         pipe.build_cache()
@@ -150,14 +185,17 @@ def main():
     log(f"chunk {ms_chunk * 1000:.1f} us")
 
     # per-solver-step latency: linear fit of denoise time over T
-    Ts = [1, 2, 5, cfg.n_steps]
+    Ts = [cfg.n_steps] if args.no_sweep else [1, 2, 5, cfg.n_steps]
     ms_T = []
     for T in Ts:
         tT = wl.uniform_schedule(T)
         for _ in range(3):
             pipe.denoise(tT)
         ms_T.append(min(time_denoise(torch, pipe, tT, max(5, args.steps // 2)) for _ in range(2)))
-    slope, intercept = np.polyfit(np.array(Ts, float), np.array(ms_T), 1)
+    if len(Ts) > 1:
+        slope, intercept = np.polyfit(np.array(Ts, float), np.array(ms_T), 1)
+    else:
+        slope, intercept = float("nan"), float("nan")
     ms_build = time_chunks(torch, pipe, tau, 1) - ms_T[-1]
 
     # live per-launch timings: launch-per-phase driver, every launch repeated
@@ -187,11 +225,11 @@ def main():
                                "prefix 816 (width 2048), chunk 50x32, 10 Euler steps",
                    "batch": 1, "solver_steps": cfg.n_steps, "prefix_len": cfg.prefix_len, "chunk": cfg.n_action,
                    "parallelism": "single GPU"},
-        "denoise_step_us": round(step_us, 2),
-        "chunk_fixed_us": round(intercept * 1000.0, 2),
+        "denoise_step_us": None if np.isnan(step_us) else round(step_us, 2),
+        "chunk_fixed_us": None if np.isnan(intercept) else round(intercept * 1000.0, 2),
         "prefix_kv_build_us": round(ms_build * 1000.0, 2),
         "denoise_T_us": {str(T): round(v * 1000.0, 2) for T, v in zip(Ts, ms_T)},
-        "step_hbm_frac": round(step_bytes / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+        "step_hbm_frac": None if np.isnan(step_us) else round(step_bytes / (step_us * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
         "roofline": roof,
     }
     pipe.close()

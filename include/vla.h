@@ -151,9 +151,9 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
 
 /* Options:
  *  VLA_OPT_LOOP_MODE: loop driver of vla_denoise, 0 = one launch per phase on
- *    the stream, 1 (default) = the same launches captured once in a HIP graph
- *    and replayed, 2 = one persistent cooperative kernel for the whole step
- *    loop where the model supports it (batch 1, bf16, joint attention,
+ *    the stream, 1 = the same launches captured once in a HIP graph and
+ *    replayed, 2 (default) = one persistent cooperative kernel for the whole
+ *    step loop where the model supports it (batch 1, bf16, joint attention,
  *    H % 8 == 0 and the shape limits of the team layout), else as 1.
  *  VLA_OPT_PROFILE: R in 1..1000 = time every launch of the following
  *    vla_denoise calls with HIP events (launch-per-phase driver; read with

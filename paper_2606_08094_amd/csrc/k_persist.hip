@@ -43,6 +43,7 @@ constexpr int LDX = 16;                  // loads of exchanged data: device-cohe
 constexpr int STL = 0;                   // stores of exchanged data: plain (write through to L2)
 constexpr int SC1 = 16;                  // device-coherent policy of the cross-team deltas
 constexpr int KBA_MAX = 2;               // 32-key blocks per attention split
+constexpr int MB = 16;                   // key splits merged per round of loads (more spills registers)
 constexpr long SPIN_LIMIT = 1L << 21;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -834,17 +835,17 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
           for (int e = 0; e < 8; ++e) acc8[e] = 0.f;
           if (m < n) {
             float mx = -INFINITY, tot = 0.f;
-            for (int s0 = 0; s0 < S; s0 += 16) {
-              uint4 v[16];
-              float2 st[16];
+            for (int s0 = 0; s0 < S; s0 += MB) {
+              uint4 v[MB];
+              float2 st[MB];
 #pragma unroll
-              for (int q = 0; q < 16; ++q) {
+              for (int q = 0; q < MB; ++q) {
                 const bool ok = s0 + q < S;   // absent splits read (0, 0): skipped below
                 st[q] = ld8f<LDX>(ASr, ok ? (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u : OOB);
                 v[q] = ld16<LDX>(APr, ok ? (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u : OOB);
               }
 #pragma unroll
-              for (int q = 0; q < 16; ++q) {
+              for (int q = 0; q < MB; ++q) {
                 if (s0 + q >= S || st[q].y <= 0.f) continue;
                 const float mnew = fmaxf(mx, st[q].x);
                 const float corr = exp2f(mx - mnew);
@@ -1033,10 +1034,7 @@ bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, 
   const int nblocks = (P + 31) / 32 + (n + 31) / 32;
   int k = 1;
   while ((nblocks + k - 1) / k > TSIZE) ++k;
-#ifndef VLA_PERSIST_KBA_MIN
-#define VLA_PERSIST_KBA_MIN 2
-#endif
-  if (k < VLA_PERSIST_KBA_MIN && nblocks > 16) k = VLA_PERSIST_KBA_MIN;  // fewer, larger splits: less merge traffic
+  if (k < 2 && nblocks > 16) k = 2;          // fewer, larger splits: one merge round, shorter phase
   if (k > KBA_MAX) return false;
   *kba = k;
   *nsplit = (nblocks + k - 1) / k;

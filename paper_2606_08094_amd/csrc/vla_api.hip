@@ -134,7 +134,7 @@ struct vla_model {
   std::vector<std::vector<SubW>> layers;
   std::map<std::tuple<int, int, int, int>, std::unique_ptr<Plan>> plans;
   std::map<std::pair<int, int>, std::unique_ptr<PrefixWs>> prefix_ws;
-  int loop_mode = 1;
+  int loop_mode = 2;
   int profile = 0;
   int trace = 0;                  // record the persistent kernel's phase timeline
   int attn_splits = 0;            // key splits of the launch-per-phase attention (0 = automatic)
