@@ -571,10 +571,14 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 
   // attention split of this rank
   const int npre = a.P, nself = n;
-  const int nbp = (npre + 31) / 32, nbs = (nself + 31) / 32;
+  const int nbp = (npre + 31) / 32;
+  // Key splits: the prefix blocks in groups of kba, then one split per block
+  // of chunk-token keys (whose K / V arrive with this step's Q phase, so the
+  // split that holds them is the phase's longest path).
+  const int nps = (nbp + a.kba - 1) / a.kba;
   const bool att_on = rank < S;
-  const int jbeg = rank * a.kba;
-  const int nblk = att_on ? min(nbp + nbs, jbeg + a.kba) - jbeg : 0;
+  const int jbeg = rank < nps ? rank * a.kba : nbp + (rank - nps);
+  const int nblk = att_on ? (rank < nps ? min(nbp, jbeg + a.kba) : jbeg + 1) - jbeg : 0;
   uint4 kpre[NKI], vp0[NVI], vp1[NVI];
   auto prefetch_kv = [&](int l) {
     const bf16_t* kc = kvbase + lt[l].cache_off + (size_t)gteam * npre * HD;
@@ -1031,13 +1035,13 @@ bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, 
   if (F % 128 != 0 || F / 8 > 1024 || F / 128 > TSIZE) return false;  // h groups: one per rank
   (void)glu;
   if (A < 1 || A > 32) return false;         // head and embedding registers
-  const int nblocks = (P + 31) / 32 + (n + 31) / 32;
+  const int nbp = (P + 31) / 32, nbs = (n + 31) / 32;   // prefix and chunk-token key blocks
   int k = 1;
-  while ((nblocks + k - 1) / k > TSIZE) ++k;
-  if (k < 2 && nblocks > 16) k = 2;          // fewer, larger splits: one merge round, shorter phase
+  while ((nbp + k - 1) / k + nbs > TSIZE) ++k;
+  if (k < 2 && nbp > 16) k = 2;              // fewer, larger splits: one merge round, shorter phase
   if (k > KBA_MAX) return false;
   *kba = k;
-  *nsplit = (nblocks + k - 1) / k;
+  *nsplit = (nbp + k - 1) / k + nbs;
   return true;
 }
 
