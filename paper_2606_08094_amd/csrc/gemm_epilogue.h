@@ -47,9 +47,11 @@ __device__ __forceinline__ void wave_epilogue(const GemmArgs& a, const f32x4 (&a
             const int n = nb + s * 16 + r16;
             if (m < M && n < N) {
               const int b = m / a.P, p = m - b * a.P;
-              const int kv = n / a.d_kv, rem = n - kv * a.d_kv;
+              const int slot = a.lay_cols > 0 ? n / a.lay_cols : 0;
+              const int nl = n - slot * a.lay_cols;
+              const int kv = nl / a.d_kv, rem = nl - kv * a.d_kv;
               const int g = rem / a.hd, c = rem - g * a.hd;
-              const size_t idx = ((((size_t)kv * a.B + b) * G + g) * a.P + p) * a.hd + c;
+              const size_t idx = (size_t)slot * a.lay_stride + ((((size_t)kv * a.B + b) * G + g) * a.P + p) * a.hd + c;
               reinterpret_cast<T*>(a.cache)[idx] = ElemTraits<T>::from_f(acc[ms][s][i]);
             }
           }

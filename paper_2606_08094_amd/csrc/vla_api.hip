@@ -127,6 +127,7 @@ struct vla_model {
   int d = 0, dq = 0, dkv = 0, ns = 0, Lc = 0;
   std::vector<void*> allocs;
   void *W_in = nullptr, *W_s = nullptr, *E_pos = nullptr, *W_out = nullptr;
+  void* kvc_all = nullptr;  // dense models: every cache slot's [W_kc | W_vc] stacked in slot order
   float *b_in = nullptr, *b_s = nullptr, *b_out = nullptr;
   void *W_t1 = nullptr, *W_t2 = nullptr, *W_fm = nullptr, *W_mod = nullptr;
   float *b_t1 = nullptr, *b_t2 = nullptr, *b_fm = nullptr, *b_mod = nullptr;
@@ -1048,6 +1049,16 @@ vla_status create_impl(const vla_config* cfg, const void* const* weights, int32_
   }
   if (tr.i != n_weights)
     return fail(VLA_E_ARG, "weight table has %d entries, expected %d", n_weights, tr.i);
+  if (!m->tern && cidx > 0) {
+    // one [Lc * 2 d_kv][d_p] matrix so that the prefix build is a single GEMM
+    const size_t slot_bytes = (size_t)2 * dkv * dp * es;
+    VLA_TRY(al(&m->kvc_all, (size_t)cidx * slot_bytes));
+    for (auto& lay : m->layers)
+      for (auto& sw : lay)
+        if (sw.cache_idx >= 0)
+          HIP_TRY(hipMemcpy((char*)m->kvc_all + (size_t)sw.cache_idx * slot_bytes, sw.kvc, slot_bytes,
+                            hipMemcpyDeviceToDevice));
+  }
   HIP_TRY(hipStreamCreateWithFlags(&m->cap_stream, hipStreamNonBlocking));
   HIP_TRY(hipDeviceSynchronize());
   *out = m.release();
@@ -1113,6 +1124,18 @@ vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t 
     QuantArgs q{};
     q.M = M; q.K = K; q.x = prefix_hidden; q.ldx = K; q.src_type = 1; q.q = w->q8; q.r = w->r8;
     HIP_TRY(launch_quantize(q, s));
+  }
+  if (m->kvc_all) {
+    // every layer's cross K/V in one GEMM: column n of slot n / (2 d_kv)
+    GemmArgs g{};
+    g.M = M; g.N = N * m->Lc; g.K = K; g.X = prefix_hidden; g.ldx = K; g.W = m->kvc_all;
+    g.epi = EPI_KVCACHE;
+    g.cache = kv_cache;
+    g.P = prefix_len; g.hd = hd; g.d_kv = m->dkv; g.B = batch;
+    g.lay_cols = N;
+    g.lay_stride = layer_block;
+    HIP_TRY(launch_dense(m->et, dense_launch(m->et, g, 1), g, s));
+    return VLA_OK;
   }
   for (auto& lay : m->layers)
     for (auto& sw : lay) {

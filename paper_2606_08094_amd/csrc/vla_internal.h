@@ -58,9 +58,11 @@ struct GemmArgs {
   int step;
   int regression;
   int last;
-  // EPI_KVCACHE: row m = b*P + p, column n = kv*d_kv + g*hd + c
-  void* cache;             // layer base: [2][B][G][P][hd]
+  // EPI_KVCACHE: row m = b*P + p, column n = slot*lay_cols + kv*d_kv + g*hd + c
+  void* cache;             // base of cache slot 0: [slots][2][B][G][P][hd]
   int P, hd, d_kv, B;
+  int lay_cols;            // columns per cache slot (2 d_kv) when one GEMM fills several slots, else 0
+  size_t lay_stride;       // elements per cache slot
 };
 
 struct AttnArgs {
