@@ -43,7 +43,7 @@ constexpr int LDX = 16;                  // loads of exchanged data: device-cohe
 constexpr int STL = 0;                   // stores of exchanged data: plain (write through to L2)
 constexpr int SC1 = 16;                  // device-coherent policy of the cross-team deltas
 constexpr int KBA_MAX = 2;               // 32-key blocks per attention split
-constexpr int MB = 16;                   // key splits merged per round of loads (more spills registers)
+constexpr int MB = 8;                    // key splits one of a vector's 4 merge threads loads (S <= 32)
 constexpr long SPIN_LIMIT = 1L << 21;
 constexpr float kLog2e = 1.4426950408889634f;
 
@@ -826,42 +826,56 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       mark();
 
       // ---- M: merge the key splits; rank (t, cb) merges query tile t, columns
-      // [cb * HTD / 8, (cb + 1) * HTD / 8) of the team's heads into o_team -------
+      // [cb * HTD / 8, (cb + 1) * HTD / 8) of the team's heads into o_team.  Four
+      // threads share each 8-column vector: thread quarter q merges splits
+      // q, q+4, ... (one round of loads), then the four combine through lane
+      // shuffles.
       if (ot < QT) {
         const int cw8 = HTD / 8;                          // merged columns per rank (8 .. 32)
-        const int nv = 16 * (cw8 / 8);                    // 16-byte vectors
-        for (int i = tid; i < nv; i += NTHR) {
+        const int nv = 16 * (cw8 / 8);                    // 16-byte vectors (<= 64)
+        const int i = tid >> 2, qtr = tid & 3;
+        if (i < nv) {
           const int rr = i / (cw8 / 8), cv = ocb * (cw8 / 8) + (i - rr * (cw8 / 8));
           const int m = 16 * ot + rr;
           const int hh = (cv * 8) / HD;
+          const bool live = m < n;
           float acc8[8];
 #pragma unroll
           for (int e = 0; e < 8; ++e) acc8[e] = 0.f;
-          if (m < n) {
-            float mx = -INFINITY, tot = 0.f;
-            for (int s0 = 0; s0 < S; s0 += MB) {
-              uint4 v[MB];
-              float2 st[MB];
+          float mx = -INFINITY, tot = 0.f;
+          uint4 v[MB];
+          float2 st[MB];
 #pragma unroll
-              for (int q = 0; q < MB; ++q) {
-                const bool ok = s0 + q < S;   // absent splits read (0, 0): skipped below
-                st[q] = ld8f<LDX>(ASr, ok ? (unsigned)((((s0 + q) * n + m) * HT + hh) * 2) * 4u : OOB);
-                v[q] = ld16<LDX>(APr, ok ? (unsigned)(((s0 + q) * n + m) * HTD + cv * 8) * 2u : OOB);
-              }
+          for (int q = 0; q < MB; ++q) {
+            const int sp = qtr + 4 * q;
+            const bool ok = live && sp < S;   // absent splits read (0, 0): skipped below
+            st[q] = ld8f<LDX>(ASr, ok ? (unsigned)(((sp * n + m) * HT + hh) * 2) * 4u : OOB);
+            v[q] = ld16<LDX>(APr, ok ? (unsigned)((sp * n + m) * HTD + cv * 8) * 2u : OOB);
+          }
 #pragma unroll
-              for (int q = 0; q < MB; ++q) {
-                if (s0 + q >= S || st[q].y <= 0.f) continue;
-                const float mnew = fmaxf(mx, st[q].x);
-                const float corr = exp2f(mx - mnew);
-                const float w = st[q].y * exp2f(st[q].x - mnew);
-                float f[8];
-                unpack16(v[q], f, bf16_t());
+          for (int q = 0; q < MB; ++q) {
+            if (st[q].y <= 0.f) continue;
+            const float mnew = fmaxf(mx, st[q].x);
+            const float corr = exp2f(mx - mnew);
+            const float w = st[q].y * exp2f(st[q].x - mnew);
+            float f[8];
+            unpack16(v[q], f, bf16_t());
 #pragma unroll
-                for (int e = 0; e < 8; ++e) acc8[e] = acc8[e] * corr + w * f[e];
-                tot = tot * corr + w;
-                mx = mnew;
-              }
-            }
+            for (int e = 0; e < 8; ++e) acc8[e] = acc8[e] * corr + w * f[e];
+            tot = tot * corr + w;
+            mx = mnew;
+          }
+#pragma unroll
+          for (int sh = 1; sh <= 2; sh <<= 1) {
+            const float mo = __shfl_xor(mx, sh, 64), to = __shfl_xor(tot, sh, 64);
+            const float mn = fmaxf(mx, mo);
+            const float cs = tot > 0.f ? exp2f(mx - mn) : 0.f, co = to > 0.f ? exp2f(mo - mn) : 0.f;
+#pragma unroll
+            for (int e = 0; e < 8; ++e) acc8[e] = acc8[e] * cs + __shfl_xor(acc8[e], sh, 64) * co;
+            tot = tot * cs + to * co;
+            mx = mn;
+          }
+          if (live && qtr == 0) {
             const float inv = tot > 0.f ? 1.0f / tot : 0.f;
 #pragma unroll
             for (int e = 0; e < 8; ++e) acc8[e] *= inv;
@@ -1038,7 +1052,7 @@ bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, 
   const int nbp = (P + 31) / 32, nbs = (n + 31) / 32;   // prefix and chunk-token key blocks
   int k = 1;
   while ((nbp + k - 1) / k + nbs > TSIZE) ++k;
-  if (k < 2 && nbp > 16) k = 2;              // fewer, larger splits: one merge round, shorter phase
+  if (k < 2 && nbp > 16) k = 2;              // fewer, larger splits: shorter attention phase
   if (k > KBA_MAX) return false;
   *kba = k;
   *nsplit = (nbp + k - 1) / k + nbs;
