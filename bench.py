@@ -134,6 +134,47 @@ def cpu_baseline(cfg, W, inp, tau):
                       f"{dt:.1f} s, numpy fp64"}
 
 
+def measure_workload(torch, wl, Pipeline, name, batch, reps):
+    """Chunk time, per-step latency and per-step roofline fractions of one
+    workload (default loop driver)."""
+    import numpy as np
+    cfg = wl.CONFIGS[name].with_(batch=batch)
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, batch)
+    T = cfg.n_steps
+    tau = wl.uniform_schedule(T)
+    pipe = Pipeline(cfg, W, inp, loop_mode=LOOP_MODE)
+    try:
+        for _ in range(2):
+            pipe.build_cache()
+            pipe.denoise(tau)
+        ms_chunk = time_chunks(torch, pipe, tau, reps)
+        Ts = [1, T] if T > 1 else [1]
+        ms_T = []
+        for t in Ts:
+            tt = wl.uniform_schedule(t)
+            pipe.denoise(tt)
+            ms_T.append(min(time_denoise(torch, pipe, tt, reps) for _ in range(2)))
+        step_ms = (ms_T[-1] - ms_T[0]) / (T - 1) if T > 1 else ms_T[0]
+        pipe.model.set_profile(5)
+        pipe.denoise(tau)
+        torch.cuda.synchronize()
+        ops = pipe.model.profile_read()
+        pipe.model.set_profile(0)
+    finally:
+        pipe.close()
+    step_bytes = sum(o["bytes"] for o in ops) / T
+    step_flops = sum(o["flops"] for o in ops) / T
+    roof = roofline_from_profile(ops, T)
+    return {"workload": name, "batch": batch, "solver_steps": T, "chunk_ms": round(ms_chunk, 4),
+            "step_us": round(step_ms * 1000.0, 2), "alg_bytes_per_step": int(step_bytes),
+            "alg_flops_per_step": int(step_flops),
+            "step_hbm_frac": round(step_bytes / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
+            "step_mfma_frac": round(step_flops / (step_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
+            "dominant_kernel": roof["kernel"], "dominant_launch_us": roof["launch_us"],
+            "dominant_frac_hbm": roof["frac"], "dominant_share": roof["share_of_profiled_time"]}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -143,6 +184,9 @@ def main():
     ap.add_argument("--no-sweep", action="store_true",
                     help="skip the T-sweep fit (every launch then runs the workload's T, so profiler "
                          "averages compare directly with the roofline launch time)")
+    ap.add_argument("--workloads", action="store_true",
+                    help="instead of the headline line, measure the other scope workloads (SmolVLA-shaped, "
+                         "ternary W2A8, pi0 stress at batch 1/4/16) and print one JSON line each")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="only run 5 plain device-to-device copies of this many MiB (calibrates the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
@@ -168,6 +212,13 @@ def main():
     import torch
     import workloads as wl
     from vla_testlib import Pipeline
+
+    if args.workloads:
+        for name, batch in (("smolvla_bf16", 1), ("ternary_w2a8", 1), ("stress_pi0", 1), ("stress_pi0", 4),
+                            ("stress_pi0", 16)):
+            log(f"workload {name} batch {batch} ...")
+            print(json.dumps(measure_workload(torch, wl, Pipeline, name, batch, 5)), flush=True)
+        return
 
     cfg = wl.CONFIGS[WORKLOAD]
     log("generating weights ...")
