@@ -6,12 +6,14 @@
 //
 // One workgroup handles (request b, 16-query tile, K/V head g, key split) with
 // one wave per query head of the group, so the split's K/V blocks (32 keys
-// each, up to KB of them) are staged in LDS once and serve every head that
-// shares them.  All global loads of the workgroup -- the Q fragments of every
-// wave and the K/V of every block of the split -- are issued before the first
-// LDS store, so the workgroup pays one memory latency, then runs the blocks
-// from LDS.  Prefix blocks and action-token blocks never mix, so a block has a
-// single source.
+// each) are staged in LDS once and serve every head that shares them.  A split
+// of any length is processed in chunks of up to KB_MAX blocks: all global
+// loads of a chunk are issued before its first LDS store, and the online
+// softmax state carries from chunk to chunk.  Workgroups that read the same
+// K/V (same request, head and split) get consecutive unit numbers, and the
+// unit numbering follows the dispatcher's round robin over the 8 XCDs so that
+// those workgroups share one XCD's L2.  Prefix blocks and action-token blocks
+// never mix, so a block has a single source.
 //
 // Scores are computed transposed, S^T = K Q^T on MFMA, so each lane's column is
 // one query and the online-softmax statistics live in the lane.  Row rho of
@@ -60,15 +62,18 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   const int per = a.H / a.G;          // query heads per K/V head
   const int hpw = per / a.hsplit;     // of them in this workgroup (= waves)
   const int QT = (a.n + 15) / 16;
-  int u = blockIdx.x;
+  // workgroup i runs on XCD i % 8: unit (i % 8) * (grid / 8) + i / 8 puts
+  // consecutive units on one XCD (the grid is padded to a multiple of 8)
+  const int units = a.B * QT * a.G * a.hsplit * a.kv_split;
+  int u = (int)(blockIdx.x % 8u) * (int)(gridDim.x / 8u) + (int)(blockIdx.x / 8u);
+  if (u >= units) return;
+  const int qh = u % (QT * a.hsplit);
+  u /= QT * a.hsplit;
+  const int qt = qh / a.hsplit, hs = qh - qt * a.hsplit;
   const int split = u % a.kv_split;
   u /= a.kv_split;
-  const int hs = u % a.hsplit;
-  u /= a.hsplit;
   const int g = u % a.G;
-  u /= a.G;
-  const int qt = u % QT;
-  const int b = u / QT;
+  const int b = u / a.G;
   const int h = g * per + hs * hpw + wave;
 
   const int npre = (a.mode == 0) ? 0 : a.P;
@@ -106,132 +111,137 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
 #pragma unroll
   for (int c = 0; c < NQV; ++c) qf[c] = (qrow < a.n) ? ldg16(qp + c * E) : make_uint4(0, 0, 0, 0);
 
-  // Stage every block of the split.  K item i: vector i % VPR of key row
-  // (i / VPR) % 32 of block i / (32 VPR).  V item i: vector i / 16 % VPR of the
-  // key pair i % 16, block i / (16 VPR); a pair is written as one 2-element
-  // column of V^T.  Keys past the end are zero (no NaN from unwritten LDS).
-  const int nk = nblk * 32 * VPR, nv = nblk * 16 * VPR;
-  for (int base = threadIdx.x; base < nk; base += UB * nthr) {
-    uint4 kr4[UB], v0[UB], v1[UB];
-#pragma unroll
-    for (int q = 0; q < UB; ++q) {
-      const int i = base + q * nthr;
-      kr4[q] = make_uint4(0, 0, 0, 0);
-      v0[q] = make_uint4(0, 0, 0, 0);
-      v1[q] = make_uint4(0, 0, 0, 0);
-      const T *kp, *vp;
-      if (i < nk) {
-        const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
-        const int kr = r / VPR, cv = r - kr * VPR;
-        if (src(jb, kr, kp, vp)) kr4[q] = ldg16(kp + cv * E);
-      }
-      if (i < nv) {
-        const int jb = i / (16 * VPR), r = i - jb * 16 * VPR;
-        const int kp2 = r & 15, cv = r >> 4;
-        if (src(jb, 2 * kp2, kp, vp)) v0[q] = ldg16(vp + cv * E);
-        if (src(jb, 2 * kp2 + 1, kp, vp)) v1[q] = ldg16(vp + cv * E);
-      }
-    }
-#pragma unroll
-    for (int q = 0; q < UB; ++q) {
-      const int i = base + q * nthr;
-      if (i < nk) {
-        const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
-        const int kr = r / VPR, cv = r - kr * VPR;
-        T* kl = reinterpret_cast<T*>(smem + jb * L::BUF);
-        *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * E) = kr4[q];
-      }
-      if (i < nv) {
-        const int jb = i / (16 * VPR), r = i - jb * 16 * VPR;
-        const int kp2 = r & 15, cv = r >> 4;
-        T* vl = reinterpret_cast<T*>(smem + jb * L::BUF + L::KBYTES);
-        const uint32_t a4[4] = {v0[q].x, v0[q].y, v0[q].z, v0[q].w};
-        const uint32_t b4[4] = {v1[q].x, v1[q].y, v1[q].z, v1[q].w};
-        if constexpr (E == 8) {
-#pragma unroll
-          for (int e = 0; e < 8; ++e) {
-            const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-            *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
-          }
-        } else {
-#pragma unroll
-          for (int e = 0; e < 4; ++e)
-            *reinterpret_cast<uint2*>(vl + (cv * 4 + e) * L::VP + 2 * kp2) = make_uint2(a4[e], b4[e]);
-        }
-      }
-    }
-  }
-  __syncthreads();
-
   f32x4 o[DT];
 #pragma unroll
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.0f;
   const float sc = a.scale * kLog2e;
 
-  for (int jb = 0; jb < nblk; ++jb) {
-    const int j = jbeg + jb;
-    const int cnt = j < nbp ? min(32, npre - j * 32) : min(32, nself - (j - nbp) * 32);
-    const T* kl = reinterpret_cast<const T*>(smem + jb * L::BUF);
-    const T* vl = reinterpret_cast<const T*>(smem + jb * L::BUF + L::KBYTES);
+  for (int c0 = 0; c0 < nblk; c0 += KB_MAX) {
+    const int cb = min(KB_MAX, nblk - c0);
+    if (c0 > 0) __syncthreads();   // the previous chunk's LDS reads are done
+    // Stage blocks c0 .. c0+cb-1 of the split into LDS slots 0 .. cb-1.  K item
+    // i: vector i % VPR of key row (i / VPR) % 32 of slot i / (32 VPR).  V item
+    // i: vector i / 16 % VPR of the key pair i % 16, slot i / (16 VPR); a pair
+    // is written as one 2-element column of V^T.  Keys past the end are zero
+    // (no NaN from unwritten LDS).
+    const int nk = cb * 32 * VPR, nv = cb * 16 * VPR;
+    for (int base = threadIdx.x; base < nk; base += UB * nthr) {
+      uint4 kr4[UB], v0[UB], v1[UB];
+#pragma unroll
+      for (int q = 0; q < UB; ++q) {
+        const int i = base + q * nthr;
+        kr4[q] = make_uint4(0, 0, 0, 0);
+        v0[q] = make_uint4(0, 0, 0, 0);
+        v1[q] = make_uint4(0, 0, 0, 0);
+        const T *kp, *vp;
+        if (i < nk) {
+          const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
+          const int kr = r / VPR, cv = r - kr * VPR;
+          if (src(c0 + jb, kr, kp, vp)) kr4[q] = ldg16(kp + cv * E);
+        }
+        if (i < nv) {
+          const int jb = i / (16 * VPR), r = i - jb * 16 * VPR;
+          const int kp2 = r & 15, cv = r >> 4;
+          if (src(c0 + jb, 2 * kp2, kp, vp)) v0[q] = ldg16(vp + cv * E);
+          if (src(c0 + jb, 2 * kp2 + 1, kp, vp)) v1[q] = ldg16(vp + cv * E);
+        }
+      }
+#pragma unroll
+      for (int q = 0; q < UB; ++q) {
+        const int i = base + q * nthr;
+        if (i < nk) {
+          const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
+          const int kr = r / VPR, cv = r - kr * VPR;
+          T* kl = reinterpret_cast<T*>(smem + jb * L::BUF);
+          *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * E) = kr4[q];
+        }
+        if (i < nv) {
+          const int jb = i / (16 * VPR), r = i - jb * 16 * VPR;
+          const int kp2 = r & 15, cv = r >> 4;
+          T* vl = reinterpret_cast<T*>(smem + jb * L::BUF + L::KBYTES);
+          const uint32_t a4[4] = {v0[q].x, v0[q].y, v0[q].z, v0[q].w};
+          const uint32_t b4[4] = {v1[q].x, v1[q].y, v1[q].z, v1[q].w};
+          if constexpr (E == 8) {
+#pragma unroll
+            for (int e = 0; e < 8; ++e) {
+              const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+              const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
+              *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
+            }
+          } else {
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+              *reinterpret_cast<uint2*>(vl + (cv * 4 + e) * L::VP + 2 * kp2) = make_uint2(a4[e], b4[e]);
+          }
+        }
+      }
+    }
+    __syncthreads();
 
-    // scores: tile t, row rho = r16 -> key 8*(rho/4) + 4t + rho%4
-    f32x4 s[2];
+    for (int jb = 0; jb < cb; ++jb) {
+      const int j = jbeg + c0 + jb;
+      const int cnt = j < nbp ? min(32, npre - j * 32) : min(32, nself - (j - nbp) * 32);
+      const T* kl = reinterpret_cast<const T*>(smem + jb * L::BUF);
+      const T* vl = reinterpret_cast<const T*>(smem + jb * L::BUF + L::KBYTES);
+
+      // scores: tile t, row rho = r16 -> key 8*(rho/4) + 4t + rho%4
+      f32x4 s[2];
 #pragma unroll
-    for (int t = 0; t < 2; ++t) {
-      s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const int kr = 8 * (r16 >> 2) + 4 * t + (r16 & 3);
-      const T* krow = kl + kr * L::KP + g4 * (HD / 4);
+      for (int t = 0; t < 2; ++t) {
+        s[t] = f32x4{0.f, 0.f, 0.f, 0.f};
+        const int kr = 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+        const T* krow = kl + kr * L::KP + g4 * (HD / 4);
 #pragma unroll
-      for (int c = 0; c < NQV; ++c) mma16(s[t], *reinterpret_cast<const uint4*>(krow + c * E), qf[c], T());
-    }
-    // lane holds keys 8*g4 + 4t + i for query r16
-    float bmax = -INFINITY;
-    float p[8];
-#pragma unroll
-    for (int t = 0; t < 2; ++t)
-#pragma unroll
-      for (int i = 0; i < 4; ++i) {
-        const int kr = 8 * g4 + 4 * t + i;
-        const float v = (kr < cnt) ? s[t][i] * sc : -INFINITY;
-        p[4 * t + i] = v;
-        bmax = fmaxf(bmax, v);
+        for (int c = 0; c < NQV; ++c) mma16(s[t], *reinterpret_cast<const uint4*>(krow + c * E), qf[c], T());
       }
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
-    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-    const float mnew = fmaxf(mrun, bmax);
-    const float corr = exp2f(mrun - mnew);
-    float psum = 0.0f;
+      // lane holds keys 8*g4 + 4t + i for query r16
+      float bmax = -INFINITY;
+      float p[8];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      p[k] = exp2f(p[k] - mnew);
-      psum += p[k];
-    }
-    psum += __shfl_xor(psum, 16, 64);
-    psum += __shfl_xor(psum, 32, 64);
-    lrun = lrun * corr + psum;
-    mrun = mnew;
+      for (int t = 0; t < 2; ++t)
 #pragma unroll
-    for (int d = 0; d < DT; ++d) o[d] *= corr;
-    // O^T += V^T P^T: k slot k of lane group g4 is key 8*g4 + k.
-    if constexpr (E == 8) {
-      uint4 pb;
-      pb.x = pack_bf16x2(p[0], p[1]);
-      pb.y = pack_bf16x2(p[2], p[3]);
-      pb.z = pack_bf16x2(p[4], p[5]);
-      pb.w = pack_bf16x2(p[6], p[7]);
+        for (int i = 0; i < 4; ++i) {
+          const int kr = 8 * g4 + 4 * t + i;
+          const float v = (kr < cnt) ? s[t][i] * sc : -INFINITY;
+          p[4 * t + i] = v;
+          bmax = fmaxf(bmax, v);
+        }
+      bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+      bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+      const float mnew = fmaxf(mrun, bmax);
+      const float corr = exp2f(mrun - mnew);
+      float psum = 0.0f;
 #pragma unroll
-      for (int d = 0; d < DT; ++d) {
-        const uint4 va = *reinterpret_cast<const uint4*>(vl + (d * 16 + r16) * L::VP + 8 * g4);
-        mma16(o[d], va, pb, T());
+      for (int k = 0; k < 8; ++k) {
+        p[k] = exp2f(p[k] - mnew);
+        psum += p[k];
       }
-    } else {
+      psum += __shfl_xor(psum, 16, 64);
+      psum += __shfl_xor(psum, 32, 64);
+      lrun = lrun * corr + psum;
+      mrun = mnew;
 #pragma unroll
-      for (int d = 0; d < DT; ++d) {
-        const float* vrow = reinterpret_cast<const float*>(vl) + (d * 16 + r16) * L::VP + 8 * g4;
+      for (int d = 0; d < DT; ++d) o[d] *= corr;
+      // O^T += V^T P^T: k slot k of lane group g4 is key 8*g4 + k.
+      if constexpr (E == 8) {
+        uint4 pb;
+        pb.x = pack_bf16x2(p[0], p[1]);
+        pb.y = pack_bf16x2(p[2], p[3]);
+        pb.z = pack_bf16x2(p[4], p[5]);
+        pb.w = pack_bf16x2(p[6], p[7]);
 #pragma unroll
-        for (int k = 0; k < 8; ++k) o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vrow[k], p[k], o[d], 0, 0, 0);
+        for (int d = 0; d < DT; ++d) {
+          const uint4 va = *reinterpret_cast<const uint4*>(vl + (d * 16 + r16) * L::VP + 8 * g4);
+          mma16(o[d], va, pb, T());
+        }
+      } else {
+#pragma unroll
+        for (int d = 0; d < DT; ++d) {
+          const float* vrow = reinterpret_cast<const float*>(vl) + (d * 16 + r16) * L::VP + 8 * g4;
+#pragma unroll
+          for (int k = 0; k < 8; ++k) o[d] = __builtin_amdgcn_mfma_f32_16x16x4f32(vrow[k], p[k], o[d], 0, 0, 0);
+        }
       }
     }
   }
@@ -321,6 +331,7 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
   const int QT = (a.n + 15) / 16;
   const int units = a.B * QT * a.G * a.hsplit * a.kv_split;
   if (units <= 0) return hipSuccess;
+  const int grid = (units + 7) / 8 * 8;   // multiple of 8: XCD-aware unit numbering
   static bool attr = false;
   if (!attr) {
     hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_kernel<T, HD>),
@@ -331,10 +342,10 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
   if (a.hsplit < 1 || (a.H / a.G) % a.hsplit) return hipErrorInvalidValue;
   const int threads = 64 * (a.H / a.G / a.hsplit);
   using L = AttnLds<T, HD>;
-  if (a.key_chunk < 1 || a.key_chunk > KB_MAX) return hipErrorInvalidValue;
-  const size_t lds = (size_t)a.key_chunk * L::BUF;
+  if (a.key_chunk < 1) return hipErrorInvalidValue;
+  const size_t lds = (size_t)(a.key_chunk < KB_MAX ? a.key_chunk : KB_MAX) * L::BUF;
   if (which != 2) {
-    hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(units), dim3(threads), lds, s, a);
+    hipLaunchKernelGGL((attn_kernel<T, HD>), dim3(grid), dim3(threads), lds, s, a);
     hipError_t e = hipGetLastError();
     if (e != hipSuccess) return e;
   }
@@ -374,14 +385,26 @@ void attention_split(AttnArgs& a, int want_splits, int want_hsplit) {
     s = (112 + base - 1) / base;
   }
   s = s < 1 ? 1 : (s > nblocks ? nblocks : s);
-  int kc = (nblocks + s - 1) / s;
+  int kc = (nblocks + s - 1) / s;                            // blocks per split
   kc = kc < (nblocks + 63) / 64 ? (nblocks + 63) / 64 : kc;  // at most 64 splits
-  if (kc > KB_MAX) kc = KB_MAX;
+  if (want_splits <= 0 && kc > KB_MAX) {
+    // Splits of at most KB_MAX blocks run without a chunk loop; past about
+    // 1024 workgroups (large batches) the grid keeps that size instead and
+    // each split loops over its chunks, which also bounds the merge traffic.
+    const int base = a.B * QT * a.G * hs;
+    const int s_flat = (nblocks + KB_MAX - 1) / KB_MAX;
+    if ((long long)base * s_flat <= 1024) {
+      kc = KB_MAX;
+    } else {
+      const int s_big = 1024 / base > 1 ? 1024 / base : 1;
+      kc = (nblocks + s_big - 1) / s_big;
+    }
+  }
   a.key_chunk = kc;
   a.kv_split = (nblocks + kc - 1) / kc;
 }
 
-int attention_max_blocks() { return 64 * KB_MAX; }
+int attention_max_blocks() { return 1024; }   // 32768 keys (no kernel limit; bounds the workspace)
 
 size_t attention_part_bytes(int et, const AttnArgs& a) {
   if (a.kv_split <= 1) return 0;

@@ -78,6 +78,7 @@ ATTN_CASES = [
     (0, 0, 1, 8, 0, 4, 1, 64),         # tiny fp32 self
     (0, 1, 1, 8, 64, 4, 1, 64),        # tiny fp32 cross
     (0, 2, 2, 19, 45, 6, 3, 128),      # ragged fp32 joint
+    (1, 2, 3, 100, 2048, 8, 1, 256),   # stress shape: 68 key blocks, looped in chunks
 ]
 
 
