@@ -44,6 +44,26 @@ vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q,
 vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
                                    float scale, float* y, void* stream);
 
+/* Residual finish + adaRMS of the next sublayer (the row kernel that closes
+ * every residual branch, scope rows a4 and a7): for every row m of M,
+ *   x[m] += alpha * sum_{s < nsplit} part[s][m]      (alpha NULL: no update)
+ *   u[m]  = x[m] / sqrt(mean(x[m]^2) + eps) * (1 + gamma) + beta
+ * x [M][d] fp32 is updated in place; part [nsplit][M][d] fp32; alpha, gamma,
+ * beta [d] fp32; u [M][d] fp32 (u_f32 = 1) or elem (bf16 when elem = 1).
+ * d % 4 == 0, d <= 4096. */
+vla_status vla_test_adarms(int32_t elem, float* x, const float* part, int32_t nsplit, const float* alpha,
+                           const float* gamma, const float* beta, int32_t M, int32_t d, float eps, void* u,
+                           int32_t u_f32, void* stream);
+
+/* Time-conditioning precompute of a time-conditioned model (scope row a2):
+ * for the HOST schedule t_schedule [n_steps+1], step k uses tau_k:
+ * e = sinusoid(tau_k), c = W_t2 SiLU(W_t1 e + b_t1) + b_t2, and
+ *   mods [n_steps][L * 3 * n_sub * d] = W_mod SiLU(c) + b_mod   (every layer, stacked)
+ *   modf [n_steps][2 d]              = W_fm SiLU(c) + b_fm
+ * both fp32 device buffers.  VLA_E_UNSUPPORTED for a regression-head model. */
+vla_status vla_test_time_cond(struct vla_model* model, const float* t_schedule, int32_t n_steps, float* mods,
+                              float* modf, void* stream);
+
 /* Phase timeline of the model's last persistent vla_denoise call made with
  * VLA_OPT_TRACE = 1: for each of the 8 teams, max_per_team 100 MHz clock
  * values (before and after every barrier, in order; unused entries hold

@@ -1379,6 +1379,66 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
   return VLA_OK;
 }
 
+vla_status vla_test_adarms(int32_t elem, float* x, const float* part, int32_t nsplit, const float* alpha,
+                           const float* gamma, const float* beta, int32_t M, int32_t d, float eps, void* u,
+                           int32_t u_f32, void* stream) {
+  if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
+  if (!x || !gamma || !beta || !u || (nsplit > 0 && (!part || !alpha))) return fail(VLA_E_ARG, "NULL buffer");
+  for (const void* q : {(const void*)x, (const void*)part, (const void*)alpha, (const void*)gamma,
+                        (const void*)beta, (const void*)u})
+    if (q && !al16(q)) return fail(VLA_E_ARG, "buffers must be 16-byte aligned");
+  if (M < 1 || d < 4 || d % 4 || d > 4096 || nsplit < 0 || !(eps > 0.0f)) return fail(VLA_E_SHAPE, "bad shape");
+  RowNormArgs a{};
+  a.mode = 0; a.M = M; a.d = d; a.x = x; a.part = part; a.nsplit = nsplit; a.alpha = alpha;
+  a.gamma = gamma; a.beta = beta; a.eps = eps; a.u = u; a.u_f32 = u_f32 ? 1 : 0;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = launch_row_norm(elem, a, s);
+  hipError_t e2 = hipStreamSynchronize(s);
+  if (e != hipSuccess || e2 != hipSuccess)
+    return fail(VLA_E_DEVICE, "adarms: %s", hipGetErrorString(e != hipSuccess ? e : e2));
+  return VLA_OK;
+}
+
+vla_status vla_test_time_cond(vla_model* m, const float* t_schedule, int32_t n_steps, float* mods, float* modf,
+                              void* stream) {
+  if (!m) return fail(VLA_E_ARG, "model is NULL");
+  const vla_config& c = m->cfg;
+  if (c.head_regression) return fail(VLA_E_UNSUPPORTED, "regression heads have no time input");
+  if (!t_schedule || !mods || !modf || !al16(mods) || !al16(modf)) return fail(VLA_E_ARG, "bad buffer");
+  if (n_steps < 1 || n_steps > VLA_MAX_STEPS) return fail(VLA_E_SHAPE, "n_steps %d not in 1..%d", n_steps, VLA_MAX_STEPS);
+  for (int k = 0; k <= n_steps; ++k)
+    if (!std::isfinite(t_schedule[k])) return fail(VLA_E_ARG, "schedule entry %d is not finite", k);
+  const int T = n_steps, d = m->d, et = m->et;
+  const size_t es = esize(et);
+  const size_t modrow = (size_t)c.n_layers * 3 * m->ns * d;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  CallParams hp{};
+  for (int k = 0; k <= T; ++k) hp.tau[k] = t_schedule[k];
+  CallParams* cp = nullptr;
+  void *e = nullptr, *h1 = nullptr, *sc = nullptr;
+  hipError_t err = hipMalloc(&cp, sizeof(CallParams));
+  if (err == hipSuccess) err = hipMalloc(&e, (size_t)T * d * es);
+  if (err == hipSuccess) err = hipMalloc(&h1, (size_t)T * d * es);
+  if (err == hipSuccess) err = hipMalloc(&sc, (size_t)T * d * es);
+  if (err == hipSuccess) err = hipMemcpy(cp, &hp, sizeof(CallParams), hipMemcpyHostToDevice);
+  // the same launches the plan builder records for every vla_denoise call
+  if (err == hipSuccess) err = launch_time_embed(et, cp, e, T, T, d, s);
+  auto gemm = [&](const void* X, const void* W, int N, const float* bias, int act, void* out, int out_f32) {
+    GemmArgs g = gemm_base(m, T, N, d, X, d, W);
+    g.epi = EPI_STORE; g.bias = bias; g.act = act; g.out = out; g.ldo = N; g.out_f32 = out_f32;
+    return launch_dense(et, dense_launch(et, g, 1), g, s);
+  };
+  if (err == hipSuccess) err = gemm(e, m->W_t1, d, m->b_t1, ACT_SILU, h1, 0);
+  if (err == hipSuccess) err = gemm(h1, m->W_t2, d, m->b_t2, ACT_SILU, sc, 0);
+  if (err == hipSuccess) err = gemm(sc, m->W_mod, (int)modrow, m->b_mod, ACT_NONE, mods, 1);
+  if (err == hipSuccess) err = gemm(sc, m->W_fm, 2 * d, m->b_fm, ACT_NONE, modf, 1);
+  hipError_t e2 = hipStreamSynchronize(s);
+  (void)hipFree(cp); (void)hipFree(e); (void)hipFree(h1); (void)hipFree(sc);
+  if (err != hipSuccess || e2 != hipSuccess)
+    return fail(VLA_E_DEVICE, "time conditioning: %s", hipGetErrorString(err != hipSuccess ? err : e2));
+  return VLA_OK;
+}
+
 vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q, float* r, void* stream) {
   if (!x || !q || !r) return fail(VLA_E_ARG, "NULL buffer");
   if (M < 1 || K < 1 || K > 16384) return fail(VLA_E_SHAPE, "bad shape");

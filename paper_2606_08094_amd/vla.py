@@ -33,7 +33,7 @@ EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_
            "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
-           "vla_test_persist_trace"]
+           "vla_test_adarms", "vla_test_time_cond", "vla_test_persist_trace"]
 
 
 class VlaError(RuntimeError):
@@ -81,6 +81,8 @@ def lib():
         "vla_test_gemm": (i32, [i32, vp, vp, i32, i32, i32, i32, vp, vp]),
         "vla_test_attention": (i32, [i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]),
         "vla_test_quantize_i8": (i32, [vp, i32, i32, vp, vp, vp]),
+        "vla_test_adarms": (i32, [i32, vp, vp, i32, vp, vp, vp, i32, i32, ctypes.c_float, vp, i32, vp]),
+        "vla_test_time_cond": (i32, [vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp]),
         "vla_test_ternary_linear": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp]),
         "vla_test_persist_trace": (i32, [vp, ctypes.POINTER(ctypes.c_uint64), i32]),
     }
@@ -254,6 +256,18 @@ def test_attention(elem: int, mode: int, q, k_self, v_self, k_cache, v_cache, B:
                    G: int, hd: int, o, kv_split: int = 0, stream=None):
     _check(lib().vla_test_attention(elem, mode, _ptr(q), _ptr(k_self), _ptr(v_self), _ptr(k_cache),
                                     _ptr(v_cache), B, n, P, H, G, hd, kv_split, _ptr(o), _stream(stream)))
+
+
+def test_adarms(elem: int, x, part, nsplit: int, alpha, gamma, beta, M: int, d: int, eps: float, u,
+                u_f32: bool, stream=None):
+    _check(lib().vla_test_adarms(elem, _ptr(x), _ptr(part), nsplit, _ptr(alpha), _ptr(gamma), _ptr(beta), M, d,
+                                 eps, _ptr(u), int(bool(u_f32)), _stream(stream)))
+
+
+def test_time_cond(model: "Model", t_schedule: Sequence[float], mods, modf, stream=None):
+    tau = (ctypes.c_float * len(t_schedule))(*[float(t) for t in t_schedule])
+    _check(lib().vla_test_time_cond(model.handle, tau, len(t_schedule) - 1, _ptr(mods), _ptr(modf),
+                                    _stream(stream)))
 
 
 def test_quantize_i8(x, M: int, K: int, q, r, stream=None):

@@ -117,6 +117,85 @@ def test_attention_parity(torch, case, kv_split):
         assert err <= tol, f"request {b}: max err {err} > {tol}"
 
 
+@pytest.mark.parametrize("elem,u_f32,M,d,nsplit", [
+    (1, 0, 50, 1024, 4),    # pi0 width, bf16 u, four split-K partials
+    (1, 0, 50, 720, 0),     # SmolVLA width (d % 1024 != 0), no residual update
+    (0, 1, 8, 256, 3),      # tiny fp32 expert
+    (1, 1, 8, 2560, 2),     # ternary width: fp32 u for the int8 quantiser
+    (1, 0, 3, 4096, 1),     # widest row the kernel takes, ragged row count
+])
+def test_adarms_parity(torch, elem, u_f32, M, d, nsplit):
+    """Residual finish + adaRMS row kernel against the oracle's ada_rms on the
+    updated residual x + alpha * sum of the partials.  x is fp32 throughout;
+    u is compared after the kernel's own rounding of its output (bf16: 2^-8
+    relative), fp32 u at 1e-5 relative."""
+    rng = np.random.default_rng(100 + d + nsplit)
+    x = (rng.standard_normal((M, d)) * 3.0).astype(np.float32)
+    part = rng.standard_normal((max(nsplit, 1), M, d)).astype(np.float32)
+    alpha = rng.uniform(-1.0, 1.0, d).astype(np.float32)
+    gamma = (0.3 * rng.standard_normal(d)).astype(np.float32)
+    beta = (0.3 * rng.standard_normal(d)).astype(np.float32)
+    eps = 1e-6
+    xd = torch.from_numpy(x).cuda()
+    dev = {k: torch.from_numpy(v).cuda() for k, v in dict(part=part, alpha=alpha, gamma=gamma, beta=beta).items()}
+    u = torch.empty((M, d), dtype=torch.float32 if u_f32 or elem == 0 else torch.bfloat16, device="cuda")
+    _vla().test_adarms(elem, xd, dev["part"] if nsplit else None, nsplit, dev["alpha"] if nsplit else None,
+                       dev["gamma"], dev["beta"], M, d, eps, u, bool(u_f32))
+    x_ref = x.astype(np.float64)
+    if nsplit:
+        x_ref = x_ref + alpha.astype(np.float64) * part[:nsplit].astype(np.float64).sum(0)
+    u_ref = O.ada_rms(x_ref, gamma, beta, eps)
+    x_got = xd.cpu().numpy().astype(np.float64)
+    u_got = u.float().cpu().numpy().astype(np.float64)
+    assert np.abs(x_got - x_ref).max() <= 1e-5 * max(1.0, np.abs(x_ref).max())
+    rel = 2.0 ** -8 if (elem == 1 and not u_f32) else 1e-5
+    assert np.all(np.abs(u_got - u_ref) <= rel * np.abs(u_ref) + 1e-5), np.abs(u_got - u_ref).max()
+
+
+@pytest.mark.parametrize("name", ["tiny_f32", "pi0_bf16", "smolvla_bf16"])
+def test_time_cond_parity(torch, name):
+    """Time-conditioning precompute (sinusoid, time MLP, every layer's W_mod and
+    W_fm) for a non-uniform schedule against the oracle's primitives, rounded to
+    bf16 exactly where the kernels store bf16 (the embedding, SiLU(W_t1 e + b_t1)
+    and SiLU(c)); what remains is fp32 accumulation order."""
+    from vla_testlib import device_weights
+    cfg = wl.CONFIGS[name]
+    W = wl.make_weights(cfg)
+    tau = np.array([1.0, 0.83, 0.51, 0.5, 0.12, 0.0], np.float32)
+    T, d = len(tau) - 1, cfg.d_model
+    vla = _vla()
+    model = vla.Model(cfg, device_weights(cfg, W))
+    try:
+        rows = cfg.n_layers * 3 * cfg.n_sub * d
+        mods = torch.empty((T, rows), dtype=torch.float32, device="cuda")
+        modf = torch.empty((T, 2 * d), dtype=torch.float32, device="cuda")
+        vla.test_time_cond(model, list(tau), mods, modf)
+        got_m = mods.cpu().numpy().astype(np.float64)
+        got_f = modf.cpu().numpy().astype(np.float64)
+    finally:
+        model.close()
+    bf = cfg.wtype != "f32"
+    st = O.round_to_bf16 if bf else (lambda v: v)
+    W_mod = np.concatenate([W[f"L{l}.W_mod"] for l in range(cfg.n_layers)], 0)
+    b_mod = np.concatenate([W[f"L{l}.b_mod"] for l in range(cfg.n_layers)], 0)
+    for k in range(T):
+        e = st(O.time_embedding(float(tau[k]), d))
+        h1 = st(O.silu(O.linear(e, W["W_t1"], W["b_t1"])))
+        sc = st(O.silu(O.linear(h1, W["W_t2"], W["b_t2"])))
+        ref_m = O.linear(sc, W_mod, b_mod)
+        ref_f = O.linear(sc, W["W_fm"], W["b_fm"])
+        # fp32: accumulation order only.  bf16: a stored value that lies at a
+        # bf16 rounding boundary may round the other way on one side (one ulp,
+        # 2^-8 relative, of an element of |x| <= 1, weighted by |w| ~ 0.02)
+        tol = 1e-3 if bf else 1e-5
+        assert np.abs(got_m[k] - ref_m).max() <= tol, (k, np.abs(got_m[k] - ref_m).max())
+        assert np.abs(got_f[k] - ref_f).max() <= tol, (k, np.abs(got_f[k] - ref_f).max())
+        if not bf:  # fp32 models: the whole chain against the oracle's own modulation()
+            mods_o, fin_o = O.modulation(cfg, W, float(tau[k]))
+            flat = np.concatenate([np.concatenate([np.concatenate(gba) for gba in ml]) for ml in mods_o])
+            assert np.abs(got_m[k] - flat).max() <= 1e-4
+
+
 def test_quantize_i8_bit_exact(torch):
     rows, codes = [], []
     import os
