@@ -253,24 +253,34 @@ Tiling tern_tiling(int M, int N, int K, int nsub) {
   return t;
 }
 
-// Dense GEMM launch: the skinny kernel when the shape allows, else the wide one.
+// Dense GEMM launch: the skinny kernel when the shape allows (M <= 128), else
+// the tiled one (bf16) or the wide one (fp32).
 struct DenseLaunch {
   bool skinny;
+  bool tile;
   SkinnyShape sk;
   WideShape wd;
-  int units() const { return skinny ? sk.units : wd.units; }
+  TileShape tl;
+  // K-splits whose fp32 partials a later kernel sums (EPI_PARTIAL only)
+  int splits() const { return skinny ? sk.nsplit : (tile ? tl.nsplit : 1); }
 };
 
-// variant: 0 = skinny when it fits (split-K only for EPI_PARTIAL), 1 = wide.
+// variant: 0 = the runtime's choice (split-K only for EPI_PARTIAL), 1 = wide,
+// 2 = skinny, 3 = tiled, 10 + i = tiled with tile i fixed.
 DenseLaunch dense_launch(int et, const GemmArgs& a, int nsub, int variant = 0) {
   DenseLaunch d{};
-  d.skinny = variant != 1 && skinny_plan(et, a.M, a.N, a.K, nsub, a.epi == EPI_PARTIAL, &d.sk);
-  if (!d.skinny) wide_plan(et, a.M, a.N, a.K, nsub, &d.wd);
+  const bool split_ok = a.epi == EPI_PARTIAL;
+  if (variant == 0 || variant == 2) d.skinny = skinny_plan(et, a.M, a.N, a.K, nsub, split_ok, &d.sk);
+  if (!d.skinny && (variant == 0 || variant == 3 || variant >= 10))
+    d.tile = tile_plan(et, a.M, a.N, a.K, split_ok, variant >= 10 ? variant - 10 : -1, &d.tl);
+  if (!d.skinny && !d.tile) wide_plan(et, a.M, a.N, a.K, nsub, &d.wd);
   return d;
 }
 
 hipError_t launch_dense(int et, const DenseLaunch& d, const GemmArgs& a, hipStream_t s) {
-  return d.skinny ? launch_gemm_skinny(et, d.sk, a, s) : launch_gemm_wide(et, d.wd, a, s);
+  if (d.skinny) return launch_gemm_skinny(et, d.sk, a, s);
+  if (d.tile) return launch_gemm_tile(d.tl, a, s);
+  return launch_gemm_wide(et, d.wd, a, s);
 }
 
 // Collects the launches of a plan and the workspace they need.
@@ -287,7 +297,7 @@ struct Builder {
     const double es = esize(et);
     const double xb = es;
     double ob = a.out_f32 ? 4.0 : es;
-    if (a.epi == EPI_PARTIAL) ob = 4.0 * (dl.skinny ? dl.sk.nsplit : 1);
+    if (a.epi == EPI_PARTIAL) ob = 4.0 * dl.splits();
     if (a.epi == EPI_RESID) ob = 8.0;                           // residual read + write
     if (a.epi == EPI_GLU) ob = es * 0.5;                        // one output per gate/up pair
     const double bytes = (double)a.N * a.K * es + (double)a.M * a.K * xb + (double)a.M * a.N * ob;
@@ -558,20 +568,20 @@ vla_status build_plan(vla_model* m, Plan* p) {
     DenseLaunch dl;
     g.epi = EPI_PARTIAL;
     dl = dense_launch(et, g, 1);
-    if (dl.skinny) {
+    if (dl.skinny || (dl.tile && dl.tl.nsplit > 1)) {
       g.out = nullptr;  // set at run time from the plan's partial buffer
       g.ldo = d;
-      part_need = std::max(part_need, (size_t)dl.sk.nsplit * M * d);
+      part_need = std::max(part_need, (size_t)dl.splits() * M * d);
       GemmArgs gg = g;
       float** partp = &p->part;
-      const double bytes = (double)g.N * g.K * es + (double)g.M * g.K * es + 4.0 * dl.sk.nsplit * g.M * g.N;
+      const double bytes = (double)g.N * g.K * es + (double)g.M * g.K * es + 4.0 * dl.splits() * g.M * g.N;
       bld.ops->push_back(Op{[=](hipStream_t s) {
                               GemmArgs q = gg;
                               q.out = *partp;
                               return launch_dense(et, dl, q, s);
                             },
                             op_info(VLA_OP_GEMM, g.M, g.N, g.K, bytes, 2.0 * g.M * g.N * g.K)});
-      rn.nsplit = dl.sk.nsplit;
+      rn.nsplit = dl.splits();
       rn.alpha = alp;
     } else {
       g.epi = EPI_RESID;
@@ -1326,7 +1336,8 @@ int32_t vla_test_persist_trace(vla_model* m, uint64_t* out, int32_t max_per_team
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                          int32_t variant, float* y, void* stream) {
   if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
-  if (variant < 0 || variant > 2) return fail(VLA_E_ARG, "variant must be 0, 1 or 2");
+  if (variant < 0 || (variant > 3 && variant < 10) || variant > 13)
+    return fail(VLA_E_ARG, "variant must be 0..3 or 10..13");
   if (!x || !w || !y || !al16(x) || !al16(w) || !al16(y)) return fail(VLA_E_ARG, "bad buffer");
   if (M < 1 || N < 1 || K < 1 || K % (elem ? 8 : 4)) return fail(VLA_E_SHAPE, "bad GEMM shape");
   const int et = elem ? ET_BF16 : ET_F32;
@@ -1336,6 +1347,7 @@ vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, 
   g.epi = EPI_STORE; g.out = y; g.ldo = N; g.out_f32 = 1;
   DenseLaunch d = dense_launch(et, g, 1, variant);
   if (variant == 2 && !d.skinny) return fail(VLA_E_UNSUPPORTED, "shape not supported by the skinny GEMM");
+  if (variant >= 3 && !d.tile) return fail(VLA_E_UNSUPPORTED, "shape not supported by the tiled GEMM");
   hipError_t e = launch_dense(et, d, g, s);
   hipError_t e2 = hipStreamSynchronize(s);
   if (e != hipSuccess || e2 != hipSuccess)

@@ -40,6 +40,7 @@ struct GemmArgs {
   int ldx;
   const void* W;           // [N][K] row-major in the element type
   int n_tiles;             // tiles along N (set by the launcher)
+  int m_tiles;             // tiles along M (tiled kernel; set by the launcher)
   int nsplit;              // K-splits (set by the launcher; > 1 only with EPI_PARTIAL)
   int kper;                // K-range of one split (skinny kernel; set by the launcher)
   // epilogue
@@ -141,6 +142,12 @@ struct WideShape {
   int ms, nsub, nc, n_tiles, m_tiles, units;
   size_t lds;
 };
+// Tiled kernel: a (32*ms) x (32*ns) output tile per workgroup, K split in
+// nsplit ranges of kper.  grid = units rounded up to a multiple of 8.
+struct TileShape {
+  int ms, ns, nsplit, kper, n_tiles, m_tiles, units, grid;
+  size_t lds;
+};
 
 // Persistent tensor-parallel denoise loop (bf16, joint attention, batch 1):
 // weights of one layer, library-owned.
@@ -193,6 +200,11 @@ bool skinny_plan(int et, int M, int N, int K, int nsub, bool allow_split, Skinny
 void wide_plan(int et, int M, int N, int K, int nsub, WideShape* sh);
 hipError_t launch_gemm_skinny(int et, const SkinnyShape& sh, GemmArgs a, hipStream_t s);
 hipError_t launch_gemm_wide(int et, const WideShape& sh, GemmArgs a, hipStream_t s);
+// Tiled bf16 kernel for M > 128.  force < 0: the cost model picks the tile and
+// the K-split (split only if allow_split); force = 0..3 fixes the tile
+// (64x128, 128x128, 256x128, 128x256) with no split.  False if not applicable.
+bool tile_plan(int et, int M, int N, int K, bool allow_split, int force, TileShape* sh);
+hipError_t launch_gemm_tile(const TileShape& sh, GemmArgs a, hipStream_t s);
 
 // which: 0 = key-split kernel and (when kv_split > 1) the merge, 1 = the
 // key-split kernel only, 2 = the merge only.

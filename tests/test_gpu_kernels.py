@@ -40,7 +40,12 @@ GEMM_SHAPES = [
     (50, 1600, 720), (50, 720, 2048), (50, 6, 720),
     (8, 384, 256), (8, 7, 256), (1, 5, 8), (17, 33, 136), (100, 2560, 1024),
     (816, 512, 2048), (10, 6144, 1024), (128, 1024, 4096), (129, 64, 64), (50, 1024, 8192),
+    # large M (batched requests, prefix K/V build): the tiled kernel, ragged in M, N and K
+    (400, 1024, 4096), (1600, 2560, 1024), (257, 136, 72), (300, 100, 200), (520, 200, 640),
 ]
+
+# 0 runtime choice, 1 wide, 2 skinny, 3 tiled (runtime tile), 10..13 tiled with a fixed tile
+GEMM_VARIANTS = (0, 1, 2, 3, 10, 11, 12, 13)
 
 
 @pytest.mark.parametrize("elem", [1, 0])
@@ -55,12 +60,13 @@ def test_gemm_parity(torch, elem, M, N, K):
     ref = O.linear(x, w)
     bound = _fp32_bound(x.astype(np.float64), w.astype(np.float64))
     vla = _vla()
-    for variant in (0, 1, 2):
+    for variant in GEMM_VARIANTS:
         y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
         try:
             vla.test_gemm(elem, _dev(torch, x, bf), _dev(torch, w, bf), M, N, K, y, variant=variant)
         except vla.VlaError as e:
-            assert variant == 2 and e.status == 3, e   # shape outside the skinny kernel
+            # shape outside the skinny kernel, or not a bf16 GEMM with M > 128 for the tiled one
+            assert e.status == 3 and (variant == 2 or (variant >= 3 and (not bf or M <= 128))), e
             continue
         got = y.cpu().numpy().astype(np.float64)
         err = np.abs(got - ref)
