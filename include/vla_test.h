@@ -30,7 +30,9 @@ vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, 
  *   q [B*n][H*hd]; k_self, v_self [B*n][G*hd]; k_cache, v_cache [B][G][P][hd];
  *   o [B*n][H*hd]; all in elem.  kv_split: key splits (kv_split % 100) and
  *   query-head groups per K/V head (kv_split / 100); 0 in either part lets
- *   the runtime choose. */
+ *   the runtime choose.  kv_split >= 1000 selects the 128-row tiled kernel
+ *   (bf16 only) with kv_split - 1000 key splits of 64-key blocks (0 = the
+ *   runtime's count). */
 vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const void* k_self,
                               const void* v_self, const void* k_cache, const void* v_cache, int32_t B,
                               int32_t n, int32_t P, int32_t H, int32_t G, int32_t hd, int32_t kv_split,

@@ -76,7 +76,17 @@ VLA_DEV void mma16(f32x4& acc, uint4 a, uint4 b, float) {
   acc = __builtin_amdgcn_mfma_f32_16x16x4f32(__uint_as_float(a.w), __uint_as_float(b.w), acc, 0, 0, 0);
 }
 
-VLA_DEV uint4 ldg16(const void* p) { return *reinterpret_cast<const uint4*>(p); }
+// 16-byte load from global memory.  The explicit global address space (on a
+// native vector type: uint4's copy constructor would take a generic
+// reference) keeps the compiler from emitting a flat load where it cannot
+// prove the pointer global, e.g. one read from memory.  Flat loads also count
+// on lgkmcnt, so every wait for an LDS read would wait for them too.
+typedef unsigned gv4u_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(1))) const gv4u_t global_v4u;
+VLA_DEV uint4 ldg16(const void* p) {
+  const gv4u_t v = *(const global_v4u*)(p);
+  return make_uint4(v.x, v.y, v.z, v.w);
+}
 VLA_DEV void stg16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
 
 // Activations (fp32).  GELU uses the tanh form.

@@ -356,11 +356,372 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
   return hipGetLastError();
 }
 
+
+// ---------------------------------------------------------------------------
+// attn_tile -- large query counts per K/V head (batched requests).  The query
+// heads that share K/V head g are flattened into rows (head, query) of one
+// group: row R = hh * n + t is query t of head g*per + hh.  A workgroup of 8
+// waves (two per SIMD, so one wave's LDS and memory waits hide behind the
+// other's MFMAs) takes 128 such rows, 16 per wave, and loops over the split's
+// keys in blocks of 64, so every K/V byte staged in LDS serves 128 rows.  Per
+// block, in LDS:
+//   K   [64 keys][HD]   16-byte chunk c of key k at slot c ^ f(k),
+//                       f(k) = (k & 3) | ((k >> 1) & 4)
+//   V^T [HD][64 keys]   chunk c (8 keys) of dim d at slot c ^ (d % 8)
+// (the XORs give the 8 rows that one operand load reads per bank cycle, keys
+// 8 (r/4) + r%4 of the score-tile permutation resp. 8 consecutive dims, 8
+// different slots).  K goes
+// straight to LDS (direct-to-LDS loads, one wave instruction = 64 slots of
+// consecutive rows); V is transposed in registers, 4 keys x 8 dims per thread.
+// The next block's loads are in flight while the current block's MFMAs run;
+// LDS is double-buffered.  Scores are computed transposed (S^T = K Q^T) with
+// the same key permutation as attn_kernel, so a lane's 8 keys of a 32-key half
+// are the k slots of its P^T operand in O^T += V^T P^T.  Split outputs use the
+// attn_kernel partial format, so attn_merge combines them.
+
+typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
+// One wave-wide global_load_lds_dwordx4: lane l's 16 bytes at g land in LDS at
+// wave-uniform lds + 16 l.  The compiler does not track it; the barrier that
+// follows (whose fence waits for every outstanding load) orders it against
+// the LDS reads.
+VLA_DEV void dma16(const void* g, void* lds) {
+  typedef __attribute__((address_space(3))) v4u_t lds_v4u;
+  const unsigned off = (unsigned)(uintptr_t)(lds_v4u*)lds;
+  const unsigned base = __builtin_amdgcn_readfirstlane(off);
+  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(base), "v"(g) : "memory", "m0");
+}
+
+// K slot swizzle of key k (see attn_tile)
+VLA_DEV int kswz(int k) { return (k & 3) | ((k >> 1) & 4); }
+
+constexpr int TQ = 128;   // rows per workgroup
+constexpr int TKB = 64;   // keys per block
+constexpr int TW = 8;     // waves per workgroup (16 rows each)
+
+template <int HD>
+struct TileLds {
+  static constexpr int CPR = HD / 8;                          // 16-byte chunks per K row
+  static constexpr size_t KB = (size_t)TKB * HD * 2;          // one K block (bf16)
+  static constexpr size_t VB = (size_t)HD * TKB * 2;          // one V^T block
+  static constexpr size_t BYTES = 2 * (KB + VB);              // double-buffered
+};
+
+template <int HD>
+__global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
+  using L = TileLds<HD>;
+  constexpr int CPR = L::CPR;
+  constexpr int NQV = HD / 32;                  // k-steps of S^T (16-byte vectors per lane)
+  constexpr int DT = HD / 16;                   // dim tiles of O^T
+  constexpr int KLD = TKB * CPR / (64 * TW);    // K load instructions per wave and block
+  constexpr int VIT = 16 * (HD / 8);            // (4-key group, 8-dim group) items of a V block
+  static_assert(KLD >= 1 && KLD * 64 * TW == TKB * CPR, "K staging");
+  extern __shared__ __align__(16) unsigned char smem[];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int per = a.H / a.G;
+  const int nrows = per * a.n;
+  const int rt = (nrows + TQ - 1) / TQ;
+  const int units = a.B * a.G * rt * a.kv_split;
+  int u = (int)(blockIdx.x % 8u) * (int)(gridDim.x / 8u) + (int)(blockIdx.x / 8u);
+  if (u >= units) return;
+  const int tile = u % rt;
+  u /= rt;
+  const int split = u % a.kv_split;
+  u /= a.kv_split;
+  const int g = u % a.G;
+  const int b = u / a.G;
+
+  const int npre = (a.mode == 0) ? 0 : a.P;
+  const int nself = (a.mode == 1) ? 0 : a.n;
+  const int nkeys = npre + nself;
+  const int nblk_all = (nkeys + TKB - 1) / TKB;
+  const int jb0 = split * a.key_chunk;
+  const int nb = min(nblk_all, jb0 + a.key_chunk) - jb0;
+
+  const bf16_t* kc = reinterpret_cast<const bf16_t*>(a.kc);
+  const bf16_t* vc = reinterpret_cast<const bf16_t*>(a.vc);
+  if (npre > 0 && kc == nullptr) {
+    kc = reinterpret_cast<const bf16_t*>(a.cp->kv_cache) + a.layer_off;
+    vc = kc + (size_t)a.B * a.G * a.P * HD;
+  }
+  kc += ((size_t)b * a.G + g) * a.P * HD;
+  vc += ((size_t)b * a.G + g) * a.P * HD;
+  const bf16_t* ksf = reinterpret_cast<const bf16_t*>(a.ks) + (size_t)b * a.n * a.ldkv + g * HD;
+  const bf16_t* vsf = reinterpret_cast<const bf16_t*>(a.vs) + (size_t)b * a.n * a.ldkv + g * HD;
+  // row pointer of key kx < nkeys (prefix rows first)
+  auto krow = [&](int kx) -> const bf16_t* {
+    return kx < npre ? kc + (size_t)kx * HD : ksf + (size_t)(kx - npre) * a.ldkv;
+  };
+  auto vrow = [&](int kx) -> const bf16_t* {
+    return kx < npre ? vc + (size_t)kx * HD : vsf + (size_t)(kx - npre) * a.ldkv;
+  };
+
+  // Q^T fragments of this wave's 16 rows
+  const int R = tile * TQ + wave * 16 + r16;
+  const bool rok = R < nrows;
+  uint4 qf[NQV];
+  {
+    const int hh = rok ? R / a.n : 0, t = rok ? R - hh * a.n : 0;
+    const bf16_t* qp = reinterpret_cast<const bf16_t*>(a.q) + (size_t)(b * a.n + t) * a.ldq + (g * per + hh) * HD + g4 * (HD / 4);
+#pragma unroll
+    for (int c = 0; c < NQV; ++c) qf[c] = rok ? ldg16(qp + c * 8) : make_uint4(0, 0, 0, 0);
+  }
+
+  // K: wave instruction i fills slots [(TW i + wave) * 64, + 64) of the block:
+  // row slot0 / CPR + lane / CPR, slot lane % CPR, which holds k-chunk
+  // slot ^ f(row).  Keys past the end read the last key (masked scores).
+  // this lane's element offset inside a block of prefix rows, per instruction
+  int koffp[KLD];
+#pragma unroll
+  for (int i = 0; i < KLD; ++i) {
+    const int slot0 = (TW * i + wave) * 64;
+    const int row = slot0 / CPR + lane / CPR, sl = lane % CPR;
+    koffp[i] = row * HD + (sl ^ kswz(row)) * 8;
+  }
+  auto kload = [&](int jb, int buf) {
+    const int kx0 = (jb0 + jb) * TKB;
+    unsigned char* kl = smem + buf * (L::KB + L::VB);
+    if (kx0 + TKB <= npre) {  // every row of the block is a prefix row
+      const bf16_t* base = kc + (size_t)kx0 * HD;
+#pragma unroll
+      for (int i = 0; i < KLD; ++i) dma16(base + koffp[i], kl + (size_t)(TW * i + wave) * 64 * 16);
+      return;
+    }
+#pragma unroll
+    for (int i = 0; i < KLD; ++i) {
+      const int slot0 = (TW * i + wave) * 64;
+      const int row = slot0 / CPR + lane / CPR, sl = lane % CPR;
+      dma16(krow(min(kx0 + row, nkeys - 1)) + (sl ^ kswz(row)) * 8, kl + (size_t)slot0 * 16);
+    }
+  };
+  // V: thread = (4-key group vkg, 8-dim group vdg); keys past the end are zero
+  uint4 vreg[4];
+  const bool vthr = tid < VIT;
+  const int vkg = tid & 15, vdg = tid >> 4;
+  const int voffp = vkg * 4 * HD + vdg * 8;        // lane offset inside a block of prefix rows
+  auto vload = [&](int jb) {
+    const int kb0 = (jb0 + jb) * TKB;
+    if (kb0 + TKB <= npre) {
+      const bf16_t* base = vc + (size_t)kb0 * HD + voffp;
+#pragma unroll
+      for (int e = 0; e < 4; ++e) vreg[e] = vthr ? ldg16(base + e * HD) : make_uint4(0, 0, 0, 0);
+      return;
+    }
+    const int kx0 = kb0 + vkg * 4;
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const bool ok = vthr && kx0 + e < nkeys;
+      vreg[e] = ok ? ldg16(vrow(kx0 + e) + vdg * 8) : make_uint4(0, 0, 0, 0);
+    }
+  };
+  auto vstore = [&](int buf) {
+    if (!vthr) return;
+    unsigned char* vl = smem + buf * (L::KB + L::VB) + L::KB;
+    const uint32_t w[4][4] = {{vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w}, {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w},
+                              {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w}, {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w}};
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      // dim vdg*8 + j of keys vkg*4 .. +3
+      uint32_t o2[2];
+#pragma unroll
+      for (int q = 0; q < 2; ++q) {
+        const uint32_t lo = w[2 * q][j >> 1], hi = w[2 * q + 1][j >> 1];
+        o2[q] = (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
+      }
+      const int d = vdg * 8 + j;
+      *reinterpret_cast<uint2*>(vl + (size_t)(d * 8 + ((vkg >> 1) ^ (d & 7))) * 16 + (vkg & 1) * 8) = make_uint2(o2[0], o2[1]);
+    }
+  };
+
+  // LDS operand slots of this lane.  Score-tile row r16 is key
+  // 32 kk + 4 t + 8 (r16/4) + r16%4, whose swizzle f(key) = r16 % 8 for every
+  // kk and t; V^T row d*16 + r16 likewise has swizzle r16 % 8.
+  int kslot[NQV], vslot[2];
+  {
+    const int key0 = 8 * (r16 >> 2) + (r16 & 3), f = r16 & 7;
+#pragma unroll
+    for (int c = 0; c < NQV; ++c) kslot[c] = key0 * CPR + ((g4 * NQV + c) ^ f);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) vslot[kk] = r16 * 8 + ((kk * 4 + g4) ^ f);
+  }
+
+  f32x4 o[DT];
+#pragma unroll
+  for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
+  float mrun = -INFINITY, lrun = 0.f;
+  const float sc = a.scale * kLog2e;
+
+  kload(0, 0);
+  vload(0);
+  vstore(0);
+  __syncthreads();
+  for (int jb = 0; jb < nb; ++jb) {
+    const int buf = jb & 1;
+    // buffer buf ^ 1 was last read in the previous block, which ended with a barrier
+    if (jb + 1 < nb) {
+      kload(jb + 1, buf ^ 1);
+      vload(jb + 1);
+    }
+    const uint4* kl = reinterpret_cast<const uint4*>(smem + buf * (L::KB + L::VB));
+    const uint4* vl = reinterpret_cast<const uint4*>(smem + buf * (L::KB + L::VB) + L::KB);
+    const int kvalid = min(TKB, nkeys - (jb0 + jb) * TKB);
+
+    // S^T for both 32-key halves: tile t row rho = key 32 kk + 8 (rho/4) + 4 t + rho%4;
+    // the four tiles' accumulation chains are interleaved
+    f32x4 s[2][2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int t = 0; t < 2; ++t) s[kk][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+    for (int c = 0; c < NQV; ++c)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t) mma16(s[kk][t], kl[kslot[c] + (kk * 32 + 4 * t) * CPR], qf[c], bf16_t());
+    // online softmax; lane keys: 32 kk + 8 g4 + 4 t + i
+    float p[2][8];
+    float bmax = -INFINITY;
+    if (kvalid == TKB) {  // full block: no key mask
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            p[kk][4 * t + i] = s[kk][t][i] * sc;
+            bmax = fmaxf(bmax, p[kk][4 * t + i]);
+          }
+    } else {
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+        for (int t = 0; t < 2; ++t)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int key = kk * 32 + 8 * g4 + 4 * t + i;
+            const float v = key < kvalid ? s[kk][t][i] * sc : -INFINITY;
+            p[kk][4 * t + i] = v;
+            bmax = fmaxf(bmax, v);
+          }
+    }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    // The reference max moves only when a score exceeds it by more than 2^8:
+    // exponentials stay below 256 and most blocks skip rescaling O.
+    const bool move = bmax > mrun + 8.0f;
+    const float mnew = move ? bmax : mrun;
+    const float corr = move ? exp2f(mrun - mnew) : 1.0f;
+    float psum = 0.f;
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int e = 0; e < 8; ++e) {
+        p[kk][e] = exp2f(p[kk][e] - mnew);
+        psum += p[kk][e];
+      }
+    psum += __shfl_xor(psum, 16, 64);
+    psum += __shfl_xor(psum, 32, 64);
+    lrun = lrun * corr + psum;
+    mrun = mnew;
+    if (__any(move)) {
+#pragma unroll
+      for (int d = 0; d < DT; ++d) o[d] *= corr;
+    }
+    uint4 pb[2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+      pb[kk] = make_uint4(pack_bf16x2(p[kk][0], p[kk][1]), pack_bf16x2(p[kk][2], p[kk][3]),
+                          pack_bf16x2(p[kk][4], p[kk][5]), pack_bf16x2(p[kk][6], p[kk][7]));
+    // O^T += V^T P^T: A = V^T rows (dims) with keys 32 kk + 8 g4 .. + 8
+#pragma unroll
+    for (int d = 0; d < DT; ++d)
+#pragma unroll
+      for (int kk = 0; kk < 2; ++kk) mma16(o[d], vl[vslot[kk] + d * 16 * 8], pb[kk], bf16_t());
+    if (jb + 1 < nb) vstore(buf ^ 1);
+    __syncthreads();  // its fence also waits for the K loads of block jb + 1
+  }
+
+  // lane holds O^T[dim 16 d + 4 g4 + i][row R]
+  if (!rok) return;
+  const int rows = a.B * a.n, dq = a.H * HD;
+  const int hh = R / a.n, t = R - hh * a.n, h = g * per + hh;
+  const float inv = lrun > 0.f ? 1.f / lrun : 0.f;
+  bf16_t* dst;
+  if (a.kv_split == 1) {
+    dst = reinterpret_cast<bf16_t*>(a.o) + (size_t)(b * a.n + t) * a.ldo + h * HD;
+  } else {
+    dst = reinterpret_cast<bf16_t*>(a.part) + ((size_t)split * rows + b * a.n + t) * dq + h * HD;
+    if (g4 == 0) {
+      float* st = a.stats + (((size_t)split * rows + b * a.n + t) * a.H + h) * 2;
+      st[0] = mrun;
+      st[1] = lrun;
+    }
+  }
+#pragma unroll
+  for (int d = 0; d < DT; ++d)
+    *reinterpret_cast<uint2*>(dst + d * 16 + 4 * g4) =
+        make_uint2(pack_bf16x2(o[d][0] * inv, o[d][1] * inv), pack_bf16x2(o[d][2] * inv, o[d][3] * inv));
+}
+
+template <int HD>
+hipError_t launch_tile_hd(const AttnArgs& a, hipStream_t s, int which) {
+  const int per = a.H / a.G;
+  const int rt = (per * a.n + TQ - 1) / TQ;
+  const int units = a.B * a.G * rt * a.kv_split;
+  if (units <= 0) return hipSuccess;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&attn_tile<HD>),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, 160 * 1024);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  if (which != 2) {
+    hipLaunchKernelGGL((attn_tile<HD>), dim3((units + 7) / 8 * 8), dim3(64 * TW), TileLds<HD>::BYTES, s, a);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+  }
+  if (which == 1 || a.kv_split == 1) return hipSuccess;
+  const int cblocks = (a.H * HD + 64 * 8 - 1) / (64 * 8);
+  hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, dim3(a.B * a.n * cblocks), dim3(64), 0, s, a);
+  return hipGetLastError();
+}
+
 }  // namespace
 
 // Keys per split in 32-key blocks (at most KB_MAX), the number of splits, and
 // the workspace.  By default the splits target about 112 workgroups.
+// The tiled kernel: bf16, head_dim 64 / 128 / 256, and enough rows per K/V
+// head (per * n) and keys to fill its 128-row, 64-key tiles.  Key splits aim
+// at about one workgroup per compute unit.
+bool attention_tile_eligible(int et, const AttnArgs& a) {
+  const int npre = (a.mode == 0) ? 0 : a.P;
+  const int nself = (a.mode == 1) ? 0 : a.n;
+  return et == ET_BF16 && (a.hd == 64 || a.hd == 128 || a.hd == 256) && (a.H / a.G) * a.n >= TQ &&
+         npre + nself >= 4 * TKB;
+}
+
+void attention_tile_split(AttnArgs& a, int want_splits) {
+  const int npre = (a.mode == 0) ? 0 : a.P;
+  const int nself = (a.mode == 1) ? 0 : a.n;
+  const int nblk = (npre + nself + TKB - 1) / TKB;
+  const int rt = ((a.H / a.G) * a.n + TQ - 1) / TQ;
+  const int base = a.B * a.G * rt;
+  int s = want_splits > 0 ? want_splits : (256 + base / 2) / base;
+  s = s < 1 ? 1 : (s > nblk ? nblk : s);
+  if (s > 64) s = 64;
+  int kc = (nblk + s - 1) / s;
+  if (kc < (nblk + 63) / 64) kc = (nblk + 63) / 64;  // at most 64 splits
+  a.tiled = 1;
+  a.hsplit = 1;
+  a.key_chunk = kc;
+  a.kv_split = (nblk + kc - 1) / kc;
+}
+
 void attention_split(AttnArgs& a, int want_splits, int want_hsplit) {
+  a.tiled = 0;
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
   const int nblocks = (npre + 31) / 32 + (nself + 31) / 32;
@@ -418,6 +779,15 @@ size_t attention_stats_bytes(const AttnArgs& a) {
 
 hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which) {
   if (a.H % a.G != 0 || a.H / a.G > 8 || a.H > 32 || a.kv_split > 64 || a.kv_split < 1) return hipErrorInvalidValue;
+  if (a.tiled) {
+    if (et != ET_BF16 || a.key_chunk < 1) return hipErrorInvalidValue;
+    switch (a.hd) {
+      case 64: return launch_tile_hd<64>(a, s, which);
+      case 128: return launch_tile_hd<128>(a, s, which);
+      case 256: return launch_tile_hd<256>(a, s, which);
+    }
+    return hipErrorInvalidValue;
+  }
   if (et == ET_BF16) {
     switch (a.hd) {
       case 64: return launch_hd<bf16_t, 64>(a, s, which);

@@ -323,8 +323,9 @@ struct Builder {
     const int QT = cdiv(a.n, 16);
     const int total = (a.mode == 0 ? 0 : a.P) + (a.mode == 1 ? 0 : a.n);
     (void)QT;
-    attention_split(a, m->attn_splits % 100, m->attn_splits / 100);
     const int et = m->et;
+    attention_split(a, m->attn_splits % 100, m->attn_splits / 100);
+    if (m->attn_splits == 0 && attention_tile_eligible(et, a)) attention_tile_split(a, 0);
     part_need = std::max(part_need, attention_part_bytes(et, a));
     stats_need = std::max(stats_need, attention_stats_bytes(a));
     void** pp = apart;
@@ -1372,8 +1373,13 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
   if (H / G > 8 || H > 32) return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head");
   if ((a.P + 31) / 32 + (mode == 1 ? 0 : (n + 31) / 32) > attention_max_blocks())
     return fail(VLA_E_UNSUPPORTED, "too many keys");
-  attention_split(a, kv_split % 100, kv_split / 100);
   const int et = elem ? ET_BF16 : ET_F32;
+  if (kv_split >= 1000) {
+    if (elem != 1) return fail(VLA_E_UNSUPPORTED, "the tiled attention kernel is bf16 only");
+    attention_tile_split(a, kv_split - 1000);
+  } else {
+    attention_split(a, kv_split % 100, kv_split / 100);
+  }
   void* part = nullptr;
   float* stats = nullptr;
   if (a.kv_split > 1) {

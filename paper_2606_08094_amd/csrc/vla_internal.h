@@ -84,7 +84,8 @@ struct AttnArgs {
   float scale;
   int kv_split;            // key splits
   int hsplit;              // groups of query heads per K/V head (workgroups per group)
-  int key_chunk;           // 32-key blocks per split
+  int key_chunk;           // 32-key blocks per split (64-key blocks when tiled)
+  int tiled;               // 1: the 128-row tiled kernel (bf16, large query counts)
   void* part;              // [kv_split][B*n][H*hd] per-split output (kv_split > 1)
   float* stats;            // [kv_split][B*n][H][2] per-split (max, sum)
 };
@@ -212,6 +213,10 @@ hipError_t launch_attention(int et, const AttnArgs& a, hipStream_t s, int which 
 // want_splits / want_hsplit 0 = automatic (at most 4 heads per workgroup,
 // about 224 workgroups)
 void attention_split(AttnArgs& a, int want_splits, int want_hsplit = 0);
+// The 128-row tiled attention kernel: whether the runtime picks it for this
+// shape, and its split plan (want_splits 0 = about one workgroup per CU).
+bool attention_tile_eligible(int et, const AttnArgs& a);
+void attention_tile_split(AttnArgs& a, int want_splits);
 int attention_max_blocks();  // most 32-key blocks (prefix blocks + action blocks) one call handles
 size_t attention_part_bytes(int et, const AttnArgs& a);
 size_t attention_stats_bytes(const AttnArgs& a);

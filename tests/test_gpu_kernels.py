@@ -89,11 +89,14 @@ ATTN_CASES = [
 
 
 @pytest.mark.parametrize("case", ATTN_CASES, ids=[str(c) for c in ATTN_CASES])
-@pytest.mark.parametrize("kv_split", [0, 1, 3, 201, 403, 800])
+@pytest.mark.parametrize("kv_split", [0, 1, 3, 201, 403, 800, 1000, 1001, 1005])
 def test_attention_parity(torch, case, kv_split):
-    """kv_split: key splits (% 100) and query-head groups per K/V head (// 100)."""
+    """kv_split: key splits (% 100) and query-head groups per K/V head (// 100);
+    1000 + s: the 128-row tiled kernel with s splits of 64-key blocks."""
     elem, mode, B, n, P, H, G, hd = case
-    if kv_split // 100 and (H // G) % (kv_split // 100):
+    if kv_split >= 1000 and elem != 1:
+        pytest.skip("the tiled kernel is bf16 only")
+    if kv_split < 1000 and kv_split // 100 and (H // G) % (kv_split // 100):
         pytest.skip("head groups must divide the heads per K/V head")
     bf = elem == 1
     s = 7 * n + P + H + hd + mode
