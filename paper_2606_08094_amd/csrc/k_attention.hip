@@ -699,7 +699,10 @@ hipError_t launch_tile_hd(const AttnArgs& a, hipStream_t s, int which) {
 bool attention_tile_eligible(int et, const AttnArgs& a) {
   const int npre = (a.mode == 0) ? 0 : a.P;
   const int nself = (a.mode == 1) ? 0 : a.n;
-  return et == ET_BF16 && (a.hd == 64 || a.hd == 128 || a.hd == 256) && (a.H / a.G) * a.n >= TQ &&
+  const int row_tiles = a.B * a.G * (((a.H / a.G) * a.n + TQ - 1) / TQ);
+  // below ~16 row tiles (e.g. one request of 50-100 action tokens) the
+  // 16-query kernel's finer split of the keys is faster
+  return et == ET_BF16 && (a.hd == 64 || a.hd == 128 || a.hd == 256) && row_tiles >= 16 &&
          npre + nself >= 4 * TKB;
 }
 
@@ -745,6 +748,8 @@ void attention_split(AttnArgs& a, int want_splits, int want_hsplit) {
     const int base = a.B * QT * a.G * hs;
     s = (112 + base - 1) / base;
   }
+  // two key blocks or fewer: one split, no merge launch (measured faster)
+  if (want_splits <= 0 && nblocks <= 2) s = 1;
   s = s < 1 ? 1 : (s > nblocks ? nblocks : s);
   int kc = (nblocks + s - 1) / s;                            // blocks per split
   kc = kc < (nblocks + 63) / 64 ? (nblocks + 63) / 64 : kc;  // at most 64 splits

@@ -135,7 +135,37 @@ __global__ __launch_bounds__(256) void row_norm_kernel(RowNormArgs a) {
       up[2] = ElemTraits<T>::from_f(u2);
       up[3] = ElemTraits<T>::from_f(u3);
     }
+    xv[i] = make_float4(u0, u1, u2, u3);  // keep u for the quantiser
   }
+  if (a.q == nullptr) return;
+  // Per-token absmax int8 quantisation of the fp32 u (same arithmetic as
+  // quantize_kernel, so the codes are identical to quantising the stored u).
+  float amax = 0.0f;
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = 4 * (t + 256 * i);
+    if (c < d) amax = fmaxf(fmaxf(fmaxf(amax, fabsf(xv[i].x)), fmaxf(fabsf(xv[i].y), fabsf(xv[i].z))), fabsf(xv[i].w));
+  }
+  amax = wave_max(amax);
+  __syncthreads();  // every thread has read red[] for rstd
+  if ((t & 63) == 0) red[t >> 6] = amax;
+  __syncthreads();
+  const float r = fmaxf(fmaxf(fmaxf(red[0], red[1]), fmaxf(red[2], red[3])), 1e-5f);
+  const float inv = __fdiv_rn(127.0f, r);
+#pragma unroll
+  for (int i = 0; i < CPT; ++i) {
+    const int c = 4 * (t + 256 * i);
+    if (c >= d) continue;
+    const float e[4] = {xv[i].x, xv[i].y, xv[i].z, xv[i].w};
+    uint32_t packed = 0;
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const float qv = fminf(fmaxf(rintf(__fmul_rn(e[k], inv)), -128.0f), 127.0f);
+      packed |= ((uint32_t)(int)qv & 0xFFu) << (8 * k);
+    }
+    *reinterpret_cast<uint32_t*>(a.q + (size_t)m * d + c) = packed;
+  }
+  if (t == 0) a.qr[m] = r;
 }
 
 // e[k] = [sin(2 pi tau_k / p_j), cos(2 pi tau_k / p_j)], p_j geometric from

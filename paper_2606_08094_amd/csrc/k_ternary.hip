@@ -8,7 +8,8 @@
 // of the activation codes, which the workgroup accumulates while staging X in
 // LDS.  All arithmetic is int32 and exact.  A workgroup walks the whole K
 // range (its K-slices one after another); only the raw int32 entry splits K
-// across workgroups, adding the exact partial sums atomically.
+// across workgroups, adding the exact partial sums atomically.  The
+// dequantised path with few token rows uses tern_skinny instead.
 #include "gemm_epilogue.h"
 
 namespace {
@@ -197,6 +198,112 @@ __global__ __launch_bounds__(256) void tern_generic_kernel(const int8_t* x, cons
   out[idx] = acc;
 }
 
+
+// 16 2-bit codes -> 16 signed int8 weights w = code - 1: one byte permute per
+// dword maps code 0, 1, 2 to 0xFF, 0x00, 0x01.
+VLA_DEV i32x4 unpack_signed(uint32_t p) {
+  const i32x4 c = unpack_codes(p);
+  i32x4 r;
+#pragma unroll
+  for (int b = 0; b < 4; ++b) r[b] = (int)__builtin_amdgcn_perm(0u, 0x000100FFu, (uint32_t)c[b]);
+  return r;
+}
+
+// Small-M dequantised W2A8 GEMM.  A workgroup owns 16 * NSUB W rows (a
+// gate/up pair of 16-row blocks for GLU) and every token row (M <= 16 MS).
+// K is cut into chunks of 256 (4 lane groups x 64); wave w takes chunks w,
+// w+4, ..., and issues all W and X loads of up to CPW chunks before their
+// MFMAs.  Weights are widened to signed int8, so the MFMA sums q * w
+// directly; the four waves' int32 partials are added through LDS (exact),
+// then waves 0 .. MS-1 dequantise and run the epilogue of one 16-row subtile.
+template <int MS, int NSUB, int CPW>
+__global__ __launch_bounds__(256) void tern_skinny(TernArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  i32x4* red = reinterpret_cast<i32x4*>(smem);  // [4][MS][NSUB][64]
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K, KB = K / 4;
+  const int n0 = blockIdx.x * 16 * NSUB;
+  const int nch = (K + 255) / 256;
+
+  i32x4 acc[MS][NSUB];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) acc[ms][s] = i32x4{0, 0, 0, 0};
+
+  for (int c0 = wave; c0 < nch; c0 += 4 * CPW) {
+    uint4 wreg[CPW][NSUB];
+    uint4 xreg[CPW][MS][4];
+#pragma unroll
+    for (int j = 0; j < CPW; ++j) {
+      const int k = (c0 + 4 * j) * 256 + g4 * 64;   // this lane group's 64 k
+      const bool kok = c0 + 4 * j < nch && k < K;
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        const int n = n0 + s * 16 + r16;
+        wreg[j][s] = (kok && n < N) ? ldg16(a.w + (size_t)n * KB + k / 4) : make_uint4(0, 0, 0, 0);
+      }
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) {
+        const int m = ms * 16 + r16;
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          xreg[j][ms][r] = (kok && m < M) ? ldg16(a.x + (size_t)m * K + k + 16 * r) : make_uint4(0, 0, 0, 0);
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < CPW; ++j)
+#pragma unroll
+      for (int s = 0; s < NSUB; ++s) {
+        const uint32_t pw[4] = {wreg[j][s].x, wreg[j][s].y, wreg[j][s].z, wreg[j][s].w};
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          const i32x4 wv = unpack_signed(pw[r]);
+#pragma unroll
+          for (int ms = 0; ms < MS; ++ms)
+            acc[ms][s] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xreg[j][ms][r]), wv, acc[ms][s], 0, 0, 0);
+        }
+      }
+  }
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int s = 0; s < NSUB; ++s) red[((wave * MS + ms) * NSUB + s) * 64 + lane] = acc[ms][s];
+  __syncthreads();
+  if (wave >= MS || wave * 16 >= M) return;
+  const int ms = wave;
+  float sw[NSUB];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    const int n = n0 + s * 16 + r16;
+    sw[s] = (n < N) ? a.wscale[n] : 0.0f;
+  }
+  f32x4 y[1][NSUB];
+#pragma unroll
+  for (int s = 0; s < NSUB; ++s) {
+    i32x4 t = red[((0 * MS + ms) * NSUB + s) * 64 + lane];
+#pragma unroll
+    for (int w = 1; w < 4; ++w) t += red[((w * MS + ms) * NSUB + s) * 64 + lane];
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = ms * 16 + g4 * 4 + i;
+      const float rm = (m < M) ? a.rscale[m] : 0.0f;
+      y[0][s][i] = (float)t[i] * (sw[s] * rm / 127.0f);
+    }
+  }
+  wave_epilogue<bf16_t, 1, NSUB>(a.e, y, ms * 16, n0, 0);
+}
+
+template <int MS, int NSUB>
+hipError_t skinny_launch(const TernArgs& a, hipStream_t s) {
+  constexpr int CPW = MS == 1 ? (NSUB == 1 ? 8 : 4) : (MS == 2 ? 4 : 2);  // <= 256 VGPRs: two waves per SIMD
+  const int grid = (a.N + 16 * NSUB - 1) / (16 * NSUB);
+  const size_t lds = (size_t)4 * MS * NSUB * 64 * 16;
+  hipLaunchKernelGGL((tern_skinny<MS, NSUB, CPW>), dim3(grid), dim3(256), lds, s, a);
+  return hipGetLastError();
+}
+
 template <int MS, int NSUB, int NC>
 hipError_t tern_launch(const TernArgs& a, int units, hipStream_t s) {
   constexpr int MT = 16 * MS;
@@ -228,8 +335,20 @@ hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t
                        a.N, a.K, a.acc_out);
     return hipGetLastError();
   }
-  const int nc = a.ks / 256;
   const int nsub = (a.rscale != nullptr && a.e.epi == EPI_GLU) ? 2 : 1;
+  if (a.rscale != nullptr && a.M <= 64) {  // token rows of the denoise loop: the skinny kernel
+    const int sms = a.M <= 16 ? 1 : (a.M <= 32 ? 2 : 4);
+    switch (sms * 10 + nsub) {
+      case 11: return skinny_launch<1, 1>(a, s);
+      case 12: return skinny_launch<1, 2>(a, s);
+      case 21: return skinny_launch<2, 1>(a, s);
+      case 22: return skinny_launch<2, 2>(a, s);
+      case 41: return skinny_launch<4, 1>(a, s);
+      case 42: return skinny_launch<4, 2>(a, s);
+    }
+    return hipErrorInvalidValue;
+  }
+  const int nc = a.ks / 256;
   switch (ms * 10 + nsub) {
     case 11: return tern_nc<1, 1>(nc, a, units, s);
     case 12: return tern_nc<1, 2>(nc, a, units, s);

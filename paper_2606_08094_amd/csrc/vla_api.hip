@@ -620,6 +620,10 @@ vla_status build_plan(vla_model* m, Plan* p) {
     if (L > 0) {
       rn.gamma = modk;
       rn.beta = modk + d;
+      if (m->tern) {  // the first sublayer's W2A8 input, quantised in the same kernel
+        rn.q = p->q8;
+        rn.qr = p->r8;
+      }
     } else {
       rn.gamma = modfk;
       rn.beta = modfk + d;
@@ -635,7 +639,12 @@ vla_status build_plan(vla_model* m, Plan* p) {
         nr.mode = 0; nr.M = M; nr.d = d; nr.x = p->x; nr.eps = c.rms_eps; nr.u = p->u; nr.u_f32 = u32;
         next_gb(l, j, &nr.gamma, &nr.beta);
         // the head projection is dense: it reads u in the element type
-        if (l == L - 1 && j == (int)subs.size() - 1) nr.u_f32 = et == ET_F32;
+        const bool last_sub = l == L - 1 && j == (int)subs.size() - 1;
+        if (last_sub) nr.u_f32 = et == ET_F32;
+        if (m->tern && !last_sub) {  // the next sublayer's W2A8 input
+          nr.q = p->q8;
+          nr.qr = p->r8;
+        }
         if (sw.kind == K_MLP) {
           const bool glu = c.mlp != VLA_MLP_GELU;
           const int ngu = glu ? 2 * F : F;
@@ -648,9 +657,8 @@ vla_status build_plan(vla_model* m, Plan* p) {
             bld.gemm(g, glu ? 2 : 1);
             resid_gemm(gemm_base(m, M, d, F, p->h, F, sw.dn), alp, nr);
           } else {
+            // u was quantised (q8, r8) by the row kernel that wrote it
             QuantArgs q{};
-            q.M = M; q.K = d; q.x = p->u; q.ldx = d; q.src_type = 0; q.q = p->q8; q.r = p->r8;
-            bld.quant(q);
             TernArgs t{};
             t.M = M; t.N = ngu; t.K = d; t.x = p->q8; t.w = (const uint8_t*)sw.gu; t.rscale = p->r8; t.wscale = sw.s_gu;
             t.e = gemm_base(m, M, ngu, d, nullptr, 0, nullptr);
@@ -680,9 +688,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
             g.ldo = ldqkv;
             bld.gemm(g, 1);
           } else {
-            QuantArgs q{};
-            q.M = M; q.K = d; q.x = p->u; q.ldx = d; q.src_type = 0; q.q = p->q8; q.r = p->r8;
-            bld.quant(q);
+            // u was quantised (q8, r8) by the row kernel that wrote it
             TernArgs t{};
             t.M = M; t.N = sw.n_qkv; t.K = d; t.x = p->q8; t.w = (const uint8_t*)sw.qkv; t.rscale = p->r8;
             t.wscale = sw.s_qkv;

@@ -120,6 +120,8 @@ struct RowNormArgs {
   float eps;
   void* u;                 // [M][d] element type (u_f32 = 0) or fp32
   int u_f32;
+  int8_t* q;               // if set (u_f32 = 1): also the int8 absmax quantisation of u, [M][d]
+  float* qr;               // and its per-row absmax [M]
 };
 
 struct TernArgs {

@@ -252,7 +252,8 @@ def test_ternary_gemm_empty(torch):
     assert int(out.cpu()[0]) == 0
 
 
-@pytest.mark.parametrize("M,N,K", [(8, 3840, 2560), (8, 2560, 6912), (512, 1280, 2560), (13, 70, 128)])
+@pytest.mark.parametrize("M,N,K", [(8, 3840, 2560), (8, 2560, 6912), (512, 1280, 2560), (13, 70, 128),
+                                   (56, 2560, 2560), (20, 512, 6912), (40, 200, 320), (64, 48, 64)])
 def test_ternary_linear(torch, M, N, K):
     x = wl.random_matrix((M, K), 3 + M, 1.0)
     w = wl.random_ternary((N, K), 4 + N)
