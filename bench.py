@@ -187,6 +187,11 @@ def main():
     ap.add_argument("--workloads", action="store_true",
                     help="instead of the headline line, measure the other scope workloads (SmolVLA-shaped, "
                          "ternary W2A8, pi0 stress at batch 1/4/16) and print one JSON line each")
+    ap.add_argument("--only", default="",
+                    help="with --workloads: measure just this workload, as NAME:BATCH (e.g. stress_pi0:16)")
+    ap.add_argument("--chunks", type=int, default=0,
+                    help="with --workloads --only: just run this many chunks (prefix K/V build + denoise) of the "
+                         "workload, with no timing and no per-launch events (a light target for profilers)")
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="only run 5 plain device-to-device copies of this many MiB (calibrates the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
@@ -214,8 +219,23 @@ def main():
     from vla_testlib import Pipeline
 
     if args.workloads:
-        for name, batch in (("smolvla_bf16", 1), ("ternary_w2a8", 1), ("stress_pi0", 1), ("stress_pi0", 4),
-                            ("stress_pi0", 16)):
+        todo = (("smolvla_bf16", 1), ("ternary_w2a8", 1), ("stress_pi0", 1), ("stress_pi0", 4), ("stress_pi0", 16))
+        if args.only:
+            name, _, batch = args.only.partition(":")
+            todo = ((name, int(batch or 1)),)
+        if args.chunks > 0 and args.only:
+            name, batch = todo[0]
+            cfg = wl.CONFIGS[name].with_(batch=batch)
+            pipe = Pipeline(cfg, wl.make_weights(cfg), wl.make_batch(cfg, batch), loop_mode=LOOP_MODE)
+            tau = wl.uniform_schedule(cfg.n_steps)
+            for _ in range(args.chunks):
+                pipe.build_cache()
+                pipe.denoise(tau)
+            torch.cuda.synchronize()
+            pipe.close()
+            print(json.dumps({"workload": name, "batch": batch, "chunks": args.chunks}))
+            return
+        for name, batch in todo:
             log(f"workload {name} batch {batch} ...")
             print(json.dumps(measure_workload(torch, wl, Pipeline, name, batch, 5)), flush=True)
         return
