@@ -171,6 +171,38 @@ def test_stress_batch_independence_and_parity(torch):
         assert e4 <= 2e-2 and e1 <= 2e-2 and dev <= 2e-2
 
 
+def test_stress_batch16_full_size_matches_single_requests(torch):
+    """The batch-16 stress workload at its full size and launch configuration
+    (P = 2048, n = 100, T = 20, the library's default driver: tiled GEMMs and
+    tiled attention): sampled requests match the same requests run alone at
+    B = 1 (untiled attention, other GEMM tiles) to the bf16 bar.  The oracle
+    is too slow at this size; the B = 1 path is itself oracle-checked above."""
+    from vla_testlib import Pipeline
+    cfg = wl.STRESS_PI0
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 16)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    p16 = Pipeline(cfg, W, inp, loop_mode=2)
+    try:
+        p16.build_cache()
+        out16 = p16.denoise(tau).cpu().numpy()
+    finally:
+        p16.close()
+    assert np.isfinite(out16).all()
+    for r in (0, 7, 15):
+        one = {k: v[r:r + 1] for k, v in inp.items()}
+        p1 = Pipeline(cfg, W, one, loop_mode=2)
+        try:
+            p1.build_cache()
+            out1 = p1.denoise(tau).cpu().numpy()
+        finally:
+            p1.close()
+        dev = np.abs(out1[0] - out16[r]).max()
+        scale = np.abs(out1[0]).max()
+        print(f"stress B=16 request {r}: max |B=16 - B=1| {dev:.3e} (max |a| {scale:.2f})")
+        assert dev <= 2e-2
+
+
 def test_cache_reuse_equals_rebuild_per_call(torch):
     """The cached K/V serve every solver step: a T-step call equals the same
     call after rebuilding the cache (bitwise)."""
