@@ -116,6 +116,28 @@ def measured_traffic(kernel_kind):
     return int(rec["traffic_bytes_per_launch"]) if sha == rec.get("source_sha256") else None
 
 
+def hbm_copy_rate(torch, mib=1024, reps=10):
+    """Measured HBM rate on this GPU: a device-to-device copy of `mib` MiB,
+    counted as bytes read + bytes written per second (GB/s)."""
+    n = mib << 18  # fp32 elements
+    src = torch.empty(n, dtype=torch.float32, device="cuda").fill_(1.0)
+    dst = torch.empty_like(src)
+    for _ in range(2):
+        dst.copy_(src)
+    start = torch.cuda.Event(enable_timing=True)
+    end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    start.record()
+    for _ in range(reps):
+        dst.copy_(src)
+    end.record()
+    torch.cuda.synchronize()
+    sec = start.elapsed_time(end) / 1000.0 / reps
+    del src, dst
+    torch.cuda.empty_cache()
+    return round(2.0 * n * 4 / sec / 1e9, 1)
+
+
 def cpu_baseline(cfg, W, inp, tau):
     """The oracle as it stands, one full chunk (prefix K/V build + T Euler
     steps) of the same workload on the host cores."""
@@ -304,6 +326,8 @@ def main():
         "roofline": roof,
     }
     pipe.close()
+    # measured peaks beside the spec ones: a plain copy for HBM
+    result["roofline"]["measured_hbm_copy_GBps"] = hbm_copy_rate(torch)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
         result["cpu_baseline"] = cpu_baseline(cfg, W, inp, tau)
