@@ -367,12 +367,17 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
 // block, in LDS:
 //   K   [64 keys][HD]   16-byte chunk c of key k at slot c ^ f(k),
 //                       f(k) = (k & 3) | ((k >> 1) & 4)
-//   V^T [HD][64 keys]   chunk c (8 keys) of dim d at slot c ^ (d % 8)
-// (the XORs give the 8 rows that one operand load reads per bank cycle, keys
-// 8 (r/4) + r%4 of the score-tile permutation resp. 8 consecutive dims, 8
-// different slots).  K goes
-// straight to LDS (direct-to-LDS loads, one wave instruction = 64 slots of
-// consecutive rows); V is transposed in registers, 4 keys x 8 dims per thread.
+//   V   [64 keys][HD]   16-byte chunk c of key k at slot c ^ 2 (k % 4)
+// Both arrive by direct-to-LDS loads (one wave instruction = 64 slots of
+// consecutive rows).  K rows are the A operand of S^T; the XOR gives the 8
+// rows one operand load reads per bank cycle (keys 8 (r/4) + r%4 of the
+// score-tile permutation) 8 different slots.  The V^T operand of
+// O^T += V^T P^T is read with ds_read_b64_tr_b16: within each 16 lanes, lane
+// i receives element i % 4 of the 8-byte blocks addressed by lanes i/4,
+// i/4 + 4, i/4 + 8 and i/4 + 12.  Lane p of a group therefore addresses key
+// row 8 g4 + p/4 (+4 for the second read) at dims 16 d + 4 (p % 4) and gets 4
+// consecutive keys of dim 16 d + p; the V swizzle puts the 4 rows one
+// 16-lane read touches in 4 disjoint 32-byte bank ranges.
 // The next block's loads are in flight while the current block's MFMAs run;
 // LDS is double-buffered.  Scores are computed transposed (S^T = K Q^T) with
 // the same key permutation as attn_kernel, so a lane's 8 keys of a 32-key half
@@ -381,9 +386,8 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
 
 typedef unsigned v4u_t __attribute__((ext_vector_type(4)));
 // One wave-wide global_load_lds_dwordx4: lane l's 16 bytes at g land in LDS at
-// wave-uniform lds + 16 l.  The compiler does not track it; the barrier that
-// follows (whose fence waits for every outstanding load) orders it against
-// the LDS reads.
+// wave-uniform lds + 16 l.  The compiler does not track it: an explicit
+// vmcnt(0) wait (dma_wait_all) before the barrier orders it against the reads.
 VLA_DEV void dma16(const void* g, void* lds) {
   typedef __attribute__((address_space(3))) v4u_t lds_v4u;
   const unsigned off = (unsigned)(uintptr_t)(lds_v4u*)lds;
@@ -391,8 +395,14 @@ VLA_DEV void dma16(const void* g, void* lds) {
   asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(base), "v"(g) : "memory", "m0");
 }
 
-// K slot swizzle of key k (see attn_tile)
+// Wait until every load this wave issued has completed, the direct-to-LDS ones
+// included: the compiler does not see those (asm) and would not wait for them
+// at a barrier by itself.
+VLA_DEV void dma_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
+
+// K and V slot swizzles of key k (see attn_tile)
 VLA_DEV int kswz(int k) { return (k & 3) | ((k >> 1) & 4); }
+VLA_DEV int vswz(int k) { return 2 * (k & 3); }
 
 constexpr int TQ = 128;   // rows per workgroup
 constexpr int TKB = 64;   // keys per block
@@ -402,7 +412,7 @@ template <int HD>
 struct TileLds {
   static constexpr int CPR = HD / 8;                          // 16-byte chunks per K row
   static constexpr size_t KB = (size_t)TKB * HD * 2;          // one K block (bf16)
-  static constexpr size_t VB = (size_t)HD * TKB * 2;          // one V^T block
+  static constexpr size_t VB = (size_t)TKB * HD * 2;          // one V block
   static constexpr size_t BYTES = 2 * (KB + VB);              // double-buffered
 };
 
@@ -413,7 +423,6 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
   constexpr int NQV = HD / 32;                  // k-steps of S^T (16-byte vectors per lane)
   constexpr int DT = HD / 16;                   // dim tiles of O^T
   constexpr int KLD = TKB * CPR / (64 * TW);    // K load instructions per wave and block
-  constexpr int VIT = 16 * (HD / 8);            // (4-key group, 8-dim group) items of a V block
   static_assert(KLD >= 1 && KLD * 64 * TW == TKB * CPR, "K staging");
   extern __shared__ __align__(16) unsigned char smem[];
 
@@ -471,13 +480,14 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
   // K: wave instruction i fills slots [(TW i + wave) * 64, + 64) of the block:
   // row slot0 / CPR + lane / CPR, slot lane % CPR, which holds k-chunk
   // slot ^ f(row).  Keys past the end read the last key (masked scores).
-  // this lane's element offset inside a block of prefix rows, per instruction
-  int koffp[KLD];
+  // this lane's element offsets inside a block of prefix rows, per instruction
+  int koffp[KLD], voffp[KLD];
 #pragma unroll
   for (int i = 0; i < KLD; ++i) {
     const int slot0 = (TW * i + wave) * 64;
     const int row = slot0 / CPR + lane / CPR, sl = lane % CPR;
     koffp[i] = row * HD + (sl ^ kswz(row)) * 8;
+    voffp[i] = row * HD + (sl ^ vswz(row)) * 8;
   }
   auto kload = [&](int jb, int buf) {
     const int kx0 = (jb0 + jb) * TKB;
@@ -495,55 +505,45 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
       dma16(krow(min(kx0 + row, nkeys - 1)) + (sl ^ kswz(row)) * 8, kl + (size_t)slot0 * 16);
     }
   };
-  // V: thread = (4-key group vkg, 8-dim group vdg); keys past the end are zero
-  uint4 vreg[4];
-  const bool vthr = tid < VIT;
-  const int vkg = tid & 15, vdg = tid >> 4;
-  const int voffp = vkg * 4 * HD + vdg * 8;        // lane offset inside a block of prefix rows
-  auto vload = [&](int jb) {
-    const int kb0 = (jb0 + jb) * TKB;
-    if (kb0 + TKB <= npre) {
-      const bf16_t* base = vc + (size_t)kb0 * HD + voffp;
+  // V: the same slots per lane as K, with the chunk swizzle 2 (row % 4).
+  // Keys past the end read the last key; their probabilities are exactly
+  // zero (masked scores), so they add nothing.
+  auto vload = [&](int jb, int buf) {
+    const int kx0 = (jb0 + jb) * TKB;
+    unsigned char* vl = smem + buf * (L::KB + L::VB) + L::KB;
+    if (kx0 + TKB <= npre) {
+      const bf16_t* base = vc + (size_t)kx0 * HD;
 #pragma unroll
-      for (int e = 0; e < 4; ++e) vreg[e] = vthr ? ldg16(base + e * HD) : make_uint4(0, 0, 0, 0);
+      for (int i = 0; i < KLD; ++i) dma16(base + voffp[i], vl + (size_t)(TW * i + wave) * 64 * 16);
       return;
     }
-    const int kx0 = kb0 + vkg * 4;
 #pragma unroll
-    for (int e = 0; e < 4; ++e) {
-      const bool ok = vthr && kx0 + e < nkeys;
-      vreg[e] = ok ? ldg16(vrow(kx0 + e) + vdg * 8) : make_uint4(0, 0, 0, 0);
-    }
-  };
-  auto vstore = [&](int buf) {
-    if (!vthr) return;
-    unsigned char* vl = smem + buf * (L::KB + L::VB) + L::KB;
-    const uint32_t w[4][4] = {{vreg[0].x, vreg[0].y, vreg[0].z, vreg[0].w}, {vreg[1].x, vreg[1].y, vreg[1].z, vreg[1].w},
-                              {vreg[2].x, vreg[2].y, vreg[2].z, vreg[2].w}, {vreg[3].x, vreg[3].y, vreg[3].z, vreg[3].w}};
-#pragma unroll
-    for (int j = 0; j < 8; ++j) {
-      // dim vdg*8 + j of keys vkg*4 .. +3
-      uint32_t o2[2];
-#pragma unroll
-      for (int q = 0; q < 2; ++q) {
-        const uint32_t lo = w[2 * q][j >> 1], hi = w[2 * q + 1][j >> 1];
-        o2[q] = (j & 1) ? ((lo >> 16) | (hi & 0xFFFF0000u)) : ((lo & 0xFFFFu) | (hi << 16));
-      }
-      const int d = vdg * 8 + j;
-      *reinterpret_cast<uint2*>(vl + (size_t)(d * 8 + ((vkg >> 1) ^ (d & 7))) * 16 + (vkg & 1) * 8) = make_uint2(o2[0], o2[1]);
+    for (int i = 0; i < KLD; ++i) {
+      const int slot0 = (TW * i + wave) * 64;
+      const int row = slot0 / CPR + lane / CPR, sl = lane % CPR;
+      dma16(vrow(min(kx0 + row, nkeys - 1)) + (sl ^ vswz(row)) * 8, vl + (size_t)slot0 * 16);
     }
   };
 
   // LDS operand slots of this lane.  Score-tile row r16 is key
   // 32 kk + 4 t + 8 (r16/4) + r16%4, whose swizzle f(key) = r16 % 8 for every
   // kk and t; V^T row d*16 + r16 likewise has swizzle r16 % 8.
-  int kslot[NQV], vslot[2];
+  int kslot[NQV];
   {
     const int key0 = 8 * (r16 >> 2) + (r16 & 3), f = r16 & 7;
 #pragma unroll
     for (int c = 0; c < NQV; ++c) kslot[c] = key0 * CPR + ((g4 * NQV + c) ^ f);
+  }
+  // V^T reads: lane p = r16 of group g4 addresses row 8 g4 + p/4 (+4, +32 kk)
+  // at dims 16 d + 4 (p % 4): chunk 2 d + (p % 4)/2, swizzled by the row's
+  // 2 (row % 4) = 2 (p / 4), byte 8 (p % 2) within it.  vb[q] is the byte
+  // offset for dim tiles with d % 4 == q; tile d adds 128 (d / 4).
+  int vb[4];
+  {
+    const int q4 = r16 >> 2;
+    const int rowb = (8 * g4 + q4) * HD * 2;
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) vslot[kk] = r16 * 8 + ((kk * 4 + g4) ^ f);
+    for (int q = 0; q < 4; ++q) vb[q] = rowb + (((2 * q + ((r16 & 3) >> 1)) ^ (2 * q4)) * 16) + (r16 & 1) * 8;
   }
 
   f32x4 o[DT];
@@ -553,15 +553,15 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
   const float sc = a.scale * kLog2e;
 
   kload(0, 0);
-  vload(0);
-  vstore(0);
+  vload(0, 0);
+  dma_wait_all();
   __syncthreads();
   for (int jb = 0; jb < nb; ++jb) {
     const int buf = jb & 1;
     // buffer buf ^ 1 was last read in the previous block, which ended with a barrier
     if (jb + 1 < nb) {
       kload(jb + 1, buf ^ 1);
-      vload(jb + 1);
+      vload(jb + 1, buf ^ 1);
     }
     const uint4* kl = reinterpret_cast<const uint4*>(smem + buf * (L::KB + L::VB));
     const uint4* vl = reinterpret_cast<const uint4*>(smem + buf * (L::KB + L::VB) + L::KB);
@@ -634,13 +634,28 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
     for (int kk = 0; kk < 2; ++kk)
       pb[kk] = make_uint4(pack_bf16x2(p[kk][0], p[kk][1]), pack_bf16x2(p[kk][2], p[kk][3]),
                           pack_bf16x2(p[kk][4], p[kk][5]), pack_bf16x2(p[kk][6], p[kk][7]));
-    // O^T += V^T P^T: A = V^T rows (dims) with keys 32 kk + 8 g4 .. + 8
+    // O^T += V^T P^T: A = V^T (dims 16 d .. + 15, keys 32 kk + 8 g4 .. + 7) from
+    // two transposing reads of 4 keys each
+    {
+      typedef short v4s_t __attribute__((ext_vector_type(4)));
+      typedef __attribute__((address_space(3))) v4s_t lds_v4s;
+      const unsigned char* vbase = reinterpret_cast<const unsigned char*>(vl);
 #pragma unroll
-    for (int d = 0; d < DT; ++d)
+      for (int d = 0; d < DT; ++d)
 #pragma unroll
-      for (int kk = 0; kk < 2; ++kk) mma16(o[d], vl[vslot[kk] + d * 16 * 8], pb[kk], bf16_t());
-    if (jb + 1 < nb) vstore(buf ^ 1);
-    __syncthreads();  // its fence also waits for the K loads of block jb + 1
+        for (int kk = 0; kk < 2; ++kk) {
+          const unsigned char* ap = vbase + vb[d & 3] + 128 * (d >> 2) + kk * 32 * HD * 2;
+          const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(ap));
+          const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(ap + 4 * HD * 2));
+          const uint4 va = make_uint4(((uint32_t)(uint16_t)lo[0]) | ((uint32_t)(uint16_t)lo[1] << 16),
+                                      ((uint32_t)(uint16_t)lo[2]) | ((uint32_t)(uint16_t)lo[3] << 16),
+                                      ((uint32_t)(uint16_t)hi[0]) | ((uint32_t)(uint16_t)hi[1] << 16),
+                                      ((uint32_t)(uint16_t)hi[2]) | ((uint32_t)(uint16_t)hi[3] << 16));
+          mma16(o[d], va, pb[kk], bf16_t());
+        }
+    }
+    dma_wait_all();   // the K / V loads of block jb + 1 have landed (this wave's) ...
+    __syncthreads();  // ... and every wave's
   }
 
   // lane holds O^T[dim 16 d + 4 g4 + i][row R]
