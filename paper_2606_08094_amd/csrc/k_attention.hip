@@ -19,8 +19,10 @@
 // one query and the online-softmax statistics live in the lane.  Row rho of
 // score tile t holds key 8*(rho/4) + 4*t + rho%4 of the block; lane group q
 // (= lane/16) then holds keys 8q .. 8q+7 across the two tiles, exactly the k
-// slots of its B operand in O^T += V^T P^T, and V is stored transposed in LDS
-// ([dim][key], written as key pairs) so the A operand is one 16-byte read.
+// slots of its B operand in O^T += V^T P^T.  bf16 V is staged row-major and
+// read as V^T with two transposing LDS loads per operand (layout as in
+// attn_tile); fp32 V is stored transposed ([dim][key], written as key pairs)
+// so the A operand is one 16-byte read.
 //
 // With more than one key split each split writes its output normalised by its
 // own sum (element type) plus its (max, sum); attn_merge combines them.
@@ -34,9 +36,11 @@ template <typename T, int HD>
 struct AttnLds {
   static constexpr int E = ElemTraits<T>::E;
   static constexpr int KP = HD + E;       // K row pitch (elements)
-  static constexpr int VP = 32 + E;       // V^T row pitch (elements)
+  static constexpr int VP = 32 + E;       // fp32: V^T row pitch (elements)
   static constexpr size_t KBYTES = 32 * KP * sizeof(T);
-  static constexpr size_t VBYTES = HD * VP * sizeof(T);
+  // bf16: V row-major [32 keys][HD], 16-byte chunk c of key k at slot
+  // c ^ 2 (k % 4), read with transposing loads; fp32: V^T [HD][VP]
+  static constexpr size_t VBYTES = E == 8 ? (size_t)32 * HD * sizeof(T) : (size_t)HD * VP * sizeof(T);
   static constexpr size_t BUF = KBYTES + VBYTES;  // one 32-key block
 };
 
@@ -116,16 +120,56 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
   for (int d = 0; d < DT; ++d) o[d] = f32x4{0.f, 0.f, 0.f, 0.f};
   float mrun = -INFINITY, lrun = 0.0f;
   const float sc = a.scale * kLog2e;
+  // bf16 V^T reads: byte offset of this lane's 8-byte block for dim tiles d
+  // with d % 4 == q (row 8 g4 + r16/4, dims 16 d + 4 (r16 % 4), swizzled)
+  int vtr[4];
+#pragma unroll
+  for (int q = 0; q < 4; ++q)
+    vtr[q] = (8 * g4 + (r16 >> 2)) * HD * 2 + (((2 * q + ((r16 & 3) >> 1)) ^ (2 * (r16 >> 2))) * 16) + (r16 & 1) * 8;
 
   for (int c0 = 0; c0 < nblk; c0 += KB_MAX) {
     const int cb = min(KB_MAX, nblk - c0);
     if (c0 > 0) __syncthreads();   // the previous chunk's LDS reads are done
     // Stage blocks c0 .. c0+cb-1 of the split into LDS slots 0 .. cb-1.  K item
-    // i: vector i % VPR of key row (i / VPR) % 32 of slot i / (32 VPR).  V item
-    // i: vector i / 16 % VPR of the key pair i % 16, slot i / (16 VPR); a pair
-    // is written as one 2-element column of V^T.  Keys past the end are zero
-    // (no NaN from unwritten LDS).
-    const int nk = cb * 32 * VPR, nv = cb * 16 * VPR;
+    // i: vector i % VPR of key row (i / VPR) % 32 of slot i / (32 VPR).  bf16 V
+    // items are the same (row-major, swizzled); fp32 V item i is vector
+    // i / 16 % VPR of the key pair i % 16, slot i / (16 VPR), written as one
+    // 2-element column of V^T.  Keys past the end are zero (no NaN from
+    // unwritten LDS).
+    const int nk = cb * 32 * VPR;
+    if constexpr (E == 8) {
+      for (int base = threadIdx.x; base < nk; base += UB * nthr) {
+        uint4 kr4[UB], vr4[UB];
+#pragma unroll
+        for (int q = 0; q < UB; ++q) {
+          const int i = base + q * nthr;
+          kr4[q] = make_uint4(0, 0, 0, 0);
+          vr4[q] = make_uint4(0, 0, 0, 0);
+          const T *kp, *vp;
+          if (i < nk) {
+            const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
+            const int kr = r / VPR, cv = r - kr * VPR;
+            if (src(c0 + jb, kr, kp, vp)) {
+              kr4[q] = ldg16(kp + cv * E);
+              vr4[q] = ldg16(vp + cv * E);
+            }
+          }
+        }
+#pragma unroll
+        for (int q = 0; q < UB; ++q) {
+          const int i = base + q * nthr;
+          if (i < nk) {
+            const int jb = i / (32 * VPR), r = i - jb * 32 * VPR;
+            const int kr = r / VPR, cv = r - kr * VPR;
+            T* kl = reinterpret_cast<T*>(smem + jb * L::BUF);
+            *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * E) = kr4[q];
+            unsigned char* vl = smem + jb * L::BUF + L::KBYTES;
+            *reinterpret_cast<uint4*>(vl + (size_t)kr * HD * 2 + (cv ^ (2 * (kr & 3))) * 16) = vr4[q];
+          }
+        }
+      }
+    } else {
+    const int nv = cb * 16 * VPR;
     for (int base = threadIdx.x; base < nk; base += UB * nthr) {
       uint4 kr4[UB], v0[UB], v1[UB];
 #pragma unroll
@@ -162,20 +206,12 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
           T* vl = reinterpret_cast<T*>(smem + jb * L::BUF + L::KBYTES);
           const uint32_t a4[4] = {v0[q].x, v0[q].y, v0[q].z, v0[q].w};
           const uint32_t b4[4] = {v1[q].x, v1[q].y, v1[q].z, v1[q].w};
-          if constexpr (E == 8) {
 #pragma unroll
-            for (int e = 0; e < 8; ++e) {
-              const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-              const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-              *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
-            }
-          } else {
-#pragma unroll
-            for (int e = 0; e < 4; ++e)
-              *reinterpret_cast<uint2*>(vl + (cv * 4 + e) * L::VP + 2 * kp2) = make_uint2(a4[e], b4[e]);
-          }
+          for (int e = 0; e < 4; ++e)
+            *reinterpret_cast<uint2*>(vl + (cv * 4 + e) * L::VP + 2 * kp2) = make_uint2(a4[e], b4[e]);
         }
       }
+    }
     }
     __syncthreads();
 
@@ -230,9 +266,20 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
         pb.y = pack_bf16x2(p[2], p[3]);
         pb.z = pack_bf16x2(p[4], p[5]);
         pb.w = pack_bf16x2(p[6], p[7]);
+        // A = V^T (dims 16 d + r16, keys 8 g4 .. + 7) from two transposing
+        // reads of the row-major V block (see attn_tile)
+        typedef short v4s_t __attribute__((ext_vector_type(4)));
+        typedef __attribute__((address_space(3))) v4s_t lds_v4s;
+        const unsigned char* vbase = reinterpret_cast<const unsigned char*>(vl);
 #pragma unroll
         for (int d = 0; d < DT; ++d) {
-          const uint4 va = *reinterpret_cast<const uint4*>(vl + (d * 16 + r16) * L::VP + 8 * g4);
+          const unsigned char* ap = vbase + vtr[d & 3] + 128 * (d >> 2);
+          const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(ap));
+          const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(ap + 4 * HD * 2));
+          const uint4 va = make_uint4(((uint32_t)(uint16_t)lo[0]) | ((uint32_t)(uint16_t)lo[1] << 16),
+                                      ((uint32_t)(uint16_t)lo[2]) | ((uint32_t)(uint16_t)lo[3] << 16),
+                                      ((uint32_t)(uint16_t)hi[0]) | ((uint32_t)(uint16_t)hi[1] << 16),
+                                      ((uint32_t)(uint16_t)hi[2]) | ((uint32_t)(uint16_t)hi[3] << 16));
           mma16(o[d], va, pb, T());
         }
       } else {
