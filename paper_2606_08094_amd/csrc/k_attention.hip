@@ -32,6 +32,12 @@ namespace {
 
 constexpr float kLog2e = 1.4426950408889634f;
 
+// K slot swizzle of attn_tile: K rows are stored unpadded with 16-byte chunk
+// c of key k at slot c ^ kswz(k).  A score-operand read takes, in one bank
+// cycle (eight lanes of 16 bytes), keys 8 (r / 4) + r % 4 for r = 0 .. 7 at
+// one chunk, and kswz maps those eight keys to eight different slots.
+VLA_DEV int kswz(int k) { return (k & 3) | ((k >> 1) & 4); }
+
 template <typename T, int HD>
 struct AttnLds {
   static constexpr int E = ElemTraits<T>::E;
@@ -447,8 +453,7 @@ VLA_DEV void dma16(const void* g, void* lds) {
 // at a barrier by itself.
 VLA_DEV void dma_wait_all() { __builtin_amdgcn_s_waitcnt(0x0F70); }  // vmcnt(0)
 
-// K and V slot swizzles of key k (see attn_tile)
-VLA_DEV int kswz(int k) { return (k & 3) | ((k >> 1) & 4); }
+// V slot swizzle of key k (see attn_tile)
 VLA_DEV int vswz(int k) { return 2 * (k & 3); }
 
 constexpr int TQ = 128;   // rows per workgroup

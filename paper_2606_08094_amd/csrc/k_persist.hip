@@ -46,6 +46,8 @@ constexpr int KBA_MAX = 2;               // 32-key blocks per attention split
 constexpr int MB = 8;                    // key splits one of a vector's 4 merge threads loads (S <= 32)
 constexpr long SPIN_LIMIT = 1L << 21;
 constexpr float kLog2e = 1.4426950408889634f;
+typedef short v4s_t __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) v4s_t lds_v4s;
 
 // Buffer resource over [base, base + bytes): loads past the end read zero,
 // stores past the end are dropped.
@@ -250,9 +252,10 @@ VLA_DEV void tile_reduce(f32x4 (&acc)[4][NS], f32x4* red) {
 template <int HD>
 struct PLds {
   static constexpr int KP = HD + 8;    // K row pitch (bf16)
-  static constexpr int VP = 32 + 8;    // V^T row pitch (bf16)
+  // V row-major [32 keys][HD], unpadded: 16-byte chunk c of key k at slot
+  // c ^ 2 (k % 4); read as the V^T operand with transposing LDS loads
   static constexpr size_t KBYTES = 32 * KP * 2;
-  static constexpr size_t BUF = KBYTES + (size_t)HD * VP * 2;
+  static constexpr size_t BUF = KBYTES + (size_t)32 * HD * 2;
 };
 
 size_t lds_main(int hd) {
@@ -268,7 +271,6 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   constexpr int NQV = HD / 32;             // Q fragments per lane
   constexpr int DTL = HD / 16;             // dim tiles of O^T
   constexpr int NKI = (KBA_MAX * 32 * VPR + NTHR - 1) / NTHR;  // K items per thread
-  constexpr int NVI = (KBA_MAX * 16 * VPR + NTHR - 1) / NTHR;  // V key-pair items per thread
   constexpr int OKS = 8;                   // O-projection k-steps of 32 (K = HT * hd <= 256)
   constexpr int OTW = 2;                   // O-projection 16-column tiles per rank
   extern __shared__ __align__(16) unsigned char smem[];
@@ -579,7 +581,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   const bool att_on = rank < S;
   const int jbeg = rank < nps ? rank * a.kba : nbp + (rank - nps);
   const int nblk = att_on ? (rank < nps ? min(nbp, jbeg + a.kba) : jbeg + 1) - jbeg : 0;
-  uint4 kpre[NKI], vp0[NVI], vp1[NVI];
+  uint4 kpre[NKI], vpre[NKI];
   auto prefetch_kv = [&](int l) {
     const bf16_t* kc = kvbase + lt[l].cache_off + (size_t)gteam * npre * HD;
     const bf16_t* vc = kc + (size_t)a.G * npre * HD;
@@ -592,39 +594,20 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       const int j = jbeg + jb, key = j * 32 + kr;
       const bool ok = i < nblk * 32 * VPR && j < nbp;   // keys past the prefix read zero
       kpre[q] = ld16<0>(KR, ok ? (unsigned)(key * HD + cv * 8) * 2u : OOB);
-    }
-#pragma unroll
-    for (int q = 0; q < NVI; ++q) {
-      const int i = tid + q * NTHR;
-      const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
-      const int kp2 = rr & 15, cv = rr >> 4;
-      const int j = jbeg + jb, key = j * 32 + 2 * kp2;
-      const bool ok = i < nblk * 16 * VPR && j < nbp;
-      vp0[q] = ld16<0>(VR, ok ? (unsigned)(key * HD + cv * 8) * 2u : OOB);
-      vp1[q] = ld16<0>(VR, ok ? (unsigned)((key + 1) * HD + cv * 8) * 2u : OOB);
+      vpre[q] = ld16<0>(VR, ok ? (unsigned)(key * HD + cv * 8) * 2u : OOB);
     }
   };
 
-  // LDS staging of one attention split's blocks: K rows as they are, V transposed
-  // (dims x keys) for the O^T = V^T P^T products.
-  auto put_k = [&](int i, uint4 v) {
+  // LDS staging of one attention split's blocks: item i is 16-byte vector
+  // i % VPR of key row (i / VPR) % 32 of block i / (32 VPR), for K and V alike.
+  // K rows go to their padded rows, V rows to their swizzled slots.
+  auto put_kv = [&](int i, uint4 k, uint4 v) {
     const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
     const int kr = rr / VPR, cv = rr - kr * VPR;
     bf16_t* kl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF);
-    *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * 8) = v;
-  };
-  auto put_v = [&](int i, uint4 v0, uint4 v1) {
-    const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
-    const int kp2 = rr & 15, cv = rr >> 4;
-    bf16_t* vl = reinterpret_cast<bf16_t*>(smem + jb * L::BUF + L::KBYTES);
-    const uint32_t a4[4] = {v0.x, v0.y, v0.z, v0.w};
-    const uint32_t b4[4] = {v1.x, v1.y, v1.z, v1.w};
-#pragma unroll
-    for (int e = 0; e < 8; ++e) {
-      const uint32_t lo = (a4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-      const uint32_t hi = (b4[e >> 1] >> (16 * (e & 1))) & 0xFFFFu;
-      *reinterpret_cast<uint32_t*>(vl + (cv * 8 + e) * L::VP + 2 * kp2) = lo | (hi << 16);
-    }
+    *reinterpret_cast<uint4*>(kl + kr * L::KP + cv * 8) = k;
+    unsigned char* vl = smem + jb * L::BUF + L::KBYTES;
+    *reinterpret_cast<uint4*>(vl + kr * HD * 2 + (cv ^ (2 * (kr & 3))) * 16) = v;
   };
   // Prefix K / V of the split, from the prefetched registers (chunk blocks get
   // zeros here and their keys after the barrier).
@@ -632,12 +615,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
     for (int q = 0; q < NKI; ++q) {
       const int i = tid + q * NTHR;
-      if (i < nblk * 32 * VPR) put_k(i, kpre[q]);
-    }
-#pragma unroll
-    for (int q = 0; q < NVI; ++q) {
-      const int i = tid + q * NTHR;
-      if (i < nblk * 16 * VPR) put_v(i, vp0[q], vp1[q]);
+      if (i < nblk * 32 * VPR) put_kv(i, kpre[q], vpre[q]);
     }
   };
 
@@ -713,7 +691,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         const unsigned qb = (unsigned)(qrow * QW + hh * HD + g4 * (HD / 4)) * 2u;
 #pragma unroll
         for (int c = 0; c < NQV; ++c) qf[c] = ld16<LDX>(Qr, qwave ? qb + 16u * c : OOB);
-        uint4 kch[NKI], vc0[NVI], vc1[NVI];
+        uint4 kch[NKI], vch[NKI];
 #pragma unroll
         for (int q = 0; q < NKI; ++q) {
           const int i = tid + q * NTHR;
@@ -721,28 +699,15 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
           const int kr = rr / VPR, cv = rr - kr * VPR;
           const int j = jbeg + jb, key = (j - nbp) * 32 + kr;
           const bool ok = i < nblk * 32 * VPR && j >= nbp;
-          kch[q] = ld16<LDX>(Qr, ok ? (unsigned)(key * QW + HTD + cv * 8) * 2u : OOB);
-        }
-#pragma unroll
-        for (int q = 0; q < NVI; ++q) {
-          const int i = tid + q * NTHR;
-          const int jb = i / (16 * VPR), rr = i - jb * 16 * VPR;
-          const int kp2 = rr & 15, cv = rr >> 4;
-          const int j = jbeg + jb, key = (j - nbp) * 32 + 2 * kp2;
-          const bool ok = i < nblk * 16 * VPR && j >= nbp;
-          vc0[q] = ld16<LDX>(Qr, ok ? (unsigned)(key * QW + HTD + HD + cv * 8) * 2u : OOB);
-          vc1[q] = ld16<LDX>(Qr, ok ? (unsigned)((key + 1) * QW + HTD + HD + cv * 8) * 2u : OOB);
+          const unsigned off = ok ? (unsigned)(key * QW + HTD + cv * 8) * 2u : OOB;
+          kch[q] = ld16<LDX>(Qr, off);
+          vch[q] = ld16<LDX>(Qr, ok ? off + HD * 2u : OOB);
         }
         if (jbeg + nblk > nbp) {   // the split holds chunk-token keys
 #pragma unroll
           for (int q = 0; q < NKI; ++q) {
             const int i = tid + q * NTHR;
-            if (i < nblk * 32 * VPR && jbeg + i / (32 * VPR) >= nbp) put_k(i, kch[q]);
-          }
-#pragma unroll
-          for (int q = 0; q < NVI; ++q) {
-            const int i = tid + q * NTHR;
-            if (i < nblk * 16 * VPR && jbeg + i / (16 * VPR) >= nbp) put_v(i, vc0[q], vc1[q]);
+            if (i < nblk * 32 * VPR && jbeg + i / (32 * VPR) >= nbp) put_kv(i, kch[q], vch[q]);
           }
         }
         __syncthreads();
@@ -750,60 +715,91 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
           f32x4 o[DTL];
 #pragma unroll
           for (int dd = 0; dd < DTL; ++dd) o[dd] = f32x4{0.f, 0.f, 0.f, 0.f};
-          float mrun = -INFINITY, lrun = 0.0f;
+          // A split holds at most KBA_MAX blocks: every score of the split is
+          // computed first and kept in registers, so the exact maximum is
+          // known before any exponent and the accumulators never need a
+          // rescale.  Score tile t of block jb, row rho: key
+          // 32 jb + 8 (rho / 4) + 4 t + rho % 4; the lane holds keys
+          // 32 jb + 8 g4 + 4 t + i of query r16.
           const float sc = a.scale * kLog2e;
-          for (int jb = 0; jb < nblk; ++jb) {
+          f32x4 sv[KBA_MAX][2];
+          float mrun = -INFINITY;
+#pragma unroll
+          for (int jb = 0; jb < KBA_MAX; ++jb) {
             const int j = jbeg + jb;
-            const int cnt = j < nbp ? min(32, npre - j * 32) : min(32, nself - (j - nbp) * 32);
+            const int cnt = jb >= nblk ? 0 : j < nbp ? min(32, npre - j * 32) : min(32, nself - (j - nbp) * 32);
             const bf16_t* kl = reinterpret_cast<const bf16_t*>(smem + jb * L::BUF);
-            const bf16_t* vl = reinterpret_cast<const bf16_t*>(smem + jb * L::BUF + L::KBYTES);
-            f32x4 sv[2];
 #pragma unroll
             for (int t = 0; t < 2; ++t) {
-              sv[t] = f32x4{0.f, 0.f, 0.f, 0.f};
-              const int kr = 8 * (r16 >> 2) + 4 * t + (r16 & 3);
-              const bf16_t* krow = kl + kr * L::KP + g4 * (HD / 4);
+              sv[jb][t] = f32x4{0.f, 0.f, 0.f, 0.f};
+              if (jb < nblk) {
+                const int kr = 8 * (r16 >> 2) + 4 * t + (r16 & 3);
+                const bf16_t* krow = kl + kr * L::KP + g4 * (HD / 4);
+                // every operand of the tile is read before its first MFMA, so
+                // the LDS latencies overlap
+                uint4 kf[NQV];
 #pragma unroll
-              for (int c = 0; c < NQV; ++c) mma16(sv[t], *reinterpret_cast<const uint4*>(krow + c * 8), qf[c], bf16_t());
+                for (int c = 0; c < NQV; ++c) kf[c] = *reinterpret_cast<const uint4*>(krow + c * 8);
+                __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+                for (int c = 0; c < NQV; ++c) mma16(sv[jb][t], kf[c], qf[c], bf16_t());
+              }
+#pragma unroll
+              for (int i = 0; i < 4; ++i) {
+                const int kr = 8 * g4 + 4 * t + i;
+                sv[jb][t][i] = (kr < cnt) ? sv[jb][t][i] * sc : -INFINITY;
+                mrun = fmaxf(mrun, sv[jb][t][i]);
+              }
             }
-            float bmax = -INFINITY;
+          }
+          mrun = fmaxf(mrun, __shfl_xor(mrun, 16, 64));
+          mrun = fmaxf(mrun, __shfl_xor(mrun, 32, 64));
+          float lrun = 0.0f;
+#pragma unroll
+          for (int jb = 0; jb < KBA_MAX; ++jb) {
+            if (jb >= nblk) continue;
+            const bf16_t* vl = reinterpret_cast<const bf16_t*>(smem + jb * L::BUF + L::KBYTES);
             float p[8];
 #pragma unroll
             for (int t = 0; t < 2; ++t)
 #pragma unroll
               for (int i = 0; i < 4; ++i) {
-                const int kr = 8 * g4 + 4 * t + i;
-                const float v = (kr < cnt) ? sv[t][i] * sc : -INFINITY;
-                p[4 * t + i] = v;
-                bmax = fmaxf(bmax, v);
+                p[4 * t + i] = exp2f(sv[jb][t][i] - mrun);
+                lrun += p[4 * t + i];
               }
-            bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
-            bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-            const float mnew = fmaxf(mrun, bmax);
-            const float corr = exp2f(mrun - mnew);
-            float psum = 0.0f;
-#pragma unroll
-            for (int kk = 0; kk < 8; ++kk) {
-              p[kk] = exp2f(p[kk] - mnew);
-              psum += p[kk];
-            }
-            psum += __shfl_xor(psum, 16, 64);
-            psum += __shfl_xor(psum, 32, 64);
-            lrun = lrun * corr + psum;
-            mrun = mnew;
-#pragma unroll
-            for (int dd = 0; dd < DTL; ++dd) o[dd] *= corr;
             uint4 pb;
             pb.x = pack_bf16x2(p[0], p[1]);
             pb.y = pack_bf16x2(p[2], p[3]);
             pb.z = pack_bf16x2(p[4], p[5]);
             pb.w = pack_bf16x2(p[6], p[7]);
+            // A operand of dim tile dd: V^T rows 16 dd + r16, keys 8 g4 .. + 7,
+            // from two transposing reads.  Within 16 lanes, lane i receives
+            // element i % 4 of the 8-byte blocks that lanes i/4, i/4 + 4,
+            // i/4 + 8 and i/4 + 12 address; lane p addresses key row
+            // 8 g4 + p / 4 (+ 4 for the second read) at dims 16 dd + 4 (p % 4)
+            // and so gets 4 consecutive keys of dim 16 dd + p.
+            constexpr int VG = DTL < 4 ? DTL : 4;   // V^T operands read ahead of their MFMAs
+            const unsigned char* vb = reinterpret_cast<const unsigned char*>(vl) + (8 * g4 + (r16 >> 2)) * HD * 2 + (r16 & 1) * 8;
 #pragma unroll
-            for (int dd = 0; dd < DTL; ++dd) {
-              const uint4 va = *reinterpret_cast<const uint4*>(vl + (dd * 16 + r16) * L::VP + 8 * g4);
-              mma16(o[dd], va, pb, bf16_t());
+            for (int d0 = 0; d0 < DTL; d0 += VG) {
+              uint4 va[VG];
+#pragma unroll
+              for (int i = 0; i < VG; ++i) {
+                const int dd = d0 + i;
+                const unsigned char* ap = vb + ((2 * dd + ((r16 & 3) >> 1)) ^ (2 * (r16 >> 2))) * 16;
+                const v4s_t lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(ap));
+                const v4s_t hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16((lds_v4s*)(ap + 4 * HD * 2));
+                va[i] = make_uint4(((uint32_t)(uint16_t)lo[0]) | ((uint32_t)(uint16_t)lo[1] << 16),
+                                   ((uint32_t)(uint16_t)lo[2]) | ((uint32_t)(uint16_t)lo[3] << 16),
+                                   ((uint32_t)(uint16_t)hi[0]) | ((uint32_t)(uint16_t)hi[1] << 16),
+                                   ((uint32_t)(uint16_t)hi[2]) | ((uint32_t)(uint16_t)hi[3] << 16));
+              }
+#pragma unroll
+              for (int i = 0; i < VG; ++i) mma16(o[d0 + i], va[i], pb, bf16_t());
             }
           }
+          lrun += __shfl_xor(lrun, 16, 64);
+          lrun += __shfl_xor(lrun, 32, 64);
           // lane holds O^T[dim 16 dd + 4 g4 + i][query r16]
           if (qrow < n) {
             const float inv = lrun > 0.0f ? 1.0f / lrun : 0.0f;
