@@ -89,12 +89,16 @@ VLA_DEV uint4 ldg16(const void* p) {
 }
 VLA_DEV void stg16(void* p, uint4 v) { *reinterpret_cast<uint4*>(p) = v; }
 
-// Activations (fp32).  GELU uses the tanh form.
-VLA_DEV float silu_f(float x) { return x / (1.0f + __expf(-x)); }
+// Activations (fp32).  GELU uses the tanh form.  Both use the hardware
+// reciprocal (about 1 ulp) instead of a correctly rounded division; the
+// results feed bf16 operands.  tanh(y) = 1 - 2 / (1 + e^(2y)): for large |y|
+// the exponential saturates to inf or 0 and the result to +-1.
+VLA_DEV float silu_f(float x) { return x * __builtin_amdgcn_rcpf(1.0f + __expf(-x)); }
+VLA_DEV float tanh_f(float y) { return 1.0f - 2.0f * __builtin_amdgcn_rcpf(1.0f + __expf(2.0f * y)); }
 VLA_DEV float gelu_tanh_f(float x) {
   const float k0 = 0.7978845608028654f;  // sqrt(2/pi)
-  float inner = k0 * (x + 0.044715f * x * x * x);
-  return 0.5f * x * (1.0f + tanhf(inner));
+  const float inner = k0 * (x + 0.044715f * x * x * x);
+  return 0.5f * x * (1.0f + tanh_f(inner));
 }
 VLA_DEV float act_f(int act, float x) {
   switch (act) {

@@ -953,12 +953,33 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         tile_reduce<2>(acc, red);
         if (rank < npairs) {
           const int f = 16 * rank + r16;
+          // one branch on the (uniform) activation for the lane's four values
+          float g[4];
+#pragma unroll
+          for (int i = 0; i < 4; ++i) g[i] = acc[0][0][i];
+          switch (a.act) {
+            case ACT_SILU:
+#pragma unroll
+              for (int i = 0; i < 4; ++i) g[i] = silu_f(g[i]);
+              break;
+            case ACT_GELU:
+#pragma unroll
+              for (int i = 0; i < 4; ++i) g[i] = gelu_tanh_f(g[i]);
+              break;
+            case ACT_RELU2:
+#pragma unroll
+              for (int i = 0; i < 4; ++i) { const float r = fmaxf(g[i], 0.0f); g[i] = r * r; }
+              break;
+            default: break;
+          }
+          if (a.glu) {
+#pragma unroll
+            for (int i = 0; i < 4; ++i) g[i] *= acc[0][1][i];
+          }
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int m = 16 * wave + 4 * g4 + i;
-            if (m >= n) continue;
-            const float h = a.glu ? act_f(a.act, acc[0][0][i]) * acc[0][1][i] : act_f(a.act, acc[0][0][i]);
-            st2(Hr, xtile_off(m, f, n), f2bf(h));   // tiled [F8/32][n][32]
+            if (m < n) st2(Hr, xtile_off(m, f, n), f2bf(g[i]));   // tiled [F8/32][n][32]
           }
         }
       }
