@@ -329,54 +329,80 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
 }
 
 // O[m][h] = sum_s w_s O_s / sum_s w_s with w_s = l_s * 2^(m_s - max_s m_s).
-// One wave per (output row, 64 16-byte vectors of the row); each lane merges
-// one vector in a single online pass (running max, rescaled sums) with the
-// (max, sum) and the partial vectors of SB splits loaded at once.
-constexpr int MERGE_SB = 16;
-
-template <typename T>
+// Q lanes per output vector (16 bytes of one row): lane q of the group merges
+// splits q, q + Q, ... (at most MB) in one online pass (running max, rescaled
+// sums) with all its loads issued at once, and the group's partial results
+// are combined through lane shuffles.  Q = 4 for more than 4 splits (up to
+// 64), else Q = 1, so that no lane of a short merge idles.
+template <typename T, int MERGE_Q, int MERGE_MB>
 __global__ __launch_bounds__(64) void attn_merge_kernel(AttnArgs a) {
   constexpr int E = ElemTraits<T>::E;
+  constexpr int VPW = 64 / MERGE_Q;   // vectors per wave
   const int rows = a.B * a.n, dq = a.H * a.hd;
-  const int cblocks = (dq + 64 * E - 1) / (64 * E);
+  const int cblocks = (dq + VPW * E - 1) / (VPW * E);
   const int m = blockIdx.x / cblocks;
-  const int c = ((blockIdx.x - m * cblocks) * 64 + threadIdx.x) * E;
-  if (c >= dq) return;
-  const int h = c / a.hd;
+  const int qt = threadIdx.x & (MERGE_Q - 1);
+  const int c = ((blockIdx.x - m * cblocks) * VPW + threadIdx.x / MERGE_Q) * E;
+  const bool live = c < dq;           // every lane stays for the shuffles
+  const int h = live ? c / a.hd : 0;
   const int S = a.kv_split, H = a.H;
   const T* part = reinterpret_cast<const T*>(a.part);
+  uint4 v[MERGE_MB];
+  float2 st[MERGE_MB];
+#pragma unroll
+  for (int j = 0; j < MERGE_MB; ++j) {
+    const int sp = qt + MERGE_Q * j;
+    const bool ok = live && sp < S;
+    st[j] = ok ? *reinterpret_cast<const float2*>(a.stats + (((size_t)sp * rows + m) * H + h) * 2)
+               : make_float2(-INFINITY, 0.0f);
+    v[j] = ok ? ldg16(part + ((size_t)sp * rows + m) * dq + c) : make_uint4(0, 0, 0, 0);
+  }
   float acc[E];
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] = 0.0f;
   float mx = -INFINITY, tot = 0.0f;
-  for (int s0 = 0; s0 < S; s0 += MERGE_SB) {
-    uint4 v[MERGE_SB];
-    float2 st[MERGE_SB];
 #pragma unroll
-    for (int q = 0; q < MERGE_SB; ++q) {
-      const bool ok = s0 + q < S;
-      st[q] = ok ? *reinterpret_cast<const float2*>(a.stats + (((size_t)(s0 + q) * rows + m) * H + h) * 2)
-                 : make_float2(-INFINITY, 0.0f);
-      v[q] = ok ? ldg16(part + ((size_t)(s0 + q) * rows + m) * dq + c) : make_uint4(0, 0, 0, 0);
-    }
+  for (int j = 0; j < MERGE_MB; ++j) {
+    if (st[j].y <= 0.0f) continue;     // absent split, or one without keys
+    const float mnew = fmaxf(mx, st[j].x);
+    const float corr = exp2f(mx - mnew);
+    const float w = st[j].y * exp2f(st[j].x - mnew);
+    float f[E];
+    unpack16(v[j], f, T());
 #pragma unroll
-    for (int q = 0; q < MERGE_SB; ++q) {
-      if (s0 + q >= S || st[q].y <= 0.0f) continue;
-      const float mnew = fmaxf(mx, st[q].x);
-      const float corr = exp2f(mx - mnew);
-      const float w = st[q].y * exp2f(st[q].x - mnew);
-      float f[E];
-      unpack16(v[q], f, T());
-#pragma unroll
-      for (int e = 0; e < E; ++e) acc[e] = acc[e] * corr + w * f[e];
-      tot = tot * corr + w;
-      mx = mnew;
-    }
+    for (int e = 0; e < E; ++e) acc[e] = acc[e] * corr + w * f[e];
+    tot = tot * corr + w;
+    mx = mnew;
   }
+#pragma unroll
+  for (int sh = 1; sh < MERGE_Q; sh <<= 1) {
+    const float mo = __shfl_xor(mx, sh, 64), to = __shfl_xor(tot, sh, 64);
+    const float mn = fmaxf(mx, mo);
+    const float cs = tot > 0.0f ? exp2f(mx - mn) : 0.0f, co = to > 0.0f ? exp2f(mo - mn) : 0.0f;
+#pragma unroll
+    for (int e = 0; e < E; ++e) acc[e] = acc[e] * cs + __shfl_xor(acc[e], sh, 64) * co;
+    tot = tot * cs + to * co;
+    mx = mn;
+  }
+  if (!live || qt != 0) return;
   const float inv = tot > 0.0f ? 1.0f / tot : 0.0f;
 #pragma unroll
   for (int e = 0; e < E; ++e) acc[e] *= inv;
   stg16(reinterpret_cast<T*>(a.o) + (size_t)m * a.ldo + c, pack16(acc, T()));
+}
+
+template <typename T>
+hipError_t launch_merge(const AttnArgs& a, hipStream_t s) {
+  constexpr int E = ElemTraits<T>::E;
+  const int dq = a.H * a.hd, rows = a.B * a.n;
+  if (a.kv_split <= 4) {
+    const int cblocks = (dq + 64 * E - 1) / (64 * E);
+    hipLaunchKernelGGL((attn_merge_kernel<T, 1, 4>), dim3(rows * cblocks), dim3(64), 0, s, a);
+  } else {
+    const int cblocks = (dq + 16 * E - 1) / (16 * E);
+    hipLaunchKernelGGL((attn_merge_kernel<T, 4, 16>), dim3(rows * cblocks), dim3(64), 0, s, a);
+  }
+  return hipGetLastError();
 }
 
 template <typename T, int HD>
@@ -403,10 +429,7 @@ hipError_t launch_hd(const AttnArgs& a, hipStream_t s, int which) {
     if (e != hipSuccess) return e;
   }
   if (which == 1 || a.kv_split == 1) return hipSuccess;
-  constexpr int E = ElemTraits<T>::E;
-  const int cblocks = (a.H * HD + 64 * E - 1) / (64 * E);
-  hipLaunchKernelGGL(attn_merge_kernel<T>, dim3(a.B * a.n * cblocks), dim3(64), 0, s, a);
-  return hipGetLastError();
+  return launch_merge<T>(a, s);
 }
 
 
@@ -751,9 +774,7 @@ hipError_t launch_tile_hd(const AttnArgs& a, hipStream_t s, int which) {
     if (e != hipSuccess) return e;
   }
   if (which == 1 || a.kv_split == 1) return hipSuccess;
-  const int cblocks = (a.H * HD + 64 * 8 - 1) / (64 * 8);
-  hipLaunchKernelGGL(attn_merge_kernel<bf16_t>, dim3(a.B * a.n * cblocks), dim3(64), 0, s, a);
-  return hipGetLastError();
+  return launch_merge<bf16_t>(a, s);
 }
 
 }  // namespace
