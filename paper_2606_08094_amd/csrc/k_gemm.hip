@@ -715,6 +715,8 @@ hipError_t skinny_t(const SkinnyShape& sh, const GemmArgs& a, hipStream_t s) {
     case 22: return skinny_cpw<T, 2, 2>(sh.cpw, a, sh.units, sh.lds, s);
     case 41: return skinny_cpw<T, 4, 1>(sh.cpw, a, sh.units, sh.lds, s);
     case 42: return skinny_cpw<T, 4, 2>(sh.cpw, a, sh.units, sh.lds, s);
+    case 24: return launch_skinny_t<T, 2, 4, 1>(a, sh.units, sh.lds, s);
+    case 44: return launch_skinny_t<T, 4, 4, 1>(a, sh.units, sh.lds, s);
   }
   return hipErrorInvalidValue;
 }
@@ -786,6 +788,13 @@ int gemm_chunk_k(int et) { return et == ET_BF16 ? 128 : 64; }
 bool skinny_plan(int et, int M, int N, int K, int nsub, bool allow_split, SkinnyShape* sh) {
   const int KC = gemm_chunk_k(et);
   if (M > 128) return false;
+  // Split-K partial outputs take any number of W subtiles: above 16 token rows
+  // four subtiles per workgroup read each X row block for 64 W rows instead
+  // of 16, which cuts the per-CU ingest that bounds these shapes -- as long as
+  // the grid still fills the chip.
+  if (nsub == 1 && allow_split && M > 16) {
+    if (skinny_plan(et, M, N, K, 4, true, sh) && sh->units >= 192) return true;
+  }
   sh->ms = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   sh->nsub = nsub;
   sh->n_tiles = cdiv_i(N, 16 * nsub);
@@ -796,6 +805,8 @@ bool skinny_plan(int et, int M, int N, int K, int nsub, bool allow_split, Skinny
   // pass over the 256 compute units.
   int nsplit = 1;
   if (allow_split) nsplit = std::max(1, std::min(chunks, 256 / std::max(1, base)));
+  // wide tiles: at least half the waves of a workgroup hold a chunk
+  if (nsub == 4) nsplit = std::max(1, std::min(nsplit, chunks / (WKS / 2)));
   const int cps = cdiv_i(chunks, nsplit);  // chunks per split
   sh->nsplit = cdiv_i(chunks, cps);
   sh->kper = cps * KC;
