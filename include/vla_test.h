@@ -18,9 +18,12 @@ extern "C" {
 /* y[M][N] (fp32) = x[M][K] w[N][K]^T on the MFMA GEMMs of the projections.
  * K % 8 == 0 (bf16) or K % 4 == 0 (fp32).  variant: 0 = the runtime's choice,
  * 1 = the wide kernel, 2 = the skinny kernel (VLA_E_UNSUPPORTED if the shape
- * does not fit it), 3 = the tiled kernel with the runtime's tile, 10..13 = the
- * tiled kernel with tile 64x128, 128x128, 256x128 or 128x256 (both
- * VLA_E_UNSUPPORTED unless bf16 with M > 128). */
+ * does not fit it), 3 = the tiled kernel with the runtime's tile, 4 = the
+ * launch of the residual projections: split-K fp32 partials (the runtime's
+ * split and tile), summed into y by the library (VLA_E_UNSUPPORTED for fp32
+ * with M > 128; a temporary partial buffer is allocated and freed),
+ * 10..13 = the tiled kernel with tile 64x128, 128x128, 256x128 or 128x256
+ * (both VLA_E_UNSUPPORTED unless bf16 with M > 128). */
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                          int32_t variant, float* y, void* stream);
 

@@ -193,6 +193,15 @@ __global__ void copy_f32_kernel(float* dst, const float* src, size_t n) {
     dst[i] = src[i];
 }
 
+// y[i] = sum over the nsplit partial arrays part[s][i], in split order.
+__global__ void sum_partials_kernel(float* y, const float* part, int nsplit, size_t n) {
+  for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
+    float v = 0.0f;
+    for (int sp = 0; sp < nsplit; ++sp) v += part[(size_t)sp * n + i];
+    y[i] = v;
+  }
+}
+
 __global__ void fill_u32_kernel(unsigned* p, unsigned v, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     p[i] = v;
@@ -275,6 +284,13 @@ hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s
   if (n == 0) return hipSuccess;
   const int blocks = (int)((n + 255) / 256 > 1024 ? 1024 : (n + 255) / 256);
   hipLaunchKernelGGL(copy_f32_kernel, dim3(blocks), dim3(256), 0, s, dst, src, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_sum_partials(float* y, const float* part, int nsplit, size_t n, hipStream_t s) {
+  if (n == 0) return hipSuccess;
+  const int blocks = (int)((n + 255) / 256 > 1024 ? 1024 : (n + 255) / 256);
+  hipLaunchKernelGGL(sum_partials_kernel, dim3(blocks), dim3(256), 0, s, y, part, nsplit, n);
   return hipGetLastError();
 }
 

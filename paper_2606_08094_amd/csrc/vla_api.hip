@@ -1343,8 +1343,8 @@ int32_t vla_test_persist_trace(vla_model* m, uint64_t* out, int32_t max_per_team
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                          int32_t variant, float* y, void* stream) {
   if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
-  if (variant < 0 || (variant > 3 && variant < 10) || variant > 13)
-    return fail(VLA_E_ARG, "variant must be 0..3 or 10..13");
+  if (variant < 0 || (variant > 4 && variant < 10) || variant > 13)
+    return fail(VLA_E_ARG, "variant must be 0..4 or 10..13");
   if (!x || !w || !y || !al16(x) || !al16(w) || !al16(y)) return fail(VLA_E_ARG, "bad buffer");
   if (M < 1 || N < 1 || K < 1 || K % (elem ? 8 : 4)) return fail(VLA_E_SHAPE, "bad GEMM shape");
   const int et = elem ? ET_BF16 : ET_F32;
@@ -1352,6 +1352,23 @@ vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, 
   GemmArgs g{};
   g.M = M; g.N = N; g.K = K; g.X = x; g.ldx = K; g.W = w;
   g.epi = EPI_STORE; g.out = y; g.ldo = N; g.out_f32 = 1;
+  if (variant == 4) {
+    // the residual projections' launch: split-K fp32 partials, summed here
+    g.epi = EPI_PARTIAL;
+    const DenseLaunch d = dense_launch(et, g, 1, 0);
+    if (!d.skinny && !d.tile) return fail(VLA_E_UNSUPPORTED, "no split-K launch for this shape");
+    float* part = nullptr;
+    if (hipMalloc(reinterpret_cast<void**>(&part), (size_t)d.splits() * M * N * sizeof(float)) != hipSuccess)
+      return fail(VLA_E_NOMEM, "gemm partials");
+    g.out = part;
+    hipError_t e = launch_dense(et, d, g, s);
+    if (e == hipSuccess) e = launch_sum_partials(y, part, d.splits(), (size_t)M * N, s);
+    hipError_t e2 = hipStreamSynchronize(s);
+    hipFree(part);
+    if (e != hipSuccess || e2 != hipSuccess)
+      return fail(VLA_E_DEVICE, "gemm: %s", hipGetErrorString(e != hipSuccess ? e : e2));
+    return VLA_OK;
+  }
   DenseLaunch d = dense_launch(et, g, 1, variant);
   if (variant == 2 && !d.skinny) return fail(VLA_E_UNSUPPORTED, "shape not supported by the skinny GEMM");
   if (variant >= 3 && !d.tile) return fail(VLA_E_UNSUPPORTED, "shape not supported by the tiled GEMM");

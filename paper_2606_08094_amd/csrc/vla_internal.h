@@ -234,6 +234,7 @@ hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s);
 hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
 hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);
+hipError_t launch_sum_partials(float* y, const float* part, int nsplit, size_t n, hipStream_t s);
 // Persistent kernel: whether a shape is supported, the dynamic LDS it needs,
 // and the cooperative launch (256 workgroups of 512 threads).
 bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, int glu, int* kba, int* nsplit);

@@ -100,7 +100,7 @@ def test_call_validation_without_device():
     assert L.vla_status_string(6) == b"VLA_E_NONFINITE"
     # test entries validate too
     assert vla.STATUS[L.vla_test_gemm(2, 16, 16, 1, 1, 8, 0, 16, None)] == "VLA_E_ARG"
-    assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 4, 16, None)] == "VLA_E_ARG"
+    assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 5, 16, None)] == "VLA_E_ARG"
     assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 14, 16, None)] == "VLA_E_ARG"
     # the tiled kernel takes bf16 with M > 128 only, refused before any device work
     assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 3, 16, None)] == "VLA_E_UNSUPPORTED"

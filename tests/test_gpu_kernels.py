@@ -40,12 +40,15 @@ GEMM_SHAPES = [
     (50, 1600, 720), (50, 720, 2048), (50, 6, 720),
     (8, 384, 256), (8, 7, 256), (1, 5, 8), (17, 33, 136), (100, 2560, 1024),
     (816, 512, 2048), (10, 6144, 1024), (128, 1024, 4096), (129, 64, 64), (50, 1024, 8192),
+    # split-K with four W subtiles per workgroup (variant 4), ragged in M, N and the last K split
+    (100, 1024, 4096), (90, 1000, 4096), (120, 1536, 3072),
     # large M (batched requests, prefix K/V build): the tiled kernel, ragged in M, N and K
     (400, 1024, 4096), (1600, 2560, 1024), (257, 136, 72), (300, 100, 200), (520, 200, 640),
 ]
 
-# 0 runtime choice, 1 wide, 2 skinny, 3 tiled (runtime tile), 10..13 tiled with a fixed tile
-GEMM_VARIANTS = (0, 1, 2, 3, 10, 11, 12, 13)
+# 0 runtime choice, 1 wide, 2 skinny, 3 tiled (runtime tile), 4 split-K partials (the residual
+# projections' launch) summed by the library, 10..13 tiled with a fixed tile
+GEMM_VARIANTS = (0, 1, 2, 3, 4, 10, 11, 12, 13)
 
 
 @pytest.mark.parametrize("elem", [1, 0])
@@ -66,7 +69,8 @@ def test_gemm_parity(torch, elem, M, N, K):
             vla.test_gemm(elem, _dev(torch, x, bf), _dev(torch, w, bf), M, N, K, y, variant=variant)
         except vla.VlaError as e:
             # shape outside the skinny kernel, or not a bf16 GEMM with M > 128 for the tiled one
-            assert e.status == 3 and (variant == 2 or (variant >= 3 and (not bf or M <= 128))), e
+            assert e.status == 3 and (variant == 2 or (variant == 4 and not bf and M > 128)
+                                      or (variant == 3 or variant >= 10) and (not bf or M <= 128)), e
             continue
         got = y.cpu().numpy().astype(np.float64)
         err = np.abs(got - ref)
