@@ -59,22 +59,26 @@ __device__ __forceinline__ void wave_epilogue(const GemmArgs& a, const f32x4 (&a
       break;
     }
     case EPI_GLU: {
-      // W rows nb .. nb+15 are gate rows, nb+16 .. nb+31 the matching up rows.
+      // W rows are interleaved 16-row blocks: gate block j at nb + 32 j, its
+      // up block at nb + 32 j + 16 (subtiles 2 j and 2 j + 1; NSUB = 2 or 4).
       const int F = N / 2;
-      const int f = (nb / 32) * 16 + r16;
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms)
+      for (int j = 0; j < NSUB / 2; ++j) {   // no pairs (and no output) in NSUB = 1 tiles
+        const int f = (nb / 32 + j) * 16 + r16;
 #pragma unroll
-        for (int i = 0; i < 4; ++i) {
-          const int m = m0 + ms * 16 + g4 * 4 + i;
-          if (m < M && f < F) {
-            const float h = act_f(a.act, acc[ms][0][i]) * acc[ms][NSUB - 1][i];
-            if (a.out_f32)
-              reinterpret_cast<float*>(a.out)[(size_t)m * a.ldo + f] = h;
-            else
-              reinterpret_cast<T*>(a.out)[(size_t)m * a.ldo + f] = ElemTraits<T>::from_f(h);
+        for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+          for (int i = 0; i < 4; ++i) {
+            const int m = m0 + ms * 16 + g4 * 4 + i;
+            if (m < M && f < F) {
+              const float h = act_f(a.act, acc[ms][2 * j][i]) * acc[ms][2 * j + 1][i];
+              if (a.out_f32)
+                reinterpret_cast<float*>(a.out)[(size_t)m * a.ldo + f] = h;
+              else
+                reinterpret_cast<T*>(a.out)[(size_t)m * a.ldo + f] = ElemTraits<T>::from_f(h);
+            }
           }
-        }
+      }
       break;
     }
     case EPI_PARTIAL: {

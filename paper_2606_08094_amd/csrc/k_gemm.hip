@@ -795,6 +795,10 @@ bool skinny_plan(int et, int M, int N, int K, int nsub, bool allow_split, Skinny
   if (nsub == 1 && allow_split && M > 16) {
     if (skinny_plan(et, M, N, K, 4, true, sh) && sh->units >= 192) return true;
   }
+  // Gate/up pairs (no split): two pairs per workgroup above 64 token rows.
+  if (nsub == 2 && M > 64) {
+    if (skinny_plan(et, M, N, K, 4, false, sh) && sh->units >= 192) return true;
+  }
   sh->ms = M <= 16 ? 1 : (M <= 32 ? 2 : 4);
   sh->nsub = nsub;
   sh->n_tiles = cdiv_i(N, 16 * nsub);
