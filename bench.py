@@ -197,6 +197,41 @@ def measure_workload(torch, wl, Pipeline, name, batch, reps):
             "dominant_frac_hbm": roof["frac"], "dominant_share": roof["share_of_profiled_time"]}
 
 
+def ternary_ablation(iters: int = 50):
+    """The paper's dot4-versus-matrix-unit question for the ternary GEMM (Sec. 4.5) on MI355X:
+    the same int8 codes and packed 2-bit weights through v_mfma_i32_16x16x64_i8 and through
+    v_dot4_i32_i8, for the ternary model's four projections (d 2560, F 6912) at 8 and 56 token
+    rows.  Algorithmic bytes: packed weights (N K / 4) + codes (M K) + fp32 output (M N 4)."""
+    import numpy as np
+    import torch
+    import workloads as wl
+    from paper_2606_08094_amd import vla
+    shapes = [("qkv", 3840, 2560), ("o", 2560, 2560), ("gate_up", 13824, 2560), ("down", 2560, 6912)]
+    rng = np.random.default_rng(2606)
+    for M in (8, 56):
+        for name, N, K in shapes:
+            q = rng.integers(-127, 128, size=(M, K), dtype=np.int8)
+            r = rng.uniform(0.5, 4.0, size=M).astype(np.float32)
+            wp = wl.pack_ternary(wl.random_ternary((N, K), 7 + N + K))
+            qd, rd = torch.from_numpy(q).cuda(), torch.from_numpy(r).cuda()
+            wd = torch.from_numpy(wp).cuda()
+            sd = torch.full((N,), 0.0244, dtype=torch.float32, device="cuda")
+            y0 = torch.empty((M, N), dtype=torch.float32, device="cuda")
+            y1 = torch.empty_like(y0)
+            us0 = vla.test_ternary_gemm(qd, rd, wd, sd, M, N, K, 0, y0, iters=iters)
+            us1 = vla.test_ternary_gemm(qd, rd, wd, sd, M, N, K, 1, y1, iters=iters)
+            same = bool(torch.equal(y0, y1))
+            alg = N * K // 4 + M * K + 4 * M * N
+            ops = 2 * M * N * K
+            print(json.dumps({"ablation": "ternary_w2a8_mfma_vs_dot4", "proj": name, "M": M, "N": N, "K": K,
+                              "mfma_us": round(us0, 2), "dot4_us": round(us1, 2),
+                              "mfma_speedup": round(us1 / us0, 2), "outputs_identical": same,
+                              "alg_bytes": alg, "mfma_hbm_frac": round(alg / (us0 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                              "dot4_hbm_frac": round(alg / (us1 * 1e-6) / 1e9 / HBM_PEAK_GBS, 4),
+                              "int8_tops_mfma": round(ops / (us0 * 1e-6) / 1e12, 2),
+                              "int8_tops_dot4": round(ops / (us1 * 1e-6) / 1e12, 2)}), flush=True)
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -217,7 +252,14 @@ def main():
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="only run 5 plain device-to-device copies of this many MiB (calibrates the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
+    ap.add_argument("--ternary-ablation", action="store_true",
+                    help="instead of the headline line, time the W2A8 GEMM of the ternary model's projections "
+                         "(M = 8 and 56) on the int8 MFMA kernel and on the VALU sdot4 kernel, one JSON line "
+                         "per shape")
     args = ap.parse_args()
+    if args.ternary_ablation:
+        ternary_ablation()
+        return
     if args.copy_mb > 0:
         import torch
         n = args.copy_mb << 18   # fp32 elements

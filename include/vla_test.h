@@ -51,6 +51,23 @@ vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q,
 vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
                                    float scale, float* y, void* stream);
 
+/* The W2A8 GEMM alone, on int8 activation codes already quantised, for the
+ * comparison of the paper's dot4 instruction path with its matrix-unit path
+ * (Sec. 4.5, the utilisation lever: the same ternary weights on dp4a versus the tensor cores; here
+ * v_dot4_i32_i8 on the vector ALUs versus v_mfma_i32_16x16x64_i8).
+ *   q [M][K] int8 codes, r [M] fp32 per-row absmax, w_packed [N][K/4] (the
+ *   2-bit layout of vla_test_ternary_linear), wscale [N] fp32, y [M][N] fp32:
+ *   y = (sum_k q w) * wscale[n] * r[m] / 127.  All device pointers, 16-byte
+ *   aligned; K % 64 == 0, 64 <= K <= 16384.
+ *   variant 0: the library's W2A8 launch (int8 MFMA); 1: the vector-ALU
+ *   sdot4 kernel.  Both sum exactly in int32, so y is identical.
+ *   iters >= 1 (at most 10000): the GEMM runs once untimed, then iters times
+ *   between two HIP events on `stream`; *us_per_launch (host, may be NULL)
+ *   receives the mean time of one launch.  Synchronises the stream. */
+vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t* w_packed, const float* wscale,
+                                 int32_t M, int32_t N, int32_t K, int32_t variant, int32_t iters, float* y,
+                                 float* us_per_launch, void* stream);
+
 /* Residual finish + adaRMS of the next sublayer (the row kernel that closes
  * every residual branch, scope rows a4 and a7): for every row m of M,
  *   x[m] += alpha * sum_{s < nsplit} part[s][m]      (alpha NULL: no update)

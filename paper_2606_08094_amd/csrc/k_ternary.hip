@@ -295,6 +295,99 @@ __global__ __launch_bounds__(256) void tern_skinny(TernArgs a) {
   wave_epilogue<bf16_t, 1, NSUB>(a.e, y, ms * 16, n0, 0);
 }
 
+// VALU variant of the small-M dequantised W2A8 GEMM (v_dot4_i32_i8 instead of
+// the int8 MFMA), for the dot4-versus-matrix-unit comparison: the same packed
+// weights and the same exact int32 sums.  A workgroup owns 16 W rows; wave w
+// takes rows 4w .. 4w+3, and lane l the 64-wide K chunks l, l + 64, ... of
+// every 4096-wide K slice.  The slice's activation codes are staged in LDS
+// for 16 token rows at a time (larger M: further passes over W).  A lane
+// widens its 4 rows' packed bytes to signed int8 once per chunk and forms the
+// 4 x 16 dot products of the chunk with sdot4 (16 per row and token row).
+// The 64 lanes' partial sums are added through LDS in lane order.  Output:
+// y = acc * s_w * r_m / 127 to e.out (fp32 or bf16, row-major, EPI_STORE).
+constexpr int D4_ROWS = 16, D4_RG = 4, D4_MB = 16, D4_KSL = 64 * 64;
+constexpr size_t D4_LDS = (size_t)D4_MB * D4_KSL + (size_t)4 * D4_RG * D4_MB * 64 * 4;
+
+__global__ __launch_bounds__(256) void tern_dot4(TernArgs a) {
+  extern __shared__ __align__(16) unsigned char smem[];
+  int8_t* xs = reinterpret_cast<int8_t*>(smem);                              // [D4_MB][D4_KSL]
+  int* red = reinterpret_cast<int*>(smem + (size_t)D4_MB * D4_KSL);          // [4][D4_RG][D4_MB][64]
+  const int t = threadIdx.x, lane = t & 63, wave = t >> 6;
+  const int M = a.M, N = a.N, K = a.K, KB = K / 4;
+  const int n0 = blockIdx.x * D4_ROWS + wave * D4_RG;
+  for (int m0 = 0; m0 < M; m0 += D4_MB) {
+    int acc[D4_RG][D4_MB];
+#pragma unroll
+    for (int r = 0; r < D4_RG; ++r)
+#pragma unroll
+      for (int m = 0; m < D4_MB; ++m) acc[r][m] = 0;
+    for (int ks = 0; ks < K; ks += D4_KSL) {
+      const int k = ks + lane * 64;
+      i32x4 wv[D4_RG][4];
+#pragma unroll
+      for (int r = 0; r < D4_RG; ++r) {
+        const int n = n0 + r;
+        const uint4 p = (n < N && k < K) ? ldg16(a.w + (size_t)n * KB + k / 4) : make_uint4(0, 0, 0, 0);
+        wv[r][0] = unpack_signed(p.x);
+        wv[r][1] = unpack_signed(p.y);
+        wv[r][2] = unpack_signed(p.z);
+        wv[r][3] = unpack_signed(p.w);
+      }
+      __syncthreads();   // the previous slice's LDS reads are done
+      constexpr int VR = D4_KSL / 16;
+      for (int i = t; i < D4_MB * VR; i += 256) {
+        const int row = i / VR, kv = i - row * VR;
+        const int m = m0 + row, kk = ks + kv * 16;
+        const uint4 v = (m < M && kk < K) ? ldg16(a.x + (size_t)m * K + kk) : make_uint4(0, 0, 0, 0);
+        *reinterpret_cast<uint4*>(xs + (size_t)row * D4_KSL + kv * 16) = v;
+      }
+      __syncthreads();
+      if (k < K) {
+#pragma unroll
+        for (int m = 0; m < D4_MB; ++m) {
+          if (m0 + m >= M) break;
+          const uint4* xp = reinterpret_cast<const uint4*>(xs + (size_t)m * D4_KSL + lane * 64);
+          uint4 xv[4];
+#pragma unroll
+          for (int q = 0; q < 4; ++q) xv[q] = xp[q];
+#pragma unroll
+          for (int r = 0; r < D4_RG; ++r) {
+            int s = acc[r][m];
+#pragma unroll
+            for (int q = 0; q < 4; ++q) {
+              s = __builtin_amdgcn_sdot4((int)xv[q].x, wv[r][q][0], s, false);
+              s = __builtin_amdgcn_sdot4((int)xv[q].y, wv[r][q][1], s, false);
+              s = __builtin_amdgcn_sdot4((int)xv[q].z, wv[r][q][2], s, false);
+              s = __builtin_amdgcn_sdot4((int)xv[q].w, wv[r][q][3], s, false);
+            }
+            acc[r][m] = s;
+          }
+        }
+      }
+    }
+#pragma unroll
+    for (int r = 0; r < D4_RG; ++r)
+#pragma unroll
+      for (int m = 0; m < D4_MB; ++m) red[((wave * D4_RG + r) * D4_MB + m) * 64 + lane] = acc[r][m];
+    __syncthreads();
+    // 16 rows x 16 token rows: one output per thread
+    {
+      const int row = t / D4_MB, m = t - row * D4_MB;
+      const int w = row / D4_RG, r = row - w * D4_RG;
+      const int* src = red + ((w * D4_RG + r) * D4_MB + m) * 64;
+      int s = 0;
+      for (int j = 0; j < 64; ++j) s += src[j];
+      const int n = blockIdx.x * D4_ROWS + row, mm = m0 + m;
+      if (n < N && mm < M) {
+        const float y = (float)s * (a.wscale[n] * a.rscale[mm] / 127.0f);
+        if (a.e.out_f32) reinterpret_cast<float*>(a.e.out)[(size_t)mm * a.e.ldo + n] = y;
+        else reinterpret_cast<bf16_t*>(a.e.out)[(size_t)mm * a.e.ldo + n] = f2bf(y);
+      }
+    }
+    __syncthreads();   // red and xs are reused by the next pass
+  }
+}
+
 template <int MS, int NSUB>
 hipError_t skinny_launch(const TernArgs& a, hipStream_t s) {
   constexpr int CPW = MS == 1 ? (NSUB == 1 ? 8 : 4) : (MS == 2 ? 4 : 2);  // <= 256 VGPRs: two waves per SIMD
@@ -324,6 +417,21 @@ hipError_t tern_nc(int nc, const TernArgs& a, int units, hipStream_t s) {
 }
 
 }  // namespace
+
+hipError_t launch_ternary_dot4(const TernArgs& a, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (a.K % 64 != 0 || a.rscale == nullptr || a.e.epi != EPI_STORE) return hipErrorInvalidValue;
+  static bool attr = false;
+  if (!attr) {
+    hipError_t e = hipFuncSetAttribute(reinterpret_cast<const void*>(&tern_dot4),
+                                       hipFuncAttributeMaxDynamicSharedMemorySize, (int)D4_LDS);
+    if (e != hipSuccess) return e;
+    attr = true;
+  }
+  const int grid = (a.N + D4_ROWS - 1) / D4_ROWS;
+  hipLaunchKernelGGL(tern_dot4, dim3(grid), dim3(256), D4_LDS, s, a);
+  return hipGetLastError();
+}
 
 // ms: m-subtiles (1, 2, 4); nsub 1 or 2 (GLU pairs); nc from a.ks / 256.
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s) {

@@ -1521,4 +1521,37 @@ vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int3
   return VLA_OK;
 }
 
+vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t* w_packed, const float* wscale,
+                                 int32_t M, int32_t N, int32_t K, int32_t variant, int32_t iters, float* y,
+                                 float* us_per_launch, void* stream) {
+  if (!q || !r || !w_packed || !wscale || !y || !al16(q) || !al16(w_packed) || !al16(y))
+    return fail(VLA_E_ARG, "bad buffer");
+  if (variant != 0 && variant != 1) return fail(VLA_E_ARG, "variant must be 0 (MFMA) or 1 (dot4)");
+  if (iters < 1 || iters > 10000) return fail(VLA_E_ARG, "iters must be 1..10000");
+  if (M < 1 || N < 1 || K < 64 || K % 64 || K > 16384) return fail(VLA_E_SHAPE, "bad shape");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  const Tiling t = tern_tiling(M, N, K, 1);
+  TernArgs a{};
+  a.M = M; a.N = N; a.K = K; a.x = q; a.w = w_packed; a.rscale = r; a.wscale = wscale;
+  a.ks = t.nc * 256; a.nsplit = 1; a.n_tiles = t.n_tiles;
+  a.e.M = M; a.e.N = N; a.e.K = K; a.e.epi = EPI_STORE; a.e.out = y; a.e.ldo = N; a.e.out_f32 = 1;
+  auto run = [&]() { return variant == 0 ? launch_ternary_gemm(a, t.ms, t.units, s) : launch_ternary_dot4(a, s); };
+  hipEvent_t e0 = nullptr, e1 = nullptr;
+  HIP_TRY(hipEventCreate(&e0));
+  HIP_TRY(hipEventCreate(&e1));
+  hipError_t e = run();
+  if (e == hipSuccess) e = hipEventRecord(e0, s);
+  for (int i = 0; i < iters && e == hipSuccess; ++i) e = run();
+  if (e == hipSuccess) e = hipEventRecord(e1, s);
+  hipError_t e2 = hipStreamSynchronize(s);
+  float ms = 0.0f;
+  if (e == hipSuccess && e2 == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
+  (void)hipEventDestroy(e0);
+  (void)hipEventDestroy(e1);
+  if (e != hipSuccess || e2 != hipSuccess)
+    return fail(VLA_E_DEVICE, "ternary gemm: %s", hipGetErrorString(e != hipSuccess ? e : e2));
+  if (us_per_launch) *us_per_launch = 1000.0f * ms / (float)iters;
+  return VLA_OK;
+}
+
 }  // extern "C"

@@ -231,6 +231,7 @@ hipError_t launch_row_norm(int et, const RowNormArgs& a, hipStream_t s);
 hipError_t launch_time_embed(int et, const CallParams* cp, void* e, int T, int Tpad, int d, hipStream_t s);
 hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
+hipError_t launch_ternary_dot4(const TernArgs& a, hipStream_t s);   // VALU sdot4 variant (EPI_STORE)
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s);
 hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
 hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);

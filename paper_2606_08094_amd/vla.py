@@ -33,6 +33,7 @@ EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_
            "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
+           "vla_test_ternary_gemm",
            "vla_test_adarms", "vla_test_time_cond", "vla_test_persist_trace"]
 
 
@@ -84,6 +85,8 @@ def lib():
         "vla_test_adarms": (i32, [i32, vp, vp, i32, vp, vp, vp, i32, i32, ctypes.c_float, vp, i32, vp]),
         "vla_test_time_cond": (i32, [vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp]),
         "vla_test_ternary_linear": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp]),
+        "vla_test_ternary_gemm": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp,
+                                        ctypes.POINTER(ctypes.c_float), vp]),
         "vla_test_persist_trace": (i32, [vp, ctypes.POINTER(ctypes.c_uint64), i32]),
     }
     for name, (res, args) in sig.items():
@@ -276,3 +279,13 @@ def test_quantize_i8(x, M: int, K: int, q, r, stream=None):
 
 def test_ternary_linear(x, w_packed, M: int, N: int, K: int, scale: float, y, stream=None):
     _check(lib().vla_test_ternary_linear(_ptr(x), _ptr(w_packed), M, N, K, float(scale), _ptr(y), _stream(stream)))
+
+
+def test_ternary_gemm(q, r, w_packed, wscale, M: int, N: int, K: int, variant: int, y, iters: int = 1,
+                      stream=None) -> float:
+    """The W2A8 GEMM alone on int8 codes: variant 0 the int8-MFMA launch, 1 the
+    VALU sdot4 kernel.  Returns the mean microseconds of one of `iters` launches."""
+    us = ctypes.c_float(0.0)
+    _check(lib().vla_test_ternary_gemm(_ptr(q), _ptr(r), _ptr(w_packed), _ptr(wscale), M, N, K, variant, iters,
+                                       _ptr(y), ctypes.byref(us), _stream(stream)))
+    return float(us.value)

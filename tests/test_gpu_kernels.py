@@ -256,6 +256,38 @@ def test_ternary_gemm_empty(torch):
     assert int(out.cpu()[0]) == 0
 
 
+# The ternary model's projections (scope row a11) at M = 8 and the alternative M = 56, plus
+# ragged shapes: more token rows than one pass of the dot4 kernel, N not a multiple of 16, and
+# K over two 4096-wide slices.
+TERN_GEMM_SHAPES = [(8, 3840, 2560), (8, 2560, 2560), (8, 13824, 2560), (8, 2560, 6912),
+                    (56, 2560, 6912), (17, 100, 320), (70, 33, 128), (1, 16, 64), (33, 4100, 8192)]
+
+
+@pytest.mark.parametrize("M,N,K", TERN_GEMM_SHAPES)
+def test_ternary_gemm_dot4_matches_mfma(torch, M, N, K):
+    """The VALU sdot4 kernel and the int8-MFMA launch on the same int8 codes and
+    packed weights: both sums are exact int32, so the dequantised outputs are
+    identical, and they match the oracle's exact sum to fp32 rounding."""
+    x = wl.random_matrix((M, K), 5 + M + K, 1.0)
+    q, r = O.quantize_int8_rows(x)
+    w = wl.random_ternary((N, K), 6 + N)
+    wp = wl.pack_ternary(w)
+    wscale = (0.01 + 0.02 * (np.arange(N) % 7) / 7.0).astype(np.float32)
+    acc = O.ternary_gemm(q, wp, K)
+    ref = acc.astype(np.float64) * (wscale.astype(np.float64)[None, :] * r.astype(np.float64)[:, None] / 127.0)
+    qd = torch.from_numpy(np.ascontiguousarray(q)).cuda()
+    rd = torch.from_numpy(r).cuda()
+    wd = torch.from_numpy(wp).cuda()
+    sd = torch.from_numpy(wscale).cuda()
+    ys = []
+    for variant in (0, 1):
+        y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        _vla().test_ternary_gemm(qd, rd, wd, sd, M, N, K, variant, y)
+        ys.append(y.cpu().numpy())
+    assert np.array_equal(ys[0], ys[1])
+    np.testing.assert_allclose(ys[1], ref, rtol=1e-6, atol=1e-7)
+
+
 @pytest.mark.parametrize("M,N,K", [(8, 3840, 2560), (8, 2560, 6912), (512, 1280, 2560), (13, 70, 128),
                                    (56, 2560, 2560), (20, 512, 6912), (40, 200, 320), (64, 48, 64)])
 def test_ternary_linear(torch, M, N, K):
