@@ -119,20 +119,32 @@ def softmax_rows(s):
     return e / np.sum(e, axis=-1, keepdims=True)
 
 
-def attention(q, k, v, n_heads: int, n_kv_heads: int, head_dim: int):
-    """Unmasked multi-head attention with grouped K/V heads.
+def attention(q, k, v, n_heads: int, n_kv_heads: int, head_dim: int, causal_from=None):
+    """Multi-head attention with grouped K/V heads.
 
     q: [n][H*hd]; k, v: [G][keys][hd].  Head i reads K/V head floor(i*G/H).
     Returns [n][H*hd] with head i in columns i*hd .. i*hd+hd-1.
+    Unmasked by default.  causal_from = c (the causal action-token variant):
+    keys c, c+1, ... are the n action tokens in order, and query i sees every
+    key before c and the action keys c .. c+i; the other scores get weight 0.
     """
     q = np.asarray(q, dtype=F64)
     n = q.shape[0]
     out = np.zeros((n, n_heads * head_dim), dtype=F64)
     scale = 1.0 / np.sqrt(head_dim)
+    mask = None
+    if causal_from is not None:
+        keys = np.asarray(k).shape[1]
+        j = np.arange(keys)[None, :]
+        i = np.arange(n)[:, None]
+        mask = (j >= causal_from) & (j - causal_from > i)
     for i in range(n_heads):
         g = (i * n_kv_heads) // n_heads
         qi = q[:, i * head_dim:(i + 1) * head_dim]
-        p = softmax_rows(qi @ np.asarray(k[g], F64).T * scale)
+        s = qi @ np.asarray(k[g], F64).T * scale
+        if mask is not None:
+            s = np.where(mask, -np.inf, s)
+        p = softmax_rows(s)
         out[:, i * head_dim:(i + 1) * head_dim] = p @ np.asarray(v[g], F64)
     return out
 
@@ -297,14 +309,18 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str 
                 if kind in ("self", "joint"):
                     ks = split_heads(rb(_lin(cfg, W, p + "W_k", u)), G, hd)
                     vs = split_heads(rb(_lin(cfg, W, p + "W_v", u)), G, hd)
+                causal = getattr(cfg, "causal_self", False)
+                cfrom = None
                 if kind == "self":
                     k_all, v_all = ks, vs
+                    cfrom = 0 if causal else None
                 elif kind == "cross":
                     k_all, v_all = kc, vc
                 else:   # joint: one softmax over [prefix rows ; action rows]
                     k_all = np.concatenate([kc, ks], axis=1)
                     v_all = np.concatenate([vc, vs], axis=1)
-                o = rb(attention(q, k_all, v_all, H, G, hd))
+                    cfrom = kc.shape[1] if causal else None
+                o = rb(attention(q, k_all, v_all, H, G, hd, causal_from=cfrom))
                 y = _lin(cfg, W, p + "W_o", o)
             x = x + np.asarray(alpha, F64) * y
     return linear(ada_rms(x, gf, bf, eps), W["W_out"], W["b_out"])

@@ -227,6 +227,57 @@ def test_attention_query_permutation_equivariance():
                                O.attention(q, k, v, 2, 2, 4)[perm], rtol=1e-12)
 
 
+@pytest.mark.parametrize("c", [0, 3])
+def test_attention_causal_rows_equal_truncated_unmasked(c):
+    """Causal action-token variant: query i sees keys 0 .. c+i (c keys before
+    the action tokens), i.e. the unmasked routine (here the brute-force one)
+    over the truncated key set."""
+    H, G, hd, n = 4, 2, 4, 5
+    r = _rng(40 + c)
+    q = r.standard_normal((n, H * hd))
+    k = r.standard_normal((G, c + n, hd))
+    v = r.standard_normal((G, c + n, hd))
+    out = O.attention(q, k, v, H, G, hd, causal_from=c)
+    for i in range(n):
+        ref = bf_attention(q[i:i + 1], k[:, :c + i + 1], v[:, :c + i + 1], H, G, hd)
+        np.testing.assert_allclose(out[i:i + 1], ref, rtol=1e-12, atol=1e-14)
+
+
+def test_attention_causal_first_and_last_query():
+    """Self attention with the causal mask: token 0 sees only key 0 (its value
+    comes back exactly); the last token sees every key (unmasked result)."""
+    r = _rng(42)
+    q = r.standard_normal((6, 2 * 4))
+    k = r.standard_normal((1, 6, 4))
+    v = r.standard_normal((1, 6, 4))
+    out = O.attention(q, k, v, 2, 1, 4, causal_from=0)
+    for h in range(2):
+        np.testing.assert_allclose(out[0, h * 4:(h + 1) * 4], v[0, 0], rtol=1e-15)
+    np.testing.assert_allclose(out[5], O.attention(q, k, v, 2, 1, 4)[5], rtol=1e-12)
+
+
+@pytest.mark.parametrize("pattern", ["self_cross", "joint"])
+def test_causal_expert_earlier_tokens_ignore_later_ones(pattern):
+    """With the causal variant, action token i of the chunk depends only on the
+    prefix and tokens 0 .. i: changing the noise of the last token leaves every
+    other row of the chunk unchanged.  Bidirectional attention (the default)
+    spreads the change to every row."""
+    for causal in (True, False):
+        cfg = TINY.with_(pattern=pattern, causal_self=causal)
+        W, inp, cache = _tiny_setup(cfg)
+        tau = wl.uniform_schedule(cfg.n_steps)
+        a = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+        noise2 = inp["noise"].copy()
+        noise2[:, -1] += 0.5
+        b = O.denoise(cfg, W, cache, noise2, inp["state"], tau)
+        moved = np.abs(a - b).max(axis=-1)[0]   # per action row of request 0
+        assert moved[-1] > 1e-3
+        if causal:
+            assert np.all(moved[:-1] == 0.0)
+        else:
+            assert np.all(moved[:-1] > 1e-9)
+
+
 # --- ternary / quantiser ------------------------------------------------------------
 
 def test_pack_golden_and_unpack_roundtrip():

@@ -42,6 +42,9 @@ class ExpertConfig:
     mlp: str               # "gelu" | "geglu" | "swiglu" | "relu2glu"
     wtype: str             # "f32" | "bf16" | "ternary"
     head_regression: bool = False
+    # variant: action token i attends only to action tokens j <= i in self and
+    # joint attention (every prefix row stays visible); default bidirectional
+    causal_self: bool = False
     rms_eps: float = 1e-6
     # workload
     prefix_len: int = 64
