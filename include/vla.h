@@ -167,8 +167,16 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *  VLA_OPT_ATTN_SPLITS: work split of the attention launches of loop modes
  *    0 and 1: key splits (value % 100, 1..64) and head groups per K/V head
  *    (value / 100, 1..8); 0 in either part = automatic (default 0).
- *    Discards the model's cached plans. */
-enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2, VLA_OPT_ATTN_SPLITS = 3 };
+ *    Discards the model's cached plans.
+ *  VLA_OPT_CAUSAL_SELF: architecture variant of the expert's attention
+ *    (the paper leaves the action-token mask open; SmolVLA-style experts
+ *    use a causal one): 1 = action token i attends only to action tokens
+ *    0 .. i in self and joint attention, every prefix row stays visible;
+ *    0 (default) = bidirectional.  Set it before the first vla_denoise that
+ *    should use it; changing it discards the cached plans.  Causal models
+ *    run on loop modes 0 and 1 (the persistent kernel is unmasked). */
+enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2, VLA_OPT_ATTN_SPLITS = 3,
+       VLA_OPT_CAUSAL_SELF = 4 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
 
 /* One timed launch of a profiled vla_denoise call. */

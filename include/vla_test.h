@@ -29,7 +29,9 @@ vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, 
 
 /* Attention of B requests of n action tokens (paper Sec. 3.1: the action head
  * cross-attends to the cached prefix).  mode 0 self (keys = the n tokens),
- * 1 cross (keys = the P cached rows), 2 joint (one softmax over both).
+ * 1 cross (keys = the P cached rows), 2 joint (one softmax over both);
+ * mode + 4 (self or joint): the causal variant, query t sees the action keys
+ * 0 .. t only (and every prefix row).
  *   q [B*n][H*hd]; k_self, v_self [B*n][G*hd]; k_cache, v_cache [B][G][P][hd];
  *   o [B*n][H*hd]; all in elem.  kv_split: key splits (kv_split % 100) and
  *   query-head groups per K/V head (kv_split / 100); 0 in either part lets

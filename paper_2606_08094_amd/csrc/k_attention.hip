@@ -237,7 +237,9 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int c = 0; c < NQV; ++c) mma16(s[t], *reinterpret_cast<const uint4*>(krow + c * E), qf[c], T());
       }
-      // lane holds keys 8*g4 + 4t + i for query r16
+      // lane holds keys 8*g4 + 4t + i for query r16; causal: action key
+      // (j - nbp) * 32 + kr is visible to query qrow when it is <= qrow
+      const int lim = (a.causal && j >= nbp) ? min(cnt, qrow - (j - nbp) * 32 + 1) : cnt;
       float bmax = -INFINITY;
       float p[8];
 #pragma unroll
@@ -245,18 +247,20 @@ __global__ __launch_bounds__(512) void attn_kernel(AttnArgs a) {
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int kr = 8 * g4 + 4 * t + i;
-          const float v = (kr < cnt) ? s[t][i] * sc : -INFINITY;
+          const float v = (kr < lim) ? s[t][i] * sc : -INFINITY;
           p[4 * t + i] = v;
           bmax = fmaxf(bmax, v);
         }
       bmax = fmaxf(bmax, __shfl_xor(bmax, 16, 64));
       bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
       const float mnew = fmaxf(mrun, bmax);
-      const float corr = exp2f(mrun - mnew);
+      // a query with no visible key so far (causal mask) keeps weight 0
+      const float mref = mnew == -INFINITY ? 0.0f : mnew;
+      const float corr = exp2f(mrun - mref);
       float psum = 0.0f;
 #pragma unroll
       for (int k = 0; k < 8; ++k) {
-        p[k] = exp2f(p[k] - mnew);
+        p[k] = exp2f(p[k] - mref);
         psum += p[k];
       }
       psum += __shfl_xor(psum, 16, 64);
@@ -544,6 +548,7 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
   // Q^T fragments of this wave's 16 rows
   const int R = tile * TQ + wave * 16 + r16;
   const bool rok = R < nrows;
+  const int tq = rok ? R % a.n : 0;   // the row's action token (query index)
   uint4 qf[NQV];
   {
     const int hh = rok ? R / a.n : 0, t = rok ? R - hh * a.n : 0;
@@ -658,7 +663,8 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
     // online softmax; lane keys: 32 kk + 8 g4 + 4 t + i
     float p[2][8];
     float bmax = -INFINITY;
-    if (kvalid == TKB) {  // full block: no key mask
+    const int kx0 = (jb0 + jb) * TKB;
+    if (kvalid == TKB && !(a.causal && kx0 + TKB > npre)) {  // full block, no causal keys: no mask
 #pragma unroll
       for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
@@ -676,7 +682,9 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
 #pragma unroll
           for (int i = 0; i < 4; ++i) {
             const int key = kk * 32 + 8 * g4 + 4 * t + i;
-            const float v = key < kvalid ? s[kk][t][i] * sc : -INFINITY;
+            // causal: action key kx0 + key - npre is visible to query tq when <= tq
+            const bool vis = key < kvalid && (!a.causal || kx0 + key - npre <= tq);
+            const float v = vis ? s[kk][t][i] * sc : -INFINITY;
             p[kk][4 * t + i] = v;
             bmax = fmaxf(bmax, v);
           }
@@ -688,12 +696,13 @@ __global__ __launch_bounds__(64 * TW) void attn_tile(AttnArgs a) {
     const bool move = bmax > mrun + 8.0f;
     const float mnew = move ? bmax : mrun;
     const float corr = move ? exp2f(mrun - mnew) : 1.0f;
+    const float mref = mnew == -INFINITY ? 0.0f : mnew;   // no visible key yet (causal): weight 0
     float psum = 0.f;
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        p[kk][e] = exp2f(p[kk][e] - mnew);
+        p[kk][e] = exp2f(p[kk][e] - mref);
         psum += p[kk][e];
       }
     psum += __shfl_xor(psum, 16, 64);

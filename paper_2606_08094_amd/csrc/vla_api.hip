@@ -138,6 +138,7 @@ struct vla_model {
   int loop_mode = 2;
   int profile = 0;
   int trace = 0;                  // record the persistent kernel's phase timeline
+  int causal = 0;                 // causal action-token attention (VLA_OPT_CAUSAL_SELF)
   int attn_splits = 0;            // key splits of the launch-per-phase attention (0 = automatic)
   void* last_profiled = nullptr;  // Plan* of the last profiled call
   void* last_traced = nullptr;    // Plan* of the last traced call
@@ -401,6 +402,7 @@ int mlp_act(int mlp) {
 // The persistent step kernel covers the batch-1 bf16 dense expert with joint
 // attention whose shape fits its team layout (see persist_supported).
 bool persist_eligible(const vla_model* m, int B, int P, int T) {
+  if (m->causal) return false;   // the persistent kernel's attention is unmasked
   const vla_config& c = m->cfg;
   int kba = 0, nsplit = 0;
   return !m->tern && m->et == ET_BF16 && c.pattern == VLA_PAT_JOINT && !c.head_regression && B == 1 &&
@@ -700,6 +702,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
           }
           AttnArgs at{};
           at.mode = sw.kind == K_SELF ? 0 : (sw.kind == K_CROSS ? 1 : 2);
+          at.causal = (m->causal && sw.kind != K_CROSS) ? 1 : 0;
           at.B = B; at.n = n; at.P = P; at.H = c.n_heads; at.G = c.n_kv_heads; at.hd = hd;
           at.q = p->qkv; at.ldq = ldqkv;
           at.ks = (const char*)p->qkv + (size_t)dq * es;
@@ -847,6 +850,16 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
       m->last_traced = nullptr;
     }
     m->attn_splits = value;
+    return VLA_OK;
+  }
+  if (option == VLA_OPT_CAUSAL_SELF) {
+    if (value < 0 || value > 1) return fail(VLA_E_ARG, "causal flag %d out of range", value);
+    if (value != m->causal) {
+      m->plans.clear();            // plans bake the mask and the loop driver in
+      m->last_profiled = nullptr;
+      m->last_traced = nullptr;
+    }
+    m->causal = value;
     return VLA_OK;
   }
   if (option == VLA_OPT_TRACE) {
@@ -1383,7 +1396,10 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
                               const void* k_cache, const void* v_cache, int32_t B, int32_t n, int32_t P, int32_t H,
                               int32_t G, int32_t hd, int32_t kv_split, void* o, void* stream) {
   if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
-  if (mode < 0 || mode > 2) return fail(VLA_E_ARG, "mode must be 0, 1 or 2");
+  const int causal = (mode & 4) ? 1 : 0;
+  mode &= ~4;
+  if (mode < 0 || mode > 2) return fail(VLA_E_ARG, "mode must be 0, 1 or 2 (+4: causal)");
+  if (causal && mode == 1) return fail(VLA_E_ARG, "cross attention has no causal variant");
   if (!q || !o || (mode != 1 && (!k_self || !v_self)) || (mode != 0 && (!k_cache || !v_cache)))
     return fail(VLA_E_ARG, "NULL buffer");
   if (B < 1 || n < 1 || (mode != 0 && P < 1) || H < 1 || G < 1 || H % G) return fail(VLA_E_SHAPE, "bad shape");
@@ -1393,6 +1409,7 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
   a.mode = mode; a.B = B; a.n = n; a.P = mode == 0 ? 0 : P; a.H = H; a.G = G; a.hd = hd;
   a.q = q; a.ldq = H * hd; a.ks = k_self; a.vs = v_self; a.ldkv = G * hd;
   a.kc = k_cache; a.vc = v_cache; a.o = o; a.ldo = H * hd; a.scale = 1.0f / std::sqrt((float)hd);
+  a.causal = causal;
   if (H / G > 8 || H > 32) return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head");
   if ((a.P + 31) / 32 + (mode == 1 ? 0 : (n + 31) / 32) > attention_max_blocks())
     return fail(VLA_E_UNSUPPORTED, "too many keys");

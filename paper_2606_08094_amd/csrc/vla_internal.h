@@ -86,6 +86,7 @@ struct AttnArgs {
   int hsplit;              // groups of query heads per K/V head (workgroups per group)
   int key_chunk;           // 32-key blocks per split (64-key blocks when tiled)
   int tiled;               // 1: the 128-row tiled kernel (bf16, large query counts)
+  int causal;              // self / joint: query t sees action keys 0 .. t only (prefix rows all)
   void* part;              // [kv_split][B*n][H*hd] per-split output (kv_split > 1)
   float* stats;            // [kv_split][B*n][H][2] per-split (max, sum)
 };

@@ -24,6 +24,7 @@ VLA_OPT_LOOP_MODE = 0
 VLA_OPT_PROFILE = 1
 VLA_OPT_TRACE = 2
 VLA_OPT_ATTN_SPLITS = 3
+VLA_OPT_CAUSAL_SELF = 4
 PERSIST_TRACE_MAX = 8192
 OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
             6: "attn_merge", 7: "persist"}
@@ -202,6 +203,11 @@ class Model:
     def set_attn_splits(self, splits: int):
         """Key splits of the launch-per-phase attention (0 = automatic)."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_ATTN_SPLITS, int(splits)))
+
+    def set_causal_self(self, on: bool):
+        """Causal action-token attention (self and joint sublayers): token i sees
+        action tokens 0 .. i and every prefix row.  Discards cached plans."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_CAUSAL_SELF, int(bool(on))))
 
     def set_trace(self, on: bool):
         """Record the persistent kernel's phase timeline on the next calls."""

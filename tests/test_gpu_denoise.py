@@ -74,6 +74,33 @@ def test_end_to_end(torch, name):
         pipe.close()
 
 
+@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16"])
+def test_end_to_end_causal_variant(torch, name):
+    """The causal action-token variant (VLA_OPT_CAUSAL_SELF) end to end against
+    the oracle with the same mask, under the default loop driver (for pi0 the
+    persistent kernel is unmasked, so the graph driver runs); the mask changes
+    the chunk."""
+    from vla_testlib import workload
+    cfg0, W, inp = workload(name, 1)
+    cfg = cfg0.with_(n_steps=3, causal_self=True)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    _, ref = _oracle(cfg, W, inp, tau)
+    _, ref0 = _oracle(cfg.with_(causal_self=False), W, inp, tau)
+    pipe = _pipe(cfg, W, inp, loop_mode=2)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        err = np.abs(got - ref).max()
+        print(f"{name} causal: max|d| = {err:.3e} (tol {TOL[cfg.wtype]}), mask effect {np.abs(ref - ref0).max():.3e}")
+        assert np.all(np.isfinite(got))
+        assert err <= TOL[cfg.wtype], f"{name}: max|d| {err}"
+        # the mask was applied: the chunk is much closer to the masked oracle than
+        # the unmasked oracle is
+        assert err < 0.5 * np.abs(ref - ref0).max()
+    finally:
+        pipe.close()
+
+
 def test_tiny_nonuniform_schedule_and_batch(torch):
     """fp32 workload, B = 3, a non-uniform schedule, stream and graph drivers."""
     cfg = wl.TINY_F32

@@ -130,6 +130,54 @@ def test_attention_parity(torch, case, kv_split):
         assert err <= tol, f"request {b}: max err {err} > {tol}"
 
 
+CAUSAL_CASES = [
+    # (elem, mode, B, n, P, H, G, hd): self and joint only
+    (1, 2, 1, 50, 816, 8, 1, 256),     # pi0 joint
+    (1, 0, 1, 50, 0, 15, 5, 64),       # SmolVLA self
+    (1, 2, 2, 100, 300, 8, 1, 256),    # batched requests, several action-key blocks
+    (0, 0, 1, 8, 0, 4, 1, 64),         # tiny fp32 self
+    (1, 2, 4, 70, 64, 16, 2, 128),     # tiled-kernel sizes, ragged blocks
+]
+
+
+@pytest.mark.parametrize("case", CAUSAL_CASES, ids=[str(c) for c in CAUSAL_CASES])
+@pytest.mark.parametrize("kv_split", [0, 1, 3, 1000, 1005])
+def test_attention_causal_parity(torch, case, kv_split):
+    """The causal action-token variant (mode + 4): query t sees every prefix
+    row and the action keys 0 .. t; compared with the oracle's masked routine
+    (whole splits can be masked for the first queries)."""
+    elem, mode, B, n, P, H, G, hd = case
+    if kv_split >= 1000 and elem != 1:
+        pytest.skip("the tiled kernel is bf16 only")
+    bf = elem == 1
+    s = 11 * n + P + H + hd + mode
+    q = wl.random_matrix((B * n, H * hd), s, 1.0, bf16=bf)
+    ks = wl.random_matrix((B * n, G * hd), s + 1, 1.0, bf16=bf)
+    vs = wl.random_matrix((B * n, G * hd), s + 2, 1.0, bf16=bf)
+    kc = wl.random_matrix((B, G, max(P, 1), hd), s + 3, 1.0, bf16=bf)
+    vc = wl.random_matrix((B, G, max(P, 1), hd), s + 4, 1.0, bf16=bf)
+    o = torch.full((B * n, H * hd), float("nan"), dtype=torch.bfloat16 if bf else torch.float32, device="cuda")
+    _vla().test_attention(elem, mode + 4, _dev(torch, q, bf), _dev(torch, ks, bf), _dev(torch, vs, bf),
+                          _dev(torch, kc, bf), _dev(torch, vc, bf), B, n, P, H, G, hd, o, kv_split=kv_split)
+    got = o.float().cpu().numpy().astype(np.float64)
+    for b in range(B):
+        rows = slice(b * n, (b + 1) * n)
+        kself = ks[rows].reshape(n, G, hd).transpose(1, 0, 2)
+        vself = vs[rows].reshape(n, G, hd).transpose(1, 0, 2)
+        if mode == 0:
+            kk, vv, c = kself, vself, 0
+        else:
+            kk, vv, c = np.concatenate([kc[b], kself], 1), np.concatenate([vc[b], vself], 1), P
+        ref = O.attention(q[rows], kk, vv, H, G, hd, causal_from=c)
+        tol = 1.2e-2 * np.abs(vv).max() if bf else 2e-5
+        err = np.abs(got[rows] - ref).max()
+        assert np.isfinite(got[rows]).all() and err <= tol, f"request {b}: max err {err} > {tol}"
+        # the kernel applied the mask: it is much closer to the masked result than
+        # the unmasked result is (with a long prefix the mask moves little)
+        eff = np.abs(ref - O.attention(q[rows], kk, vv, H, G, hd)).max()
+        assert err < 0.5 * eff, f"request {b}: err {err} vs mask effect {eff}"
+
+
 @pytest.mark.parametrize("elem,u_f32,M,d,nsplit", [
     (1, 0, 50, 1024, 4),    # pi0 width, bf16 u, four split-K partials
     (1, 0, 50, 720, 0),     # SmolVLA width (d % 1024 != 0), no residual update

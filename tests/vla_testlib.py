@@ -63,6 +63,8 @@ class Pipeline:
         self.dw = device_weights(cfg, W)
         self.model = vla.Model(cfg, self.dw)
         self.model.set_loop_mode(loop_mode)
+        if getattr(cfg, "causal_self", False):
+            self.model.set_causal_self(True)
         B = inputs["noise"].shape[0]
         self.B, self.P = B, cfg.prefix_len
         self.prefix = to_device(inputs["prefix"], bf16=cfg.wtype != "f32")
