@@ -283,7 +283,8 @@ def main():
     from vla_testlib import Pipeline
 
     if args.workloads:
-        todo = (("smolvla_bf16", 1), ("ternary_w2a8", 1), ("stress_pi0", 1), ("stress_pi0", 4), ("stress_pi0", 16))
+        todo = (("smolvla_bf16", 1), ("ternary_w2a8", 1), ("stress_pi0", 1), ("stress_pi0", 4), ("stress_pi0", 16),
+                ("gr00t_alt_bf16", 1), ("evo1_cross_bf16", 1))
         if args.only:
             name, _, batch = args.only.partition(":")
             todo = ((name, int(batch or 1)),)

@@ -45,8 +45,11 @@ typedef enum { VLA_W_F32 = 0, VLA_W_BF16 = 1, VLA_W_TERNARY = 2 } vla_wtype;
 /* Sublayer pattern of each expert layer (execution order):
  *   SELF_CROSS     : self-attention, cross-attention, MLP
  *   JOINT          : joint attention (one softmax over [prefix ; chunk]), MLP
- *   ALT_CROSS_SELF : even layers cross-attention + MLP, odd layers self-attention + MLP */
-typedef enum { VLA_PAT_SELF_CROSS = 0, VLA_PAT_JOINT = 1, VLA_PAT_ALT_CROSS_SELF = 2 } vla_pattern;
+ *   ALT_CROSS_SELF : even layers cross-attention + MLP, odd layers self-attention + MLP
+ *                    (SmolVLA's expert; the alternating DiT head of the GR00T series)
+ *   CROSS          : cross-attention + MLP in every layer (Evo-1's cross-attention DiT
+ *                    head); the action tokens interact only through the prefix */
+typedef enum { VLA_PAT_SELF_CROSS = 0, VLA_PAT_JOINT = 1, VLA_PAT_ALT_CROSS_SELF = 2, VLA_PAT_CROSS = 3 } vla_pattern;
 
 /* MLP form: GELU(u W1^T) W2^T, or act(u Wg^T) * (u Wu^T) then Wd, with act
  * GELU (tanh form) for GEGLU, SiLU for SWIGLU, relu^2 for RELU2GLU. */

@@ -54,6 +54,7 @@ std::vector<int> sublayers(const vla_config& c, int l) {
   switch (c.pattern) {
     case VLA_PAT_SELF_CROSS: return {K_SELF, K_CROSS, K_MLP};
     case VLA_PAT_JOINT: return {K_JOINT, K_MLP};
+    case VLA_PAT_CROSS: return {K_CROSS, K_MLP};
     default: return (l % 2 == 0) ? std::vector<int>{K_CROSS, K_MLP} : std::vector<int>{K_SELF, K_MLP};
   }
 }
@@ -70,7 +71,7 @@ int cache_layers(const vla_config& c) {
 
 vla_status validate_config(const vla_config* c) {
   if (!c) return fail(VLA_E_ARG, "config is NULL");
-  if (c->pattern < 0 || c->pattern > 2) return fail(VLA_E_ARG, "pattern %d out of range", c->pattern);
+  if (c->pattern < 0 || c->pattern > 3) return fail(VLA_E_ARG, "pattern %d out of range", c->pattern);
   if (c->mlp < 0 || c->mlp > 3) return fail(VLA_E_ARG, "mlp %d out of range", c->mlp);
   if (c->wtype < 0 || c->wtype > 2) return fail(VLA_E_ARG, "wtype %d out of range", c->wtype);
   if (c->n_layers < 1 || c->d_model < 2 || c->n_heads < 1 || c->n_kv_heads < 1 || c->d_ff < 16 ||

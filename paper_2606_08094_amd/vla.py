@@ -15,7 +15,7 @@ from typing import Dict, List, Optional, Sequence
 _HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_HERE, "libvla.so")
 
-PATTERNS = {"self_cross": 0, "joint": 1, "alt": 2}
+PATTERNS = {"self_cross": 0, "joint": 1, "alt": 2, "cross": 3}
 MLPS = {"gelu": 0, "geglu": 1, "swiglu": 2, "relu2glu": 3}
 WTYPES = {"f32": 0, "bf16": 1, "ternary": 2}
 STATUS = {0: "VLA_OK", 1: "VLA_E_ARG", 2: "VLA_E_SHAPE", 3: "VLA_E_UNSUPPORTED", 4: "VLA_E_NOMEM",
@@ -147,6 +147,8 @@ def weight_order(cfg) -> List[str]:
             kinds = ["self", "cross", "mlp"]
         elif cfg.pattern == "joint":
             kinds = ["joint", "mlp"]
+        elif cfg.pattern == "cross":
+            kinds = ["cross", "mlp"]
         else:
             kinds = ["cross", "mlp"] if l % 2 == 0 else ["self", "mlp"]
         for k in kinds:

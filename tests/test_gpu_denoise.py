@@ -50,7 +50,7 @@ def _check_cache(pipe, cache_ref, cfg):
     assert err <= tol, f"cache max err {err} > {tol}"
 
 
-@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16"])
+@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16", "gr00t_alt_bf16", "evo1_cross_bf16"])
 def test_end_to_end(torch, name):
     from vla_testlib import workload
     cfg, W, inp = workload(name, 1)

@@ -278,6 +278,25 @@ def test_causal_expert_earlier_tokens_ignore_later_ones(pattern):
             assert np.all(moved[:-1] > 1e-9)
 
 
+def test_cross_only_pattern_tokens_interact_only_through_prefix():
+    """Cross-attention-only layers (Evo-1's DiT head): the action tokens never
+    attend to one another, so changing one token's noise leaves every other
+    row of the chunk unchanged; the prefix still reaches every row."""
+    cfg = TINY.with_(pattern="cross")
+    assert cfg.sublayers(0) == ["cross", "mlp"] and cfg.sublayers(1) == ["cross", "mlp"]
+    W, inp, cache = _tiny_setup(cfg)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    a = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+    noise2 = inp["noise"].copy()
+    noise2[:, 2] += 0.5
+    b = O.denoise(cfg, W, cache, noise2, inp["state"], tau)
+    moved = np.abs(a - b).max(axis=-1)[0]
+    assert moved[2] > 1e-3 and np.all(np.delete(moved, 2) == 0.0)
+    cache2 = O.prefix_kv_build(cfg, W, inp["prefix"] * 1.5)
+    c = O.denoise(cfg, W, cache2, inp["noise"], inp["state"], tau)
+    assert np.all(np.abs(a - c).max(axis=-1)[0] > 1e-6)
+
+
 # --- ternary / quantiser ------------------------------------------------------------
 
 def test_pack_golden_and_unpack_roundtrip():

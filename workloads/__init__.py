@@ -38,7 +38,7 @@ class ExpertConfig:
     n_action: int          # chunk length n (action tokens)
     d_action: int          # action dim A
     d_state: int           # proprio state dim S
-    pattern: str           # "self_cross" | "joint" | "alt"
+    pattern: str           # "self_cross" | "joint" | "alt" | "cross"
     mlp: str               # "gelu" | "geglu" | "swiglu" | "relu2glu"
     wtype: str             # "f32" | "bf16" | "ternary"
     head_regression: bool = False
@@ -68,6 +68,8 @@ class ExpertConfig:
             return ["joint", "mlp"]
         if self.pattern == "alt":
             return ["cross", "mlp"] if layer % 2 == 0 else ["self", "mlp"]
+        if self.pattern == "cross":
+            return ["cross", "mlp"]
         raise ValueError(self.pattern)
 
     @property
@@ -117,8 +119,26 @@ TERNARY_W2A8 = ExpertConfig(
 STRESS_PI0 = PI0_BF16.with_(name="stress_pi0", n_action=100, prefix_len=2048, n_steps=20,
                             seed_base=5000)
 
+# DiT-style heads (the paper's Table of served architectures gives their layer pattern, solver
+# steps and chunk length; widths are not given and are stand-ins of the same order):
+#   GR00T-series alternating DiT: cross-attention to the VL prefix and self-attention in turn,
+#   T = 4, 16 action tokens, multi-head attention, GELU MLP;
+#   Evo-1 cross-attention DiT: cross-attention in every layer, T = 32, 8 action tokens.
+GR00T_ALT_BF16 = ExpertConfig(
+    name="gr00t_alt_bf16", n_layers=32, d_model=1024, n_heads=16, head_dim=64, n_kv_heads=16,
+    d_ff=4096, d_prefix=2048, n_action=16, d_action=32, d_state=32,
+    pattern="alt", mlp="gelu", wtype="bf16",
+    prefix_len=200, n_steps=4, seed_base=6000)
+
+EVO1_CROSS_BF16 = ExpertConfig(
+    name="evo1_cross_bf16", n_layers=8, d_model=896, n_heads=14, head_dim=64, n_kv_heads=2,
+    d_ff=3584, d_prefix=896, n_action=8, d_action=7, d_state=8,
+    pattern="cross", mlp="swiglu", wtype="bf16",
+    prefix_len=256, n_steps=32, seed_base=7000)
+
 CONFIGS: Dict[str, ExpertConfig] = {
-    c.name: c for c in (TINY_F32, PI0_BF16, SMOLVLA_BF16, TERNARY_W2A8, STRESS_PI0)}
+    c.name: c for c in (TINY_F32, PI0_BF16, SMOLVLA_BF16, TERNARY_W2A8, STRESS_PI0, GR00T_ALT_BF16,
+                        EVO1_CROSS_BF16)}
 
 # Prefix segment structure of the pi0-shaped workloads (camera patches + text).
 # The expert attends to every prefix row, so the segments do not change the
