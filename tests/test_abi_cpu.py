@@ -69,6 +69,24 @@ def test_config_validation(bad, status):
     assert vla.lib().vla_weight_count(ctypes.byref(c)) == -1
 
 
+@pytest.mark.parametrize("name", sorted(wl.CONFIGS))
+def test_weight_count_matches_table_order(name):
+    """Every layer pattern (self_cross, joint, alt, cross) and weight type: the
+    library's weight table length equals the binding's name list."""
+    vla = _vla()
+    cfg = wl.CONFIGS[name]
+    c = vla.make_config(cfg)
+    assert vla.lib().vla_weight_count(ctypes.byref(c)) == len(vla.weight_order(cfg))
+
+
+def test_pattern_out_of_range_rejected():
+    vla = _vla()
+    c = vla.make_config(wl.TINY_F32.with_(pattern="cross"))
+    assert vla.lib().vla_weight_count(ctypes.byref(c)) > 0
+    c.pattern = 4
+    assert vla.lib().vla_weight_count(ctypes.byref(c)) == -1
+
+
 def test_null_table_entries_rejected_before_device_use():
     vla = _vla()
     cfg = wl.TINY_F32
