@@ -1555,17 +1555,17 @@ vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t*
   a.e.M = M; a.e.N = N; a.e.K = K; a.e.epi = EPI_STORE; a.e.out = y; a.e.ldo = N; a.e.out_f32 = 1;
   auto run = [&]() { return variant == 0 ? launch_ternary_gemm(a, t.ms, t.units, s) : launch_ternary_dot4(a, s); };
   hipEvent_t e0 = nullptr, e1 = nullptr;
-  HIP_TRY(hipEventCreate(&e0));
-  HIP_TRY(hipEventCreate(&e1));
-  hipError_t e = run();
+  hipError_t e = hipEventCreate(&e0);
+  if (e == hipSuccess) e = hipEventCreate(&e1);
+  if (e == hipSuccess) e = run();
   if (e == hipSuccess) e = hipEventRecord(e0, s);
   for (int i = 0; i < iters && e == hipSuccess; ++i) e = run();
   if (e == hipSuccess) e = hipEventRecord(e1, s);
   hipError_t e2 = hipStreamSynchronize(s);
   float ms = 0.0f;
   if (e == hipSuccess && e2 == hipSuccess) e = hipEventElapsedTime(&ms, e0, e1);
-  (void)hipEventDestroy(e0);
-  (void)hipEventDestroy(e1);
+  if (e0) (void)hipEventDestroy(e0);
+  if (e1) (void)hipEventDestroy(e1);
   if (e != hipSuccess || e2 != hipSuccess)
     return fail(VLA_E_DEVICE, "ternary gemm: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   if (us_per_launch) *us_per_launch = 1000.0f * ms / (float)iters;
