@@ -149,6 +149,24 @@ def attention(q, k, v, n_heads: int, n_kv_heads: int, head_dim: int, causal_from
     return out
 
 
+def rope(x, positions, n_heads: int, head_dim: int, base: float):
+    """Rotary position embedding, rotate-half form, of every head of x
+    [rows][n_heads*hd]: with h = hd/2 and w_i = base^(-2i/hd), the pair
+    (x_i, x_{i+h}) of a row at position p turns by the angle p*w_i:
+    x_i' = x_i cos - x_{i+h} sin, x_{i+h}' = x_{i+h} cos + x_i sin."""
+    x = np.array(x, dtype=F64)
+    half = head_dim // 2
+    w = float(base) ** (-2.0 * np.arange(half, dtype=F64) / head_dim)
+    ang = np.asarray(positions, dtype=F64)[:, None] * w[None, :]
+    c, s = np.cos(ang), np.sin(ang)
+    for h in range(n_heads):
+        lo = x[:, h * head_dim:h * head_dim + half].copy()
+        hi = x[:, h * head_dim + half:(h + 1) * head_dim].copy()
+        x[:, h * head_dim:h * head_dim + half] = lo * c - hi * s
+        x[:, h * head_dim + half:(h + 1) * head_dim] = hi * c + lo * s
+    return x
+
+
 def split_heads(x, n_kv_heads: int, head_dim: int):
     """[rows][G*hd] -> [G][rows][hd]."""
     x = np.asarray(x, dtype=F64)
@@ -219,17 +237,22 @@ def prefix_kv_build(cfg, W: Dict[str, np.ndarray], prefix_hidden) -> np.ndarray:
     """Cross-attention K/V cache from the final-layer prefix hidden states.
 
     For every layer with a cross or joint sublayer (in layer order):
-    Kc = X_p W_kc^T, Vc = X_p W_vc^T, no norm, bias or position encoding.
+    Kc = X_p W_kc^T, Vc = X_p W_vc^T, no norm, bias or position encoding (in the
+    RoPE variant the joint layers' Kc rows are rotated to positions 0 .. P-1).
     prefix_hidden: [B][P][d_p].  Returns [Lc][2][B][G][P][hd] float64.
     """
     xp = np.asarray(prefix_hidden, dtype=F64)
     B, P = xp.shape[0], xp.shape[1]
     layers = [l for l in range(cfg.n_layers) if cfg.has_prefix(l)]
     cache = np.zeros((len(layers), 2, B, cfg.n_kv_heads, P, cfg.head_dim), dtype=F64)
+    base = getattr(cfg, "rope_base", 0.0)
     for c, l in enumerate(layers):
         for b in range(B):
             kc = _lin(cfg, W, f"L{l}.W_kc", xp[b])
             vc = _lin(cfg, W, f"L{l}.W_vc", xp[b])
+            if base > 0 and "joint" in cfg.sublayers(l):
+                # RoPE variant: prefix rows hold positions 0 .. P-1 of the joint sequence
+                kc = rope(kc, np.arange(P), cfg.n_kv_heads, cfg.head_dim, base)
             cache[c, 0, b] = split_heads(kc, cfg.n_kv_heads, cfg.head_dim)
             cache[c, 1, b] = split_heads(vc, cfg.n_kv_heads, cfg.head_dim)
     return cache
@@ -307,7 +330,15 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str 
             else:
                 q = rb(_lin(cfg, W, p + "W_q", u))
                 if kind in ("self", "joint"):
-                    ks = split_heads(rb(_lin(cfg, W, p + "W_k", u)), G, hd)
+                    k2 = rb(_lin(cfg, W, p + "W_k", u))
+                    base = getattr(cfg, "rope_base", 0.0)
+                    if base > 0:
+                        # RoPE variant: action token i at position i (self) or P + i
+                        # (joint, after the prefix rows)
+                        pos = np.arange(q.shape[0]) + (kc.shape[1] if kind == "joint" else 0)
+                        q = rb(rope(q, pos, H, hd, base))
+                        k2 = rb(rope(k2, pos, G, hd, base))
+                    ks = split_heads(k2, G, hd)
                     vs = split_heads(rb(_lin(cfg, W, p + "W_v", u)), G, hd)
                 causal = getattr(cfg, "causal_self", False)
                 cfrom = None

@@ -297,6 +297,58 @@ def test_cross_only_pattern_tokens_interact_only_through_prefix():
     assert np.all(np.abs(a - c).max(axis=-1)[0] > 1e-6)
 
 
+def test_rope_two_dims_is_plane_rotation():
+    """head_dim 2: w_0 = 1, so position p turns (x0, x1) by p radians."""
+    r = _rng(50)
+    x = r.standard_normal((5, 2 * 3))   # 3 heads of 2 dims
+    pos = np.array([0.0, 1.0, 2.5, -3.0, 7.0])
+    y = O.rope(x, pos, 3, 2, 10000.0)
+    for i, p in enumerate(pos):
+        rot = np.array([[np.cos(p), -np.sin(p)], [np.sin(p), np.cos(p)]])
+        for h in range(3):
+            np.testing.assert_allclose(y[i, 2 * h:2 * h + 2], rot @ x[i, 2 * h:2 * h + 2], rtol=1e-13, atol=1e-15)
+
+
+def test_rope_identity_norms_and_relative_positions():
+    """Position 0 is the identity; every rotated pair keeps its norm; scores of
+    rotated queries and keys depend only on the position difference."""
+    r = _rng(51)
+    hd, base = 8, 10000.0
+    q = r.standard_normal((4, hd))
+    k = r.standard_normal((4, hd))
+    np.testing.assert_array_equal(O.rope(q, np.zeros(4), 1, hd, base), q)
+    y = O.rope(q, np.arange(4) * 3.0, 1, hd, base)
+    h = hd // 2
+    np.testing.assert_allclose(y[:, :h] ** 2 + y[:, h:] ** 2, q[:, :h] ** 2 + q[:, h:] ** 2, rtol=1e-12)
+    pm, pn = np.array([5.0, 9.0, 2.0, 0.0]), np.array([1.0, 4.0, 8.0, 3.0])
+    s1 = np.sum(O.rope(q, pm, 1, hd, base) * O.rope(k, pn, 1, hd, base), axis=1)
+    s2 = np.sum(O.rope(q, pm + 11, 1, hd, base) * O.rope(k, pn + 11, 1, hd, base), axis=1)
+    np.testing.assert_allclose(s1, s2, rtol=1e-10, atol=1e-12)
+
+
+def test_rope_variant_joint_positions_follow_the_prefix():
+    """RoPE on the joint sequence: rotating every key and query by one extra
+    position (prefix and action rows alike) leaves the chunk unchanged, since
+    only position differences enter the scores."""
+    cfg = TINY.with_(pattern="joint", rope_base=10000.0)
+    W, inp, cache = _tiny_setup(cfg)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    a = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
+    b0 = O.denoise(cfg.with_(rope_base=0.0), W, O.prefix_kv_build(cfg.with_(rope_base=0.0), W, inp["prefix"]),
+                   inp["noise"], inp["state"], tau)
+    # the positions matter (small weights keep the effect small, 5e-8 here); the
+    # shift check below resolves far less than that
+    assert np.abs(a - b0).max() > 1e-8
+    real_rope = O.rope
+    try:
+        O.rope = lambda x, pos, nh, hd, base: real_rope(x, np.asarray(pos) + 1.0, nh, hd, base)
+        cache1 = O.prefix_kv_build(cfg, W, inp["prefix"])
+        c = O.denoise(cfg, W, cache1, inp["noise"], inp["state"], tau)
+    finally:
+        O.rope = real_rope
+    np.testing.assert_allclose(c, a, rtol=1e-11, atol=1e-13)
+
+
 # --- ternary / quantiser ------------------------------------------------------------
 
 def test_pack_golden_and_unpack_roundtrip():

@@ -45,6 +45,9 @@ class ExpertConfig:
     # variant: action token i attends only to action tokens j <= i in self and
     # joint attention (every prefix row stays visible); default bidirectional
     causal_self: bool = False
+    # variant: rotary position embedding (rotate-half form, this base; 0 = none)
+    # on the queries and keys of self and joint attention
+    rope_base: float = 0.0
     rms_eps: float = 1e-6
     # workload
     prefix_len: int = 64
