@@ -177,9 +177,17 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *    0 .. i in self and joint attention, every prefix row stays visible;
  *    0 (default) = bidirectional.  Set it before the first vla_denoise that
  *    should use it; changing it discards the cached plans.  Causal models
- *    run on loop modes 0 and 1 (the persistent kernel is unmasked). */
+ *    run on loop modes 0 and 1 (the persistent kernel is unmasked).
+ *  VLA_OPT_ROPE_BASE: architecture variant (the paper's expert has no
+ *    positions beyond the learned E_pos): value = base > 1 of a rotary
+ *    position embedding (rotate-half form) on the queries and keys of self
+ *    and joint attention; 0 (default) = none.  Action token i sits at
+ *    position i in self attention and P + i in joint attention, whose cached
+ *    prefix keys vla_prefix_kv_build rotates to positions 0 .. P-1 (build
+ *    the cache after setting it).  Discards the cached plans; such models run
+ *    on loop modes 0 and 1. */
 enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2, VLA_OPT_ATTN_SPLITS = 3,
-       VLA_OPT_CAUSAL_SELF = 4 };
+       VLA_OPT_CAUSAL_SELF = 4, VLA_OPT_ROPE_BASE = 5 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
 
 /* One timed launch of a profiled vla_denoise call. */

@@ -53,6 +53,14 @@ vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q,
 vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
                                    float scale, float* y, void* stream);
 
+/* Rotary position embedding in place (the VLA_OPT_ROPE_BASE variant's
+ * kernel): x [rows][ld] in elem (0 fp32, 1 bf16), heads h < nheads of hd
+ * values from column col0; row r is at position pos0 + r % rows_per_request.
+ * With h2 = hd/2 and w_i = base^(-2i/hd), the pair (i, i+h2) of a head turns
+ * by pos * w_i (rotate-half form).  hd even, base > 1.  Synchronises. */
+vla_status vla_test_rope(int32_t elem, void* x, int32_t rows, int32_t rows_per_request, int32_t ld, int32_t col0,
+                         int32_t nheads, int32_t hd, int32_t pos0, float base, void* stream);
+
 /* The W2A8 GEMM alone, on int8 activation codes already quantised, for the
  * comparison of the paper's dot4 instruction path with its matrix-unit path
  * (Sec. 4.5, the utilisation lever: the same ternary weights on dp4a versus the tensor cores; here

@@ -1,6 +1,7 @@
 // Small per-chunk and per-step kernels of the denoise loop: per-call
 // parameters, chunk start, input embedding, solver-time embedding, the int8
 // activation quantiser of the W2A8 path, and finite checks.
+#include <cmath>
 #include "device_common.h"
 
 namespace {
@@ -193,6 +194,31 @@ __global__ void copy_f32_kernel(float* dst, const float* src, size_t n) {
     dst[i] = src[i];
 }
 
+// Rotary position embedding in place (rotate-half form): row r of x holds
+// nheads heads of hd values from column col0 (row pitch ld); its position is
+// pos0 + r % rpr.  With h = hd / 2 and w_i = base^(-2i/hd) the pair (i, i+h)
+// turns by the angle pos * w_i (lbase = log2(base)).  One thread per pair.
+template <typename T>
+__global__ __launch_bounds__(256) void rope_kernel(T* x, int rows, int rpr, int ld, int col0, int nheads, int hd,
+                                                   int pos0, float lbase) {
+  const int half = hd / 2;
+  const long long total = (long long)rows * nheads * half;
+  for (long long idx = blockIdx.x * 256LL + threadIdx.x; idx < total; idx += (long long)gridDim.x * 256LL) {
+    const int i = (int)(idx % half);
+    const long long rh = idx / half;
+    const int h = (int)(rh % nheads);
+    const int r = (int)(rh / nheads);
+    const float pos = (float)(pos0 + r % rpr);
+    const float w = exp2f(-2.0f * (float)i / (float)hd * lbase);
+    float sn, cs;
+    sincosf(pos * w, &sn, &cs);
+    T* row = x + (size_t)r * ld + col0 + (size_t)h * hd;
+    const float lo = ElemTraits<T>::to_f(row[i]), hi = ElemTraits<T>::to_f(row[i + half]);
+    row[i] = ElemTraits<T>::from_f(lo * cs - hi * sn);
+    row[i + half] = ElemTraits<T>::from_f(hi * cs + lo * sn);
+  }
+}
+
 // y[i] = sum over the nsplit partial arrays part[s][i], in split order.
 __global__ void sum_partials_kernel(float* y, const float* part, int nsplit, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x) {
@@ -284,6 +310,22 @@ hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s
   if (n == 0) return hipSuccess;
   const int blocks = (int)((n + 255) / 256 > 1024 ? 1024 : (n + 255) / 256);
   hipLaunchKernelGGL(copy_f32_kernel, dim3(blocks), dim3(256), 0, s, dst, src, n);
+  return hipGetLastError();
+}
+
+hipError_t launch_rope(int et, void* x, int rows, int rpr, int ld, int col0, int nheads, int hd, int pos0, float base,
+                       hipStream_t s) {
+  if (rows <= 0 || nheads <= 0) return hipSuccess;
+  if (hd % 2 || base <= 1.0f || rpr < 1) return hipErrorInvalidValue;
+  const long long total = (long long)rows * nheads * (hd / 2);
+  const int blocks = (int)((total + 255) / 256 > 2048 ? 2048 : (total + 255) / 256);
+  const float lbase = std::log2(base);
+  if (et == ET_BF16)
+    hipLaunchKernelGGL(rope_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, reinterpret_cast<bf16_t*>(x), rows, rpr,
+                       ld, col0, nheads, hd, pos0, lbase);
+  else
+    hipLaunchKernelGGL(rope_kernel<float>, dim3(blocks), dim3(256), 0, s, reinterpret_cast<float*>(x), rows, rpr, ld,
+                       col0, nheads, hd, pos0, lbase);
   return hipGetLastError();
 }
 

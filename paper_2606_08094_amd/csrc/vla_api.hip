@@ -140,6 +140,7 @@ struct vla_model {
   int profile = 0;
   int trace = 0;                  // record the persistent kernel's phase timeline
   int causal = 0;                 // causal action-token attention (VLA_OPT_CAUSAL_SELF)
+  float rope_base = 0.0f;         // rotary position embedding base, 0 = none (VLA_OPT_ROPE_BASE)
   int attn_splits = 0;            // key splits of the launch-per-phase attention (0 = automatic)
   void* last_profiled = nullptr;  // Plan* of the last profiled call
   void* last_traced = nullptr;    // Plan* of the last traced call
@@ -403,7 +404,7 @@ int mlp_act(int mlp) {
 // The persistent step kernel covers the batch-1 bf16 dense expert with joint
 // attention whose shape fits its team layout (see persist_supported).
 bool persist_eligible(const vla_model* m, int B, int P, int T) {
-  if (m->causal) return false;   // the persistent kernel's attention is unmasked
+  if (m->causal || m->rope_base > 0.0f) return false;   // its attention is unmasked and unrotated
   const vla_config& c = m->cfg;
   int kba = 0, nsplit = 0;
   return !m->tern && m->et == ET_BF16 && c.pattern == VLA_PAT_JOINT && !c.head_regression && B == 1 &&
@@ -701,6 +702,17 @@ vla_status build_plan(vla_model* m, Plan* p) {
             t.e.ldo = ldqkv;
             bld.tern(t, 1);
           }
+          if (m->rope_base > 0.0f && sw.kind != K_CROSS) {
+            // RoPE variant: action token i at position i (self) or P + i (joint)
+            void* qkvp = p->qkv;
+            const int et = m->et, H = c.n_heads, G = c.n_kv_heads, pos0 = sw.kind == K_JOINT ? P : 0;
+            const float base = m->rope_base;
+            const double rb = 2.0 * M * (dq + dkv) * esize(et);
+            bld.small([=](hipStream_t st) {
+              hipError_t e = launch_rope(et, qkvp, M, n, ldqkv, 0, H, hd, pos0, base, st);
+              return e != hipSuccess ? e : launch_rope(et, qkvp, M, n, ldqkv, dq, G, hd, pos0, base, st);
+            }, M, dq + dkv, 0, rb);
+          }
           AttnArgs at{};
           at.mode = sw.kind == K_SELF ? 0 : (sw.kind == K_CROSS ? 1 : 2);
           at.causal = (m->causal && sw.kind != K_CROSS) ? 1 : 0;
@@ -851,6 +863,16 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
       m->last_traced = nullptr;
     }
     m->attn_splits = value;
+    return VLA_OK;
+  }
+  if (option == VLA_OPT_ROPE_BASE) {
+    if (value < 0 || value == 1 || value > 10000000) return fail(VLA_E_ARG, "RoPE base %d out of range", value);
+    if ((float)value != m->rope_base) {
+      m->plans.clear();            // plans bake the rotation in
+      m->last_profiled = nullptr;
+      m->last_traced = nullptr;
+    }
+    m->rope_base = (float)value;
     return VLA_OK;
   }
   if (option == VLA_OPT_CAUSAL_SELF) {
@@ -1135,6 +1157,26 @@ vla_status vla_model_create(const vla_config* cfg, const void* const* weights, i
   return create_impl(cfg, weights, n_weights, out);
 }
 
+}  // extern "C"
+
+// RoPE variant: the cached K of every joint layer holds prefix row p at
+// position p (cache block [2][B][G][P][hd], K first).
+static vla_status rope_prefix(vla_model* m, void* kv_cache, int batch, int prefix_len, size_t layer_block,
+                              hipStream_t s) {
+  if (m->rope_base <= 0.0f) return VLA_OK;
+  const size_t es = m->et == ET_BF16 ? 2 : 4;
+  for (auto& lay : m->layers)
+    for (auto& sw : lay) {
+      if (sw.cache_idx < 0 || sw.kind != K_JOINT) continue;
+      void* kb = (char*)kv_cache + (size_t)sw.cache_idx * layer_block * es;
+      const int rows = batch * m->cfg.n_kv_heads * prefix_len;
+      HIP_TRY(launch_rope(m->et, kb, rows, prefix_len, m->cfg.head_dim, 0, 1, m->cfg.head_dim, 0, m->rope_base, s));
+    }
+  return VLA_OK;
+}
+
+extern "C" {
+
 vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t batch, int32_t prefix_len,
                                void* kv_cache, size_t kv_cache_bytes, void* stream) {
   if (!m) return fail(VLA_E_ARG, "model is NULL");
@@ -1166,7 +1208,7 @@ vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t 
     g.lay_cols = N;
     g.lay_stride = layer_block;
     HIP_TRY(launch_dense(m->et, dense_launch(m->et, g, 1), g, s));
-    return VLA_OK;
+    return rope_prefix(m, kv_cache, batch, prefix_len, layer_block, s);
   }
   for (auto& lay : m->layers)
     for (auto& sw : lay) {
@@ -1186,7 +1228,7 @@ vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t 
         HIP_TRY(launch_ternary_gemm(ta, t.ms, t.units, s));
       }
     }
-  return VLA_OK;
+  return rope_prefix(m, kv_cache, batch, prefix_len, layer_block, s);
 }
 
 vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes, int32_t batch, int32_t prefix_len,
@@ -1569,6 +1611,21 @@ vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t*
   if (e != hipSuccess || e2 != hipSuccess)
     return fail(VLA_E_DEVICE, "ternary gemm: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   if (us_per_launch) *us_per_launch = 1000.0f * ms / (float)iters;
+  return VLA_OK;
+}
+
+vla_status vla_test_rope(int32_t elem, void* x, int32_t rows, int32_t rows_per_request, int32_t ld, int32_t col0,
+                         int32_t nheads, int32_t hd, int32_t pos0, float base, void* stream) {
+  if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
+  if (!x) return fail(VLA_E_ARG, "NULL buffer");
+  if (rows < 1 || rows_per_request < 1 || nheads < 1 || hd < 2 || hd % 2 || col0 < 0 || pos0 < 0 ||
+      col0 + nheads * hd > ld || !(base > 1.0f))
+    return fail(VLA_E_SHAPE, "bad RoPE shape");
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = launch_rope(elem ? ET_BF16 : ET_F32, x, rows, rows_per_request, ld, col0, nheads, hd, pos0, base, s);
+  hipError_t e2 = hipStreamSynchronize(s);
+  if (e != hipSuccess || e2 != hipSuccess)
+    return fail(VLA_E_DEVICE, "rope: %s", hipGetErrorString(e != hipSuccess ? e : e2));
   return VLA_OK;
 }
 

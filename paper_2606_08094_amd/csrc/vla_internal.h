@@ -237,6 +237,9 @@ hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t
 hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
 hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);
 hipError_t launch_sum_partials(float* y, const float* part, int nsplit, size_t n, hipStream_t s);
+// rotary position embedding in place (rotate-half); positions pos0 + row % rpr
+hipError_t launch_rope(int et, void* x, int rows, int rpr, int ld, int col0, int nheads, int hd, int pos0, float base,
+                       hipStream_t s);
 // Persistent kernel: whether a shape is supported, the dynamic LDS it needs,
 // and the cooperative launch (256 workgroups of 512 threads).
 bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, int glu, int* kba, int* nsplit);

@@ -25,6 +25,7 @@ VLA_OPT_PROFILE = 1
 VLA_OPT_TRACE = 2
 VLA_OPT_ATTN_SPLITS = 3
 VLA_OPT_CAUSAL_SELF = 4
+VLA_OPT_ROPE_BASE = 5
 PERSIST_TRACE_MAX = 8192
 OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
             6: "attn_merge", 7: "persist"}
@@ -34,7 +35,7 @@ EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_
            "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
-           "vla_test_ternary_gemm",
+           "vla_test_ternary_gemm", "vla_test_rope",
            "vla_test_adarms", "vla_test_time_cond", "vla_test_persist_trace"]
 
 
@@ -86,6 +87,7 @@ def lib():
         "vla_test_adarms": (i32, [i32, vp, vp, i32, vp, vp, vp, i32, i32, ctypes.c_float, vp, i32, vp]),
         "vla_test_time_cond": (i32, [vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp]),
         "vla_test_ternary_linear": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp]),
+        "vla_test_rope": (i32, [i32, vp, i32, i32, i32, i32, i32, i32, i32, ctypes.c_float, vp]),
         "vla_test_ternary_gemm": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp,
                                         ctypes.POINTER(ctypes.c_float), vp]),
         "vla_test_persist_trace": (i32, [vp, ctypes.POINTER(ctypes.c_uint64), i32]),
@@ -211,6 +213,11 @@ class Model:
         action tokens 0 .. i and every prefix row.  Discards cached plans."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_CAUSAL_SELF, int(bool(on))))
 
+    def set_rope_base(self, base: float):
+        """Rotary position embedding of self / joint queries and keys (0 = none).
+        Discards cached plans; build the prefix cache after setting it."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_ROPE_BASE, int(base)))
+
     def set_trace(self, on: bool):
         """Record the persistent kernel's phase timeline on the next calls."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_TRACE, int(bool(on))))
@@ -297,3 +304,10 @@ def test_ternary_gemm(q, r, w_packed, wscale, M: int, N: int, K: int, variant: i
     _check(lib().vla_test_ternary_gemm(_ptr(q), _ptr(r), _ptr(w_packed), _ptr(wscale), M, N, K, variant, iters,
                                        _ptr(y), ctypes.byref(us), _stream(stream)))
     return float(us.value)
+
+
+def test_rope(elem: int, x, rows: int, rows_per_request: int, ld: int, col0: int, nheads: int, hd: int, pos0: int,
+              base: float, stream=None):
+    """Rotary position embedding in place on x (the RoPE variant's kernel)."""
+    _check(lib().vla_test_rope(elem, _ptr(x), rows, rows_per_request, ld, col0, nheads, hd, pos0, float(base),
+                               _stream(stream)))

@@ -101,6 +101,32 @@ def test_end_to_end_causal_variant(torch, name):
         pipe.close()
 
 
+@pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16"])
+def test_end_to_end_rope_variant(torch, name):
+    """The rotary position embedding variant (VLA_OPT_ROPE_BASE) end to end
+    against the oracle with the same rotation: the cached prefix keys of joint
+    layers (rotated to positions 0 .. P-1) and the chunk, under the default
+    loop driver (the graph driver runs it)."""
+    from vla_testlib import workload
+    cfg0, W, inp = workload(name, 1)
+    cfg = cfg0.with_(n_steps=3, rope_base=10000.0)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    cache_ref, ref = _oracle(cfg, W, inp, tau)
+    _, ref0 = _oracle(cfg.with_(rope_base=0.0), W, inp, tau)
+    pipe = _pipe(cfg, W, inp, loop_mode=2)
+    try:
+        pipe.build_cache()
+        _check_cache(pipe, cache_ref, cfg)
+        got = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        err = np.abs(got - ref).max()
+        print(f"{name} rope: max|d| = {err:.3e} (tol {TOL[cfg.wtype]}), rotation effect {np.abs(ref - ref0).max():.3e}")
+        assert np.all(np.isfinite(got))
+        assert err <= TOL[cfg.wtype], f"{name}: max|d| {err}"
+        assert err < 0.5 * np.abs(ref - ref0).max()   # the rotation was applied
+    finally:
+        pipe.close()
+
+
 def test_tiny_nonuniform_schedule_and_batch(torch):
     """fp32 workload, B = 3, a non-uniform schedule, stream and graph drivers."""
     cfg = wl.TINY_F32

@@ -304,6 +304,34 @@ def test_ternary_gemm_empty(torch):
     assert int(out.cpu()[0]) == 0
 
 
+@pytest.mark.parametrize("elem,rows,rpr,nheads,hd,col0,ld,pos0", [
+    (1, 100, 50, 8, 256, 0, 2560, 816),     # pi0 queries of 2 requests after an 816-row prefix
+    (1, 100, 50, 1, 256, 2048, 2560, 816),  # their keys (columns after the 2048 query columns)
+    (1, 3 * 241, 241, 1, 64, 0, 64, 0),     # cached prefix keys, positions 0 .. P-1
+    (0, 16, 8, 4, 64, 0, 256, 0),           # fp32 self attention
+])
+def test_rope_kernel(torch, elem, rows, rpr, nheads, hd, col0, ld, pos0):
+    """The RoPE kernel against the oracle's rotation on the same (bf16 or
+    fp32) inputs: columns outside the heads stay untouched."""
+    bf = elem == 1
+    x = wl.random_matrix((rows, ld), 60 + rows + hd, 1.0, bf16=bf)
+    base = 10000.0
+    pos = pos0 + np.arange(rows) % rpr
+    ref = x.astype(np.float64).copy()
+    ref[:, col0:col0 + nheads * hd] = O.rope(x[:, col0:col0 + nheads * hd], pos, nheads, hd, base)
+    xd = _dev(torch, x, bf)
+    _vla().test_rope(elem, xd, rows, rpr, ld, col0, nheads, hd, pos0, base)
+    got = xd.float().cpu().numpy().astype(np.float64)
+    # bf16: one rounding of the stored result (2^-9 relative) on values of norm <= |x|;
+    # fp32 angles lose about 1e-7 relative at positions up to ~1000
+    tol = 8e-3 * np.abs(x).max() if bf else 2e-4 * np.abs(x).max()
+    err = np.abs(got - ref).max()
+    assert err <= tol, f"max err {err} > {tol}"
+    outside = np.ones(ld, bool)
+    outside[col0:col0 + nheads * hd] = False
+    assert np.array_equal(got[:, outside], x[:, outside].astype(np.float64))
+
+
 # The ternary model's projections (scope row a11) at M = 8 and the alternative M = 56, plus
 # ragged shapes: more token rows than one pass of the dot4 kernel, N not a multiple of 16, and
 # K over two 4096-wide slices.
