@@ -286,9 +286,15 @@ def modulation(cfg, W: Dict[str, np.ndarray], t: float):
 
 
 def input_embedding(cfg, W, a, s):
-    """x = a W_in^T + b_in + (s W_s^T + b_s) on every token + E_pos."""
+    """x = a W_in^T + b_in + (s W_s^T + b_s) on every token + E_pos.
+
+    State-token variant: row 0 is s W_s^T + b_s alone and rows 1 .. n are
+    a W_in^T + b_in + E_pos (n + 1 rows)."""
     xs = linear(np.asarray(s, F64)[None, :], W["W_s"], W["b_s"])
-    return linear(a, W["W_in"], W["b_in"]) + xs + np.asarray(W["E_pos"], F64)
+    xa = linear(a, W["W_in"], W["b_in"]) + np.asarray(W["E_pos"], F64)
+    if getattr(cfg, "state_token", False):
+        return np.concatenate([xs, xa], axis=0)
+    return xa + xs
 
 
 def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str = "fp64") -> np.ndarray:
@@ -354,6 +360,8 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str 
                 o = rb(attention(q, k_all, v_all, H, G, hd, causal_from=cfrom))
                 y = _lin(cfg, W, p + "W_o", o)
             x = x + np.asarray(alpha, F64) * y
+    if getattr(cfg, "state_token", False):
+        x = x[1:]           # the state token has no action output
     return linear(ada_rms(x, gf, bf, eps), W["W_out"], W["b_out"])
 
 

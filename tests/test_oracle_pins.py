@@ -349,6 +349,32 @@ def test_rope_variant_joint_positions_follow_the_prefix():
     np.testing.assert_allclose(c, a, rtol=1e-11, atol=1e-13)
 
 
+@pytest.mark.parametrize("pattern", ["self_cross", "joint"])
+def test_state_token_variant(pattern):
+    """State as its own token: with zero state weights and bias, the state
+    token is a zero row that still takes part in attention (so the chunk
+    differs from the added-state model); in a cross-only expert the action
+    rows never see it, and the chunk equals the added-state model with a zero
+    state contribution."""
+    cfg = TINY.with_(pattern=pattern, state_token=True)
+    W, inp, cache = _tiny_setup(cfg)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    W0 = dict(W)
+    W0["W_s"] = np.zeros_like(W["W_s"])
+    W0["b_s"] = np.zeros_like(W["b_s"])
+    a = O.denoise(cfg, W0, cache, inp["noise"], inp["state"], tau)
+    b = O.denoise(cfg.with_(state_token=False), W0, cache, inp["noise"], inp["state"], tau)
+    assert a.shape == b.shape and np.abs(a - b).max() > 1e-9
+    cfgc = TINY.with_(pattern="cross", state_token=True)
+    Wc, inpc, cachec = _tiny_setup(cfgc)
+    Wc0 = dict(Wc)
+    Wc0["W_s"] = np.zeros_like(Wc["W_s"])
+    Wc0["b_s"] = np.zeros_like(Wc["b_s"])
+    c = O.denoise(cfgc, Wc0, cachec, inpc["noise"], inpc["state"], tau)
+    d = O.denoise(cfgc.with_(state_token=False), Wc0, cachec, inpc["noise"], inpc["state"], tau)
+    np.testing.assert_allclose(c, d, rtol=1e-13, atol=1e-15)
+
+
 # --- ternary / quantiser ------------------------------------------------------------
 
 def test_pack_golden_and_unpack_roundtrip():

@@ -48,6 +48,9 @@ class ExpertConfig:
     # variant: rotary position embedding (rotate-half form, this base; 0 = none)
     # on the queries and keys of self and joint attention
     rope_base: float = 0.0
+    # variant: the state enters as its own token ahead of the n action tokens
+    # (pi0-style) instead of being added to every action token
+    state_token: bool = False
     rms_eps: float = 1e-6
     # workload
     prefix_len: int = 64
