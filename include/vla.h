@@ -185,9 +185,17 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *    position i in self attention and P + i in joint attention, whose cached
  *    prefix keys vla_prefix_kv_build rotates to positions 0 .. P-1 (build
  *    the cache after setting it).  Discards the cached plans; such models run
- *    on loop modes 0 and 1. */
+ *    on loop modes 0 and 1.
+ *  VLA_OPT_STATE_TOKEN: architecture variant of the input embedding (the
+ *    paper adds the projected state to every action token; pi0-style experts
+ *    give it a token of its own): 1 = each request runs n + 1 token rows, row
+ *    0 = s W_s^T + b_s and row 1 + i = a_i W_in^T + b_in + E_pos[i]; the
+ *    state row takes part in attention (and is token 0 for the causal mask and
+ *    RoPE) but yields no action, so actions_out keeps its [B, n, d_action]
+ *    layout.  0 (default) = the paper's embedding.  Discards the cached plans;
+ *    such models run on loop modes 0 and 1. */
 enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2, VLA_OPT_ATTN_SPLITS = 3,
-       VLA_OPT_CAUSAL_SELF = 4, VLA_OPT_ROPE_BASE = 5 };
+       VLA_OPT_CAUSAL_SELF = 4, VLA_OPT_ROPE_BASE = 5, VLA_OPT_STATE_TOKEN = 6 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
 
 /* One timed launch of a profiled vla_denoise call. */

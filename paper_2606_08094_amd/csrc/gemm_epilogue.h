@@ -120,16 +120,19 @@ __device__ __forceinline__ void wave_epilogue(const GemmArgs& a, const f32x4 (&a
 #pragma unroll
         for (int i = 0; i < 4; ++i) {
           const int m = m0 + ms * 16 + g4 * 4 + i;
-          if (m < M && n < N) {
+          // state-token rows carry no action: skipped, the rest map to action rows
+          const int t = a.stok ? m % a.stok : 1;
+          const int am = a.stok ? (m / a.stok) * (a.stok - 1) + t - 1 : m;
+          if (m < M && n < N && t != 0) {
             const float v = acc[ms][0][i] + a.bias[n];
-            float* ap = a.a + (size_t)m * N + n;
+            float* ap = a.a + (size_t)am * N + n;
             const float an = a.regression ? v : (*ap + dt * v);
             *ap = an;
             if (a.last) {
               float o = an;
               if (cp->act_std) o *= cp->act_std[n];
               if (cp->act_mean) o += cp->act_mean[n];
-              cp->actions_out[(size_t)m * N + n] = o;
+              cp->actions_out[(size_t)am * N + n] = o;
             }
           }
         }

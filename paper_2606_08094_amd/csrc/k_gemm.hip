@@ -380,18 +380,21 @@ VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, i
       const float dt = cp->tau[a.step + 1] - cp->tau[a.step];
       auto f = [&](int r, int n, int nv, float4 v) {
         const int m = m0 + r;
+        const int t = a.stok ? m % a.stok : 1;   // state-token rows: no action
+        const int am = a.stok ? (m / a.stok) * (a.stok - 1) + t - 1 : m;
+        if (t == 0) return;
         const float e[4] = {v.x, v.y, v.z, v.w};
         for (int j = 0; j < 4 && j < nv; ++j) {
           const int nn = n + j;
           const float vv = e[j] + a.bias[nn];
-          float* ap = a.a + (size_t)m * N + nn;
+          float* ap = a.a + (size_t)am * N + nn;
           const float an = a.regression ? vv : (*ap + dt * vv);
           *ap = an;
           if (a.last) {
             float o = an;
             if (cp->act_std) o *= cp->act_std[nn];
             if (cp->act_mean) o += cp->act_mean[nn];
-            cp->actions_out[(size_t)m * N + nn] = o;
+            cp->actions_out[(size_t)am * N + nn] = o;
           }
         }
       };

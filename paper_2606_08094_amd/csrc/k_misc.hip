@@ -19,7 +19,7 @@ __global__ __launch_bounds__(256) void init_chunk_kernel(const CallParams* cp, f
   const int b = blockIdx.x;
   const float* st = cp->state + (size_t)b * S;
   for (int j = threadIdx.x; j < d; j += 256) {
-    float acc = b_in[j] + b_s[j];
+    float acc = (b_in ? b_in[j] : 0.0f) + b_s[j];   // b_in NULL: the state token's own row
     for (int s = 0; s < S; ++s) acc += st[s] * ElemTraits<T>::to_f(W_s[(size_t)j * S + s]);
     xs[(size_t)b * d + j] = acc;
   }
@@ -81,17 +81,28 @@ __global__ __launch_bounds__(256) void row_norm_kernel(RowNormArgs a) {
     }
   } else {
     const int b = m / a.n, tok = m - b * a.n;
+    // state-token variant: row 0 of a request is the projected state alone
+    const bool srow = a.stok && tok == 0;
+    const int ai = a.stok ? b * (a.n - 1) + tok - 1 : m;   // action row
+    const int et = a.stok ? tok - 1 : tok;                  // its E_pos row
     __shared__ float arow[64];
-    if (t < a.A) arow[t] = a.a[(size_t)m * a.A + t];
+    if (t < a.A) arow[t] = srow ? 0.0f : a.a[(size_t)ai * a.A + t];
     __syncthreads();
     const T* W = reinterpret_cast<const T*>(a.W_in);
-    const T* ep = reinterpret_cast<const T*>(a.E_pos) + (size_t)tok * d;
+    const T* ep = reinterpret_cast<const T*>(a.E_pos) + (size_t)(srow ? 0 : et) * d;
+    const float* base = a.stok && !srow ? a.b_in : a.xs + (size_t)b * d;
 #pragma unroll
     for (int i = 0; i < CPT; ++i) {
       const int c = 4 * (t + 256 * i);
       float v[4] = {0.f, 0.f, 0.f, 0.f};
-      if (c < d) {
-        const float4 x4 = *reinterpret_cast<const float4*>(a.xs + (size_t)b * d + c);
+      if (c < d && srow) {
+        const float4 x4 = *reinterpret_cast<const float4*>(base + c);
+        v[0] = x4.x;
+        v[1] = x4.y;
+        v[2] = x4.z;
+        v[3] = x4.w;
+      } else if (c < d) {
+        const float4 x4 = *reinterpret_cast<const float4*>(base + c);
         v[0] = x4.x + ElemTraits<T>::to_f(ep[c]);
         v[1] = x4.y + ElemTraits<T>::to_f(ep[c + 1]);
         v[2] = x4.z + ElemTraits<T>::to_f(ep[c + 2]);

@@ -140,6 +140,7 @@ struct vla_model {
   int profile = 0;
   int trace = 0;                  // record the persistent kernel's phase timeline
   int causal = 0;                 // causal action-token attention (VLA_OPT_CAUSAL_SELF)
+  int state_token = 0;            // state as its own leading token (VLA_OPT_STATE_TOKEN)
   float rope_base = 0.0f;         // rotary position embedding base, 0 = none (VLA_OPT_ROPE_BASE)
   int attn_splits = 0;            // key splits of the launch-per-phase attention (0 = automatic)
   void* last_profiled = nullptr;  // Plan* of the last profiled call
@@ -404,7 +405,8 @@ int mlp_act(int mlp) {
 // The persistent step kernel covers the batch-1 bf16 dense expert with joint
 // attention whose shape fits its team layout (see persist_supported).
 bool persist_eligible(const vla_model* m, int B, int P, int T) {
-  if (m->causal || m->rope_base > 0.0f) return false;   // its attention is unmasked and unrotated
+  // its attention is unmasked and unrotated, its rows are the action tokens alone
+  if (m->causal || m->rope_base > 0.0f || m->state_token) return false;
   const vla_config& c = m->cfg;
   int kba = 0, nsplit = 0;
   return !m->tern && m->et == ET_BF16 && c.pattern == VLA_PAT_JOINT && !c.head_regression && B == 1 &&
@@ -417,14 +419,16 @@ vla_status build_plan(vla_model* m, Plan* p) {
   const vla_config& c = m->cfg;
   const int B = p->B, P = p->P, T = p->T;
   const int n = c.n_action, A = c.d_action, S = c.d_state, d = m->d, F = c.d_ff;
-  const int M = B * n, L = c.n_layers, ns = m->ns, dq = m->dq, dkv = m->dkv, hd = c.head_dim;
+  // token rows per request: the n action tokens, after the state token when it is on
+  const int nt = n + (m->state_token ? 1 : 0), stok = m->state_token ? nt : 0;
+  const int M = B * nt, L = c.n_layers, ns = m->ns, dq = m->dq, dkv = m->dkv, hd = c.head_dim;
   const int et = m->et;
   const size_t es = esize(et);
   const bool u32 = m->tern || et == ET_F32;   // W2A8 quantiser input and fp32 models keep u in fp32
   const size_t modrow = (size_t)L * 3 * ns * d;
   Alloc al{p->allocs};
   VLA_TRY(al((void**)&p->cp, sizeof(CallParams)));
-  VLA_TRY(al((void**)&p->a, (size_t)M * A * 4));
+  VLA_TRY(al((void**)&p->a, (size_t)B * n * A * 4));
   VLA_TRY(al((void**)&p->xs, (size_t)B * d * 4));
   VLA_TRY(al((void**)&p->x, (size_t)M * d * 4));
   VLA_TRY(al(&p->u, (size_t)M * d * (u32 ? 4 : es)));
@@ -451,8 +455,10 @@ vla_status build_plan(vla_model* m, Plan* p) {
   size_t part_need = 0;
 
   bld.small([=](hipStream_t s) {
-    return launch_init_chunk(et, cp, p->a, p->xs, m->W_s, m->b_s, m->b_in, B, n, A, S, d, s);
-  }, B, d, S, (double)d * S * es + (double)B * (S + d) * 4 + (double)M * A * 8);
+    // with the state token b_in belongs to the action rows only, added by the embedding
+    return launch_init_chunk(et, cp, p->a, p->xs, m->W_s, m->b_s, stok ? nullptr : m->b_in, B, n, A,
+                             S, d, s);
+  }, B, d, S, (double)d * S * es + (double)B * (S + d) * 4 + (double)B * n * A * 8);
   if (!c.head_regression) {
     bld.small([=](hipStream_t s) { return launch_time_embed(et, cp, p->e, T, T, d, s); }, T, d, 0,
               (double)T * d * es);
@@ -620,7 +626,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
     };
     RowNormArgs rn{};
     rn.mode = 1; rn.M = M; rn.d = d; rn.x = p->x; rn.a = p->a; rn.W_in = m->W_in; rn.xs = p->xs;
-    rn.E_pos = m->E_pos; rn.n = n; rn.A = A; rn.eps = c.rms_eps; rn.u = p->u; rn.u_f32 = u32;
+    rn.E_pos = m->E_pos; rn.n = nt; rn.stok = stok; rn.b_in = m->b_in; rn.A = A; rn.eps = c.rms_eps; rn.u = p->u; rn.u_f32 = u32;
     if (L > 0) {
       rn.gamma = modk;
       rn.beta = modk + d;
@@ -709,14 +715,14 @@ vla_status build_plan(vla_model* m, Plan* p) {
             const float base = m->rope_base;
             const double rb = 2.0 * M * (dq + dkv) * esize(et);
             bld.small([=](hipStream_t st) {
-              hipError_t e = launch_rope(et, qkvp, M, n, ldqkv, 0, H, hd, pos0, base, st);
-              return e != hipSuccess ? e : launch_rope(et, qkvp, M, n, ldqkv, dq, G, hd, pos0, base, st);
+              hipError_t e = launch_rope(et, qkvp, M, nt, ldqkv, 0, H, hd, pos0, base, st);
+              return e != hipSuccess ? e : launch_rope(et, qkvp, M, nt, ldqkv, dq, G, hd, pos0, base, st);
             }, M, dq + dkv, 0, rb);
           }
           AttnArgs at{};
           at.mode = sw.kind == K_SELF ? 0 : (sw.kind == K_CROSS ? 1 : 2);
           at.causal = (m->causal && sw.kind != K_CROSS) ? 1 : 0;
-          at.B = B; at.n = n; at.P = P; at.H = c.n_heads; at.G = c.n_kv_heads; at.hd = hd;
+          at.B = B; at.n = nt; at.P = P; at.H = c.n_heads; at.G = c.n_kv_heads; at.hd = hd;
           at.q = p->qkv; at.ldq = ldqkv;
           at.ks = (const char*)p->qkv + (size_t)dq * es;
           at.vs = (const char*)p->qkv + (size_t)(dq + dkv) * es;
@@ -765,6 +771,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
     g.step = k;
     g.regression = c.head_regression;
     g.last = (k == T - 1);
+    g.stok = stok;
     bld.gemm(g, 1);
   }
 
@@ -873,6 +880,16 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
       m->last_traced = nullptr;
     }
     m->rope_base = (float)value;
+    return VLA_OK;
+  }
+  if (option == VLA_OPT_STATE_TOKEN) {
+    if (value < 0 || value > 1) return fail(VLA_E_ARG, "state-token flag %d out of range", value);
+    if (value != m->state_token) {
+      m->plans.clear();            // plans bake the row count and the loop driver in
+      m->last_profiled = nullptr;
+      m->last_traced = nullptr;
+    }
+    m->state_token = value;
     return VLA_OK;
   }
   if (option == VLA_OPT_CAUSAL_SELF) {
@@ -1242,9 +1259,10 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
                         (const void*)actions_out})
     if (q && !al16(q)) return fail(VLA_E_ARG, "device buffers must be 16-byte aligned");
   if (batch < 1 || prefix_len < 1) return fail(VLA_E_SHAPE, "batch and prefix_len must be >= 1");
-  if ((long long)batch * c.n_action > 65536) return fail(VLA_E_UNSUPPORTED, "batch * n_action too large");
-  if ((prefix_len + 31) / 32 + (c.n_action + 31) / 32 > attention_max_blocks())
-    return fail(VLA_E_UNSUPPORTED, "prefix_len + n_action beyond %d keys", 32 * attention_max_blocks() - 32);
+  const int ntok = c.n_action + (m->state_token ? 1 : 0);   // token rows per request
+  if ((long long)batch * ntok > 65536) return fail(VLA_E_UNSUPPORTED, "batch * tokens too large");
+  if ((prefix_len + 31) / 32 + (ntok + 31) / 32 > attention_max_blocks())
+    return fail(VLA_E_UNSUPPORTED, "prefix_len + tokens beyond %d keys", 32 * attention_max_blocks() - 32);
   if (n_steps < 1 || n_steps > VLA_MAX_STEPS) return fail(VLA_E_SHAPE, "n_steps %d not in 1..%d", n_steps, VLA_MAX_STEPS);
   if (c.head_regression && n_steps != 1) return fail(VLA_E_SHAPE, "the regression head takes n_steps == 1");
   if (kv_cache_bytes != vla_kv_cache_bytes(m, batch, prefix_len))

@@ -59,6 +59,8 @@ struct GemmArgs {
   int step;
   int regression;
   int last;
+  int stok;                // tokens per request when row 0 of each request is a state token (no
+                           // action output: skipped; action row = b (stok-1) + t-1), else 0
   // EPI_KVCACHE: row m = b*P + p, column n = slot*lay_cols + kv*d_kv + g*hd + c
   void* cache;             // base of cache slot 0: [slots][2][B][G][P][hd]
   int P, hd, d_kv, B;
@@ -115,7 +117,10 @@ struct RowNormArgs {
   const void* W_in;        // [d][A]
   const float* xs;         // [B][d]
   const void* E_pos;       // [n][d]
-  int n, A;
+  int n, A;                // n: token rows per request
+  int stok;                // mode 1, state-token variant: row 0 of a request = xs, action row t
+                           // (t >= 1) = b_in + E_pos[t-1] + a W_in; 0 = xs + E_pos + a W_in
+  const float* b_in;
   const float* gamma;
   const float* beta;
   float eps;

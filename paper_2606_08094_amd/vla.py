@@ -26,6 +26,7 @@ VLA_OPT_TRACE = 2
 VLA_OPT_ATTN_SPLITS = 3
 VLA_OPT_CAUSAL_SELF = 4
 VLA_OPT_ROPE_BASE = 5
+VLA_OPT_STATE_TOKEN = 6
 PERSIST_TRACE_MAX = 8192
 OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
             6: "attn_merge", 7: "persist"}
@@ -212,6 +213,10 @@ class Model:
         """Causal action-token attention (self and joint sublayers): token i sees
         action tokens 0 .. i and every prefix row.  Discards cached plans."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_CAUSAL_SELF, int(bool(on))))
+
+    def set_state_token(self, on: bool):
+        """The pi0-style embedding: the state as its own leading token."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_STATE_TOKEN, 1 if on else 0))
 
     def set_rope_base(self, base: float):
         """Rotary position embedding of self / joint queries and keys (0 = none).

@@ -101,6 +101,37 @@ def test_end_to_end_causal_variant(torch, name):
         pipe.close()
 
 
+@pytest.mark.parametrize("name,extra", [
+    ("tiny_f32", {}), ("smolvla_bf16", {}), ("pi0_bf16", {}),
+    ("tiny_f32", dict(causal_self=True, rope_base=10000.0)),
+    ("smolvla_bf16", dict(causal_self=True)),
+])
+def test_end_to_end_state_token_variant(torch, name, extra):
+    """The prepended state-token variant (VLA_OPT_STATE_TOKEN) end to end
+    against the oracle: n + 1 token rows per request, the state row feeding
+    attention only, actions_out in the [B, n, d_action] layout; also combined
+    with the causal mask and RoPE, where the state row is token 0."""
+    from vla_testlib import workload
+    cfg0, W, inp = workload(name, 1)
+    cfg = cfg0.with_(n_steps=3, state_token=True, **extra)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    _, ref = _oracle(cfg, W, inp, tau)
+    _, ref0 = _oracle(cfg.with_(state_token=False), W, inp, tau)
+    pipe = _pipe(cfg, W, inp, loop_mode=2)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        err = np.abs(got - ref).max()
+        print(f"{name} {extra} state token: max|d| = {err:.3e} (tol {TOL[cfg.wtype]}), "
+              f"variant effect {np.abs(ref - ref0).max():.3e}")
+        assert got.shape == ref.shape == ref0.shape
+        assert np.all(np.isfinite(got))
+        assert err <= TOL[cfg.wtype], f"{name}: max|d| {err}"
+        assert err < 0.5 * np.abs(ref - ref0).max()   # the state token was used
+    finally:
+        pipe.close()
+
+
 @pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16"])
 def test_end_to_end_rope_variant(torch, name):
     """The rotary position embedding variant (VLA_OPT_ROPE_BASE) end to end

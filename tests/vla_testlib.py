@@ -67,6 +67,8 @@ class Pipeline:
             self.model.set_causal_self(True)
         if getattr(cfg, "rope_base", 0.0) > 0:
             self.model.set_rope_base(cfg.rope_base)
+        if getattr(cfg, "state_token", False):
+            self.model.set_state_token(True)
         B = inputs["noise"].shape[0]
         self.B, self.P = B, cfg.prefix_len
         self.prefix = to_device(inputs["prefix"], bf16=cfg.wtype != "f32")
