@@ -156,11 +156,12 @@ def cpu_baseline(cfg, W, inp, tau):
                       f"{dt:.1f} s, numpy fp64"}
 
 
-def measure_workload(torch, wl, Pipeline, name, batch, reps):
+def measure_workload(torch, wl, Pipeline, name, batch, reps, variant=None):
     """Chunk time, per-step latency and per-step roofline fractions of one
-    workload (default loop driver)."""
+    workload (default loop driver), optionally with architecture-variant
+    overrides (state_token, causal_self, rope_base)."""
     import numpy as np
-    cfg = wl.CONFIGS[name].with_(batch=batch)
+    cfg = wl.CONFIGS[name].with_(batch=batch, **(variant or {}))
     W = wl.make_weights(cfg)
     inp = wl.make_batch(cfg, batch)
     T = cfg.n_steps
@@ -252,6 +253,9 @@ def main():
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="only run 5 plain device-to-device copies of this many MiB (calibrates the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
+    ap.add_argument("--variant", default="",
+                    help="with --workloads: comma list of architecture variants applied to every "
+                         "workload: state_token, causal_self, rope (base 10000)")
     ap.add_argument("--ternary-ablation", action="store_true",
                     help="instead of the headline line, time the W2A8 GEMM of the ternary model's projections "
                          "(M = 8 and 56) on the int8 MFMA kernel and on the VALU sdot4 kernel, one JSON line "
@@ -300,9 +304,17 @@ def main():
             pipe.close()
             print(json.dumps({"workload": name, "batch": batch, "chunks": args.chunks}))
             return
+        variant = {}
+        for v in filter(None, args.variant.split(",")):
+            if v not in ("state_token", "causal_self", "rope"):
+                sys.exit(f"unknown variant {v!r}")
+            variant["rope_base" if v == "rope" else v] = 10000.0 if v == "rope" else True
         for name, batch in todo:
-            log(f"workload {name} batch {batch} ...")
-            print(json.dumps(measure_workload(torch, wl, Pipeline, name, batch, 5)), flush=True)
+            log(f"workload {name} batch {batch} {args.variant} ...")
+            r = measure_workload(torch, wl, Pipeline, name, batch, 5, variant)
+            if variant:
+                r["variant"] = args.variant
+            print(json.dumps(r), flush=True)
         return
 
     cfg = wl.CONFIGS[WORKLOAD]
