@@ -157,7 +157,8 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *    the stream, 1 = the same launches captured once in a HIP graph and
  *    replayed, 2 (default) = one persistent cooperative kernel for the whole
  *    step loop where the model supports it (batch 1, bf16, joint attention,
- *    H % 8 == 0 and the shape limits of the team layout), else as 1.
+ *    H % 8 == 0, the shape limits of the team layout, none of the causal,
+ *    RoPE or state-token variants), else as 1.
  *  VLA_OPT_PROFILE: R in 1..1000 = time every launch of the following
  *    vla_denoise calls with HIP events (launch-per-phase driver; read with
  *    vla_profile_read).  Each launch runs R times back to back between its
