@@ -132,6 +132,29 @@ def test_end_to_end_state_token_variant(torch, name, extra):
         pipe.close()
 
 
+@pytest.mark.parametrize("name,batch", [("tiny_f32", 3), ("smolvla_bf16", 2)])
+def test_state_token_batched_requests(torch, name, batch):
+    """State token with several requests: request b's token rows sit at
+    b (n + 1) .. b (n + 1) + n on the device and its actions at b n .. b n + n - 1
+    in actions_out. Stream and graph drivers, a non-uniform schedule."""
+    cfg = wl.CONFIGS[name].with_(state_token=True, batch=batch)
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, batch)
+    tau = np.array([1.0, 0.7, 0.35, 0.0], np.float32)
+    _, ref = _oracle(cfg, W, inp, tau)
+    for mode in (0, 1):
+        pipe = _pipe(cfg, W, inp, loop_mode=mode)
+        try:
+            pipe.build_cache()
+            got = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+            err = np.abs(got - ref).max()
+            print(f"{name} B={batch} mode {mode} state token: max|d| = {err:.3e}")
+            assert got.shape == ref.shape
+            assert err <= TOL[cfg.wtype], f"{name} mode {mode}: max|d| {err}"
+        finally:
+            pipe.close()
+
+
 @pytest.mark.parametrize("name", ["tiny_f32", "smolvla_bf16", "pi0_bf16"])
 def test_end_to_end_rope_variant(torch, name):
     """The rotary position embedding variant (VLA_OPT_ROPE_BASE) end to end
