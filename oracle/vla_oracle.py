@@ -22,8 +22,10 @@ library primitive; nothing is blocked, fused or reordered beyond the
 definitions below.
 
 Parity status: every function here is pinned by tests/test_oracle_pins.py
-except the full expert forward on random weights, which is pinned only
-through its components and the closed-form end-to-end special cases
+(closed forms, invariants, hand-derived fixtures in tests/golden/, brute
+force on tiny inputs).  The full expert forward on random weights has no
+closed form: it is pinned through its components, the one-sublayer
+brute-force evaluations and the closed-form end-to-end special cases
 (zero / constant velocity field, zero residual gates).
 """
 from __future__ import annotations
@@ -44,8 +46,10 @@ ABSMAX_FLOOR = np.float32(1e-5)
 # --- storage precision ------------------------------------------------------
 
 def round_to_bf16(x):
-    """Nearest-even bf16 value of float32(x), as float64 (fp32 first, as a
-    kernel that accumulates in fp32 and stores bf16 would)."""
+    """Nearest-even bf16 value of float32(x), as float64 (float32 first, then
+    bf16: the value a bf16 store of a float32 result holds).  The expert below
+    never calls it; kernel-level tests use it to state what a bf16 store may
+    change."""
     f = np.ascontiguousarray(np.asarray(x, dtype=F64).astype(np.float32))
     u = f.view(np.uint32).astype(np.uint64)
     u = (u + 0x7FFF + ((u >> 16) & 1)) & 0xFFFF0000
@@ -297,20 +301,15 @@ def input_embedding(cfg, W, a, s):
     return xa + xs
 
 
-def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str = "fp64") -> np.ndarray:
+def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None) -> np.ndarray:
     """One pass of the action head over the chunk a [n][A]: returns the velocity
     (or, for the regression head, the action chunk) v [n][A].
 
     cache_b: [Lc][2][G][P][hd] for this request.  If prefix_b is given the
     cross K/V are recomputed from it here instead of being read from cache_b
     (used to check that caching changes nothing).
-
-    storage="kernel" rounds to bf16 the values a bf16 kernel stores between
-    steps of the W2A8 path (the projected Q, K, V and the attention output that
-    the O-projection quantiser reads), so that every int8 quantisation decision
-    is taken on inputs of the kernel's precision; "fp64" keeps them exact.
+    Every value between the operations is kept in float64.
     """
-    rb = round_to_bf16 if storage == "kernel" else (lambda v: v)
     mods, (gf, bf) = modulation(cfg, W, t)
     x = input_embedding(cfg, W, a, s)
     H, G, hd, eps = cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.rms_eps
@@ -334,18 +333,18 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str 
                     h = mlp_activation(cfg.mlp, _lin(cfg, W, p + "W_g", u), _lin(cfg, W, p + "W_u", u))
                     y = _lin(cfg, W, p + "W_d", h)
             else:
-                q = rb(_lin(cfg, W, p + "W_q", u))
+                q = _lin(cfg, W, p + "W_q", u)
                 if kind in ("self", "joint"):
-                    k2 = rb(_lin(cfg, W, p + "W_k", u))
+                    k2 = _lin(cfg, W, p + "W_k", u)
                     base = getattr(cfg, "rope_base", 0.0)
                     if base > 0:
                         # RoPE variant: action token i at position i (self) or P + i
                         # (joint, after the prefix rows)
                         pos = np.arange(q.shape[0]) + (kc.shape[1] if kind == "joint" else 0)
-                        q = rb(rope(q, pos, H, hd, base))
-                        k2 = rb(rope(k2, pos, G, hd, base))
+                        q = rope(q, pos, H, hd, base)
+                        k2 = rope(k2, pos, G, hd, base)
                     ks = split_heads(k2, G, hd)
-                    vs = split_heads(rb(_lin(cfg, W, p + "W_v", u)), G, hd)
+                    vs = split_heads(_lin(cfg, W, p + "W_v", u), G, hd)
                 causal = getattr(cfg, "causal_self", False)
                 cfrom = None
                 if kind == "self":
@@ -357,7 +356,7 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None, storage: str 
                     k_all = np.concatenate([kc, ks], axis=1)
                     v_all = np.concatenate([vc, vs], axis=1)
                     cfrom = kc.shape[1] if causal else None
-                o = rb(attention(q, k_all, v_all, H, G, hd, causal_from=cfrom))
+                o = attention(q, k_all, v_all, H, G, hd, causal_from=cfrom)
                 y = _lin(cfg, W, p + "W_o", o)
             x = x + np.asarray(alpha, F64) * y
     if getattr(cfg, "state_token", False):
@@ -385,19 +384,15 @@ def denormalize(a, mean=None, std=None):
 
 
 def denoise(cfg, W, cache, noise, state, tau, act_mean=None, act_std=None,
-            prefix_hidden=None, requests: Optional[List[int]] = None, storage: str = "fp64") -> np.ndarray:
+            prefix_hidden=None, requests: Optional[List[int]] = None) -> np.ndarray:
     """The whole chunk for every request: Euler over T solver steps (the
     regression head takes one pass and returns its output), then denormalise.
 
     cache [Lc][2][B][G][P][hd]; noise [B][n][A]; state [B][S]; tau [T+1].
     With prefix_hidden given, cross K/V are recomputed at every step instead of
     read from the cache.  requests restricts the evaluation to some of the B.
-    storage="kernel" (see expert_forward) also reads the cache as bf16, its
-    element type in a bf16 kernel.
     """
     noise = np.asarray(noise, F64)
-    if storage == "kernel" and cache is not None:
-        cache = round_to_bf16(cache)
     B = noise.shape[0]
     reqs = range(B) if requests is None else requests
     out = np.zeros((len(reqs),) + noise.shape[1:], dtype=F64)
@@ -406,7 +401,7 @@ def denoise(cfg, W, cache, noise, state, tau, act_mean=None, act_std=None,
         pb = None if prefix_hidden is None else np.asarray(prefix_hidden, F64)[b]
 
         def vel(a, k, t, cb=cb, pb=pb, b=b):
-            return expert_forward(cfg, W, cb, a, state[b], t, prefix_b=pb, storage=storage)
+            return expert_forward(cfg, W, cb, a, state[b], t, prefix_b=pb)
 
         if cfg.head_regression:
             a = vel(noise[b], 0, float(tau[0]))

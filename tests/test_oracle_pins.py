@@ -601,3 +601,153 @@ def test_final_modulation_slot_order():
     expect = (2 * x0 / rms + 0.5) @ W["W_out"].T.astype(np.float64) + W["b_out"]
     v = O.expert_forward(cfg, W, cache[:, :, 0], inp["noise"][0], inp["state"][0], 0.7)
     np.testing.assert_allclose(v, expect, rtol=1e-13)
+
+
+# --- storage rounding ---------------------------------------------------------------
+
+def test_round_to_bf16_golden():
+    """Hand-derived cases (tests/golden/bf16_rounding.txt): float32 first, then
+    nearest-even bf16 (catches truncation, ties away from zero, rounding the
+    float64 value directly, a lost carry into the exponent, a lost sign)."""
+    n = 0
+    with open(os.path.join(GOLDEN, "bf16_rounding.txt")) as f:
+        for line in f:
+            if line.startswith("#") or not line.strip():
+                continue
+            a, b = line.split()[:2]
+            x = float.fromhex(a)
+            want = math.inf if b == "inf" else float.fromhex(b)
+            got = float(O.round_to_bf16(np.array([x]))[0])
+            assert got == want and math.copysign(1.0, got) == math.copysign(1.0, want), (a, got, b)
+            n += 1
+    assert n >= 15
+
+
+# --- time-conditioning chain and modulation slots ------------------------------------
+
+def _silu_s(v):
+    return v / (1.0 + math.exp(-v))
+
+
+def _gelu_s(v):
+    return 0.5 * v * (1.0 + math.tanh(math.sqrt(2.0 / math.pi) * (v + 0.044715 * v ** 3)))
+
+
+@pytest.mark.parametrize("case", ["t1_zero", "t1_t2_zero", "identity"])
+def test_time_mlp_chain_closed_forms(case):
+    """The time MLP c = W_t2 SiLU(W_t1 e + b_t1) + b_t2 and the modulation
+    m^l = W_mod^l SiLU(c) + b_mod^l, (gamma_f, beta_f) = W_fm SiLU(c) + b_fm,
+    evaluated by scalar loops in three closed forms:
+      W_t1 = 0            -> c = W_t2 SiLU(b_t1) + b_t2;
+      W_t1 = W_t2 = 0     -> c = b_t2;
+      W_t1 = W_t2 = I, b_t1 = b_t2 = 0 -> c = SiLU(e(t)).
+    Catches a dropped SiLU (before W_t2 or before W_mod / W_fm), W_t1 and W_t2
+    applied in the wrong order, a missing bias, and a time embedding that
+    never reaches the chain."""
+    cfg = TINY
+    W = wl.make_weights(cfg)
+    d, t = cfg.d_model, 0.37
+    if case in ("t1_zero", "t1_t2_zero"):
+        W["W_t1"] = np.zeros_like(W["W_t1"])
+    if case == "t1_t2_zero":
+        W["W_t2"] = np.zeros_like(W["W_t2"])
+    if case == "identity":
+        W["W_t1"] = np.eye(d, dtype=np.float32)
+        W["W_t2"] = np.eye(d, dtype=np.float32)
+        W["b_t1"] = np.zeros(d, np.float32)
+        W["b_t2"] = np.zeros(d, np.float32)
+    bt1 = [float(v) for v in W["b_t1"]]
+    bt2 = [float(v) for v in W["b_t2"]]
+    if case == "t1_zero":
+        h = [_silu_s(v) for v in bt1]
+        c = [a + b for a, b in zip(bf_linear([h], W["W_t2"])[0], bt2)]
+    elif case == "t1_t2_zero":
+        c = bt2
+    else:
+        c = [_silu_s(float(v)) for v in O.time_embedding(t, d)]   # e(t) is pinned above
+    sc = [_silu_s(v) for v in c]
+    mods, (gf, bfin) = O.modulation(cfg, W, t)
+    for l in range(cfg.n_layers):
+        m = [a + float(b) for a, b in zip(bf_linear([sc], W[f"L{l}.W_mod"])[0], W[f"L{l}.b_mod"])]
+        for j in range(cfg.n_sub):
+            for s in range(3):
+                np.testing.assert_allclose(mods[l][j][s], m[(3 * j + s) * d:(3 * j + s + 1) * d],
+                                           rtol=1e-12, atol=1e-15)
+    fin = [a + float(b) for a, b in zip(bf_linear([sc], W["W_fm"])[0], W["b_fm"])]
+    np.testing.assert_allclose(gf, fin[:d], rtol=1e-12, atol=1e-15)
+    np.testing.assert_allclose(bfin, fin[d:], rtol=1e-12, atol=1e-15)
+
+
+def _bf_rows_rms(x, eps):
+    return [math.sqrt(sum(v * v for v in row) / len(row) + eps) for row in x]
+
+
+def _bf_one_sublayer(cfg, W, kind, x0, prefix, alpha):
+    """Brute-force velocity of a one-layer expert in which only sublayer `kind`
+    is gated on (alpha) with gamma = 1, beta = 0.5, and the final modulation is
+    zero: v = (x1 / rms(x1)) W_out^T + b_out, x1 = x0 + alpha * y(u),
+    u = 2 x0 / rms(x0) + 0.5."""
+    eps, H, G, hd = cfg.rms_eps, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim
+    r0 = _bf_rows_rms(x0, eps)
+    u = [[2.0 * v / r0[i] + 0.5 for v in row] for i, row in enumerate(x0)]
+    if kind == "mlp":
+        hid = [[_gelu_s(v) for v in row] for row in bf_linear(u, W["L0.W1"])]
+        y = bf_linear(hid, W["L0.W2"])
+    else:
+        q = bf_linear(u, W["L0.W_q"])
+
+        def heads(rows):
+            return [[r[g * hd:(g + 1) * hd] for r in rows] for g in range(G)]
+        if kind == "cross":
+            k = heads(bf_linear(prefix, W["L0.W_kc"]))
+            v = heads(bf_linear(prefix, W["L0.W_vc"]))
+        else:
+            k = heads(bf_linear(u, W["L0.W_k"]))
+            v = heads(bf_linear(u, W["L0.W_v"]))
+            if kind == "joint":      # prefix rows first, one softmax
+                kc = heads(bf_linear(prefix, W["L0.W_kc"]))
+                vc = heads(bf_linear(prefix, W["L0.W_vc"]))
+                k = [kc[g] + k[g] for g in range(G)]
+                v = [vc[g] + v[g] for g in range(G)]
+        o = bf_attention(q, k, v, H, G, hd).tolist()
+        y = bf_linear(o, W["L0.W_o"])
+    x1 = [[x0[i][c] + float(alpha[c]) * y[i][c] for c in range(len(x0[0]))] for i in range(len(x0))]
+    r1 = _bf_rows_rms(x1, eps)
+    xn = [[v / r1[i] for v in row] for i, row in enumerate(x1)]
+    return np.array(bf_linear(xn, W["W_out"])) + W["b_out"].astype(np.float64)
+
+
+@pytest.mark.parametrize("pattern,j", [("self_cross", 0), ("self_cross", 1), ("self_cross", 2),
+                                       ("joint", 0), ("joint", 1), ("alt", 0), ("alt", 1), ("cross", 0)])
+def test_sublayer_slot_order_single_active_sublayer(pattern, j):
+    """W_mod = 0 and b_mod = (gamma, beta, alpha) = (1, 0.5, a) in sublayer j
+    of the layer, alpha = 0 in every other sublayer, zero final modulation:
+    the expert's velocity equals a brute-force evaluation of that one sublayer
+    on u = 2 x0 / rms(x0) + 0.5.  Catches gamma and beta (or alpha) swapped
+    within a sublayer's slots, one sublayer reading another's slots, and a
+    sublayer of another kind run at position j."""
+    cfg = TINY.with_(pattern=pattern, n_layers=1)
+    W, inp, cache = _tiny_setup(cfg)
+    d = cfg.d_model
+    W["L0.W_mod"] = np.zeros_like(W["L0.W_mod"])
+    bm = np.zeros_like(W["L0.b_mod"])
+    bm[(3 * j) * d:(3 * j + 1) * d] = 1.0
+    bm[(3 * j + 1) * d:(3 * j + 2) * d] = 0.5
+    alpha = _rng(60 + j).uniform(0.5, 1.5, d).astype(np.float32)
+    bm[(3 * j + 2) * d:(3 * j + 3) * d] = alpha
+    W["L0.b_mod"] = bm
+    W["W_fm"] = np.zeros_like(W["W_fm"])
+    W["b_fm"] = np.zeros_like(W["b_fm"])
+    a, s = inp["noise"][0].astype(np.float64), inp["state"][0].astype(np.float64)
+    x0 = [[sum(a[i][k] * float(W["W_in"][c][k]) for k in range(cfg.d_action)) + float(W["b_in"][c]) +
+           sum(s[k] * float(W["W_s"][c][k]) for k in range(cfg.d_state)) + float(W["b_s"][c]) +
+           float(W["E_pos"][i][c]) for c in range(d)] for i in range(cfg.n_action)]
+    prefix = inp["prefix"][0].astype(np.float64).tolist()
+    kind = cfg.sublayers(0)[j]
+    want = _bf_one_sublayer(cfg, W, kind, x0, prefix, alpha)
+    got = O.expert_forward(cfg, W, cache[:, :, 0], a, s, 0.6)
+    np.testing.assert_allclose(got, want, rtol=1e-11, atol=1e-13)
+    # the gated-on sublayer matters: without it the velocity moves by far more
+    # than the tolerance above
+    bm[(3 * j + 2) * d:(3 * j + 3) * d] = 0.0
+    assert np.abs(O.expert_forward(cfg, W, cache[:, :, 0], a, s, 0.6) - got).max() > 1e-5
