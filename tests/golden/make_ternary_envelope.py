@@ -6,7 +6,7 @@ random weights most activation codes are small, so any rounding difference
 upstream of a quantiser (fp32 vs fp64 accumulation order, bf16 storage)
 flips codes and the flips compound over the layers.  Two equally valid
 evaluations therefore differ by the stack's own quantisation noise.  This
-script measures that spread: the oracle (storage="kernel") is re-run with
+script measures that spread: the plain fp64 oracle is re-run with
 every quantiser input multiplied by (1 + 1e-5 * N(0,1)) for several seeds,
 and the largest max|d| and mean|d| against the unperturbed run are recorded.
 
@@ -33,7 +33,7 @@ def main():
     inp = wl.make_batch(cfg, 1)
     tau = wl.uniform_schedule(cfg.n_steps)
     cache = O.prefix_kv_build(cfg, W, inp["prefix"])
-    ref = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau, storage="kernel")
+    ref = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
     orig = O.quantize_int8_rows
     maxes, means = [], []
     for seed in range(SEEDS):
@@ -45,7 +45,7 @@ def main():
 
         O.quantize_int8_rows = jittered
         try:
-            out = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau, storage="kernel")
+            out = O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
         finally:
             O.quantize_int8_rows = orig
         d = np.abs(out - ref)

@@ -39,7 +39,9 @@ def test_exports_every_declared_symbol():
 
 
 @pytest.mark.parametrize("name", list(wl.CONFIGS))
-def test_weight_count_matches_table_order(name):
+def test_binding_weight_order_matches_generator(name):
+    """The binding's weight-table order is the generator's name order, with
+    each ternary matrix followed by its scale."""
     vla = _vla()
     cfg = wl.CONFIGS[name]
     assert vla.weight_count(cfg) == len(vla.weight_order(cfg))
@@ -107,6 +109,8 @@ def test_call_validation_without_device():
     assert L.vla_denoise(None, 16, 0, 1, 1, 16, 16, f, 2, None, None, 16, None) == 1
     assert L.vla_prefix_kv_build(None, 16, 1, 1, 16, 0, None) == 1
     assert L.vla_kv_cache_bytes(None, 1, 1) == 0
+    assert vla.STATUS[L.vla_model_check(None, None)] == "VLA_E_ARG"
+    assert vla.STATUS[L.vla_model_set_option(None, 7, 0)] == "VLA_E_ARG"
     # ternary GEMM: K % 4, negative sizes, NULL, misaligned
     assert vla.STATUS[L.vla_ternary_gemm(16, 16, 2, 2, 6, 16, None)] == "VLA_E_SHAPE"
     assert vla.STATUS[L.vla_ternary_gemm(16, 16, -1, 2, 8, 16, None)] == "VLA_E_SHAPE"

@@ -216,9 +216,11 @@ def test_adarms_parity(torch, elem, u_f32, M, d, nsplit):
 @pytest.mark.parametrize("name", ["tiny_f32", "pi0_bf16", "smolvla_bf16"])
 def test_time_cond_parity(torch, name):
     """Time-conditioning precompute (sinusoid, time MLP, every layer's W_mod and
-    W_fm) for a non-uniform schedule against the oracle's primitives, rounded to
-    bf16 exactly where the kernels store bf16 (the embedding, SiLU(W_t1 e + b_t1)
-    and SiLU(c)); what remains is fp32 accumulation order."""
+    W_fm) for a non-uniform schedule: (1) against the oracle's primitives
+    rounded to bf16 exactly where the kernels store bf16 (the embedding,
+    SiLU(W_t1 e + b_t1) and SiLU(c)), leaving fp32 accumulation order; (2)
+    against the plain oracle's modulation() within the bound those bf16 stores
+    can produce (fp32 models: within fp32 accumulation)."""
     from vla_testlib import device_weights
     cfg = wl.CONFIGS[name]
     W = wl.make_weights(cfg)
@@ -251,10 +253,29 @@ def test_time_cond_parity(torch, name):
         tol = 1e-3 if bf else 1e-5
         assert np.abs(got_m[k] - ref_m).max() <= tol, (k, np.abs(got_m[k] - ref_m).max())
         assert np.abs(got_f[k] - ref_f).max() <= tol, (k, np.abs(got_f[k] - ref_f).max())
+        mods_o, fin_o = O.modulation(cfg, W, float(tau[k]))
+        flat = np.concatenate([np.concatenate([np.concatenate(gba) for gba in ml]) for ml in mods_o])
+        flat_f = np.concatenate(fin_o)
         if not bf:  # fp32 models: the whole chain against the oracle's own modulation()
-            mods_o, fin_o = O.modulation(cfg, W, float(tau[k]))
-            flat = np.concatenate([np.concatenate([np.concatenate(gba) for gba in ml]) for ml in mods_o])
             assert np.abs(got_m[k] - flat).max() <= 1e-4
+            assert np.abs(got_f[k] - flat_f).max() <= 1e-4
+        else:
+            # bf16 models against the plain oracle: each of the kernels' three
+            # bf16 stores (e, SiLU(W_t1 e + b_t1), SiLU(c)) moves a value v by
+            # an independent error of at most 2^-9 |v| (variance (2^-9 v)^2 / 3
+            # if uniform); propagated through W^2 with |SiLU'| <= 1.1, six
+            # standard deviations of the result bound the difference, plus
+            # fp32 accumulation
+            e64 = O.time_embedding(float(tau[k]), d)
+            h64 = O.silu(O.linear(e64, W["W_t1"], W["b_t1"]))
+            sc64 = O.silu(O.linear(h64, W["W_t2"], W["b_t2"]))
+            u = 2.0 ** -9
+            vh = 1.21 * (W["W_t1"].astype(np.float64) ** 2 @ ((u * e64) ** 2 / 3)) + (u * h64) ** 2 / 3
+            vsc = 1.21 * (W["W_t2"].astype(np.float64) ** 2 @ vh) + (u * sc64) ** 2 / 3
+            bm = 6.0 * np.sqrt(W_mod.astype(np.float64) ** 2 @ vsc) + 1e-5
+            bfm = 6.0 * np.sqrt(W["W_fm"].astype(np.float64) ** 2 @ vsc) + 1e-5
+            assert np.all(np.abs(got_m[k] - flat) <= bm), np.abs(got_m[k] - flat).max()
+            assert np.all(np.abs(got_f[k] - flat_f) <= bfm), np.abs(got_f[k] - flat_f).max()
 
 
 def test_quantize_i8_bit_exact(torch):
@@ -375,3 +396,79 @@ def test_ternary_linear(torch, M, N, K):
     ref = O.ternary_linear(x, w, scale)
     # identical int8 codes and int32 sums; only the fp32 dequantisation rounds
     np.testing.assert_allclose(y.cpu().numpy(), ref, rtol=1e-6, atol=1e-7)
+
+
+def test_ternary_layer_quantiser_codes_differ_by_one(torch):
+    """One W2A8 attention branch of the ternary expert's first layer (full
+    widths: d 2560, 20 x 128 query heads, 5 K/V heads, 512 cached prefix rows),
+    both sides starting from the same float32 sublayer input u: the kernels
+    project Q, K, V (W2A8, stored bf16 as the expert stores them), run joint
+    attention over the bf16 cache built by vla_prefix_kv_build, and quantise
+    the attention output for W_o; the oracle does the same in float64.  The
+    quantiser codes of u itself are identical (both quantise the same float32
+    values).  At the O-projection input the two sides' values differ by the
+    kernel's bf16 storage and fp32 sums, so some codes differ: each by exactly
+    one, each explained by a rounding boundary lying between the two sides'
+    scaled values, and at most 15% of them (the bf16 steps are 2^-9 relative
+    against a quantiser step of max|o| / 127)."""
+    from vla_testlib import Pipeline, device_weights
+    vla = _vla()
+    cfg = wl.TERNARY_W2A8.with_(n_layers=1)
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    d, H, G, hd, n, P = cfg.d_model, cfg.n_heads, cfg.n_kv_heads, cfg.head_dim, cfg.n_action, cfg.prefix_len
+    mods, _ = O.modulation(cfg, W, 0.0)
+    gamma, beta, _ = mods[0][0]
+    x0 = O.input_embedding(cfg, W, inp["noise"][0], inp["state"][0])
+    u = O.ada_rms(x0, gamma, beta, cfg.rms_eps).astype(np.float32)
+    # codes of the sublayer input: same float32 values on both sides
+    qd = torch.empty((n, d), dtype=torch.int8, device="cuda")
+    rd = torch.empty(n, dtype=torch.float32, device="cuda")
+    vla.test_quantize_i8(_dev(torch, u), n, d, qd, rd)
+    q_u, r_u = O.quantize_int8_rows(u)
+    assert np.array_equal(qd.cpu().numpy(), q_u) and np.array_equal(rd.cpu().numpy(), r_u)
+    # oracle branch in float64
+    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+    q_ref = O._lin(cfg, W, "L0.W_q", u)
+    k_ref = O.split_heads(O._lin(cfg, W, "L0.W_k", u), G, hd)
+    v_ref = O.split_heads(O._lin(cfg, W, "L0.W_v", u), G, hd)
+    o_ref = O.attention(q_ref, np.concatenate([cache[0, 0, 0], k_ref], 1),
+                        np.concatenate([cache[0, 1, 0], v_ref], 1), H, G, hd)
+    # kernel branch: W2A8 projections from u, bf16 stores, the library's cache
+    dw = device_weights(cfg, W)
+    ud = _dev(torch, u)
+    proj = {}
+    for name, N in (("W_q", H * hd), ("W_k", G * hd), ("W_v", G * hd)):
+        y = torch.empty((n, N), dtype=torch.float32, device="cuda")
+        vla.test_ternary_linear(ud, dw["L0." + name], n, N, d, float(W["L0." + name + ".scale"]), y)
+        proj[name] = y.to(torch.bfloat16).contiguous()
+    pipe = Pipeline(cfg, W, inp)
+    try:
+        pipe.build_cache()
+        c = pipe.cache.view(torch.bfloat16).view(1, 2, 1, G, P, hd)
+        kc, vc = c[0, 0].contiguous(), c[0, 1].contiguous()
+        o = torch.empty((n, H * hd), dtype=torch.bfloat16, device="cuda")
+        vla.test_attention(1, 2, proj["W_q"], proj["W_k"], proj["W_v"], kc, vc, 1, n, P, H, G, hd, o)
+        of = o.float().contiguous()
+        qo = torch.empty((n, H * hd), dtype=torch.int8, device="cuda")
+        ro = torch.empty(n, dtype=torch.float32, device="cuda")
+        vla.test_quantize_i8(of, n, H * hd, qo, ro)
+        torch.cuda.synchronize()
+        o_got = of.cpu().numpy()
+        c_got, r_got = qo.cpu().numpy().astype(np.int64), ro.cpu().numpy()
+    finally:
+        pipe.close()
+    c_ref, r_ref = O.quantize_int8_rows(o_ref.astype(np.float32))
+    c_ref = c_ref.astype(np.int64)
+    diff = c_got != c_ref
+    frac = float(diff.mean())
+    s_ref = o_ref * (127.0 / r_ref.astype(np.float64))[:, None]
+    s_got = o_got.astype(np.float64) * (127.0 / r_got.astype(np.float64))[:, None]
+    print(f"W2A8 layer 0: O-projection codes differing from the oracle: {int(diff.sum())} of {diff.size} "
+          f"({100 * frac:.2f}%), max |d o| = {np.abs(o_got - o_ref).max():.2e}")
+    assert np.all(np.abs(c_got - c_ref) <= 1)
+    bnd = 0.5 * (c_got + c_ref)                      # the boundary the two values straddle
+    lo, hi = np.minimum(s_ref, s_got), np.maximum(s_ref, s_got)
+    slack = 1e-5 * (1.0 + np.abs(bnd))
+    assert np.all((bnd[diff] >= lo[diff] - slack[diff]) & (bnd[diff] <= hi[diff] + slack[diff]))
+    assert frac <= 0.15
