@@ -35,7 +35,8 @@ typedef enum {
   VLA_E_SHAPE = 2,        /* inconsistent or unsupported dimensions */
   VLA_E_UNSUPPORTED = 3,  /* valid request this build does not implement */
   VLA_E_NOMEM = 4,        /* device allocation failed */
-  VLA_E_DEVICE = 5,       /* a HIP call or kernel launch failed */
+  VLA_E_DEVICE = 5,       /* a HIP call or kernel launch failed, or an earlier call failed on the
+                             device (see vla_model_check) */
   VLA_E_NONFINITE = 6     /* NaN/Inf in the output (VLA_CHECK_FINITE=1 only) */
 } vla_status;
 
@@ -134,12 +135,27 @@ vla_status vla_prefix_kv_build(vla_model* model, const void* prefix_hidden, int3
  *   actions_out: [batch][n][A] fp32; may alias noise
  * Requests are independent; weights and the schedule are shared.
  * With the environment variable VLA_CHECK_FINITE=1 the call synchronises the
- * stream and returns VLA_E_NONFINITE if any output is NaN or Inf.
+ * stream and returns VLA_E_DEVICE if the integration failed on the device,
+ * else VLA_E_NONFINITE if any output is NaN or Inf.
+ * Device-side failure: every barrier wait of the persistent step kernel (loop
+ * mode 2) is bounded; if one times out, every workgroup leaves, that call's
+ * actions_out is filled with NaN, and the failure is recorded in the model.
+ * It is reported, once, as VLA_E_DEVICE by the first vla_denoise (before it
+ * enqueues anything) or vla_model_check on the same model that runs after the
+ * failed call has completed.  Each launch starts with a cleared record, so
+ * one failure does not affect later calls.
  */
 vla_status vla_denoise(vla_model* model, const void* kv_cache, size_t kv_cache_bytes, int32_t batch,
                        int32_t prefix_len, const float* noise, const float* state,
                        const float* t_schedule, int32_t n_steps, const float* act_mean,
                        const float* act_std, float* actions_out, void* stream);
+
+/*
+ * Synchronise `stream` and report a device-side failure of an earlier
+ * vla_denoise on this model that has not been reported yet (VLA_E_DEVICE,
+ * once; see vla_denoise), else VLA_OK.  Errors: VLA_E_ARG, VLA_E_DEVICE.
+ */
+vla_status vla_model_check(vla_model* model, void* stream);
 
 /*
  * W2A8 GEMM (Sec. 4.5): acc[m][n] = sum_k x[m][k] * w[n][k], int32, exact.
@@ -155,8 +171,9 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
 /* Options:
  *  VLA_OPT_LOOP_MODE: loop driver of vla_denoise, 0 = one launch per phase on
  *    the stream, 1 = the same launches captured once in a HIP graph and
- *    replayed, 2 (default) = one persistent cooperative kernel for the whole
- *    step loop where the model supports it (batch 1, bf16, joint attention,
+ *    replayed, 2 (default) = one persistent kernel (every workgroup resident
+ *    at once) for the whole step loop where the model and device support it
+ *    (batch 1, bf16, joint attention,
  *    H % 8 == 0, the shape limits of the team layout, none of the causal,
  *    RoPE or state-token variants), else as 1.
  *  VLA_OPT_PROFILE: R in 1..1000 = time every launch of the following
@@ -194,9 +211,14 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *    state row takes part in attention (and is token 0 for the causal mask and
  *    RoPE) but yields no action, so actions_out keeps its [B, n, d_action]
  *    layout.  0 (default) = the paper's embedding.  Discards the cached plans;
- *    such models run on loop modes 0 and 1. */
+ *    such models run on loop modes 0 and 1.
+ *  VLA_OPT_PERSIST_SPIN_LIMIT: polls of one barrier wait of the persistent
+ *    step kernel before it gives up (value >= 0; -1 = the default, about
+ *    0.2 s).  For tests of the failure path: a small value makes waits time
+ *    out, which every workgroup survives (see vla_denoise). */
 enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2, VLA_OPT_ATTN_SPLITS = 3,
-       VLA_OPT_CAUSAL_SELF = 4, VLA_OPT_ROPE_BASE = 5, VLA_OPT_STATE_TOKEN = 6 };
+       VLA_OPT_CAUSAL_SELF = 4, VLA_OPT_ROPE_BASE = 5, VLA_OPT_STATE_TOKEN = 6,
+       VLA_OPT_PERSIST_SPIN_LIMIT = 7 };
 vla_status vla_model_set_option(vla_model* model, int32_t option, int32_t value);
 
 /* One timed launch of a profiled vla_denoise call. */

@@ -1,5 +1,5 @@
 // Persistent tensor-parallel denoise loop for the batch-1 bf16 expert with
-// joint attention: one cooperative launch runs every solver step, layer and
+// joint attention: one launch of co-resident workgroups runs every solver step, layer and
 // sublayer of vla_denoise (Algorithm 1's loop), with no kernel boundary inside.
 //
 // The 256 workgroups (4 waves each: one wave per SIMD, so a wave may hold up to
@@ -44,7 +44,6 @@ constexpr int STL = 0;                   // stores of exchanged data: plain (wri
 constexpr int SC1 = 16;                  // device-coherent policy of the cross-team deltas
 constexpr int KBA_MAX = 2;               // 32-key blocks per attention split
 constexpr int MB = 8;                    // key splits one of a vector's 4 merge threads loads (S <= 32)
-constexpr long SPIN_LIMIT = 1L << 21;
 constexpr float kLog2e = 1.4426950408889634f;
 typedef short v4s_t __attribute__((ext_vector_type(4)));
 typedef __attribute__((address_space(3))) v4s_t lds_v4s;
@@ -103,6 +102,7 @@ struct Sync {
   unsigned* flag;   // [8][32]
   int* err;
   unsigned bk;      // barriers this workgroup has arrived at
+  long spin_limit;  // polls before a wait gives up
 };
 
 VLA_DEV void arrive(Sync& s, int team, int rank) {
@@ -138,7 +138,7 @@ VLA_DEV bool wait_flags(Sync& s, int team, int* lds_flag, unsigned peek) {
       while (true) {
         __builtin_amdgcn_s_sleep(1);
         if (__all(flag_peek<GRID>(s, team) >= target)) break;
-        if (++it > SPIN_LIMIT) {
+        if (++it > s.spin_limit) {
           if (threadIdx.x == 0) __hip_atomic_fetch_or(s.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
           ok = false;
           break;
@@ -307,7 +307,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   for (int i = tid; i < a.L; i += NTHR) lt[i] = a.layers[i];
   const bf16_t* kvbase = reinterpret_cast<const bf16_t*>(a.cp->kv_cache);
 
-  Sync sy{a.sync, a.err, 0u};
+  Sync sy{a.sync, a.err, 0u, a.spin_limit};
   unsigned long long* trace = (a.trace && rank == 0) ? a.trace + (size_t)team * PERSIST_TRACE_MAX : nullptr;
   int tev = 0;
   auto mark = [&]() {
@@ -1082,21 +1082,44 @@ size_t persist_lds_bytes(int hd, int HT) {
   return mainb > otile ? mainb : otile;
 }
 
+namespace {
+const void* persist_fn(int hd, int d) {
+  const int dpt = d / NTHR;
+  switch (hd * 10 + dpt) {
+    case 2564: return reinterpret_cast<const void*>(&persist_kernel<256, 4>);
+    case 2562: return reinterpret_cast<const void*>(&persist_kernel<256, 2>);
+    case 1284: return reinterpret_cast<const void*>(&persist_kernel<128, 4>);
+    case 1282: return reinterpret_cast<const void*>(&persist_kernel<128, 2>);
+    case 644: return reinterpret_cast<const void*>(&persist_kernel<64, 4>);
+    case 642: return reinterpret_cast<const void*>(&persist_kernel<64, 2>);
+    default: return nullptr;
+  }
+}
+}  // namespace
+
+bool persist_resident(int d, int hd, int HT) {
+  const void* fn = persist_fn(hd, d);
+  if (!fn) return false;
+  int dev = 0, cus = 0, nb = 0;
+  if (hipGetDevice(&dev) != hipSuccess) return false;
+  if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus != NWG)
+    return false;
+  const size_t lds = persist_lds_bytes(hd, HT);
+  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) return false;
+  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, NTHR, lds) != hipSuccess) return false;
+  return nb >= 1;
+}
+
+// A plain launch: the plan builder has checked that every workgroup fits on
+// the device at once (persist_resident), and every barrier wait of the kernel
+// is bounded, so a workgroup that never started would end the run through the
+// error word, not hang it.
 hipError_t launch_persist(const PersistArgs& a, hipStream_t s) {
   const size_t lds = persist_lds_bytes(a.hd, a.HT);
   void* args[] = {const_cast<PersistArgs*>(&a)};
-  const void* fn = nullptr;
-  const int dpt = a.d / NTHR;
-  switch (a.hd * 10 + dpt) {
-    case 2564: fn = reinterpret_cast<const void*>(&persist_kernel<256, 4>); break;
-    case 2562: fn = reinterpret_cast<const void*>(&persist_kernel<256, 2>); break;
-    case 1284: fn = reinterpret_cast<const void*>(&persist_kernel<128, 4>); break;
-    case 1282: fn = reinterpret_cast<const void*>(&persist_kernel<128, 2>); break;
-    case 644: fn = reinterpret_cast<const void*>(&persist_kernel<64, 4>); break;
-    case 642: fn = reinterpret_cast<const void*>(&persist_kernel<64, 2>); break;
-    default: return hipErrorInvalidValue;
-  }
+  const void* fn = persist_fn(a.hd, a.d);
+  if (!fn) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;
-  return hipLaunchCooperativeKernel(fn, dim3(NWG), dim3(NTHR), args, (unsigned)lds, s);
+  return hipLaunchKernel(fn, dim3(NWG), dim3(NTHR), args, lds, s);
 }

@@ -143,6 +143,8 @@ struct vla_model {
   int state_token = 0;            // state as its own leading token (VLA_OPT_STATE_TOKEN)
   float rope_base = 0.0f;         // rotary position embedding base, 0 = none (VLA_OPT_ROPE_BASE)
   int attn_splits = 0;            // key splits of the launch-per-phase attention (0 = automatic)
+  long spin_limit = PERSIST_SPIN_DEFAULT;  // persistent kernel: polls of a barrier wait (VLA_OPT_PERSIST_SPIN_LIMIT)
+  int persist_dev_ok = -1;        // the device holds the persistent kernel's whole grid (-1 = not yet asked)
   void* last_profiled = nullptr;  // Plan* of the last profiled call
   void* last_traced = nullptr;    // Plan* of the last traced call
   hipStream_t cap_stream = nullptr;
@@ -206,7 +208,7 @@ vla_op_time op_info(int kind, int M, int N, int K, double bytes, double flops) {
 
 struct Plan {
   int B = 0, P = 0, T = 0;
-  bool persist = false;       // one cooperative launch runs the whole step loop
+  bool persist = false;       // one launch of co-resident workgroups runs the whole step loop
   std::vector<void*> allocs;
   CallParams* cp = nullptr;
   float *a = nullptr, *xs = nullptr, *x = nullptr, *mods = nullptr, *modf = nullptr;
@@ -221,9 +223,14 @@ struct Plan {
   hipGraphExec_t exec = nullptr;
   std::vector<hipEvent_t> events;  // 2 per op when profiled
   int prof_reps = 1;
-  int* persist_err = nullptr;       // persistent kernel: set if a barrier timed out
+  int* persist_err = nullptr;       // persistent kernel: set if a barrier timed out (device word)
+  int* persist_err_host = nullptr;  // pinned host copy of it, written after every launch
   unsigned long long* trace = nullptr;  // persistent kernel: phase timeline (8 x PERSIST_TRACE_MAX)
   ~Plan() {
+    if (persist_err_host) {
+      (void)hipDeviceSynchronize();   // no copy into the host word is still in flight
+      (void)hipHostFree(persist_err_host);
+    }
     for (hipEvent_t e : events) (void)hipEventDestroy(e);
     if (exec) (void)hipGraphExecDestroy(exec);
     for (void* p : allocs) (void)hipFree(p);
@@ -404,15 +411,32 @@ int mlp_act(int mlp) {
 
 // The persistent step kernel covers the batch-1 bf16 dense expert with joint
 // attention whose shape fits its team layout (see persist_supported).
-bool persist_eligible(const vla_model* m, int B, int P, int T) {
+bool persist_eligible(vla_model* m, int B, int P, int T) {
   // its attention is unmasked and unrotated, its rows are the action tokens alone
   if (m->causal || m->rope_base > 0.0f || m->state_token) return false;
   const vla_config& c = m->cfg;
   int kba = 0, nsplit = 0;
-  return !m->tern && m->et == ET_BF16 && c.pattern == VLA_PAT_JOINT && !c.head_regression && B == 1 &&
-         T >= 1 && c.n_layers >= 1 && c.n_layers <= PERSIST_MAX_LAYERS &&
-         persist_supported(m->d, c.head_dim, c.n_heads, c.n_kv_heads, c.d_ff, c.n_action, P, c.d_action,
-                           c.mlp != VLA_MLP_GELU, &kba, &nsplit);
+  const bool shape_ok = !m->tern && m->et == ET_BF16 && c.pattern == VLA_PAT_JOINT && !c.head_regression &&
+                        B == 1 && T >= 1 && c.n_layers >= 1 && c.n_layers <= PERSIST_MAX_LAYERS &&
+                        persist_supported(m->d, c.head_dim, c.n_heads, c.n_kv_heads, c.d_ff, c.n_action, P,
+                                          c.d_action, c.mlp != VLA_MLP_GELU, &kba, &nsplit);
+  if (!shape_ok) return false;
+  if (m->persist_dev_ok < 0) m->persist_dev_ok = persist_resident(m->d, c.head_dim, c.n_heads / 8) ? 1 : 0;
+  return m->persist_dev_ok == 1;
+}
+
+// A device-side failure of an earlier call (a persistent-kernel barrier that
+// timed out) that has become visible on the host: report it once.
+vla_status take_device_error(vla_model* m) {
+  for (auto& kv : m->plans) {
+    Plan* p = kv.second.get();
+    if (p->persist_err_host && *reinterpret_cast<volatile int*>(p->persist_err_host) != 0) {
+      *reinterpret_cast<volatile int*>(p->persist_err_host) = 0;
+      return fail(VLA_E_DEVICE, "an earlier vla_denoise failed on the device: a barrier of the persistent "
+                                "kernel timed out, and that call's actions_out holds NaN");
+    }
+  }
+  return VLA_OK;
 }
 
 vla_status build_plan(vla_model* m, Plan* p) {
@@ -543,12 +567,18 @@ vla_status build_plan(vla_model* m, Plan* p) {
     VLA_TRY(al(&pa.hbuf, (size_t)8 * n * (F / 8) * 2));
     VLA_TRY(al((void**)&pa.delta, (size_t)2 * 8 * n * d * 4));
     VLA_TRY(al((void**)&pa.sync, (size_t)PERSIST_SYNC_WORDS * 4));
-    VLA_TRY(al((void**)&pa.err, 16));
-    HIP_TRY(hipMemset(pa.err, 0, 16));
+    pa.err = reinterpret_cast<int*>(pa.sync + PERSIST_ERR_OFF);
     p->persist_err = pa.err;
+    if (hipHostMalloc((void**)&p->persist_err_host, 16, hipHostMallocDefault) != hipSuccess) {
+      p->persist_err_host = nullptr;
+      return fail(VLA_E_NOMEM, "hipHostMalloc of the error word failed");
+    }
+    *p->persist_err_host = 0;
     VLA_TRY(al((void**)&p->trace, (size_t)8 * PERSIST_TRACE_MAX * 8));
     pa.trace = nullptr;
     const int* tracing = &m->trace;
+    const long* spin = &m->spin_limit;
+    int* err_host = p->persist_err_host;
     unsigned long long* tbuf = p->trace;
     // Per step and layer: the weights once, the cache once (algorithmic bytes).
     double wbytes = 0.0;
@@ -560,12 +590,18 @@ vla_status build_plan(vla_model* m, Plan* p) {
     }
     const double cbytes = (double)L * 2 * c.n_kv_heads * P * hd * es;
     const double gflop = (double)T * (2.0 * n * wbytes / es + 4.0 * n * c.n_heads * hd * (P + n) * L);
+    // Every launch starts from cleared barrier flags, rank counters and error
+    // word; the error word is copied to pinned host memory after the kernel,
+    // where the next call (or vla_model_check) finds it.
     bld.ops->push_back(Op{[=](hipStream_t s) {
                             hipError_t e = launch_fill_u32(pa.sync, 0u, PERSIST_SYNC_WORDS, s);
                             if (e != hipSuccess) return e;
                             PersistArgs q = pa;
                             q.trace = *tracing ? tbuf : nullptr;
-                            return launch_persist(q, s);
+                            q.spin_limit = *spin;
+                            e = launch_persist(q, s);
+                            if (e != hipSuccess) return e;
+                            return hipMemcpyAsync(err_host, pa.err, 4, hipMemcpyDeviceToHost, s);
                           },
                           op_info(VLA_OP_PERSIST, n, L, T, (double)T * (wbytes + cbytes), gflop)});
     HIP_TRY(hipDeviceSynchronize());
@@ -902,6 +938,11 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
     m->causal = value;
     return VLA_OK;
   }
+  if (option == VLA_OPT_PERSIST_SPIN_LIMIT) {
+    if (value < -1) return fail(VLA_E_ARG, "spin limit %d out of range", value);
+    m->spin_limit = value < 0 ? PERSIST_SPIN_DEFAULT : (long)value;
+    return VLA_OK;
+  }
   if (option == VLA_OPT_TRACE) {
     if (value < 0 || value > 1) return fail(VLA_E_ARG, "trace flag %d out of range", value);
     m->trace = value;
@@ -916,6 +957,13 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
 }
 
 void vla_model_destroy(vla_model* m) { delete m; }
+
+vla_status vla_model_check(vla_model* m, void* stream) {
+  if (!m) return fail(VLA_E_ARG, "model is NULL");
+  const hipError_t e = hipStreamSynchronize(reinterpret_cast<hipStream_t>(stream));
+  if (e != hipSuccess) return fail(VLA_E_DEVICE, "hipStreamSynchronize: %s", hipGetErrorString(e));
+  return take_device_error(m);
+}
 
 size_t vla_kv_cache_bytes(const vla_model* m, int32_t batch, int32_t prefix_len) {
   if (!m || batch < 1 || prefix_len < 1) return 0;
@@ -1268,6 +1316,7 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
   if (kv_cache_bytes != vla_kv_cache_bytes(m, batch, prefix_len))
     return fail(VLA_E_SHAPE, "kv_cache_bytes %zu != %zu for batch %d, prefix_len %d", kv_cache_bytes,
                 vla_kv_cache_bytes(m, batch, prefix_len), batch, prefix_len);
+  VLA_TRY(take_device_error(m));
   CallParams cpv{};
   for (int k = 0; k <= n_steps; ++k) {
     if (!std::isfinite(t_schedule[k])) return fail(VLA_E_ARG, "t_schedule[%d] is not finite", k);
@@ -1340,12 +1389,8 @@ vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes
     hipError_t e = hipStreamSynchronize(s);
     (void)hipFree(flag);
     if (e != hipSuccess) return fail(VLA_E_DEVICE, "hipStreamSynchronize: %s", hipGetErrorString(e));
+    VLA_TRY(take_device_error(m));   // a timed-out barrier also leaves NaN: name the cause first
     if (h) return fail(VLA_E_NONFINITE, "non-finite value in the action chunk");
-    if (p->persist_err) {
-      int perr = 0;
-      if (hipMemcpy(&perr, p->persist_err, 4, hipMemcpyDeviceToHost) == hipSuccess && perr)
-        return fail(VLA_E_DEVICE, "persistent kernel: a barrier timed out");
-    }
   }
   return VLA_OK;
 }

@@ -192,14 +192,17 @@ struct PersistArgs {
   void* omerged;             // [8][n][HT hd]: merged attention output of the team's heads
   void* hbuf;                // [8][n][F / 8]
   float* delta;              // [2][8][n][d]: per-team partial residual updates
-  unsigned* sync;            // PERSIST_SYNC_WORDS words (barrier flags, rank counters), zero at launch
-  int* err;                  // set when a barrier times out
+  unsigned* sync;            // PERSIST_SYNC_WORDS words (barrier flags, rank counters, error word), zero at launch
+  int* err;                  // = sync + PERSIST_ERR_OFF: set when a barrier times out
+  long spin_limit;           // polls of one barrier wait before it gives up (sets *err)
   // optional phase timeline: workgroup 0 of each team records the 100 MHz
   // clock before and after every barrier, PERSIST_TRACE_MAX entries per team
   unsigned long long* trace;
 };
-constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 32;  // barrier flags [8][32], then the per-XCD rank counters
 constexpr int PERSIST_RANK_OFF = 8 * 32;          // 8 per-XCD arrival counters (team ranks)
+constexpr int PERSIST_ERR_OFF = 8 * 32 + 32;      // the error word, on a line of its own
+constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 64;   // barrier flags [8][32], rank counters, error word
+constexpr long PERSIST_SPIN_DEFAULT = 1L << 21;   // barrier polls before a timeout (about 0.2 s)
 constexpr int PERSIST_TRACE_MAX = 8192;
 constexpr int PERSIST_MAX_LAYERS = 64;
 
@@ -248,5 +251,8 @@ hipError_t launch_rope(int et, void* x, int rows, int rpr, int ld, int col0, int
 // Persistent kernel: whether a shape is supported, the dynamic LDS it needs,
 // and the cooperative launch (256 workgroups of 512 threads).
 bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, int glu, int* kba, int* nsplit);
+// The device can hold every workgroup of the persistent kernel at once (its
+// 256 workgroups, one per compute unit, 32 on each of the 8 XCDs).
+bool persist_resident(int d, int hd, int HT);
 size_t persist_lds_bytes(int hd, int HT);
 hipError_t launch_persist(const PersistArgs& a, hipStream_t s);

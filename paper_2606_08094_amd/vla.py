@@ -27,12 +27,13 @@ VLA_OPT_ATTN_SPLITS = 3
 VLA_OPT_CAUSAL_SELF = 4
 VLA_OPT_ROPE_BASE = 5
 VLA_OPT_STATE_TOKEN = 6
+VLA_OPT_PERSIST_SPIN_LIMIT = 7
 PERSIST_TRACE_MAX = 8192
 OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "quantize", 5: "small",
             6: "attn_merge", 7: "persist"}
 
 # Every symbol the headers declare.
-EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_kv_cache_bytes",
+EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_model_check", "vla_kv_cache_bytes",
            "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
@@ -74,6 +75,7 @@ def lib():
         "vla_weight_count": (i32, [ctypes.POINTER(VlaConfig)]),
         "vla_model_create": (i32, [ctypes.POINTER(VlaConfig), ctypes.POINTER(vp), i32, ctypes.POINTER(vp)]),
         "vla_model_destroy": (None, [vp]),
+        "vla_model_check": (i32, [vp, vp]),
         "vla_kv_cache_bytes": (sz, [vp, i32, i32]),
         "vla_prefix_kv_build": (i32, [vp, vp, i32, i32, vp, sz, vp]),
         "vla_denoise": (i32, [vp, vp, sz, i32, i32, vp, vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp, vp]),
@@ -222,6 +224,16 @@ class Model:
         """Rotary position embedding of self / joint queries and keys (0 = none).
         Discards cached plans; build the prefix cache after setting it."""
         _check(lib().vla_model_set_option(self.handle, VLA_OPT_ROPE_BASE, int(base)))
+
+    def set_spin_limit(self, polls: int):
+        """Polls of one barrier wait of the persistent step kernel before it
+        gives up (-1 = the library default); small values force the failure path."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_PERSIST_SPIN_LIMIT, int(polls)))
+
+    def check(self, stream=None):
+        """Synchronise the stream; raise VlaError(VLA_E_DEVICE) if an earlier
+        denoise call of this model failed on the device."""
+        _check(lib().vla_model_check(self.handle, _stream(stream)))
 
     def set_trace(self, on: bool):
         """Record the persistent kernel's phase timeline on the next calls."""

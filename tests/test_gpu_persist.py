@@ -1,5 +1,5 @@
-"""Parity of the persistent step-loop driver (loop mode 2: one cooperative
-kernel runs every solver step) against the fp64 oracle, against the
+"""Parity of the persistent step-loop driver (loop mode 2: one kernel of
+co-resident workgroups runs every solver step) against the fp64 oracle, against the
 launch-per-phase graph driver, and run-to-run determinism.
 
 The driver covers batch-1 bf16 experts with joint attention whose shape fits
@@ -107,3 +107,45 @@ def test_ineligible_model_falls_back(torch):
     a = _run(cfg, W, inp, tau, loop_mode=2)[0]
     b = _run(cfg, W, inp, tau, loop_mode=1)[0]
     assert np.array_equal(a, b)
+
+
+def test_persist_barrier_timeout_is_reported(torch):
+    """The failure path, forced from the host: with a spin limit of 0 every
+    barrier wait that is not satisfied at its first look gives up, so every
+    workgroup leaves early (each wait is bounded: no kernel hangs).  The
+    call's chunk is NaN; vla_model_check then reports VLA_E_DEVICE once; the
+    next call (default limit) starts from a cleared error word and matches
+    the oracle.  A failure that has completed before the next vla_denoise is
+    reported by that call, before it enqueues anything."""
+    from paper_2606_08094_amd.vla import VlaError
+    from vla_testlib import Pipeline
+    cfg = CASES["small_geglu"]
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    ref = O.denoise(cfg, W, O.prefix_kv_build(cfg, W, inp["prefix"]), inp["noise"], inp["state"], tau)
+    pipe = Pipeline(cfg, W, inp, loop_mode=2)
+    try:
+        pipe.build_cache()
+        pipe.model.set_spin_limit(0)
+        bad = pipe.denoise(tau).cpu().numpy()
+        with pytest.raises(VlaError, match="VLA_E_DEVICE"):
+            pipe.model.check()
+        assert np.isnan(bad).all()
+        pipe.model.check()                      # reported once
+        pipe.model.set_spin_limit(-1)
+        good = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        pipe.model.check()
+        assert np.abs(good - ref).max() <= TOL
+        # a completed failure is reported by the next denoise call itself
+        pipe.model.set_spin_limit(0)
+        pipe.denoise(tau)
+        torch.cuda.synchronize()
+        pipe.model.set_spin_limit(-1)
+        with pytest.raises(VlaError, match="VLA_E_DEVICE"):
+            pipe.denoise(tau)
+        again = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        pipe.model.check()
+        assert np.array_equal(again, good)
+    finally:
+        pipe.close()
