@@ -37,6 +37,20 @@ def log(*a):
     print(*a, file=sys.stderr, flush=True)
 
 
+def time_chunks_each(torch, pipe, tau, iters):
+    """Per-chunk durations (ms) from a HIP event pair around every chunk on the
+    stream that runs it."""
+    ev = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(iters)]
+    torch.cuda.synchronize()
+    for a, b in ev:
+        a.record()
+        pipe.build_cache()
+        pipe.denoise(tau)
+        b.record()
+    torch.cuda.synchronize()
+    return [a.elapsed_time(b) for a, b in ev]
+
+
 def time_chunks(torch, pipe, tau, iters):
     start = torch.cuda.Event(enable_timing=True)
     end = torch.cuda.Event(enable_timing=True)
@@ -138,22 +152,91 @@ def hbm_copy_rate(torch, mib=1024, reps=10):
     return round(2.0 * n * 4 / sec / 1e9, 1)
 
 
-def cpu_baseline(cfg, W, inp, tau):
-    """The oracle as it stands, one full chunk (prefix K/V build + T Euler
-    steps) of the same workload on the host cores."""
-    from oracle import vla_oracle as O
+def cpu_env():
+    """What the oracle runs on: logical CPUs, the affinity set, the CPU model
+    and the BLAS thread pool numpy uses."""
+    model = "unknown"
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    model = line.split(":", 1)[1].strip()
+                    break
+    except OSError:
+        pass
     try:
         from threadpoolctl import threadpool_info
-        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+        blas = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
-        threads = os.cpu_count() or 1
-    t0 = time.perf_counter()
-    cache = O.prefix_kv_build(cfg, W, inp["prefix"])
-    O.denoise(cfg, W, cache, inp["noise"], inp["state"], tau)
-    dt = time.perf_counter() - t0
-    return {"value": round(1.0 / dt, 5), "unit": "chunks/s", "cores": int(threads), "kind": "oracle",
-            "sample": f"1 chunk of {cfg.name} (prefix K/V build + {cfg.n_steps} Euler steps, batch 1), "
-                      f"{dt:.1f} s, numpy fp64"}
+        blas = None
+    return {"nproc": os.cpu_count(), "affinity": len(os.sched_getaffinity(0)), "cpu_model": model,
+            "blas_threads": blas}
+
+
+def oracle_fit(cfg, W, inp, threads=None):
+    """The oracle as it stands on this host: the prefix K/V build, then the
+    denoise loop at T = 1 and T = 2 (the paper's inference(T) = prefill +
+    T * step fit).  Returns seconds for the build, the fixed part and one step.
+    threads: limit numpy's BLAS pool (None = all)."""
+    import contextlib
+    import workloads as wl
+    from oracle import vla_oracle as O
+    ctx = contextlib.nullcontext()
+    if threads is not None:
+        from threadpoolctl import threadpool_limits
+        ctx = threadpool_limits(limits=threads)
+    with ctx:
+        # untimed warm-up: starts the BLAS thread pool and touches the weights
+        O.denoise(cfg, W, O.prefix_kv_build(cfg, W, inp["prefix"]), inp["noise"], inp["state"],
+                  wl.uniform_schedule(1))
+        t0 = time.perf_counter()
+        cache = O.prefix_kv_build(cfg, W, inp["prefix"])
+        t_build = time.perf_counter() - t0
+        ts = {}
+        for T in ((1,) if cfg.head_regression else (1, 2)):
+            t0 = time.perf_counter()
+            O.denoise(cfg, W, cache, inp["noise"], inp["state"], wl.uniform_schedule(T))
+            ts[T] = time.perf_counter() - t0
+    step = ts[2] - ts[1] if 2 in ts else ts[1]
+    fixed = ts[1] - step if 2 in ts else 0.0
+    return t_build, max(fixed, 0.0), step
+
+
+def cpu_baseline(cfg, W, inp):
+    """The oracle timed on this host's cores on a bounded sample of the
+    headline workload (prefix K/V build + T = 1 and T = 2 denoise calls), all
+    BLAS threads and one; a chunk is build + fixed + T_cfg * step."""
+    env = cpu_env()
+    b, f, st = oracle_fit(cfg, W, inp)
+    chunk = b + f + cfg.n_steps * st
+    b1, f1, st1 = oracle_fit(cfg, W, inp, threads=1)
+    chunk1 = b1 + f1 + cfg.n_steps * st1
+    return {"value": round(1.0 / chunk, 5), "unit": "chunks/s", "cores": env["blas_threads"] or env["affinity"],
+            "kind": "oracle",
+            "sample": f"{cfg.name} batch 1: prefix K/V build + denoise at T = 1 and T = 2 (numpy fp64), "
+                      f"chunk = build + fixed + {cfg.n_steps} x step",
+            "step_s": round(st, 4), "build_s": round(b, 4), "chunk_s": round(chunk, 3),
+            "one_thread": {"chunks_per_s": round(1.0 / chunk1, 5), "step_s": round(st1, 4),
+                           "chunk_s": round(chunk1, 3)},
+            "env": env}
+
+
+def cpu_baseline_all():
+    """The oracle on every scope workload (tiny fp32, pi0-, SmolVLA-shaped,
+    ternary W2A8, stress batch 1), one BLAS thread and all: one JSON line each."""
+    import workloads as wl
+    env = cpu_env()
+    for name in ("tiny_f32", "pi0_bf16", "smolvla_bf16", "ternary_w2a8", "stress_pi0"):
+        cfg = wl.CONFIGS[name]
+        W = wl.make_weights(cfg)
+        inp = wl.make_batch(cfg, 1)
+        for threads in (None, 1):
+            b, f, st = oracle_fit(cfg, W, inp, threads)
+            chunk = b + f + cfg.n_steps * st
+            print(json.dumps({"cpu_oracle": name, "threads": threads or env["blas_threads"], "T": cfg.n_steps,
+                              "build_s": round(b, 4), "fixed_s": round(f, 4), "step_s": round(st, 4),
+                              "chunk_s": round(chunk, 3), "chunks_per_s": round(1.0 / chunk, 5),
+                              "env": env}), flush=True)
 
 
 def measure_workload(torch, wl, Pipeline, name, batch, reps, variant=None):
@@ -236,7 +319,7 @@ def ternary_ablation(iters: int = 50):
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
-    ap.add_argument("--steps", type=int, default=30, help="timed chunks")
+    ap.add_argument("--steps", type=int, default=200, help="timed chunks")
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-sweep", action="store_true",
@@ -256,11 +339,17 @@ def main():
     ap.add_argument("--variant", default="",
                     help="with --workloads: comma list of architecture variants applied to every "
                          "workload: state_token, causal_self, rope (base 10000)")
+    ap.add_argument("--cpu-baseline-all", action="store_true",
+                    help="instead of the headline line, time the CPU oracle on every scope workload with one "
+                         "BLAS thread and with all, one JSON line each (no GPU used)")
     ap.add_argument("--ternary-ablation", action="store_true",
                     help="instead of the headline line, time the W2A8 GEMM of the ternary model's projections "
                          "(M = 8 and 56) on the int8 MFMA kernel and on the VALU sdot4 kernel, one JSON line "
                          "per shape")
     args = ap.parse_args()
+    if args.cpu_baseline_all:
+        cpu_baseline_all()
+        return
     if args.ternary_ablation:
         ternary_ablation()
         return
@@ -331,6 +420,8 @@ def main():
     log("timed region ...")
     ms_chunk = time_chunks(torch, pipe, tau, args.steps)
     log(f"chunk {ms_chunk * 1000:.1f} us")
+    each = np.array(time_chunks_each(torch, pipe, tau, args.steps))
+    log(f"per-chunk events: median {np.median(each) * 1000:.1f} us, p95 {np.percentile(each, 95) * 1000:.1f} us")
 
     # per-solver-step latency: linear fit of denoise time over T
     Ts = [cfg.n_steps] if args.no_sweep else [1, 2, 5, cfg.n_steps]
@@ -345,6 +436,17 @@ def main():
     else:
         slope, intercept = float("nan"), float("nan")
     ms_build = time_chunks(torch, pipe, tau, 1) - ms_T[-1]
+
+    # cross-check of the per-step latency on the other driver: the same
+    # launches captured in a HIP graph, slope over T in {1, 2}
+    pipe.model.set_loop_mode(1)
+    ms_g = []
+    for T in (1, 2):
+        tT = wl.uniform_schedule(T)
+        for _ in range(3):
+            pipe.denoise(tT)
+        ms_g.append(min(time_denoise(torch, pipe, tT, 10) for _ in range(2)))
+    pipe.model.set_loop_mode(LOOP_MODE)
 
     # live per-launch timings: launch-per-phase driver, every launch repeated
     # PROFILE_REPS times between one HIP event pair on the plan's stream
@@ -373,7 +475,11 @@ def main():
                                "prefix 816 (width 2048), chunk 50x32, 10 Euler steps",
                    "batch": 1, "solver_steps": cfg.n_steps, "prefix_len": cfg.prefix_len, "chunk": cfg.n_action,
                    "parallelism": "single GPU"},
+        "chunk_us_median": round(float(np.median(each)) * 1000.0, 2),
+        "chunk_us_p95": round(float(np.percentile(each, 95)) * 1000.0, 2),
+        "chunks_timed_each": int(len(each)),
         "denoise_step_us": None if np.isnan(step_us) else round(step_us, 2),
+        "graph_driver_step_us": round((ms_g[1] - ms_g[0]) * 1000.0, 2),
         "chunk_fixed_us": None if np.isnan(intercept) else round(intercept * 1000.0, 2),
         "prefix_kv_build_us": round(ms_build * 1000.0, 2),
         "denoise_T_us": {str(T): round(v * 1000.0, 2) for T, v in zip(Ts, ms_T)},
@@ -385,7 +491,7 @@ def main():
     result["roofline"]["measured_hbm_copy_GBps"] = hbm_copy_rate(torch)
     if not args.no_cpu_baseline:
         log("cpu baseline (oracle) ...")
-        result["cpu_baseline"] = cpu_baseline(cfg, W, inp, tau)
+        result["cpu_baseline"] = cpu_baseline(cfg, W, inp)
     print(json.dumps(result), flush=True)
 
 
