@@ -364,6 +364,52 @@ def expert_forward(cfg, W, cache_b, a, s, t: float, prefix_b=None) -> np.ndarray
     return linear(ada_rms(x, gf, bf, eps), W["W_out"], W["b_out"])
 
 
+# --- the prefix stage: backbone prefill -------------------------------------------
+
+def backbone_layer(bcfg, Wb, l: int, x):
+    """One pre-norm backbone layer over the P prefix rows x [P][d]: the
+    attention sublayer, then the MLP sublayer, each added to the residual
+    stream.  Attention is bidirectional (every prefix row attends to every
+    other, no mask) with grouped K/V heads; with rope_base > 0 the queries and
+    keys of row i are rotated to position i.  Norms scale by (1 + g) with the
+    layer's learned gains g."""
+    p = f"B{l}."
+    P = x.shape[0]
+    H, G, hd, eps = bcfg.n_heads, bcfg.n_kv_heads, bcfg.head_dim, bcfg.rms_eps
+    u = ada_rms(x, Wb[p + "g_att"], 0.0, eps)
+    q = _lin(bcfg, Wb, p + "W_q", u)
+    k = _lin(bcfg, Wb, p + "W_k", u)
+    v = _lin(bcfg, Wb, p + "W_v", u)
+    if bcfg.rope_base > 0:
+        q = rope(q, np.arange(P), H, hd, bcfg.rope_base)
+        k = rope(k, np.arange(P), G, hd, bcfg.rope_base)
+    o = attention(q, split_heads(k, G, hd), split_heads(v, G, hd), H, G, hd)
+    x = x + _lin(bcfg, Wb, p + "W_o", o)
+    u = ada_rms(x, Wb[p + "g_mlp"], 0.0, eps)
+    if bcfg.mlp == "gelu":
+        y = _lin(bcfg, Wb, p + "W2", mlp_activation("gelu", _lin(bcfg, Wb, p + "W1", u)))
+    else:
+        h = mlp_activation(bcfg.mlp, _lin(bcfg, Wb, p + "W_g", u), _lin(bcfg, Wb, p + "W_u", u))
+        y = _lin(bcfg, Wb, p + "W_d", h)
+    return x + y
+
+
+def prefix_prefill(bcfg, Wb, embeds) -> np.ndarray:
+    """The prefix stage (Algorithm 1, h = VLM-Prefix(...), bidirectional): the
+    prefix token embeddings [B][P][d] pass through every backbone layer, and
+    the final-layer hidden states, after the final norm (the tensor a language
+    model feeds its output projection), are returned [B][P][d] in float64.
+    They are the cross-attention source of prefix_kv_build."""
+    e = np.asarray(embeds, dtype=F64)
+    out = np.zeros_like(e)
+    for b in range(e.shape[0]):
+        x = e[b]
+        for l in range(bcfg.n_layers):
+            x = backbone_layer(bcfg, Wb, l, x)
+        out[b] = ada_rms(x, Wb["g_f"], 0.0, bcfg.rms_eps)
+    return out
+
+
 def euler_integrate(velocity: Callable[[np.ndarray, int, float], np.ndarray], a0, tau) -> np.ndarray:
     """Explicit Euler from tau_0 to tau_T: a_{k+1} = a_k + (tau_{k+1} - tau_k) v(a_k, k, tau_k)."""
     a = np.asarray(a0, dtype=F64).copy()

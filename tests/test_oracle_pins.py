@@ -751,3 +751,105 @@ def test_sublayer_slot_order_single_active_sublayer(pattern, j):
     # than the tolerance above
     bm[(3 * j + 2) * d:(3 * j + 3) * d] = 0.0
     assert np.abs(O.expert_forward(cfg, W, cache[:, :, 0], a, s, 0.6) - got).max() > 1e-5
+
+
+# --- the prefix stage: backbone prefill ----------------------------------------------
+
+BB_TINY = wl.BackboneConfig(name="bb_tiny", n_layers=1, d_model=8, n_heads=2, head_dim=4, n_kv_heads=1,
+                            d_ff=12, mlp="geglu", wtype="bf16", rope_base=0.0, prefix_len=5, seed_base=91)
+
+
+def _bf_norm(rows, g, eps):
+    r = _bf_rows_rms(rows, eps)
+    return [[v / r[i] * (1.0 + float(g[c])) for c, v in enumerate(row)] for i, row in enumerate(rows)]
+
+
+def _bf_backbone(bcfg, W, x, rotate=False):
+    """Brute-force prefill of a one-layer bf16 backbone over rows x: norm,
+    bidirectional GQA attention (q, k optionally rotated to positions
+    0 .. P-1 by the pinned rope), residual, norm, GeGLU MLP, residual, final
+    norm."""
+    eps, H, G, hd = bcfg.rms_eps, bcfg.n_heads, bcfg.n_kv_heads, bcfg.head_dim
+    P = len(x)
+    u = _bf_norm(x, W["B0.g_att"], eps)
+    q, k, v = bf_linear(u, W["B0.W_q"]), bf_linear(u, W["B0.W_k"]), bf_linear(u, W["B0.W_v"])
+    if rotate:
+        q = O.rope(np.array(q), np.arange(P), H, hd, bcfg.rope_base).tolist()
+        k = O.rope(np.array(k), np.arange(P), G, hd, bcfg.rope_base).tolist()
+
+    def heads(rows):
+        return [[r[g * hd:(g + 1) * hd] for r in rows] for g in range(G)]
+    o = bf_attention(q, heads(k), heads(v), H, G, hd).tolist()
+    y = bf_linear(o, W["B0.W_o"])
+    x1 = [[x[i][c] + y[i][c] for c in range(len(x[0]))] for i in range(P)]
+    u2 = _bf_norm(x1, W["B0.g_mlp"], eps)
+    gt, up = bf_linear(u2, W["B0.W_g"]), bf_linear(u2, W["B0.W_u"])
+    h = [[_gelu_s(gt[i][f]) * up[i][f] for f in range(len(gt[0]))] for i in range(P)]
+    y2 = bf_linear(h, W["B0.W_d"])
+    x2 = [[x1[i][c] + y2[i][c] for c in range(len(x[0]))] for i in range(P)]
+    return np.array(_bf_norm(x2, W["g_f"], eps))
+
+
+@pytest.mark.parametrize("rotate", [False, True])
+def test_prefill_one_layer_bruteforce(rotate):
+    """One backbone layer by scalar loops (catches a missing residual, the norm
+    gain applied as g instead of 1 + g, a transposed projection, the gate and
+    up roles swapped, RoPE applied to the values or at wrong positions)."""
+    bcfg = BB_TINY.with_(rope_base=10000.0 if rotate else 0.0)
+    W = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, 2)
+    got = O.prefix_prefill(bcfg, W, e)
+    for b in range(2):
+        want = _bf_backbone(bcfg, W, e[b].astype(np.float64).tolist(), rotate)
+        np.testing.assert_allclose(got[b], want, rtol=1e-11, atol=1e-12)
+
+
+def test_prefill_zero_layers_and_zero_branches_are_the_final_norm():
+    """No layers, or every W_o and W_d zero: the prefill returns the final
+    norm of the embeddings, x / rms(x) (1 + g_f) (catches an extra term on the
+    residual stream)."""
+    bcfg = BB_TINY.with_(n_layers=2)
+    W = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, 1)
+    want = np.array(_bf_norm(e[0].astype(np.float64).tolist(), W["g_f"], bcfg.rms_eps))
+    np.testing.assert_allclose(O.prefix_prefill(bcfg.with_(n_layers=0), W, e)[0], want, rtol=1e-13)
+    for l in range(2):
+        W[f"B{l}.W_o"] = np.zeros_like(W[f"B{l}.W_o"])
+        W[f"B{l}.W_d"] = np.zeros_like(W[f"B{l}.W_d"])
+    np.testing.assert_allclose(O.prefix_prefill(bcfg, W, e)[0], want, rtol=1e-13)
+
+
+def test_prefill_is_bidirectional():
+    """Without positions the prefill is permutation-equivariant over the
+    prefix rows, and the first row's output depends on the last row's input
+    (a causal mask, the failure the paper's bidirectional prefix avoids,
+    breaks both)."""
+    bcfg = BB_TINY.with_(n_layers=2)
+    W = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, 1)
+    perm = _rng(70).permutation(bcfg.prefix_len)
+    a = O.prefix_prefill(bcfg, W, e)
+    np.testing.assert_allclose(O.prefix_prefill(bcfg, W, e[:, perm]), a[:, perm], rtol=1e-12, atol=1e-13)
+    e2 = e.copy()
+    e2[0, -1] += 1.0
+    assert np.abs(O.prefix_prefill(bcfg, W, e2)[0, 0] - a[0, 0]).max() > 1e-6
+    # with RoPE the rows carry positions: permuting them changes the result
+    r = bcfg.with_(rope_base=10000.0)
+    assert np.abs(O.prefix_prefill(r, W, e[:, perm]) - O.prefix_prefill(r, W, e)[:, perm]).max() > 1e-6
+
+
+def test_prefill_ternary_projections_use_their_scales():
+    """Ternary backbone: with the W_o and W_d scales at 0 every residual
+    branch vanishes (each projection is the W2A8 linear times its per-tensor
+    scale), leaving the final norm of the embeddings."""
+    bcfg = BB_TINY.with_(n_layers=2, wtype="ternary", mlp="relu2glu", d_model=16, d_ff=16)
+    W = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, 1)
+    assert W["B0.W_q"].dtype == np.int8 and "B0.W_q.scale" in W
+    full = O.prefix_prefill(bcfg, W, e)
+    for l in range(2):
+        W[f"B{l}.W_o.scale"] = np.float32(0.0)
+        W[f"B{l}.W_d.scale"] = np.float32(0.0)
+    want = np.array(_bf_norm(e[0].astype(np.float64).tolist(), W["g_f"], bcfg.rms_eps))
+    np.testing.assert_allclose(O.prefix_prefill(bcfg, W, e)[0], want, rtol=1e-13)
+    assert np.abs(full[0] - want).max() > 1e-4

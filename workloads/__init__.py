@@ -322,3 +322,101 @@ def random_ternary(shape, seed: int) -> np.ndarray:
 
 def random_int8(shape, seed: int) -> np.ndarray:
     return np.random.default_rng(seed).integers(-128, 128, size=shape, dtype=np.int64).astype(np.int8)
+
+
+# --- the vision-language backbone of the prefix (prefill) ---------------------
+
+@dataclasses.dataclass(frozen=True)
+class BackboneConfig:
+    """Language-model backbone that encodes the prefix tokens in one
+    bidirectional pass (the prefix stage of the paper's inference loop), plus
+    the workload it runs on."""
+    name: str
+    n_layers: int
+    d_model: int
+    n_heads: int
+    head_dim: int
+    n_kv_heads: int
+    d_ff: int
+    mlp: str               # "gelu" | "geglu" | "swiglu" | "relu2glu"
+    wtype: str             # "bf16" | "ternary"
+    rope_base: float = 10000.0   # rotary position embedding of q and k (0 = none)
+    rms_eps: float = 1e-6
+    prefix_len: int = 512
+    batch: int = 1
+    seed_base: int = 8000
+
+    @property
+    def d_q(self) -> int:
+        return self.n_heads * self.head_dim
+
+    @property
+    def d_kv(self) -> int:
+        return self.n_kv_heads * self.head_dim
+
+    def with_(self, **kw) -> "BackboneConfig":
+        return dataclasses.replace(self, **kw)
+
+
+# Gemma-2B-shaped bf16 backbone of the pi0-shaped workload (its 816 prefix
+# tokens: 3 x 256 image patches + 48 text tokens); width 2048 is the expert's d_p.
+PI0_VLM_BF16 = BackboneConfig(
+    name="pi0_vlm_bf16", n_layers=18, d_model=2048, n_heads=8, head_dim=256, n_kv_heads=1,
+    d_ff=16384, mlp="geglu", wtype="bf16", prefix_len=816, seed_base=8000)
+
+# BitNet-2B-shaped ternary backbone of the BitVLA-shaped workload: the paper's
+# 30-layer one-shot prefill, at the ternary expert's widths, over its 512-token prefix.
+BITNET_W2A8 = BackboneConfig(
+    name="bitnet_w2a8", n_layers=30, d_model=2560, n_heads=20, head_dim=128, n_kv_heads=5,
+    d_ff=6912, mlp="relu2glu", wtype="ternary", prefix_len=512, seed_base=9000)
+
+BACKBONES: Dict[str, BackboneConfig] = {c.name: c for c in (PI0_VLM_BF16, BITNET_W2A8)}
+
+
+def backbone_weight_names(bcfg: BackboneConfig) -> List[str]:
+    """Backbone weight names in the order of the C-ABI weight table."""
+    names = ["g_f"]
+    mats = ["W1", "W2"] if bcfg.mlp == "gelu" else ["W_g", "W_u", "W_d"]
+    for l in range(bcfg.n_layers):
+        p = f"B{l}."
+        names += [p + "g_att", p + "W_q", p + "W_k", p + "W_v", p + "W_o", p + "g_mlp"] + [p + m for m in mats]
+    return names
+
+
+def backbone_weight_shape(bcfg: BackboneConfig, name: str):
+    d, F = bcfg.d_model, bcfg.d_ff
+    return {"g_f": (d,), "g_att": (d,), "g_mlp": (d,),
+            "W_q": (bcfg.d_q, d), "W_k": (bcfg.d_kv, d), "W_v": (bcfg.d_kv, d), "W_o": (d, bcfg.d_q),
+            "W1": (F, d), "W2": (d, F), "W_g": (F, d), "W_u": (F, d), "W_d": (d, F)}[name.split(".")[-1]]
+
+
+def is_backbone_ternary(bcfg: BackboneConfig, name: str) -> bool:
+    return bcfg.wtype == "ternary" and name.split(".")[-1] in TERNARY_MATS
+
+
+def make_backbone_weights(bcfg: BackboneConfig, seed: int | None = None) -> Dict[str, np.ndarray]:
+    """Seeded random-init backbone weights: norm gains g N(0, 0.02^2) (the
+    norm scales by 1 + g), matrices N(0, 0.02^2) rounded to bf16, or ternary
+    codes with the per-tensor scale under name + ".scale"."""
+    rng = np.random.default_rng(bcfg.seed_base + 1 if seed is None else seed)
+    out: Dict[str, np.ndarray] = {}
+    for name in backbone_weight_names(bcfg):
+        shape = backbone_weight_shape(bcfg, name)
+        if is_backbone_ternary(bcfg, name):
+            out[name] = _ternary(rng, shape)
+            out[name + ".scale"] = np.float32(TERNARY_SCALE)
+        elif len(shape) == 1:
+            out[name] = _normal(rng, shape, 0.02)
+        else:
+            out[name] = round_bf16(_normal(rng, shape, 0.02))
+    return out
+
+
+def make_prefix_embeds(bcfg: BackboneConfig, batch: int | None = None) -> np.ndarray:
+    """Seeded prefix token embeddings [B][P][d], N(0, 1) rounded to bf16: the
+    stand-in for the vision encoder's patch tokens and the text embeddings.
+    Request r draws from seed_base + 2 + 10 r."""
+    b = bcfg.batch if batch is None else batch
+    rows = [np.random.default_rng(bcfg.seed_base + 2 + 10 * r).standard_normal(
+        size=(bcfg.prefix_len, bcfg.d_model)).astype(np.float32) for r in range(b)]
+    return round_bf16(np.stack(rows))
