@@ -281,6 +281,98 @@ def measure_workload(torch, wl, Pipeline, name, batch, reps, variant=None):
             "dominant_frac_hbm": roof["frac"], "dominant_share": roof["share_of_profiled_time"]}
 
 
+INT8_PEAK_TOPS = 5000.0       # dense int8 MFMA
+
+
+def prefill_work(bcfg, P):
+    """Algorithmic work of one request's prefill: (GEMM ops, attention flops,
+    weight bytes).  GEMM ops are int8 for a W2A8 backbone, bf16 flops else."""
+    d, dq, dkv, F = bcfg.d_model, bcfg.d_q, bcfg.d_kv, bcfg.d_ff
+    per_layer = d * (dq + 2 * dkv) + dq * d + (1 if bcfg.mlp == "gelu" else 2) * F * d + F * d
+    gemm = 2.0 * P * per_layer * bcfg.n_layers
+    attn = 4.0 * P * P * bcfg.n_heads * bcfg.head_dim * bcfg.n_layers
+    wbytes = per_layer * bcfg.n_layers * (0.25 if bcfg.wtype == "ternary" else 2.0)
+    return gemm, attn, wbytes
+
+
+def measure_prefill(torch, name, reps):
+    """The backbone's prefill of one request (event-timed, median of reps),
+    against the matrix-core peak of its GEMMs' element type."""
+    import numpy as np
+    import workloads as wl
+    from vla_testlib import Prefill
+    bcfg = wl.BACKBONES[name]
+    log(f"prefill {name}: generating weights ...")
+    Wb = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, 1)
+    pre = Prefill(bcfg, Wb, e)
+    try:
+        for _ in range(2):
+            pre.run()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            pre.run()
+            b.record()
+            ts.append((a, b))
+        torch.cuda.synchronize()
+        ms = float(np.median([a.elapsed_time(b) for a, b in ts]))
+    finally:
+        pre.close()
+    gemm, attn, wbytes = prefill_work(bcfg, bcfg.prefix_len)
+    tern = bcfg.wtype == "ternary"
+    sec = ms * 1e-3
+    out = {"prefill": name, "layers": bcfg.n_layers, "prefix_len": bcfg.prefix_len, "d_model": bcfg.d_model,
+           "wtype": bcfg.wtype, "ms": round(ms, 4), "gemm_ops": gemm, "attn_flops": attn,
+           "weight_bytes": int(wbytes)}
+    if tern:
+        # int8 matrix-core ops of the W2A8 GEMMs plus the bf16 attention, each
+        # against its own peak: the time the two would take at peak
+        ideal = gemm / (INT8_PEAK_TOPS * 1e12) + attn / (BF16_PEAK_TFLOPS * 1e12)
+        out.update({"int8_tops_if_all_time": round(gemm / sec / 1e12, 1), "mfma_frac": round(ideal / sec, 4),
+                    "peak": "int8 5.0 POP/s (GEMMs) + bf16 2.5 PFLOP/s (attention)"})
+    else:
+        out.update({"tflops": round((gemm + attn) / sec / 1e12, 1),
+                    "mfma_frac": round((gemm + attn) / sec / 1e12 / BF16_PEAK_TFLOPS, 4),
+                    "peak": "bf16 2.5 PFLOP/s"})
+    return out
+
+
+def measure_observation(torch, reps):
+    """The whole pi0-shaped observation path of one request: backbone prefill
+    (816 rows), cross K/V build, denoise at T = 10 (event-timed, median)."""
+    import numpy as np
+    import workloads as wl
+    from vla_testlib import Pipeline, Prefill
+    bcfg, cfg = wl.PI0_VLM_BF16, wl.PI0_BF16
+    log("observation path: generating weights ...")
+    pre = Prefill(bcfg, wl.make_backbone_weights(bcfg), wl.make_prefix_embeds(bcfg, 1))
+    pipe = Pipeline(cfg, wl.make_weights(cfg), wl.make_batch(cfg, 1), loop_mode=LOOP_MODE)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    try:
+        def once():
+            h = pre.run()
+            pipe.model.prefix_kv_build(h, 1, bcfg.prefix_len, pipe.cache, pipe.cache_bytes)
+            pipe.denoise(tau)
+        for _ in range(2):
+            once()
+        ts = []
+        for _ in range(reps):
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            once()
+            b.record()
+            ts.append((a, b))
+        torch.cuda.synchronize()
+        ms = float(np.median([a.elapsed_time(b) for a, b in ts]))
+    finally:
+        pipe.close()
+        pre.close()
+    return {"observation_path": "pi0: Gemma-2B-shaped prefill (816 rows) + cross K/V + 10 Euler steps",
+            "ms": round(ms, 3), "observations_per_s": round(1000.0 / ms, 2)}
+
+
 def ternary_ablation(iters: int = 50):
     """The paper's dot4-versus-matrix-unit question for the ternary GEMM (Sec. 4.5) on MI355X:
     the same int8 codes and packed 2-bit weights through v_mfma_i32_16x16x64_i8 and through
@@ -339,6 +431,10 @@ def main():
     ap.add_argument("--variant", default="",
                     help="with --workloads: comma list of architecture variants applied to every "
                          "workload: state_token, causal_self, rope (base 10000)")
+    ap.add_argument("--prefill", action="store_true",
+                    help="instead of the headline line, time the prefix stage: the Gemma-2B-shaped bf16 and the "
+                         "BitNet-2B-shaped W2A8 backbone prefills and the whole pi0-shaped observation path, one "
+                         "JSON line each")
     ap.add_argument("--cpu-baseline-all", action="store_true",
                     help="instead of the headline line, time the CPU oracle on every scope workload with one "
                          "BLAS thread and with all, one JSON line each (no GPU used)")
@@ -375,6 +471,11 @@ def main():
     import workloads as wl
     from vla_testlib import Pipeline
 
+    if args.prefill:
+        for name in ("pi0_vlm_bf16", "bitnet_w2a8"):
+            print(json.dumps(measure_prefill(torch, name, 10)), flush=True)
+        print(json.dumps(measure_observation(torch, 10)), flush=True)
+        return
     if args.workloads:
         todo = (("smolvla_bf16", 1), ("ternary_w2a8", 1), ("stress_pi0", 1), ("stress_pi0", 4), ("stress_pi0", 16),
                 ("gr00t_alt_bf16", 1), ("evo1_cross_bf16", 1))

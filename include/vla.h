@@ -239,6 +239,65 @@ typedef struct vla_op_time {
  * launches of that call, or -1 if nothing was profiled. */
 int32_t vla_profile_read(vla_model* model, vla_op_time* out, int32_t max_ops);
 
+/* ---- The prefix stage: backbone prefill --------------------------------------
+ * The vision-language backbone encodes the prefix tokens in one bidirectional
+ * pass (Algorithm 1: h = VLM-Prefix(I, l, s); Sec. 3.1: the prefix stage is
+ * compute-bound like LLM prefill), and its final-layer hidden states, taken
+ * before the output projection, are the cross-attention source that
+ * vla_prefix_kv_build projects (App. A.2 items 1 and 2: full hidden states, a
+ * bidirectional mask so that every prefix token attends to every other).
+ * The paper gives no layer equations; this library's layer is a pre-norm
+ * transformer layer:
+ *   x += W_o Attn(RMS(x)(1 + g_att))   (bidirectional, GQA, RoPE on q and k)
+ *   x += MLP(RMS(x)(1 + g_mlp))        (vla_mlp forms, as in the expert)
+ * and the output is RMS(x)(1 + g_f), RMS(x) = x / sqrt(mean(x^2) + rms_eps).
+ * With VLA_W_TERNARY every projection is the W2A8 linear of vla_model_create
+ * (per-token int8 activations, packed 2-bit weights, int8 matrix cores). */
+typedef struct vla_backbone_config {
+  int32_t n_layers;        /* L */
+  int32_t d_model;         /* d (multiple of 8, of 64 for ternary; <= 4096) */
+  int32_t n_heads;         /* H */
+  int32_t head_dim;        /* 64, 128 or 256 */
+  int32_t n_kv_heads;      /* G (H % G == 0, H / G <= 8) */
+  int32_t d_ff;            /* F */
+  int32_t mlp;             /* vla_mlp */
+  int32_t wtype;           /* VLA_W_BF16 or VLA_W_TERNARY */
+  float rope_base;         /* > 1: rotate-half RoPE of q and k, row p of a request at position p; 0: none */
+  float rms_eps;
+} vla_backbone_config;
+
+typedef struct vla_backbone vla_backbone; /* opaque */
+
+/* Entries vla_backbone_create expects, or -1 for an invalid config. */
+int32_t vla_backbone_weight_count(const vla_backbone_config* cfg);
+
+/*
+ * Create a backbone from a table of device pointers (copied into library
+ * memory; the caller may free its buffers once this returns).  Synchronous.
+ * Order: g_f [d] fp32; then per layer g_att [d] fp32, W_q [H*hd][d],
+ * W_k [G*hd][d], W_v [G*hd][d], W_o [d][H*hd], g_mlp [d] fp32, then
+ * W1 [F][d], W2 [d][F] (GELU) or W_g, W_u [F][d], W_d [d][F].  Matrices are
+ * bf16 [out][in], or with VLA_W_TERNARY packed 2-bit [N][K/4] each followed
+ * by a pointer to its fp32 per-tensor scale (the layout of vla_model_create).
+ * Errors: VLA_E_ARG, VLA_E_SHAPE, VLA_E_UNSUPPORTED, VLA_E_NOMEM, VLA_E_DEVICE.
+ */
+vla_status vla_backbone_create(const vla_backbone_config* cfg, const void* const* weights, int32_t n_weights,
+                               vla_backbone** out);
+void vla_backbone_destroy(vla_backbone* backbone);
+
+/*
+ * Prefill: embeds [batch][prefix_len][d] bf16 (the prefix token embeddings:
+ * vision-encoder patches, text, state) -> hidden_out [batch][prefix_len][d]
+ * bf16, the final-layer hidden states after the final norm, ready for
+ * vla_prefix_kv_build of an expert with d_prefix = d.  Requests are
+ * independent; rows of one request attend to each other bidirectionally.
+ * The workspace for (batch, prefix_len) is allocated by the first call of
+ * that shape and kept by the backbone.  batch * prefix_len <= 65536.
+ * Errors: VLA_E_ARG, VLA_E_SHAPE, VLA_E_UNSUPPORTED, VLA_E_NOMEM, VLA_E_DEVICE.
+ */
+vla_status vla_prefix_prefill(vla_backbone* backbone, const void* embeds, int32_t batch, int32_t prefix_len,
+                              void* hidden_out, void* stream);
+
 /* Thread-local message for the last non-OK status of this thread. */
 const char* vla_last_error(void);
 const char* vla_status_string(int32_t status);

@@ -28,8 +28,8 @@ __global__ __launch_bounds__(256) void init_chunk_kernel(const CallParams* cp, f
 }
 
 // One workgroup per token row: finish the residual stream x (add the split-K
-// partials of a residual projection, or form the input embedding) and write
-// the next sublayer's adaRMS input u.  A thread owns the columns
+// partials of a residual projection, form the input embedding, or take the
+// backbone's input rows) and write the next sublayer's adaRMS input u.  A thread owns the columns
 // 4*(tid + 256*i); all of its loads are issued before the row reduction.
 template <typename T>
 __global__ __launch_bounds__(256) void row_norm_kernel(RowNormArgs a) {
@@ -78,6 +78,15 @@ __global__ __launch_bounds__(256) void row_norm_kernel(RowNormArgs a) {
         xv[i].x += al[i].x * ps[i].x; xv[i].y += al[i].y * ps[i].y;
         xv[i].z += al[i].z * ps[i].z; xv[i].w += al[i].w * ps[i].w;
       }
+    }
+  } else if (a.mode == 2) {
+    const T* xr = reinterpret_cast<const T*>(a.x_in) + (size_t)m * d;
+#pragma unroll
+    for (int i = 0; i < CPT; ++i) {
+      const int c = 4 * (t + 256 * i);
+      xv[i] = c < d ? make_float4(ElemTraits<T>::to_f(xr[c]), ElemTraits<T>::to_f(xr[c + 1]),
+                                  ElemTraits<T>::to_f(xr[c + 2]), ElemTraits<T>::to_f(xr[c + 3]))
+                    : make_float4(0.f, 0.f, 0.f, 0.f);
     }
   } else {
     const int b = m / a.n, tok = m - b * a.n;

@@ -1226,6 +1226,19 @@ vla_status vla_model_create(const vla_config* cfg, const void* const* weights, i
 
 // RoPE variant: the cached K of every joint layer holds prefix row p at
 // position p (cache block [2][B][G][P][hd], K first).
+static vla_status check_prefix_args(vla_model* m, const void* prefix_hidden, int batch, int prefix_len,
+                                    const void* kv_cache, size_t kv_cache_bytes) {
+  if (!m) return fail(VLA_E_ARG, "model is NULL");
+  if (!prefix_hidden || !kv_cache) return fail(VLA_E_ARG, "prefix_hidden / kv_cache is NULL");
+  if (!al16(prefix_hidden) || !al16(kv_cache)) return fail(VLA_E_ARG, "buffers must be 16-byte aligned");
+  if (batch < 1 || prefix_len < 1) return fail(VLA_E_SHAPE, "batch and prefix_len must be >= 1");
+  if ((long long)batch * prefix_len > (1LL << 24)) return fail(VLA_E_UNSUPPORTED, "batch * prefix_len too large");
+  if (kv_cache_bytes != vla_kv_cache_bytes(m, batch, prefix_len))
+    return fail(VLA_E_SHAPE, "kv_cache_bytes %zu != %zu for batch %d, prefix_len %d", kv_cache_bytes,
+                vla_kv_cache_bytes(m, batch, prefix_len), batch, prefix_len);
+  return VLA_OK;
+}
+
 static vla_status rope_prefix(vla_model* m, void* kv_cache, int batch, int prefix_len, size_t layer_block,
                               hipStream_t s) {
   if (m->rope_base <= 0.0f) return VLA_OK;
@@ -1240,27 +1253,17 @@ static vla_status rope_prefix(vla_model* m, void* kv_cache, int batch, int prefi
   return VLA_OK;
 }
 
-extern "C" {
-
-vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t batch, int32_t prefix_len,
-                               void* kv_cache, size_t kv_cache_bytes, void* stream) {
-  if (!m) return fail(VLA_E_ARG, "model is NULL");
-  if (!prefix_hidden || !kv_cache) return fail(VLA_E_ARG, "prefix_hidden / kv_cache is NULL");
-  if (!al16(prefix_hidden) || !al16(kv_cache)) return fail(VLA_E_ARG, "buffers must be 16-byte aligned");
-  if (batch < 1 || prefix_len < 1) return fail(VLA_E_SHAPE, "batch and prefix_len must be >= 1");
-  if ((long long)batch * prefix_len > (1LL << 24)) return fail(VLA_E_UNSUPPORTED, "batch * prefix_len too large");
-  if (kv_cache_bytes != vla_kv_cache_bytes(m, batch, prefix_len))
-    return fail(VLA_E_SHAPE, "kv_cache_bytes %zu != %zu for batch %d, prefix_len %d", kv_cache_bytes,
-                vla_kv_cache_bytes(m, batch, prefix_len), batch, prefix_len);
-  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
-  PrefixWs* w = nullptr;
-  VLA_TRY(get_prefix_ws(m, batch, prefix_len, &w));
+// The prefix build proper: quantise the prefix rows into (q8, r8) for W2A8
+// models, then one GEMM over every layer's stacked cross K/V weights (dense)
+// or one W2A8 GEMM per layer, with the cache-slot epilogue; RoPE variant last.
+static vla_status prefix_kv_build_impl(vla_model* m, const void* prefix_hidden, int batch, int prefix_len,
+                                       void* kv_cache, int8_t* q8, float* r8, hipStream_t s) {
   const int M = batch * prefix_len, N = 2 * m->dkv, K = m->cfg.d_prefix, hd = m->cfg.head_dim;
   const size_t layer_block = (size_t)2 * batch * m->cfg.n_kv_heads * prefix_len * hd;
   const size_t es = esize(m->et);
   if (m->tern) {
     QuantArgs q{};
-    q.M = M; q.K = K; q.x = prefix_hidden; q.ldx = K; q.src_type = 1; q.q = w->q8; q.r = w->r8;
+    q.M = M; q.K = K; q.x = prefix_hidden; q.ldx = K; q.src_type = 1; q.q = q8; q.r = r8;
     HIP_TRY(launch_quantize(q, s));
   }
   if (m->kvc_all) {
@@ -1288,12 +1291,23 @@ vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t 
       } else {
         TernArgs ta{};
         const Tiling t = tern_tiling(M, N, K, 1);
-        ta.M = M; ta.N = N; ta.K = K; ta.x = w->q8; ta.w = (const uint8_t*)sw.kvc; ta.rscale = w->r8;
+        ta.M = M; ta.N = N; ta.K = K; ta.x = q8; ta.w = (const uint8_t*)sw.kvc; ta.rscale = r8;
         ta.wscale = sw.s_kvc; ta.ks = t.nc * 256; ta.nsplit = 1; ta.n_tiles = t.n_tiles; ta.e = g;
         HIP_TRY(launch_ternary_gemm(ta, t.ms, t.units, s));
       }
     }
   return rope_prefix(m, kv_cache, batch, prefix_len, layer_block, s);
+}
+
+extern "C" {
+
+vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t batch, int32_t prefix_len,
+                               void* kv_cache, size_t kv_cache_bytes, void* stream) {
+  VLA_TRY(check_prefix_args(m, prefix_hidden, batch, prefix_len, kv_cache, kv_cache_bytes));
+  PrefixWs* w = nullptr;
+  VLA_TRY(get_prefix_ws(m, batch, prefix_len, &w));
+  return prefix_kv_build_impl(m, prefix_hidden, batch, prefix_len, kv_cache, w->q8, w->r8,
+                              reinterpret_cast<hipStream_t>(stream));
 }
 
 vla_status vla_denoise(vla_model* m, const void* kv_cache, size_t kv_cache_bytes, int32_t batch, int32_t prefix_len,
@@ -1689,6 +1703,440 @@ vla_status vla_test_rope(int32_t elem, void* x, int32_t rows, int32_t rows_per_r
   hipError_t e2 = hipStreamSynchronize(s);
   if (e != hipSuccess || e2 != hipSuccess)
     return fail(VLA_E_DEVICE, "rope: %s", hipGetErrorString(e != hipSuccess ? e : e2));
+  return VLA_OK;
+}
+
+}  // extern "C"
+
+// ----------------------------------------------------------------------------
+// The prefix stage: a vision-language backbone's prefill (Algorithm 1's
+// h = VLM-Prefix(...), one bidirectional pass over the prefix tokens; App. A.2
+// items 1-2: the final-layer hidden states before the output projection are
+// the cross-attention source).  A backbone layer is a self-attention sublayer
+// and an MLP sublayer with pre-norms, so it is held as a vla_model of such
+// layers whose static modulation table carries the norm gains as
+// (gamma = g, beta = 0, alpha = 1); the prefill runs the expert's kernels at
+// M = B * P token rows.
+
+namespace {
+
+struct PrefillPlan {
+  int B = 0, P = 0;
+  std::vector<void*> allocs;
+  CallParams* cp = nullptr;     // a valid parameter block for the attention launches (no cache is read)
+  float* x = nullptr;           // residual stream [M][d] fp32
+  void* u = nullptr;            // norm output [M][d] (fp32 for W2A8 backbones)
+  void *qkv = nullptr, *o = nullptr, *h = nullptr;
+  float* part = nullptr;        // split-K partials of the residual projections
+  void* apart = nullptr;        // attention key-split partials
+  float* astats = nullptr;
+  int8_t* q8 = nullptr;
+  float* r8 = nullptr;
+  const void* embeds = nullptr;  // this call's input rows
+  void* out = nullptr;           // this call's output rows
+  std::vector<Op> ops;
+  ~PrefillPlan() {
+    for (void* p : allocs) (void)hipFree(p);
+  }
+};
+
+vla_status validate_backbone(const vla_backbone_config* c) {
+  if (!c) return fail(VLA_E_ARG, "config is NULL");
+  if (c->mlp < 0 || c->mlp > 3) return fail(VLA_E_ARG, "mlp %d out of range", c->mlp);
+  if (c->wtype != VLA_W_BF16 && c->wtype != VLA_W_TERNARY)
+    return fail(VLA_E_UNSUPPORTED, "backbone wtype must be VLA_W_BF16 or VLA_W_TERNARY");
+  if (c->n_layers < 1 || c->d_model < 8 || c->n_heads < 1 || c->n_kv_heads < 1 || c->d_ff < 16)
+    return fail(VLA_E_SHAPE, "non-positive dimension in backbone config");
+  if (c->n_heads % c->n_kv_heads) return fail(VLA_E_SHAPE, "n_heads %% n_kv_heads != 0");
+  if (!(c->head_dim == 64 || c->head_dim == 128 || c->head_dim == 256))
+    return fail(VLA_E_UNSUPPORTED, "head_dim %d unsupported (64, 128, 256)", c->head_dim);
+  const int m = c->wtype == VLA_W_TERNARY ? 64 : 8;
+  if (c->d_model % m || (c->n_heads * c->head_dim) % m || c->d_ff % (m > 16 ? m : 16))
+    return fail(VLA_E_SHAPE, "d_model and H*hd must be multiples of %d, d_ff of %d", m, m > 16 ? m : 16);
+  if (c->d_model > 4096) return fail(VLA_E_UNSUPPORTED, "d_model > 4096");
+  if (c->n_heads / c->n_kv_heads > 8 || c->n_heads > 32)
+    return fail(VLA_E_UNSUPPORTED, "more than 8 query heads per K/V head or more than 32 heads");
+  if (c->d_ff > 65536) return fail(VLA_E_UNSUPPORTED, "d_ff > 65536");
+  if (!std::isfinite(c->rope_base) || (c->rope_base != 0.0f && !(c->rope_base > 1.0f)))
+    return fail(VLA_E_ARG, "rope_base must be 0 or > 1");
+  if (!(c->rms_eps > 0.0f) || !std::isfinite(c->rms_eps)) return fail(VLA_E_ARG, "rms_eps must be finite and > 0");
+  return VLA_OK;
+}
+
+int backbone_weight_count(const vla_backbone_config& c) {
+  const int mats = 4 + (c.mlp == VLA_MLP_GELU ? 2 : 3);
+  return 1 + c.n_layers * (2 + mats * (c.wtype == VLA_W_TERNARY ? 2 : 1));
+}
+
+}  // namespace
+
+struct vla_backbone {
+  vla_backbone_config cfg{};
+  std::unique_ptr<vla_model> m;
+  std::map<std::pair<int, int>, std::unique_ptr<PrefillPlan>> plans;
+  ~vla_backbone() {
+    plans.clear();
+    m.reset();
+  }
+};
+
+namespace {
+
+vla_status backbone_create_impl(const vla_backbone_config* bc, const void* const* weights, int32_t n_weights,
+                                vla_backbone** out) {
+  std::unique_ptr<vla_backbone> bb(new vla_backbone());
+  bb->cfg = *bc;
+  bb->m.reset(new vla_model());
+  vla_model* m = bb->m.get();
+  vla_config& c = m->cfg;
+  c.n_layers = bc->n_layers;
+  c.d_model = bc->d_model;
+  c.n_heads = bc->n_heads;
+  c.head_dim = bc->head_dim;
+  c.n_kv_heads = bc->n_kv_heads;
+  c.d_ff = bc->d_ff;
+  c.mlp = bc->mlp;
+  c.wtype = bc->wtype;
+  c.rms_eps = bc->rms_eps;
+  c.head_regression = 1;      // static modulation, no time input
+  m->tern = bc->wtype == VLA_W_TERNARY;
+  m->et = ET_BF16;
+  m->d = bc->d_model;
+  m->dq = bc->n_heads * bc->head_dim;
+  m->dkv = bc->n_kv_heads * bc->head_dim;
+  m->ns = 2;
+  const int d = m->d, F = bc->d_ff, L = bc->n_layers, dq = m->dq, dkv = m->dkv;
+  TableReader tr{weights, n_weights};
+  const void* p;
+  // norm gains as the static modulation table [L][2][3][d] = (g, 0, 1) per
+  // sublayer, the final one as [2][d] = (g_f, 0)
+  std::vector<float> tab((size_t)L * 2 * 3 * d, 0.0f), fin((size_t)2 * d, 0.0f);
+  auto gain = [&](const char* what, float* dst) -> vla_status {
+    VLA_TRY(tr.next(&p, what));
+    HIP_TRY(hipMemcpy(dst, p, (size_t)d * 4, hipMemcpyDeviceToHost));
+    for (int i = 0; i < d; ++i)
+      if (!std::isfinite(dst[i])) return fail(VLA_E_ARG, "norm gain %s is not finite", what);
+    return VLA_OK;
+  };
+  auto mat = [&](const char* what, const void** src, float* scale) -> vla_status {
+    VLA_TRY(tr.next(src, what));
+    *scale = 1.0f;
+    if (!m->tern) return VLA_OK;
+    const void* sp;
+    VLA_TRY(tr.next(&sp, "ternary scale"));
+    vla_status st = VLA_OK;
+    *scale = read_scale(sp, &st);
+    return st;
+  };
+  VLA_TRY(gain("g_f", fin.data()));
+  m->layers.resize(L);
+  for (int l = 0; l < L; ++l) {
+    float* row = tab.data() + (size_t)l * 2 * 3 * d;
+    VLA_TRY(gain("g_att", row));
+    for (int i = 0; i < d; ++i) row[2 * d + i] = 1.0f;
+    SubW at;
+    at.kind = K_SELF;
+    const void *wq, *wk, *wv, *wo;
+    float sq, sk, sv, so;
+    VLA_TRY(mat("W_q", &wq, &sq));
+    VLA_TRY(mat("W_k", &wk, &sk));
+    VLA_TRY(mat("W_v", &wv, &sv));
+    VLA_TRY(mat("W_o", &wo, &so));
+    at.n_qkv = dq + 2 * dkv;
+    VLA_TRY(fuse(m, &at.qkv, &at.s_qkv, {{wq, dq, sq}, {wk, dkv, sk}, {wv, dkv, sv}}, d, false));
+    VLA_TRY(fuse(m, &at.o, &at.s_o, {{wo, d, so}}, dq, false));
+    VLA_TRY(gain("g_mlp", row + 3 * d));
+    for (int i = 0; i < d; ++i) row[5 * d + i] = 1.0f;
+    SubW ml;
+    ml.kind = K_MLP;
+    if (bc->mlp == VLA_MLP_GELU) {
+      const void *w1, *w2;
+      float s1, s2;
+      VLA_TRY(mat("W1", &w1, &s1));
+      VLA_TRY(mat("W2", &w2, &s2));
+      VLA_TRY(fuse(m, &ml.gu, &ml.s_gu, {{w1, F, s1}}, d, false));
+      VLA_TRY(fuse(m, &ml.dn, &ml.s_dn, {{w2, d, s2}}, F, false));
+    } else {
+      const void *wg, *wu, *wd;
+      float sg, su, sd;
+      VLA_TRY(mat("W_g", &wg, &sg));
+      VLA_TRY(mat("W_u", &wu, &su));
+      VLA_TRY(mat("W_d", &wd, &sd));
+      VLA_TRY(fuse(m, &ml.gu, &ml.s_gu, {{wg, F, sg}, {wu, F, su}}, d, true));
+      VLA_TRY(fuse(m, &ml.dn, &ml.s_dn, {{wd, d, sd}}, F, false));
+    }
+    m->layers[l] = {at, ml};
+  }
+  if (tr.i != n_weights) return fail(VLA_E_ARG, "weight table has %d entries, expected %d", n_weights, tr.i);
+  Alloc al{m->allocs};
+  VLA_TRY(al((void**)&m->mod_static, tab.size() * 4));
+  HIP_TRY(hipMemcpy(m->mod_static, tab.data(), tab.size() * 4, hipMemcpyHostToDevice));
+  VLA_TRY(al((void**)&m->modf_static, fin.size() * 4));
+  HIP_TRY(hipMemcpy(m->modf_static, fin.data(), fin.size() * 4, hipMemcpyHostToDevice));
+  HIP_TRY(hipDeviceSynchronize());
+  *out = bb.release();
+  return VLA_OK;
+}
+
+vla_status build_prefill_plan(vla_backbone* bb, PrefillPlan* p) {
+  vla_model* m = bb->m.get();
+  const vla_backbone_config& bc = bb->cfg;
+  const int B = p->B, P = p->P, M = B * P, d = m->d, dq = m->dq, dkv = m->dkv, F = bc.d_ff, L = bc.n_layers;
+  const int H = bc.n_heads, G = bc.n_kv_heads, hd = bc.head_dim, nqkv = dq + 2 * dkv;
+  const int et = m->et;
+  const size_t es = esize(et);
+  const bool tern = m->tern;
+  const bool glu = bc.mlp != VLA_MLP_GELU;
+  Alloc al{p->allocs};
+  VLA_TRY(al((void**)&p->cp, sizeof(CallParams)));
+  HIP_TRY(hipMemset(p->cp, 0, sizeof(CallParams)));
+  VLA_TRY(al((void**)&p->x, (size_t)M * d * 4));
+  VLA_TRY(al(&p->u, (size_t)M * d * (tern ? 4 : es)));
+  VLA_TRY(al(&p->qkv, (size_t)M * nqkv * es));
+  VLA_TRY(al(&p->o, (size_t)M * dq * es));
+  VLA_TRY(al(&p->h, (size_t)M * F * (tern ? 4 : es)));
+  if (tern) {
+    VLA_TRY(al((void**)&p->q8, (size_t)M * std::max(std::max(d, dq), F)));
+    VLA_TRY(al((void**)&p->r8, (size_t)M * 4));
+  }
+  Builder bld{m, &p->ops, &p->apart, &p->astats};
+  const size_t modrow = (size_t)2 * 3 * d;
+  auto gam = [&](int l, int j) { return m->mod_static + (size_t)l * modrow + (size_t)j * 3 * d; };
+  size_t part_need = 0;
+  PrefillPlan* pp = p;
+  float** partp = &p->part;
+
+  {  // the residual stream starts as the input rows; first norm
+    RowNormArgs r{};
+    r.mode = 2; r.M = M; r.d = d; r.x = p->x; r.gamma = gam(0, 0); r.beta = gam(0, 0) + d; r.eps = bc.rms_eps;
+    r.u = p->u; r.u_f32 = tern ? 1 : 0;
+    if (tern) {
+      r.q = p->q8;
+      r.qr = p->r8;
+    }
+    bld.ops->push_back(Op{[=](hipStream_t s) {
+                            RowNormArgs q = r;
+                            q.x_in = pp->embeds;
+                            return launch_row_norm(et, q, s);
+                          },
+                          op_info(VLA_OP_SMALL, M, d, 0, (double)M * d * (es + 4.0 + (tern ? 5.0 : es)), 0.0)});
+  }
+  // residual projection of a dense backbone: split-K partials summed by the
+  // following row kernel, or the residual update in the GEMM's epilogue
+  auto resid_gemm = [&](GemmArgs g, const float* alp, RowNormArgs& rn) {
+    g.epi = EPI_PARTIAL;
+    const DenseLaunch dl = dense_launch(et, g, 1);
+    if (dl.skinny || (dl.tile && dl.tl.nsplit > 1)) {
+      g.out = nullptr;
+      g.ldo = d;
+      part_need = std::max(part_need, (size_t)dl.splits() * M * d);
+      const GemmArgs gg = g;
+      const double bytes = (double)g.N * g.K * es + (double)g.M * g.K * es + 4.0 * dl.splits() * g.M * g.N;
+      bld.ops->push_back(Op{[=](hipStream_t s) {
+                              GemmArgs q = gg;
+                              q.out = *partp;
+                              return launch_dense(et, dl, q, s);
+                            },
+                            op_info(VLA_OP_GEMM, g.M, g.N, g.K, bytes, 2.0 * g.M * g.N * g.K)});
+      rn.nsplit = dl.splits();
+      rn.alpha = alp;
+    } else {
+      g.epi = EPI_RESID;
+      g.xres = p->x;
+      g.ldxr = d;
+      g.alpha = alp;
+      bld.gemm(g, 1);
+      rn.nsplit = 0;
+      rn.alpha = nullptr;
+    }
+  };
+  auto tern_resid = [&](const SubW& sw, const void* W, const float* ws, int K, const float* alp) {
+    TernArgs t{};
+    t.M = M; t.N = d; t.K = K; t.x = p->q8; t.w = (const uint8_t*)W; t.rscale = p->r8; t.wscale = ws;
+    t.e = gemm_base(m, M, d, K, nullptr, 0, nullptr);
+    t.e.epi = EPI_RESID;
+    t.e.xres = p->x;
+    t.e.ldxr = d;
+    t.e.alpha = alp;
+    bld.tern(t, 1);
+    (void)sw;
+  };
+  // row kernel finishing a residual update and normalising for what follows;
+  // after the last layer it writes the final norm into the call's output
+  auto norm_op = [&](RowNormArgs nr, bool final_out) {
+    const double bytes = (double)M * d * (8.0 + 4.0 * nr.nsplit + (nr.u_f32 ? 4.0 : es));
+    bld.ops->push_back(Op{[=](hipStream_t s) {
+                            RowNormArgs r = nr;
+                            r.part = *partp;
+                            if (final_out) r.u = pp->out;
+                            return launch_row_norm(et, r, s);
+                          },
+                          op_info(VLA_OP_SMALL, M, d, nr.nsplit, bytes, 0.0)});
+  };
+
+  for (int l = 0; l < L; ++l) {
+    const SubW& at = m->layers[l][0];
+    const SubW& ml = m->layers[l][1];
+    // ---- attention sublayer: [q | k | v] = u W^T, RoPE, bidirectional attention, W_o
+    if (!tern) {
+      GemmArgs g = gemm_base(m, M, nqkv, d, p->u, d, at.qkv);
+      g.epi = EPI_STORE;
+      g.out = p->qkv;
+      g.ldo = nqkv;
+      bld.gemm(g, 1);
+    } else {
+      TernArgs t{};
+      t.M = M; t.N = nqkv; t.K = d; t.x = p->q8; t.w = (const uint8_t*)at.qkv; t.rscale = p->r8; t.wscale = at.s_qkv;
+      t.e = gemm_base(m, M, nqkv, d, nullptr, 0, nullptr);
+      t.e.epi = EPI_STORE;
+      t.e.out = p->qkv;
+      t.e.ldo = nqkv;
+      bld.tern(t, 1);
+    }
+    if (bc.rope_base > 0.0f) {
+      void* qkvp = p->qkv;
+      const float base = bc.rope_base;
+      bld.small([=](hipStream_t s) {
+        hipError_t e = launch_rope(et, qkvp, M, P, nqkv, 0, H, hd, 0, base, s);
+        return e != hipSuccess ? e : launch_rope(et, qkvp, M, P, nqkv, dq, G, hd, 0, base, s);
+      }, M, dq + dkv, 0, 2.0 * M * (dq + dkv) * es);
+    }
+    AttnArgs a{};
+    a.mode = 0;
+    a.causal = 0;
+    a.B = B; a.n = P; a.P = 0; a.H = H; a.G = G; a.hd = hd;
+    a.q = p->qkv; a.ldq = nqkv;
+    a.ks = (const char*)p->qkv + (size_t)dq * es;
+    a.vs = (const char*)p->qkv + (size_t)(dq + dkv) * es;
+    a.ldkv = nqkv;
+    a.kc = nullptr;
+    a.vc = nullptr;
+    a.cp = p->cp;
+    a.layer_off = 0;
+    a.o = p->o;
+    a.ldo = dq;
+    a.scale = 1.0f / std::sqrt((float)hd);
+    bld.attn(a);
+    RowNormArgs nr{};
+    nr.mode = 0; nr.M = M; nr.d = d; nr.x = p->x; nr.eps = bc.rms_eps; nr.u = p->u; nr.u_f32 = tern ? 1 : 0;
+    nr.gamma = gam(l, 1);
+    nr.beta = gam(l, 1) + d;
+    if (tern) {
+      nr.q = p->q8;
+      nr.qr = p->r8;
+    }
+    if (!tern) {
+      resid_gemm(gemm_base(m, M, d, dq, p->o, dq, at.o), gam(l, 0) + 2 * d, nr);
+    } else {
+      QuantArgs q{};
+      q.M = M; q.K = dq; q.x = p->o; q.ldx = dq; q.src_type = 1; q.q = p->q8; q.r = p->r8;
+      bld.quant(q);
+      tern_resid(at, at.o, at.s_o, dq, gam(l, 0) + 2 * d);
+    }
+    norm_op(nr, false);
+    // ---- MLP sublayer
+    const bool last = l == L - 1;
+    RowNormArgs nm{};
+    nm.mode = 0; nm.M = M; nm.d = d; nm.x = p->x; nm.eps = bc.rms_eps;
+    if (!last) {
+      nm.gamma = gam(l + 1, 0);
+      nm.beta = gam(l + 1, 0) + d;
+      nm.u = p->u;
+      nm.u_f32 = tern ? 1 : 0;
+      if (tern) {
+        nm.q = p->q8;
+        nm.qr = p->r8;
+      }
+    } else {   // final norm, written as the element type into the call's output
+      nm.gamma = m->modf_static;
+      nm.beta = m->modf_static + d;
+      nm.u_f32 = 0;
+    }
+    const int ngu = glu ? 2 * F : F;
+    if (!tern) {
+      GemmArgs g = gemm_base(m, M, ngu, d, p->u, d, ml.gu);
+      g.epi = glu ? EPI_GLU : EPI_STORE;
+      g.act = mlp_act(bc.mlp);
+      g.out = p->h;
+      g.ldo = F;
+      bld.gemm(g, glu ? 2 : 1);
+      resid_gemm(gemm_base(m, M, d, F, p->h, F, ml.dn), gam(l, 1) + 2 * d, nm);
+    } else {
+      TernArgs t{};
+      t.M = M; t.N = ngu; t.K = d; t.x = p->q8; t.w = (const uint8_t*)ml.gu; t.rscale = p->r8; t.wscale = ml.s_gu;
+      t.e = gemm_base(m, M, ngu, d, nullptr, 0, nullptr);
+      t.e.epi = glu ? EPI_GLU : EPI_STORE;
+      t.e.act = mlp_act(bc.mlp);
+      t.e.out = p->h;
+      t.e.ldo = F;
+      t.e.out_f32 = 1;
+      bld.tern(t, glu ? 2 : 1);
+      QuantArgs q{};
+      q.M = M; q.K = F; q.x = p->h; q.ldx = F; q.src_type = 0; q.q = p->q8; q.r = p->r8;
+      bld.quant(q);
+      tern_resid(ml, ml.dn, ml.s_dn, F, gam(l, 1) + 2 * d);
+    }
+    norm_op(nm, last);
+  }
+  if (part_need) VLA_TRY(al((void**)&p->part, part_need * 4));
+  if (bld.part_need) VLA_TRY(al(&p->apart, bld.part_need));
+  if (bld.stats_need) VLA_TRY(al((void**)&p->astats, bld.stats_need));
+  HIP_TRY(hipDeviceSynchronize());
+  return VLA_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int32_t vla_backbone_weight_count(const vla_backbone_config* cfg) {
+  if (!cfg || validate_backbone(cfg) != VLA_OK) return -1;
+  return backbone_weight_count(*cfg);
+}
+
+vla_status vla_backbone_create(const vla_backbone_config* cfg, const void* const* weights, int32_t n_weights,
+                               vla_backbone** out) {
+  if (!out) return fail(VLA_E_ARG, "out is NULL");
+  *out = nullptr;
+  VLA_TRY(validate_backbone(cfg));
+  if (!weights) return fail(VLA_E_ARG, "weight table is NULL");
+  const int want = backbone_weight_count(*cfg);
+  if (n_weights != want) return fail(VLA_E_ARG, "weight table has %d entries, expected %d", n_weights, want);
+  for (int i = 0; i < n_weights; ++i) {
+    if (!weights[i]) return fail(VLA_E_ARG, "weight entry %d is NULL", i);
+    if (!al16(weights[i])) return fail(VLA_E_ARG, "weight entry %d is not 16-byte aligned", i);
+  }
+  return backbone_create_impl(cfg, weights, n_weights, out);
+}
+
+void vla_backbone_destroy(vla_backbone* bb) { delete bb; }
+
+vla_status vla_prefix_prefill(vla_backbone* bb, const void* embeds, int32_t batch, int32_t prefix_len,
+                              void* hidden_out, void* stream) {
+  if (!bb) return fail(VLA_E_ARG, "backbone is NULL");
+  if (!embeds || !hidden_out) return fail(VLA_E_ARG, "embeds / hidden_out is NULL");
+  if (!al16(embeds) || !al16(hidden_out)) return fail(VLA_E_ARG, "buffers must be 16-byte aligned");
+  if (batch < 1 || prefix_len < 1) return fail(VLA_E_SHAPE, "batch and prefix_len must be >= 1");
+  if ((long long)batch * prefix_len > 65536) return fail(VLA_E_UNSUPPORTED, "batch * prefix_len > 65536");
+  if ((prefix_len + 31) / 32 > attention_max_blocks())
+    return fail(VLA_E_UNSUPPORTED, "prefix_len beyond %d rows", 32 * attention_max_blocks());
+  auto key = std::make_pair((int)batch, (int)prefix_len);
+  auto it = bb->plans.find(key);
+  PrefillPlan* p;
+  if (it == bb->plans.end()) {
+    if (bb->plans.size() >= 4) bb->plans.erase(bb->plans.begin());
+    std::unique_ptr<PrefillPlan> np(new PrefillPlan());
+    np->B = batch;
+    np->P = prefix_len;
+    VLA_TRY(build_prefill_plan(bb, np.get()));
+    p = np.get();
+    bb->plans[key] = std::move(np);
+  } else {
+    p = it->second.get();
+  }
+  p->embeds = embeds;
+  p->out = hidden_out;
+  VLA_TRY(run_ops(p->ops, reinterpret_cast<hipStream_t>(stream)));
   return VLA_OK;
 }
 

@@ -107,7 +107,8 @@ struct QuantArgs {
 //   x[m] = a[m] W_in^T + xs[b] + E_pos[token]    (mode 1, the input embedding)
 //   u[m] = x[m] / sqrt(mean(x[m]^2) + eps) * (1 + gamma) + beta
 struct RowNormArgs {
-  int mode;
+  int mode;                // 0: residual stream x (+ alpha * sum of partials); 1: input embedding;
+                           // 2: x = x_in (element type), the first norm of a backbone prefill
   int M, d;
   float* x;                // [M][d]
   const float* part;       // [nsplit][M][d]
@@ -128,6 +129,7 @@ struct RowNormArgs {
   int u_f32;
   int8_t* q;               // if set (u_f32 = 1): also the int8 absmax quantisation of u, [M][d]
   float* qr;               // and its per-row absmax [M]
+  const void* x_in;        // mode 2: [M][d] element type
 };
 
 struct TernArgs {

@@ -38,7 +38,8 @@ EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_mod
            "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
            "vla_test_ternary_gemm", "vla_test_rope",
-           "vla_test_adarms", "vla_test_time_cond", "vla_test_persist_trace"]
+           "vla_test_adarms", "vla_test_time_cond", "vla_test_persist_trace",
+           "vla_backbone_weight_count", "vla_backbone_create", "vla_backbone_destroy", "vla_prefix_prefill"]
 
 
 class VlaError(RuntimeError):
@@ -52,6 +53,12 @@ class VlaConfig(ctypes.Structure):
         "n_layers", "d_model", "n_heads", "head_dim", "n_kv_heads", "d_ff", "d_prefix",
         "n_action", "d_action", "d_state", "pattern", "mlp", "wtype", "head_regression")] + [
         ("rms_eps", ctypes.c_float)]
+
+
+class VlaBackboneConfig(ctypes.Structure):
+    _fields_ = [(n, ctypes.c_int32) for n in (
+        "n_layers", "d_model", "n_heads", "head_dim", "n_kv_heads", "d_ff", "mlp", "wtype")] + [
+        ("rope_base", ctypes.c_float), ("rms_eps", ctypes.c_float)]
 
 
 class VlaOpTime(ctypes.Structure):
@@ -94,6 +101,11 @@ def lib():
         "vla_test_ternary_gemm": (i32, [vp, vp, vp, vp, i32, i32, i32, i32, i32, vp,
                                         ctypes.POINTER(ctypes.c_float), vp]),
         "vla_test_persist_trace": (i32, [vp, ctypes.POINTER(ctypes.c_uint64), i32]),
+        "vla_backbone_weight_count": (i32, [ctypes.POINTER(VlaBackboneConfig)]),
+        "vla_backbone_create": (i32, [ctypes.POINTER(VlaBackboneConfig), ctypes.POINTER(vp), i32,
+                                      ctypes.POINTER(vp)]),
+        "vla_backbone_destroy": (None, [vp]),
+        "vla_prefix_prefill": (i32, [vp, vp, i32, i32, vp, vp]),
     }
     for name, (res, args) in sig.items():
         f = getattr(L, name)
@@ -328,3 +340,59 @@ def test_rope(elem: int, x, rows: int, rows_per_request: int, ld: int, col0: int
     """Rotary position embedding in place on x (the RoPE variant's kernel)."""
     _check(lib().vla_test_rope(elem, _ptr(x), rows, rows_per_request, ld, col0, nheads, hd, pos0, float(base),
                                _stream(stream)))
+
+
+# ---- the prefix stage: backbone prefill -------------------------------------
+
+def make_backbone_config(bcfg) -> VlaBackboneConfig:
+    """vla_backbone_config from an object with the backbone's attributes."""
+    return VlaBackboneConfig(
+        n_layers=bcfg.n_layers, d_model=bcfg.d_model, n_heads=bcfg.n_heads, head_dim=bcfg.head_dim,
+        n_kv_heads=bcfg.n_kv_heads, d_ff=bcfg.d_ff, mlp=MLPS[bcfg.mlp], wtype=WTYPES[bcfg.wtype],
+        rope_base=float(bcfg.rope_base), rms_eps=float(bcfg.rms_eps))
+
+
+def backbone_weight_order(bcfg) -> List[str]:
+    """Backbone weight-table names in the order vla.h documents (ternary
+    matrices followed by '<name>.scale')."""
+    tern = bcfg.wtype == "ternary"
+    mats = ["W1", "W2"] if bcfg.mlp == "gelu" else ["W_g", "W_u", "W_d"]
+    names = ["g_f"]
+    for l in range(bcfg.n_layers):
+        p = f"B{l}."
+        for n in ["g_att", "W_q", "W_k", "W_v", "W_o", "g_mlp"] + mats:
+            names.append(p + n)
+            if tern and n.startswith("W"):
+                names.append(p + n + ".scale")
+    return names
+
+
+class Backbone:
+    """A vla_backbone created from device tensors keyed by weight-table name."""
+
+    def __init__(self, bcfg, device_weights: Dict[str, object]):
+        self.cfg = bcfg
+        self._c = make_backbone_config(bcfg)
+        names = backbone_weight_order(bcfg)
+        want = lib().vla_backbone_weight_count(ctypes.byref(self._c))
+        if want != len(names):
+            raise VlaError(1, f"backbone weight table length mismatch ({want} vs {len(names)})")
+        table = (ctypes.c_void_p * len(names))(*[_ptr(device_weights[n]) for n in names])
+        h = ctypes.c_void_p()
+        _check(lib().vla_backbone_create(ctypes.byref(self._c), table, len(names), ctypes.byref(h)))
+        self.handle = h
+
+    def close(self):
+        if getattr(self, "handle", None):
+            lib().vla_backbone_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def prefill(self, embeds, batch: int, prefix_len: int, hidden_out, stream=None):
+        _check(lib().vla_prefix_prefill(self.handle, _ptr(embeds), batch, prefix_len, _ptr(hidden_out),
+                                        _stream(stream)))

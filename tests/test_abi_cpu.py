@@ -137,3 +137,51 @@ def test_missing_library_fails_loudly(monkeypatch, tmp_path):
     monkeypatch.setattr(vla, "_lib", None)
     with pytest.raises(RuntimeError, match="missing"):
         vla.lib()
+
+
+@pytest.mark.parametrize("name", sorted(wl.BACKBONES))
+def test_backbone_weight_count_matches_binding_order(name):
+    """The library's backbone table length equals the binding's name list,
+    which follows the generator's names (ternary matrices plus scales)."""
+    vla = _vla()
+    bcfg = wl.BACKBONES[name]
+    c = vla.make_backbone_config(bcfg)
+    order = vla.backbone_weight_order(bcfg)
+    assert vla.lib().vla_backbone_weight_count(ctypes.byref(c)) == len(order)
+    gen = []
+    for n in wl.backbone_weight_names(bcfg):
+        gen += [n, n + ".scale"] if wl.is_backbone_ternary(bcfg, n) else [n]
+    assert gen == order
+
+
+@pytest.mark.parametrize("bad,status", [
+    (dict(wtype="f32"), "VLA_E_UNSUPPORTED"),
+    (dict(n_kv_heads=3), "VLA_E_SHAPE"),
+    (dict(head_dim=96), "VLA_E_UNSUPPORTED"),
+    (dict(d_model=8192), "VLA_E_UNSUPPORTED"),
+    (dict(rope_base=0.5), "VLA_E_ARG"),
+    (dict(rms_eps=0.0), "VLA_E_ARG"),
+    (dict(n_layers=0), "VLA_E_SHAPE"),
+])
+def test_backbone_config_validation(bad, status):
+    vla = _vla()
+    c = vla.make_backbone_config(wl.PI0_VLM_BF16.with_(**bad))
+    h = ctypes.c_void_p()
+    table = (ctypes.c_void_p * 1)()
+    st = vla.lib().vla_backbone_create(ctypes.byref(c), table, 1, ctypes.byref(h))
+    assert vla.STATUS[st] == status, vla.lib().vla_last_error()
+    assert h.value is None
+    assert vla.lib().vla_backbone_weight_count(ctypes.byref(c)) == -1
+
+
+def test_backbone_calls_rejected_before_device_use():
+    vla = _vla()
+    L = vla.lib()
+    c = vla.make_backbone_config(wl.PI0_VLM_BF16)
+    n = L.vla_backbone_weight_count(ctypes.byref(c))
+    h = ctypes.c_void_p()
+    table = (ctypes.c_void_p * n)()
+    assert vla.STATUS[L.vla_backbone_create(ctypes.byref(c), table, n, ctypes.byref(h))] == "VLA_E_ARG"
+    assert b"NULL" in L.vla_last_error()
+    assert vla.STATUS[L.vla_backbone_create(ctypes.byref(c), table, n - 1, ctypes.byref(h))] == "VLA_E_ARG"
+    assert vla.STATUS[L.vla_prefix_prefill(None, 16, 1, 1, 16, None)] == "VLA_E_ARG"

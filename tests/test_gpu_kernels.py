@@ -299,7 +299,8 @@ def test_quantize_i8_bit_exact(torch):
 
 
 TERN_SHAPES = [(8, 3840, 2560), (8, 2560, 2560), (8, 13824, 2560), (8, 2560, 6912), (56, 2560, 6912),
-               (512, 1280, 2560), (3, 17, 64), (20, 100, 192), (5, 7, 68), (2, 3, 4)]
+               (512, 1280, 2560), (512, 3840, 2560), (512, 13824, 2560), (512, 2560, 6912), (300, 200, 640),
+               (3, 17, 64), (20, 100, 192), (5, 7, 68), (2, 3, 4)]
 
 
 @pytest.mark.parametrize("M,N,K", TERN_SHAPES)

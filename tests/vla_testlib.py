@@ -97,3 +97,40 @@ class Pipeline:
 
     def close(self):
         self.model.close()
+
+
+def device_backbone_weights(bcfg: wl.BackboneConfig, Wb: Dict[str, np.ndarray]):
+    """Backbone weight-table tensors on the GPU, keyed as the binding expects."""
+    torch = torch_mod()
+    out = {}
+    for name, arr in Wb.items():
+        if name.endswith(".scale"):
+            out[name] = torch.tensor([float(arr)], dtype=torch.float32, device="cuda")
+        elif wl.is_backbone_ternary(bcfg, name):
+            out[name] = torch.from_numpy(wl.pack_ternary(arr)).cuda()
+        elif arr.ndim == 2:
+            out[name] = to_device(arr, bf16=True)
+        else:
+            out[name] = to_device(np.asarray(arr, np.float32))
+    return out
+
+
+class Prefill:
+    """A backbone plus device buffers for one (batch, prefix_len) shape."""
+
+    def __init__(self, bcfg, Wb, embeds: np.ndarray):
+        from paper_2606_08094_amd import vla
+        torch = torch_mod()
+        self.cfg = bcfg
+        self.dw = device_backbone_weights(bcfg, Wb)
+        self.bb = vla.Backbone(bcfg, self.dw)
+        self.B, self.P = embeds.shape[0], embeds.shape[1]
+        self.embeds = to_device(embeds, bf16=True)
+        self.hidden = torch.empty((self.B, self.P, bcfg.d_model), dtype=torch.bfloat16, device="cuda")
+
+    def run(self, stream=None):
+        self.bb.prefill(self.embeds, self.B, self.P, self.hidden, stream)
+        return self.hidden
+
+    def close(self):
+        self.bb.close()

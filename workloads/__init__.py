@@ -405,10 +405,10 @@ def make_backbone_weights(bcfg: BackboneConfig, seed: int | None = None) -> Dict
         if is_backbone_ternary(bcfg, name):
             out[name] = _ternary(rng, shape)
             out[name + ".scale"] = np.float32(TERNARY_SCALE)
-        elif len(shape) == 1:
-            out[name] = _normal(rng, shape, 0.02)
         else:
-            out[name] = round_bf16(_normal(rng, shape, 0.02))
+            # float32 draws: the Gemma-shaped backbone has two billion weights
+            x = rng.standard_normal(size=shape, dtype=np.float32) * np.float32(0.02)
+            out[name] = x if len(shape) == 1 else round_bf16(x)
     return out
 
 
