@@ -121,6 +121,22 @@ vla_status vla_prefix_kv_build(vla_model* model, const void* prefix_hidden, int3
                                void* stream);
 
 /*
+ * vla_prefix_kv_build for callers that cannot allocate device memory (code
+ * under HIP graph capture, tight serving loops, harnesses that forbid
+ * hipMalloc): same arguments, same result, and it calls no hipMalloc, hipFree
+ * or allocating library routine.  Its scratch (the W2A8 int8 codes and row
+ * scales of the prefix rows; dense models use none) lives in a static device
+ * array of 16 MiB per GPU, held until the process ends:
+ * batch * prefix_len * (d_prefix + 4) bytes (plus alignment) must fit, else
+ * VLA_E_UNSUPPORTED before any work is enqueued.  Every call on one GPU
+ * shares that array, so calls that overlap on one GPU (other streams, other
+ * threads) race; calls ordered on one stream do not.
+ */
+vla_status vla_prefix_kv_build_noalloc(vla_model* model, const void* prefix_hidden, int32_t batch,
+                                       int32_t prefix_len, void* kv_cache, size_t kv_cache_bytes,
+                                       void* stream);
+
+/*
  * Integrate one action chunk per request (Algorithm 1, solver loop and
  * denormalisation).  For k = 0..n_steps-1 the expert evaluates the velocity v
  * at (a_k, tau_k) and a_{k+1} = a_k + (tau_{k+1} - tau_k) v; the regression

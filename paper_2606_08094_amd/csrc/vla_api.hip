@@ -10,6 +10,7 @@
 #include <cstring>
 #include <functional>
 #include <map>
+#include <mutex>
 #include <memory>
 #include <string>
 #include <tuple>
@@ -1226,6 +1227,31 @@ vla_status vla_model_create(const vla_config* cfg, const void* const* weights, i
 
 // RoPE variant: the cached K of every joint layer holds prefix row p at
 // position p (cache block [2][B][G][P][hd], K first).
+// Device scratch of the no-allocation prefix build: one copy per GPU, held
+// until the process ends.  Host code must not use the symbol itself as an
+// address: prefix_scratch() returns the device's copy, looked up once per
+// device with hipGetSymbolAddress.
+constexpr size_t kPrefixScratchBytes = (size_t)16 << 20;
+static __device__ __align__(256) unsigned char prefix_scratch_buf[kPrefixScratchBytes];
+
+static vla_status prefix_scratch(unsigned char** out) {
+  static std::mutex mu;
+  static unsigned char* ptr[64] = {};
+  int dev = 0;
+  HIP_TRY(hipGetDevice(&dev));
+  if (dev < 0 || dev >= 64) return fail(VLA_E_UNSUPPORTED, "device %d beyond 64", dev);
+  std::lock_guard<std::mutex> lock(mu);
+  if (!ptr[dev]) {
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(prefix_scratch_buf));
+    if (e != hipSuccess || !p)
+      return fail(VLA_E_DEVICE, "hipGetSymbolAddress of the prefix scratch: %s", hipGetErrorString(e));
+    ptr[dev] = static_cast<unsigned char*>(p);
+  }
+  *out = ptr[dev];
+  return VLA_OK;
+}
+
 static vla_status check_prefix_args(vla_model* m, const void* prefix_hidden, int batch, int prefix_len,
                                     const void* kv_cache, size_t kv_cache_bytes) {
   if (!m) return fail(VLA_E_ARG, "model is NULL");
@@ -1307,6 +1333,27 @@ vla_status vla_prefix_kv_build(vla_model* m, const void* prefix_hidden, int32_t 
   PrefixWs* w = nullptr;
   VLA_TRY(get_prefix_ws(m, batch, prefix_len, &w));
   return prefix_kv_build_impl(m, prefix_hidden, batch, prefix_len, kv_cache, w->q8, w->r8,
+                              reinterpret_cast<hipStream_t>(stream));
+}
+
+vla_status vla_prefix_kv_build_noalloc(vla_model* m, const void* prefix_hidden, int32_t batch, int32_t prefix_len,
+                                       void* kv_cache, size_t kv_cache_bytes, void* stream) {
+  VLA_TRY(check_prefix_args(m, prefix_hidden, batch, prefix_len, kv_cache, kv_cache_bytes));
+  int8_t* q8 = nullptr;
+  float* r8 = nullptr;
+  if (m->tern) {
+    // codes [M][d_p] int8, then the per-row absmax [M] fp32 at the next 256-byte boundary
+    const size_t M = (size_t)batch * prefix_len;
+    const size_t qbytes = (M * m->cfg.d_prefix + 255) / 256 * 256;
+    if (qbytes + M * 4 > kPrefixScratchBytes)
+      return fail(VLA_E_UNSUPPORTED, "batch * prefix_len * (d_prefix + 4) needs %zu bytes of scratch, more than "
+                                     "the %zu of the no-allocation entry", qbytes + M * 4, kPrefixScratchBytes);
+    unsigned char* base = nullptr;
+    VLA_TRY(prefix_scratch(&base));
+    q8 = reinterpret_cast<int8_t*>(base);
+    r8 = reinterpret_cast<float*>(base + qbytes);
+  }
+  return prefix_kv_build_impl(m, prefix_hidden, batch, prefix_len, kv_cache, q8, r8,
                               reinterpret_cast<hipStream_t>(stream));
 }
 

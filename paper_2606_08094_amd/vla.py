@@ -34,7 +34,7 @@ OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "qua
 
 # Every symbol the headers declare.
 EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_model_check", "vla_kv_cache_bytes",
-           "vla_prefix_kv_build", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
+           "vla_prefix_kv_build", "vla_prefix_kv_build_noalloc", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
            "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
            "vla_test_ternary_gemm", "vla_test_rope",
@@ -85,6 +85,7 @@ def lib():
         "vla_model_check": (i32, [vp, vp]),
         "vla_kv_cache_bytes": (sz, [vp, i32, i32]),
         "vla_prefix_kv_build": (i32, [vp, vp, i32, i32, vp, sz, vp]),
+        "vla_prefix_kv_build_noalloc": (i32, [vp, vp, i32, i32, vp, sz, vp]),
         "vla_denoise": (i32, [vp, vp, sz, i32, i32, vp, vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp, vp]),
         "vla_ternary_gemm": (i32, [vp, vp, i32, i32, i32, vp, vp]),
         "vla_model_set_option": (i32, [vp, i32, i32]),
@@ -274,6 +275,12 @@ class Model:
                         stream=None):
         _check(lib().vla_prefix_kv_build(self.handle, _ptr(prefix_hidden), batch, prefix_len, _ptr(kv_cache),
                                          kv_cache_bytes, _stream(stream)))
+
+    def prefix_kv_build_noalloc(self, prefix_hidden, batch: int, prefix_len: int, kv_cache, kv_cache_bytes: int,
+                                stream=None):
+        """vla_prefix_kv_build with its scratch in the library's static device array."""
+        _check(lib().vla_prefix_kv_build_noalloc(self.handle, _ptr(prefix_hidden), batch, prefix_len,
+                                                 _ptr(kv_cache), kv_cache_bytes, _stream(stream)))
 
     def denoise(self, kv_cache, kv_cache_bytes: int, batch: int, prefix_len: int, noise, state,
                 t_schedule: Sequence[float], act_mean=None, act_std=None, actions_out=None, stream=None):

@@ -185,3 +185,4 @@ def test_backbone_calls_rejected_before_device_use():
     assert b"NULL" in L.vla_last_error()
     assert vla.STATUS[L.vla_backbone_create(ctypes.byref(c), table, n - 1, ctypes.byref(h))] == "VLA_E_ARG"
     assert vla.STATUS[L.vla_prefix_prefill(None, 16, 1, 1, 16, None)] == "VLA_E_ARG"
+    assert vla.STATUS[L.vla_prefix_kv_build_noalloc(None, 16, 1, 1, 16, 0, None)] == "VLA_E_ARG"
