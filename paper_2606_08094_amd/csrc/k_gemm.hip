@@ -532,27 +532,6 @@ struct Ring {
   static constexpr int RP = (64 * (BN + 4) * 4 <= SB * 16) ? 64 : (32 * (BN + 4) * 4 <= SB * 16 ? 32 : 16);
 };
 
-typedef unsigned v4u __attribute__((ext_vector_type(4)));  // one 16-byte LDS slot
-
-// One wave-wide global_load_lds_dwordx4: lane l's 16 bytes at g land in LDS
-// at wave-uniform lds + 16 l.  Written as asm so that the compiler adds no
-// waits of its own for it; the kernel's explicit vmcnt waits and barriers
-// order it against the LDS reads.
-VLA_DEV void dma16(const void* g, v4u* lds) {
-  typedef __attribute__((address_space(3))) v4u lds_v4u;
-  const unsigned off = (unsigned)(uintptr_t)(lds_v4u*)lds;  // byte offset in the workgroup's LDS
-  const unsigned base = __builtin_amdgcn_readfirstlane(off);
-  asm volatile("s_mov_b32 m0, %0\n\tglobal_load_lds_dwordx4 %1, off" : : "s"(base), "v"(g) : "memory", "m0");
-}
-
-// Workgroup barrier after this wave's LDS reads have completed; the memory
-// clobber keeps the compiler from moving LDS accesses across it.
-VLA_DEV void lds_barrier() { asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" : : : "memory"); }
-
-VLA_DEV constexpr unsigned vm_wait(int n) {  // s_waitcnt: vmcnt(n), no wait on the other counters
-  return (unsigned)((n & 15) | ((n >> 4) << 14) | (7 << 4) | (15 << 8));
-}
-
 template <int MS, int NS>
 __global__ __launch_bounds__(256) void gemm_tile(GemmArgs a) {
   using R = Ring<MS, NS>;

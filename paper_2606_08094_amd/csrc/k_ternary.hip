@@ -434,6 +434,202 @@ hipError_t launch_ternary_dot4(const TernArgs& a, hipStream_t s) {
 }
 
 // ms: m-subtiles (1, 2, 4); nsub 1 or 2 (GLU pairs); nc from a.ks / 256.
+namespace {
+
+// ---------------------------------------------------------------------------
+// tern_tile: the W2A8 GEMM with many token rows (the backbone prefill and the
+// prefix K/V build, M = B * P), where the int8 matrix cores, not the weight
+// bytes, set the pace.  A 2 x 2 wave workgroup owns a (32 MS) x 128 output
+// tile.  128-deep K-slices of the activation codes (BM rows x 128 bytes) and of
+// the packed weights (128 rows x 32 bytes) stream into a ring of NST LDS
+// stages by direct-to-LDS loads, NST - 1 slices ahead of the MFMAs.  Code rows
+// are XOR-swizzled (16-byte chunk c of row r at c ^ (r % 8)), weight rows swap
+// their two halves every 8 rows, so the operand reads of 16 rows spread over
+// the banks.  Right before its MFMA a lane widens its 16 weights (one dword) to
+// signed int8, so v_mfma_i32_16x16x64_i8 sums q * w directly (exact int32).
+// Requires K % 128 == 0; rows past M or N load a valid row and are not stored.
+template <int MS>
+struct TRing {
+  static constexpr int BM = 32 * MS, BN = 128;
+  static constexpr int SX = BM * 8;        // 16-byte slots of codes per stage
+  static constexpr int SW = BN * 2;        // 16-byte slots of packed weights per stage
+  static constexpr int SB = SX + SW;
+  static constexpr int NST = 4;
+  static constexpr int LX = SX / 256;      // code loads per thread and slice (weights: one)
+};
+
+template <int MS>
+__global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
+  using R = TRing<MS>;
+  constexpr int BM = R::BM, BN = R::BN, SX = R::SX, SB = R::SB, NST = R::NST, LX = R::LX, D = NST - 1;
+  __shared__ v4u st0[SB], st1[SB], st2[SB], st3[SB];
+  auto stage = [&](auto j) -> v4u* {
+    constexpr int J = decltype(j)::value;
+    if constexpr (J == 0) return st0;
+    else if constexpr (J == 1) return st1;
+    else if constexpr (J == 2) return st2;
+    else return st3;
+  };
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int wm = wave >> 1, wn = wave & 1;
+  const int M = a.M, N = a.N, K = a.K, KB = K / 4;
+  const int per = gridDim.x >> 3;
+  const int u = (blockIdx.x & 7) * per + (blockIdx.x >> 3);   // tiles of one W column block stay on one XCD
+  const int tiles = a.m_tiles * a.n_tiles;
+  if (u >= tiles) return;
+  const int ntile = u / a.m_tiles, mtile = u - ntile * a.m_tiles;
+  const int m0 = mtile * BM, n0 = ntile * BN;
+  const int nsl = K / 128;
+
+  // sources of this lane's slots: codes (instruction i: row (4 i + wave) * 8 + lane / 8),
+  // weights (row wave * 32 + lane / 2, half lane % 2)
+  const int8_t* xsrc[LX];
+#pragma unroll
+  for (int i = 0; i < LX; ++i) {
+    const int row = (i * 4 + wave) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (row & 7);
+    xsrc[i] = a.x + (size_t)min(m0 + row, M - 1) * K + c * 16;
+  }
+  const int wrow = wave * 32 + (lane >> 1);
+  const uint8_t* wsrc = a.w + (size_t)min(n0 + wrow, N - 1) * KB + (((lane & 1) ^ ((wrow >> 3) & 1)) * 16);
+  auto issue = [&](auto j, int sl) {
+    v4u* b = stage(j);
+#pragma unroll
+    for (int i = 0; i < LX; ++i) dma16(xsrc[i] + sl * 128, b + (i * 4 + wave) * 64);
+    dma16(wsrc + sl * 32, b + SX + wave * 64);
+  };
+
+  i32x4 acc[MS][4];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = i32x4{0, 0, 0, 0};
+
+  // MFMA kk of a slice: lane group g4 holds k = 64 kk + 16 g4 .. + 15 of both operands
+  auto compute = [&](const v4u* b) {
+    v4u xf[2][MS];
+    uint32_t wp[2][4];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) {
+        const int row = wm * 16 * MS + ms * 16 + r16;
+        xf[kk][ms] = b[row * 8 + ((kk * 4 + g4) ^ (row & 7))];
+      }
+#pragma unroll
+      for (int ns = 0; ns < 4; ++ns) {
+        const int row = wn * 64 + ns * 16 + r16;
+        const uint32_t* slot = reinterpret_cast<const uint32_t*>(b + SX + row * 2 + (kk ^ ((row >> 3) & 1)));
+        wp[kk][ns] = slot[g4];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int ns = 0; ns < 4; ++ns) {
+        const i32x4 w = unpack_signed(wp[kk][ns]);
+#pragma unroll
+        for (int ms = 0; ms < MS; ++ms)
+          acc[ms][ns] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[kk][ms]), w, acc[ms][ns],
+                                                               0, 0, 0);
+      }
+  };
+
+  [&]<int... J>(std::integer_sequence<int, J...>) {
+    ((J < nsl ? issue(std::integral_constant<int, J>{}, J) : void()), ...);
+  }(std::make_integer_sequence<int, D>{});
+  for (int it0 = 0; it0 < nsl; it0 += NST) {
+    [&]<int... J>(std::integer_sequence<int, J...>) {
+      (
+          [&] {
+            const int it = it0 + J;
+            if (it >= nsl) return;
+            // slice `it` has landed once at most the D-1 later slices are pending
+            if (it + D - 1 < nsl)
+              __builtin_amdgcn_s_waitcnt(vm_wait((D - 1) * (LX + 1)));
+            else
+              __builtin_amdgcn_s_waitcnt(vm_wait(0));
+            lds_barrier();
+            if (it + D < nsl) issue(std::integral_constant<int, (J + D) % NST>{}, it + D);
+            compute(stage(std::integral_constant<int, J>{}));
+          }(),
+          ...);
+    }(std::make_integer_sequence<int, NST>{});
+  }
+
+  const int mw = m0 + wm * 16 * MS, nw = n0 + wn * 64;
+  if (a.rscale == nullptr) {   // raw int32 sums
+#pragma unroll
+    for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = mw + ms * 16 + g4 * 4 + i;
+#pragma unroll
+        for (int ns = 0; ns < 4; ++ns) {
+          const int n = nw + ns * 16 + r16;
+          if (m < M && n < N) a.acc_out[(size_t)m * N + n] = acc[ms][ns][i];
+        }
+      }
+    return;
+  }
+  // y = acc * (s_w * r_m / 127) (the dequantisation of the other W2A8 kernels)
+  float sw[4];
+#pragma unroll
+  for (int ns = 0; ns < 4; ++ns) {
+    const int n = nw + ns * 16 + r16;
+    sw[ns] = (n < N) ? a.wscale[n] : 0.0f;
+  }
+  f32x4 y[MS][4];
+#pragma unroll
+  for (int ms = 0; ms < MS; ++ms)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = mw + ms * 16 + g4 * 4 + i;
+      const float rm = (m < M) ? a.rscale[m] : 0.0f;
+#pragma unroll
+      for (int ns = 0; ns < 4; ++ns) y[ms][ns][i] = (float)acc[ms][ns][i] * (sw[ns] * rm / 127.0f);
+    }
+  if (a.e.epi == EPI_GLU) {          // gate / up 16-row blocks pair up at 32-row boundaries
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      f32x4 yp[MS][2];
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) {
+        yp[ms][0] = y[ms][2 * j];
+        yp[ms][1] = y[ms][2 * j + 1];
+      }
+      wave_epilogue<bf16_t, MS, 2>(a.e, yp, mw, nw + 32 * j, 0);
+    }
+  } else if (a.e.epi == EPI_RESID) {  // one 16-column subtile at a time
+#pragma unroll
+    for (int ns = 0; ns < 4; ++ns) {
+      f32x4 y1[MS][1];
+#pragma unroll
+      for (int ms = 0; ms < MS; ++ms) y1[ms][0] = y[ms][ns];
+      wave_epilogue<bf16_t, MS, 1>(a.e, y1, mw, nw + 16 * ns, 0);
+    }
+  } else {
+    wave_epilogue<bf16_t, MS, 4>(a.e, y, mw, nw, 0);
+  }
+}
+
+template <int MS>
+hipError_t tile_launch(const TernArgs& a0, hipStream_t s) {
+  TernArgs a = a0;
+  a.m_tiles = (a.M + 32 * MS - 1) / (32 * MS);
+  a.n_tiles = (a.N + 127) / 128;
+  const int tiles = a.m_tiles * a.n_tiles;
+  const int grid = (tiles + 7) / 8 * 8;
+  hipLaunchKernelGGL((tern_tile<MS>), dim3(grid), dim3(256), 0, s, a);
+  return hipGetLastError();
+}
+
+}  // namespace
+
+bool tern_tile_eligible(int M, int N, int K) { return M >= 128 && N >= 1 && K >= 128 && K % 128 == 0; }
+
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.K % 64 != 0) {
@@ -444,6 +640,11 @@ hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t
     return hipGetLastError();
   }
   const int nsub = (a.rscale != nullptr && a.e.epi == EPI_GLU) ? 2 : 1;
+  if (a.nsplit <= 1 && tern_tile_eligible(a.M, a.N, a.K)) {
+    // many token rows: the tiled kernel; 128-row tiles once they fill the device
+    const long long t4 = (long long)((a.M + 127) / 128) * ((a.N + 127) / 128);
+    return t4 >= 256 ? tile_launch<4>(a, s) : tile_launch<2>(a, s);
+  }
   if (a.rscale != nullptr && a.M <= 64) {  // token rows of the denoise loop: the skinny kernel
     const int sms = a.M <= 16 ? 1 : (a.M <= 32 ? 2 : 4);
     switch (sms * 10 + nsub) {

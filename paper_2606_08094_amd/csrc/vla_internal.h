@@ -140,6 +140,7 @@ struct TernArgs {
   const float* wscale;     // [N] per W-row scale (the per-tensor scale of its matrix)
   int32_t* acc_out;        // raw int32 output (when rscale == NULL); zero-filled if nsplit > 1
   int ks, nsplit, n_tiles;  // nsplit > 1 only for the raw int32 output (atomic accumulation)
+  int m_tiles;              // tiled kernel: row tiles (set by its launcher)
   // dequantised epilogue (same meaning as GemmArgs)
   GemmArgs e;
 };
@@ -200,12 +201,14 @@ struct PersistArgs {
   // optional phase timeline: workgroup 0 of each team records the 100 MHz
   // clock before and after every barrier, PERSIST_TRACE_MAX entries per team
   unsigned long long* trace;
+  int trace_all;             // 1: every workgroup records its first PERSIST_TRACE_WG marks (row team * 32 + rank)
 };
 constexpr int PERSIST_RANK_OFF = 8 * 32;          // 8 per-XCD arrival counters (team ranks)
 constexpr int PERSIST_ERR_OFF = 8 * 32 + 32;      // the error word, on a line of its own
 constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 64;   // barrier flags [8][32], rank counters, error word
 constexpr long PERSIST_SPIN_DEFAULT = 1L << 21;   // barrier polls before a timeout (about 0.2 s)
 constexpr int PERSIST_TRACE_MAX = 8192;
+constexpr int PERSIST_TRACE_WG = 8 * PERSIST_TRACE_MAX / 256;   // marks per workgroup when all record
 constexpr int PERSIST_MAX_LAYERS = 64;
 
 // ---- launchers (each enqueues on `s`, returns hipError_t) ----
@@ -243,6 +246,8 @@ hipError_t launch_time_embed(int et, const CallParams* cp, void* e, int T, int T
 hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
 hipError_t launch_quantize(const QuantArgs& a, hipStream_t s);
 hipError_t launch_ternary_dot4(const TernArgs& a, hipStream_t s);   // VALU sdot4 variant (EPI_STORE)
+// The tiled W2A8 kernel takes the shape (many token rows, K % 128 == 0).
+bool tern_tile_eligible(int M, int N, int K);
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s);
 hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
 hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);

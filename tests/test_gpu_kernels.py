@@ -387,7 +387,8 @@ def test_ternary_gemm_dot4_matches_mfma(torch, M, N, K):
 
 
 @pytest.mark.parametrize("M,N,K", [(8, 3840, 2560), (8, 2560, 6912), (512, 1280, 2560), (13, 70, 128),
-                                   (56, 2560, 2560), (20, 512, 6912), (40, 200, 320), (64, 48, 64)])
+                                   (56, 2560, 2560), (20, 512, 6912), (40, 200, 320), (64, 48, 64),
+                                   (512, 13824, 2560), (512, 2560, 6912), (300, 200, 640), (129, 130, 128)])
 def test_ternary_linear(torch, M, N, K):
     x = wl.random_matrix((M, K), 3 + M, 1.0)
     w = wl.random_ternary((N, K), 4 + N)
