@@ -599,6 +599,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
                             if (e != hipSuccess) return e;
                             PersistArgs q = pa;
                             q.trace = *tracing ? tbuf : nullptr;
+                            q.trace_all = *tracing == 2 ? 1 : 0;
                             q.spin_limit = *spin;
                             e = launch_persist(q, s);
                             if (e != hipSuccess) return e;
@@ -945,7 +946,7 @@ vla_status vla_model_set_option(vla_model* m, int32_t option, int32_t value) {
     return VLA_OK;
   }
   if (option == VLA_OPT_TRACE) {
-    if (value < 0 || value > 1) return fail(VLA_E_ARG, "trace flag %d out of range", value);
+    if (value < 0 || value > 2) return fail(VLA_E_ARG, "trace mode %d out of range", value);
     m->trace = value;
     return VLA_OK;
   }
@@ -1477,7 +1478,7 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
   if (K % 64 != 0) t = Tiling{1, 1, 1, 1, 1, 1, 1};
   // Few output tiles: split K across workgroups; the int32 partial sums are
   // exact and are added atomically into the zero-filled output.
-  if (K % 64 == 0 && t.units < 256 && K > 256) {
+  if (!tern_tile_eligible(M, N, K) && K % 64 == 0 && t.units < 256 && K > 256) {
     t.nc = 1;
     t.nsplit = std::min(cdiv(K, 256), cdiv(256, t.units));
     while ((long long)t.nc * 256 * t.nsplit < K) ++t.nsplit;
@@ -1511,11 +1512,12 @@ int32_t vla_test_persist_trace(vla_model* m, uint64_t* out, int32_t max_per_team
   Plan* p = static_cast<Plan*>(m->last_traced);
   if (!p->trace || max_per_team < 0) return -1;
   if (hipDeviceSynchronize() != hipSuccess) return -1;
-  const int n = std::min(max_per_team, PERSIST_TRACE_MAX);
+  const bool all = m->trace == 2;
+  const int rows = all ? 256 : 8, cap = all ? PERSIST_TRACE_WG : PERSIST_TRACE_MAX;
+  const int n = std::min(max_per_team, cap);
   if (out)
-    for (int t = 0; t < 8; ++t)
-      if (hipMemcpy(out + (size_t)t * n, p->trace + (size_t)t * PERSIST_TRACE_MAX, (size_t)n * 8,
-                    hipMemcpyDeviceToHost) != hipSuccess)
+    for (int t = 0; t < rows; ++t)
+      if (hipMemcpy(out + (size_t)t * n, p->trace + (size_t)t * cap, (size_t)n * 8, hipMemcpyDeviceToHost) != hipSuccess)
         return -1;
   return n;
 }
