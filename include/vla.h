@@ -200,7 +200,8 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *    not the integration's.  0 = off.
  *  VLA_OPT_TRACE: 1 = the persistent kernel records a phase timeline (the
  *    100 MHz device clock before and after every barrier, one workgroup per
- *    team); read it with vla_test_persist_trace (vla_test.h).
+ *    team); 2 = every workgroup records its first 256 marks; read it with
+ *    vla_test_persist_trace (vla_test.h).
  *  VLA_OPT_ATTN_SPLITS: work split of the attention launches of loop modes
  *    0 and 1: key splits (value % 100, 1..64) and head groups per K/V head
  *    (value / 100, 1..8); 0 in either part = automatic (default 0).

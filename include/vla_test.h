@@ -101,8 +101,10 @@ vla_status vla_test_time_cond(struct vla_model* model, const float* t_schedule, 
 /* Phase timeline of the model's last persistent vla_denoise call made with
  * VLA_OPT_TRACE = 1: for each of the 8 teams, max_per_team 100 MHz clock
  * values (before and after every barrier, in order; unused entries hold
- * stale data) copied to out [8][max_per_team] (host).  Synchronises the
- * device.  Returns the entries copied per team, or -1 if nothing was traced. */
+ * stale data) copied to out [8][max_per_team] (host).  With VLA_OPT_TRACE = 2
+ * every workgroup records its first 256 marks: out [256][n], row
+ * team * 32 + rank, n = min(max_per_team, 256).  Synchronises the device.
+ * Returns the entries copied per row, or -1 if nothing was traced. */
 int32_t vla_test_persist_trace(struct vla_model* model, uint64_t* out, int32_t max_per_team);
 
 #ifdef __cplusplus

@@ -308,10 +308,13 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   const bf16_t* kvbase = reinterpret_cast<const bf16_t*>(a.cp->kv_cache);
 
   Sync sy{a.sync, a.err, 0u, a.spin_limit};
-  unsigned long long* trace = (a.trace && rank == 0) ? a.trace + (size_t)team * PERSIST_TRACE_MAX : nullptr;
+  unsigned long long* trace = !a.trace ? nullptr
+                              : a.trace_all ? a.trace + (size_t)(team * TSIZE + rank) * PERSIST_TRACE_WG
+                              : (rank == 0 ? a.trace + (size_t)team * PERSIST_TRACE_MAX : nullptr);
+  const int tcap = a.trace_all ? PERSIST_TRACE_WG : PERSIST_TRACE_MAX;
   int tev = 0;
   auto mark = [&]() {
-    if (trace && tid == 0 && tev < PERSIST_TRACE_MAX) trace[tev] = __builtin_amdgcn_s_memrealtime();
+    if (trace && tid == 0 && tev < tcap) trace[tev] = __builtin_amdgcn_s_memrealtime();
     ++tev;
   };
   // A barrier timed out: leave, marking the chunk as failed (NaN).

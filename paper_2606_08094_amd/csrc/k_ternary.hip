@@ -454,7 +454,7 @@ struct TRing {
   static constexpr int SX = BM * 8;        // 16-byte slots of codes per stage
   static constexpr int SW = BN * 2;        // 16-byte slots of packed weights per stage
   static constexpr int SB = SX + SW;
-  static constexpr int NST = 4;
+  static constexpr int NST = 4;   // 80 KB / 48 KB of LDS: two or three workgroups fit a CU
   static constexpr int LX = SX / 256;      // code loads per thread and slice (weights: one)
 };
 
@@ -462,14 +462,9 @@ template <int MS>
 __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
   using R = TRing<MS>;
   constexpr int BM = R::BM, BN = R::BN, SX = R::SX, SB = R::SB, NST = R::NST, LX = R::LX, D = NST - 1;
-  __shared__ v4u st0[SB], st1[SB], st2[SB], st3[SB];
-  auto stage = [&](auto j) -> v4u* {
-    constexpr int J = decltype(j)::value;
-    if constexpr (J == 0) return st0;
-    else if constexpr (J == 1) return st1;
-    else if constexpr (J == 2) return st2;
-    else return st3;
-  };
+  static_assert((D - 1) * (LX + 1) < 64, "vmcnt range");
+  __shared__ v4u ring[NST][SB];
+  auto stage = [&](auto j) -> v4u* { return ring[decltype(j)::value]; };
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
   const int wm = wave >> 1, wn = wave & 1;

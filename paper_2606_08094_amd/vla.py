@@ -248,17 +248,19 @@ class Model:
         denoise call of this model failed on the device."""
         _check(lib().vla_model_check(self.handle, _stream(stream)))
 
-    def set_trace(self, on: bool):
-        """Record the persistent kernel's phase timeline on the next calls."""
-        _check(lib().vla_model_set_option(self.handle, VLA_OPT_TRACE, int(bool(on))))
+    def set_trace(self, mode):
+        """Record the persistent kernel's phase timeline on the next calls:
+        0 off, 1 one workgroup per team, 2 every workgroup (first 256 marks)."""
+        _check(lib().vla_model_set_option(self.handle, VLA_OPT_TRACE, int(mode)))
 
-    def trace_read(self):
-        """[8][PERSIST_TRACE_MAX] uint64 clock values (100 MHz) of the last
-        traced persistent call, or None."""
+    def trace_read(self, all_workgroups: bool = False):
+        """uint64 clock values (100 MHz) of the last traced persistent call:
+        [8][PERSIST_TRACE_MAX] (mode 1) or [256][256] (mode 2); None if none."""
         import numpy as np
-        out = np.zeros((8, PERSIST_TRACE_MAX), np.uint64)
+        shape = (256, 256) if all_workgroups else (8, PERSIST_TRACE_MAX)
+        out = np.zeros(shape, np.uint64)
         n = lib().vla_test_persist_trace(self.handle, out.ctypes.data_as(ctypes.POINTER(ctypes.c_uint64)),
-                                         PERSIST_TRACE_MAX)
+                                         shape[1])
         return None if n < 0 else out
 
     def profile_read(self) -> List[dict]:
