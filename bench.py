@@ -428,6 +428,12 @@ def main():
     ap.add_argument("--copy-mb", type=int, default=0,
                     help="only run 5 plain device-to-device copies of this many MiB (calibrates the "
                          "rocprofv3 FETCH_SIZE / WRITE_SIZE counters against a known byte count)")
+    ap.add_argument("--read-mb", type=int, default=0,
+                    help="only run 5 read-only passes (a sum) over this many MiB (a second calibration of the "
+                         "FETCH_SIZE counter, with no write stream beside the reads)")
+    ap.add_argument("--prefill-only", default="",
+                    help="with --chunks K: just run K prefills of this backbone (pi0_vlm_bf16 or bitnet_w2a8), "
+                         "no timing (a light target for profilers)")
     ap.add_argument("--variant", default="",
                     help="with --workloads: comma list of architecture variants applied to every "
                          "workload: state_token, causal_self, rope (base 10000)")
@@ -448,6 +454,28 @@ def main():
         return
     if args.ternary_ablation:
         ternary_ablation()
+        return
+    if args.read_mb > 0:
+        import torch
+        x = torch.ones(args.read_mb << 18, dtype=torch.float32, device="cuda")
+        tot = 0.0
+        for _ in range(5):
+            tot += float(x.sum())
+        torch.cuda.synchronize()
+        print(json.dumps({"read_mib": args.read_mb, "passes": 5, "sum": tot}))
+        return
+    if args.prefill_only:
+        import torch
+        import workloads as wl
+        from vla_testlib import Prefill
+        bcfg = wl.BACKBONES[args.prefill_only]
+        log(f"prefill {bcfg.name}: generating weights ...")
+        pre = Prefill(bcfg, wl.make_backbone_weights(bcfg), wl.make_prefix_embeds(bcfg, 1))
+        for _ in range(max(1, args.chunks)):
+            pre.run()
+        torch.cuda.synchronize()
+        pre.close()
+        print(json.dumps({"prefill": bcfg.name, "runs": max(1, args.chunks)}))
         return
     if args.copy_mb > 0:
         import torch
