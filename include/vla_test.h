@@ -47,6 +47,13 @@ vla_status vla_test_attention(int32_t elem, int32_t mode, const void* q, const v
  * q [M][K] int8, r [M] fp32. */
 vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q, float* r, void* stream);
 
+/* The same quantiser on bf16 rows with a row pitch: x [M][ldx] bf16 bits
+ * (ldx >= K, K <= 16384) -> q [M][K] int8, r [M] fp32.  Rows whose values
+ * fill whole aligned 16-byte vectors take the register-resident kernel,
+ * others the looping one; both give the same codes. */
+vla_status vla_test_quantize_bf16(const uint16_t* x, int32_t M, int32_t K, int32_t ldx, int8_t* q, float* r,
+                                  void* stream);
+
 /* W2A8 linear: quantise x [M][K] fp32 per token, multiply by the packed
  * ternary w [N][K/4] (K % 64 == 0) and dequantise with the per-tensor scale
  * `scale`: y [M][N] fp32 = acc * scale * r_m / 127. */

@@ -1679,6 +1679,20 @@ vla_status vla_test_quantize_i8(const float* x, int32_t M, int32_t K, int8_t* q,
   return VLA_OK;
 }
 
+vla_status vla_test_quantize_bf16(const uint16_t* x, int32_t M, int32_t K, int32_t ldx, int8_t* q, float* r,
+                                  void* stream) {
+  if (!x || !q || !r) return fail(VLA_E_ARG, "NULL buffer");
+  if (M < 1 || K < 1 || K > 16384 || ldx < K) return fail(VLA_E_SHAPE, "bad shape");
+  QuantArgs a{};
+  a.M = M; a.K = K; a.x = x; a.ldx = ldx; a.src_type = 1; a.q = q; a.r = r;
+  hipStream_t s = reinterpret_cast<hipStream_t>(stream);
+  hipError_t e = launch_quantize(a, s);
+  hipError_t e2 = hipStreamSynchronize(s);
+  if (e != hipSuccess || e2 != hipSuccess)
+    return fail(VLA_E_DEVICE, "quantize: %s", hipGetErrorString(e != hipSuccess ? e : e2));
+  return VLA_OK;
+}
+
 vla_status vla_test_ternary_linear(const float* x, const uint8_t* w_packed, int32_t M, int32_t N, int32_t K,
                                    float scale, float* y, void* stream) {
   if (!x || !w_packed || !y || !al16(x) || !al16(w_packed) || !al16(y)) return fail(VLA_E_ARG, "bad buffer");

@@ -36,7 +36,7 @@ OP_KINDS = {0: "gemm", 1: "gemm_glu", 2: "attention", 3: "ternary_gemm", 4: "qua
 EXPORTS = ["vla_weight_count", "vla_model_create", "vla_model_destroy", "vla_model_check", "vla_kv_cache_bytes",
            "vla_prefix_kv_build", "vla_prefix_kv_build_noalloc", "vla_denoise", "vla_ternary_gemm", "vla_model_set_option",
            "vla_last_error", "vla_status_string", "vla_profile_read",
-           "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_ternary_linear",
+           "vla_test_gemm", "vla_test_attention", "vla_test_quantize_i8", "vla_test_quantize_bf16", "vla_test_ternary_linear",
            "vla_test_ternary_gemm", "vla_test_rope",
            "vla_test_adarms", "vla_test_time_cond", "vla_test_persist_trace",
            "vla_backbone_weight_count", "vla_backbone_create", "vla_backbone_destroy", "vla_prefix_prefill"]
@@ -95,6 +95,7 @@ def lib():
         "vla_test_gemm": (i32, [i32, vp, vp, i32, i32, i32, i32, vp, vp]),
         "vla_test_attention": (i32, [i32, i32, vp, vp, vp, vp, vp, i32, i32, i32, i32, i32, i32, i32, vp, vp]),
         "vla_test_quantize_i8": (i32, [vp, i32, i32, vp, vp, vp]),
+        "vla_test_quantize_bf16": (i32, [vp, i32, i32, i32, vp, vp, vp]),
         "vla_test_adarms": (i32, [i32, vp, vp, i32, vp, vp, vp, i32, i32, ctypes.c_float, vp, i32, vp]),
         "vla_test_time_cond": (i32, [vp, ctypes.POINTER(ctypes.c_float), i32, vp, vp, vp]),
         "vla_test_ternary_linear": (i32, [vp, vp, i32, i32, i32, ctypes.c_float, vp, vp]),
@@ -328,6 +329,10 @@ def test_time_cond(model: "Model", t_schedule: Sequence[float], mods, modf, stre
 
 def test_quantize_i8(x, M: int, K: int, q, r, stream=None):
     _check(lib().vla_test_quantize_i8(_ptr(x), M, K, _ptr(q), _ptr(r), _stream(stream)))
+
+
+def test_quantize_bf16(x, M: int, K: int, ldx: int, q, r, stream=None):
+    _check(lib().vla_test_quantize_bf16(_ptr(x), M, K, ldx, _ptr(q), _ptr(r), _stream(stream)))
 
 
 def test_ternary_linear(x, w_packed, M: int, N: int, K: int, scale: float, y, stream=None):

@@ -278,13 +278,18 @@ def test_time_cond_parity(torch, name):
             assert np.all(np.abs(got_f[k] - flat_f) <= bfm), np.abs(got_f[k] - flat_f).max()
 
 
-def test_quantize_i8_bit_exact(torch):
-    rows, codes = [], []
+def _tie_rows():
     import os
+    rows = []
     for line in open(os.path.join(os.path.dirname(__file__), "golden", "quantizer_ties.txt")):
         if line.startswith("row:"):
             rows.append([float(v) for v in line.split()[1:]])
-    K = 300
+    return rows
+
+
+@pytest.mark.parametrize("K", [300, 301])   # whole 16-byte vectors / a ragged row (looping kernel)
+def test_quantize_i8_bit_exact(torch, K):
+    rows = _tie_rows()
     x = wl.random_matrix((37, K), 5, 3.0)
     for i, r in enumerate(rows):
         x[i, :] = 0
@@ -294,6 +299,31 @@ def test_quantize_i8_bit_exact(torch):
     rd = torch.empty(37, dtype=torch.float32, device="cuda")
     _vla().test_quantize_i8(_dev(torch, x), 37, K, qd, rd)
     q_ref, r_ref = O.quantize_int8_rows(x)
+    assert np.array_equal(qd.cpu().numpy(), q_ref)
+    assert np.array_equal(rd.cpu().numpy(), r_ref)
+
+
+# (M, K, row pitch): the W2A8 expert's O / down inputs, the largest row, a
+# pitched row, and rows the register-resident kernel does not take (K or the
+# pitch not a multiple of 8 values)
+@pytest.mark.parametrize("M,K,ldx", [(8, 2560, 2560), (8, 6912, 6912), (37, 16384, 16384), (512, 6912, 6912),
+                                     (9, 256, 264), (5, 130, 130), (3, 136, 140)])
+def test_quantize_bf16_rows_bit_exact(torch, M, K, ldx):
+    """bf16 rows (the attention output and the GLU output of the W2A8 path)
+    quantise to the oracle's codes and scales exactly: the bf16 values are
+    exact in fp32, so both sides quantise the same numbers."""
+    x = wl.random_matrix((M, ldx), 17 + K, 2.0)
+    rows = _tie_rows()
+    for i, r in enumerate(rows[:max(0, M - 1)]):
+        x[i, :] = 0
+        x[i, :min(len(r), K)] = r[:K]
+    if M > len(rows):
+        x[len(rows), :] = 0.0
+    xb = wl.round_bf16(x)
+    qd = torch.empty((M, K), dtype=torch.int8, device="cuda")
+    rd = torch.empty(M, dtype=torch.float32, device="cuda")
+    _vla().test_quantize_bf16(_dev(torch, xb, bf16=True), M, K, ldx, qd, rd)
+    q_ref, r_ref = O.quantize_int8_rows(np.ascontiguousarray(xb[:, :K]))
     assert np.array_equal(qd.cpu().numpy(), q_ref)
     assert np.array_equal(rd.cpu().numpy(), r_ref)
 
