@@ -454,7 +454,9 @@ struct TRing {
   static constexpr int SX = BM * 8;        // 16-byte slots of codes per stage
   static constexpr int SW = BN * 2;        // 16-byte slots of packed weights per stage
   static constexpr int SB = SX + SW;
-  static constexpr int NST = 4;   // 80 KB / 48 KB of LDS: two or three workgroups fit a CU
+  // 80 / 48 / 32 KB of LDS (MS = 4 / 2 / 1): two or more workgroups fit a CU.
+  // Eight stages time the same as four here.
+  static constexpr int NST = 4;
   static constexpr int LX = SX / 256;      // code loads per thread and slice (weights: one)
 };
 
@@ -625,6 +627,17 @@ hipError_t tile_launch(const TernArgs& a0, hipStream_t s) {
 
 bool tern_tile_eligible(int M, int N, int K) { return M >= 128 && N >= 1 && K >= 128 && K % 128 == 0; }
 
+hipError_t launch_ternary_tile(const TernArgs& a, int ms, hipStream_t s) {
+  if (a.M <= 0 || a.N <= 0) return hipSuccess;
+  if (!tern_tile_eligible(a.M, a.N, a.K) || a.nsplit > 1) return hipErrorInvalidValue;
+  switch (ms) {
+    case 1: return tile_launch<1>(a, s);
+    case 2: return tile_launch<2>(a, s);
+    case 4: return tile_launch<4>(a, s);
+    default: return hipErrorInvalidValue;
+  }
+}
+
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (a.K % 64 != 0) {
@@ -636,9 +649,11 @@ hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t
   }
   const int nsub = (a.rscale != nullptr && a.e.epi == EPI_GLU) ? 2 : 1;
   if (a.nsplit <= 1 && tern_tile_eligible(a.M, a.N, a.K)) {
-    // many token rows: the tiled kernel; 128-row tiles once they fill the device
-    const long long t4 = (long long)((a.M + 127) / 128) * ((a.N + 127) / 128);
-    return t4 >= 256 ? tile_launch<4>(a, s) : tile_launch<2>(a, s);
+    // many token rows: the tiled kernel; 128-row tiles once they fill the
+    // device, 32-row tiles when 64-row ones would leave half of it idle
+    const long long nt = (a.N + 127) / 128;
+    const long long t4 = (long long)((a.M + 127) / 128) * nt, t2 = (long long)((a.M + 63) / 64) * nt;
+    return t4 >= 256 ? tile_launch<4>(a, s) : t2 >= 128 ? tile_launch<2>(a, s) : tile_launch<1>(a, s);
   }
   if (a.rscale != nullptr && a.M <= 64) {  // token rows of the denoise loop: the skinny kernel
     const int sms = a.M <= 16 ? 1 : (a.M <= 32 ? 2 : 4);

@@ -416,6 +416,38 @@ def test_ternary_gemm_dot4_matches_mfma(torch, M, N, K):
     np.testing.assert_allclose(ys[1], ref, rtol=1e-6, atol=1e-7)
 
 
+TILE_VARIANTS = {2: "32-row tiles", 3: "64-row tiles", 4: "128-row tiles"}
+
+
+@pytest.mark.parametrize("M,N,K", [(512, 2560, 2560), (512, 2560, 6912), (512, 3840, 2560), (300, 200, 640),
+                                   (129, 130, 128), (160, 1000, 384)])
+def test_ternary_tile_configurations_identical(torch, M, N, K):
+    """Every row-tile height of the many-row tiled kernel (ragged row and
+    column tiles included) gives the library launch's
+    dequantised outputs bit for bit (exact int32 sums), and those match the
+    oracle's exact sum to fp32 rounding."""
+    x = wl.random_matrix((M, K), 7 + M + K, 1.0)
+    q, r = O.quantize_int8_rows(x)
+    q[0, :] = -128
+    w = wl.random_ternary((N, K), 8 + N)
+    wp = wl.pack_ternary(w)
+    wscale = (0.01 + 0.02 * (np.arange(N) % 5) / 5.0).astype(np.float32)
+    acc = O.ternary_gemm(q, wp, K)
+    ref = acc.astype(np.float64) * (wscale.astype(np.float64)[None, :] * r.astype(np.float64)[:, None] / 127.0)
+    qd = torch.from_numpy(np.ascontiguousarray(q)).cuda()
+    rd = torch.from_numpy(r).cuda()
+    wd = torch.from_numpy(wp).cuda()
+    sd = torch.from_numpy(wscale).cuda()
+    ys = {}
+    for variant in [0] + sorted(TILE_VARIANTS):
+        y = torch.full((M, N), float("nan"), dtype=torch.float32, device="cuda")
+        _vla().test_ternary_gemm(qd, rd, wd, sd, M, N, K, variant, y)
+        ys[variant] = y.cpu().numpy()
+    np.testing.assert_allclose(ys[0], ref, rtol=1e-6, atol=1e-7)
+    for v in TILE_VARIANTS:
+        assert np.array_equal(ys[v], ys[0]), TILE_VARIANTS[v]
+
+
 @pytest.mark.parametrize("M,N,K", [(8, 3840, 2560), (8, 2560, 6912), (512, 1280, 2560), (13, 70, 128),
                                    (56, 2560, 2560), (20, 512, 6912), (40, 200, 320), (64, 48, 64),
                                    (512, 13824, 2560), (512, 2560, 6912), (300, 200, 640), (129, 130, 128)])
