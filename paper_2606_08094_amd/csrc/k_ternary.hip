@@ -439,8 +439,10 @@ namespace {
 // ---------------------------------------------------------------------------
 // tern_tile: the W2A8 GEMM with many token rows (the backbone prefill and the
 // prefix K/V build, M = B * P), where the int8 matrix cores, not the weight
-// bytes, set the pace.  A 2 x 2 wave workgroup owns a (32 MS) x 128 output
-// tile.  128-deep K-slices of the activation codes (BM rows x 128 bytes) and of
+// bytes, set the pace.  A workgroup owns a (32 MS) x 128 output tile; wave w
+// owns its columns 32 w .. 32 w + 31 over all of its rows, so each packed
+// weight dword is widened by one wave only (widening costs more vector-ALU
+// instructions than the MFMAs it feeds).  128-deep K-slices of the activation codes (BM rows x 128 bytes) and of
 // the packed weights (128 rows x 32 bytes) stream into a ring of NST LDS
 // stages by direct-to-LDS loads, NST - 1 slices ahead of the MFMAs.  Code rows
 // are XOR-swizzled (16-byte chunk c of row r at c ^ (r % 8)), weight rows swap
@@ -469,7 +471,7 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
   auto stage = [&](auto j) -> v4u* { return ring[decltype(j)::value]; };
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;
+  constexpr int RS = 2 * MS;               // 16-row subtiles of the tile, all in every wave
   const int M = a.M, N = a.N, K = a.K, KB = K / 4;
   const int per = gridDim.x >> 3;
   const int u = (blockIdx.x & 7) * per + (blockIdx.x >> 3);   // tiles of one W column block stay on one XCD
@@ -497,26 +499,26 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
     dma16(wsrc + sl * 32, b + SX + wave * 64);
   };
 
-  i32x4 acc[MS][4];
+  i32x4 acc[RS][2];
 #pragma unroll
-  for (int ms = 0; ms < MS; ++ms)
+  for (int ms = 0; ms < RS; ++ms)
 #pragma unroll
-    for (int ns = 0; ns < 4; ++ns) acc[ms][ns] = i32x4{0, 0, 0, 0};
+    for (int ns = 0; ns < 2; ++ns) acc[ms][ns] = i32x4{0, 0, 0, 0};
 
   // MFMA kk of a slice: lane group g4 holds k = 64 kk + 16 g4 .. + 15 of both operands
   auto compute = [&](const v4u* b) {
-    v4u xf[2][MS];
-    uint32_t wp[2][4];
+    v4u xf[2][RS];
+    uint32_t wp[2][2];
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk) {
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) {
-        const int row = wm * 16 * MS + ms * 16 + r16;
+      for (int ms = 0; ms < RS; ++ms) {
+        const int row = ms * 16 + r16;
         xf[kk][ms] = b[row * 8 + ((kk * 4 + g4) ^ (row & 7))];
       }
 #pragma unroll
-      for (int ns = 0; ns < 4; ++ns) {
-        const int row = wn * 64 + ns * 16 + r16;
+      for (int ns = 0; ns < 2; ++ns) {
+        const int row = wave * 32 + ns * 16 + r16;
         const uint32_t* slot = reinterpret_cast<const uint32_t*>(b + SX + row * 2 + (kk ^ ((row >> 3) & 1)));
         wp[kk][ns] = slot[g4];
       }
@@ -525,10 +527,10 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
 #pragma unroll
     for (int kk = 0; kk < 2; ++kk)
 #pragma unroll
-      for (int ns = 0; ns < 4; ++ns) {
+      for (int ns = 0; ns < 2; ++ns) {
         const i32x4 w = unpack_signed(wp[kk][ns]);
 #pragma unroll
-        for (int ms = 0; ms < MS; ++ms)
+        for (int ms = 0; ms < RS; ++ms)
           acc[ms][ns] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[kk][ms]), w, acc[ms][ns],
                                                                0, 0, 0);
       }
@@ -556,15 +558,15 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
     }(std::make_integer_sequence<int, NST>{});
   }
 
-  const int mw = m0 + wm * 16 * MS, nw = n0 + wn * 64;
+  const int nw = n0 + wave * 32;
   if (a.rscale == nullptr) {   // raw int32 sums
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms)
+    for (int ms = 0; ms < RS; ++ms)
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        const int m = mw + ms * 16 + g4 * 4 + i;
+        const int m = m0 + ms * 16 + g4 * 4 + i;
 #pragma unroll
-        for (int ns = 0; ns < 4; ++ns) {
+        for (int ns = 0; ns < 2; ++ns) {
           const int n = nw + ns * 16 + r16;
           if (m < M && n < N) a.acc_out[(size_t)m * N + n] = acc[ms][ns][i];
         }
@@ -572,43 +574,32 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
     return;
   }
   // y = acc * (s_w * r_m / 127) (the dequantisation of the other W2A8 kernels)
-  float sw[4];
+  float sw[2];
 #pragma unroll
-  for (int ns = 0; ns < 4; ++ns) {
+  for (int ns = 0; ns < 2; ++ns) {
     const int n = nw + ns * 16 + r16;
     sw[ns] = (n < N) ? a.wscale[n] : 0.0f;
   }
-  f32x4 y[MS][4];
+  f32x4 y[RS][2];
 #pragma unroll
-  for (int ms = 0; ms < MS; ++ms)
+  for (int ms = 0; ms < RS; ++ms)
 #pragma unroll
     for (int i = 0; i < 4; ++i) {
-      const int m = mw + ms * 16 + g4 * 4 + i;
+      const int m = m0 + ms * 16 + g4 * 4 + i;
       const float rm = (m < M) ? a.rscale[m] : 0.0f;
 #pragma unroll
-      for (int ns = 0; ns < 4; ++ns) y[ms][ns][i] = (float)acc[ms][ns][i] * (sw[ns] * rm / 127.0f);
+      for (int ns = 0; ns < 2; ++ns) y[ms][ns][i] = (float)acc[ms][ns][i] * (sw[ns] * rm / 127.0f);
     }
-  if (a.e.epi == EPI_GLU) {          // gate / up 16-row blocks pair up at 32-row boundaries
+  if (a.e.epi == EPI_RESID) {         // one 16-column subtile at a time
 #pragma unroll
-    for (int j = 0; j < 2; ++j) {
-      f32x4 yp[MS][2];
+    for (int ns = 0; ns < 2; ++ns) {
+      f32x4 y1[RS][1];
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) {
-        yp[ms][0] = y[ms][2 * j];
-        yp[ms][1] = y[ms][2 * j + 1];
-      }
-      wave_epilogue<bf16_t, MS, 2>(a.e, yp, mw, nw + 32 * j, 0);
+      for (int ms = 0; ms < RS; ++ms) y1[ms][0] = y[ms][ns];
+      wave_epilogue<bf16_t, RS, 1>(a.e, y1, m0, nw + 16 * ns, 0);
     }
-  } else if (a.e.epi == EPI_RESID) {  // one 16-column subtile at a time
-#pragma unroll
-    for (int ns = 0; ns < 4; ++ns) {
-      f32x4 y1[MS][1];
-#pragma unroll
-      for (int ms = 0; ms < MS; ++ms) y1[ms][0] = y[ms][ns];
-      wave_epilogue<bf16_t, MS, 1>(a.e, y1, mw, nw + 16 * ns, 0);
-    }
-  } else {
-    wave_epilogue<bf16_t, MS, 4>(a.e, y, mw, nw, 0);
+  } else {                            // GLU: the wave's 32 columns are one gate / up pair of 16-row blocks
+    wave_epilogue<bf16_t, RS, 2>(a.e, y, m0, nw, 0);
   }
 }
 
