@@ -223,20 +223,24 @@ def cpu_baseline(cfg, W, inp):
 
 def cpu_baseline_all():
     """The oracle on every scope workload (tiny fp32, pi0-, SmolVLA-shaped,
-    ternary W2A8, stress batch 1), one BLAS thread and all: one JSON line each."""
+    ternary W2A8, stress batch 1), one BLAS thread and all, then the stress
+    workload at batch 2 (the oracle's cost grows with the batch, so larger
+    batches are quoted per request): one JSON line each."""
     import workloads as wl
     env = cpu_env()
-    for name in ("tiny_f32", "pi0_bf16", "smolvla_bf16", "ternary_w2a8", "stress_pi0"):
-        cfg = wl.CONFIGS[name]
+    for name, batch in (("tiny_f32", 1), ("pi0_bf16", 1), ("smolvla_bf16", 1), ("ternary_w2a8", 1),
+                        ("stress_pi0", 1), ("stress_pi0", 2)):
+        cfg = wl.CONFIGS[name].with_(batch=batch)
         W = wl.make_weights(cfg)
-        inp = wl.make_batch(cfg, 1)
-        for threads in (None, 1):
+        inp = wl.make_batch(cfg, batch)
+        for threads in ((None, 1) if batch == 1 else (None,)):
             b, f, st = oracle_fit(cfg, W, inp, threads)
             chunk = b + f + cfg.n_steps * st
-            print(json.dumps({"cpu_oracle": name, "threads": threads or env["blas_threads"], "T": cfg.n_steps,
-                              "build_s": round(b, 4), "fixed_s": round(f, 4), "step_s": round(st, 4),
-                              "chunk_s": round(chunk, 3), "chunks_per_s": round(1.0 / chunk, 5),
-                              "env": env}), flush=True)
+            print(json.dumps({"cpu_oracle": name, "batch": batch, "threads": threads or env["blas_threads"],
+                              "T": cfg.n_steps, "build_s": round(b, 4), "fixed_s": round(f, 4),
+                              "step_s": round(st, 4), "chunk_s": round(chunk, 3),
+                              "chunks_per_s": round(1.0 / chunk, 5),
+                              "per_request_chunk_s": round(chunk / batch, 3), "env": env}), flush=True)
 
 
 def measure_workload(torch, wl, Pipeline, name, batch, reps, variant=None):
