@@ -270,9 +270,15 @@ def measure_workload(torch, wl, Pipeline, name, batch, reps, variant=None):
         pipe.denoise(tau)
         torch.cuda.synchronize()
         ops = pipe.model.profile_read()
+        n_ops_1 = len(ops)
+        if T > 1:   # launches of one extra solver step: a T = 1 call's count against the T call's
+            pipe.denoise(wl.uniform_schedule(1))
+            torch.cuda.synchronize()
+            n_ops_1 = len(pipe.model.profile_read())
         pipe.model.set_profile(0)
     finally:
         pipe.close()
+    launches_step = (len(ops) - n_ops_1) / (T - 1) if T > 1 else len(ops)
     step_bytes = sum(o["bytes"] for o in ops) / T
     step_flops = sum(o["flops"] for o in ops) / T
     roof = roofline_from_profile(ops, T)
@@ -282,7 +288,8 @@ def measure_workload(torch, wl, Pipeline, name, batch, reps, variant=None):
             "step_hbm_frac": round(step_bytes / (step_ms * 1e-3) / 1e9 / HBM_PEAK_GBS, 4),
             "step_mfma_frac": round(step_flops / (step_ms * 1e-3) / 1e12 / BF16_PEAK_TFLOPS, 4),
             "dominant_kernel": roof["kernel"], "dominant_launch_us": roof["launch_us"],
-            "dominant_frac_hbm": roof["frac"], "dominant_share": roof["share_of_profiled_time"]}
+            "dominant_frac_hbm": roof["frac"], "dominant_share": roof["share_of_profiled_time"],
+            "launches_per_chunk": len(ops), "launches_per_step": round(launches_step, 1)}
 
 
 INT8_PEAK_TOPS = 5000.0       # dense int8 MFMA

@@ -146,6 +146,28 @@ def _tern(n_layers, **scale_of):
     return bcfg, W, wl.make_prefix_embeds(bcfg, 1)
 
 
+@pytest.mark.parametrize("P,B,seed", [(77, 2, 9300), (50, 1, 9400), (200, 1, 9500)])
+def test_ternary_prefill_small_batched(torch, P, B, seed):
+    """Two W2A8 layers at small widths (d 512, 4 x 128 heads over 2 K/V heads,
+    ReLU^2-GLU 1536), both branches on: 154 rows of two requests (the tiled
+    W2A8 kernel with a ragged last row tile), 50 rows (the few-row kernel) and
+    200 rows.  The CPU study with the kernels' bf16 storage points emulated
+    gives max 9.6e-3 / mean 1.4e-3 on these cases; the bf16 output adds up to
+    2^-9 relative.  The layers move the hidden states by mean 0.10."""
+    bcfg = wl.BITNET_W2A8.with_(name="tern_small", n_layers=2, d_model=512, n_heads=4, head_dim=128,
+                                n_kv_heads=2, d_ff=1536, prefix_len=P, seed_base=seed)
+    W = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, B)
+    got = _prefill(bcfg, W, e)
+    ref = O.prefix_prefill(bcfg, W, e)
+    _cmp(f"ternary small P={P} B={B}", got, ref, 4e-2, 6e-3)
+    W0 = dict(W)
+    for l in range(2):
+        W0[f"B{l}.W_o.scale"] = np.float32(0.0)
+        W0[f"B{l}.W_d.scale"] = np.float32(0.0)
+    assert np.abs(ref - O.prefix_prefill(bcfg, W0, e)).mean() > 0.05
+
+
 def test_ternary_prefill_mlp_branch(torch):
     """One BitNet-width W2A8 layer (d 2560, 20 x 128 heads over 5 K/V heads,
     ReLU^2-GLU 6912, 512 rows) with the attention branch off (W_o scale 0):
