@@ -22,8 +22,9 @@ extern "C" {
  * launch of the residual projections: split-K fp32 partials (the runtime's
  * split and tile), summed into y by the library (VLA_E_UNSUPPORTED for fp32
  * with M > 128; a temporary partial buffer is allocated and freed),
- * 10..13 = the tiled kernel with tile 64x128, 128x128, 256x128 or 128x256
- * (both VLA_E_UNSUPPORTED unless bf16 with M > 128). */
+ * 10..14 = the tiled kernel with tile 64x128, 128x128, 256x128, 128x256 or
+ * 256x256 (eight waves; needs K % 64 == 0) (VLA_E_UNSUPPORTED unless bf16
+ * with M > 128, and for 256x256 with K % 64 != 0). */
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                          int32_t variant, float* y, void* stream);
 

@@ -228,6 +228,9 @@ __global__ __launch_bounds__(256) void gemm_wide(GemmArgs a) {
 
 // ---------------------------------------------------------------------------
 constexpr int TBK = 64;           // K-slice of gemm_tile
+#ifndef GEMM_TILE88_SLICE_US
+#define GEMM_TILE88_SLICE_US 1.6   // modelled time of one 64-wide K-slice of the 256 x 256 tile
+#endif
 constexpr int TPITCH = TBK + 8;   // LDS row pitch in elements (16 bytes of padding)
 
 // LDS of gemm_tile_rs: two K-slice buffers of X and W rows, reused for the
@@ -268,30 +271,30 @@ VLA_DEV float4 act4(int act, float4 v) { return make_float4(act_f(act, v.x), act
 // rows (nv = columns left in the matrix from n, v = the tile's 4 values; for
 // GLU the 4 gate and 4 up values come as g and u).  The loop is unrolled with
 // every LDS read issued before the first store.
-template <int RP, int BN, int CP, typename Fn>
+template <int RP, int BN, int CP, int NT, typename Fn>
 VLA_DEV void epi_rows(const float* ct, int rows, int n0, int N, Fn&& f) {
-  constexpr int TPR = BN / 4, IT = (RP * TPR + 255) / 256;
+  constexpr int TPR = BN / 4, IT = (RP * TPR + NT - 1) / NT;
   float4 v[IT];
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const int idx = threadIdx.x + 256 * j;
+    const int idx = threadIdx.x + NT * j;
     const int r = idx / TPR, c = (idx % TPR) * 4;
     v[j] = (r < RP) ? *reinterpret_cast<const float4*>(ct + r * CP + c) : make_float4(0.f, 0.f, 0.f, 0.f);
   }
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const int idx = threadIdx.x + 256 * j;
+    const int idx = threadIdx.x + NT * j;
     const int r = idx / TPR, c = (idx % TPR) * 4;
     if (r < rows && n0 + c < N) f(r, n0 + c, N - (n0 + c), v[j]);
   }
 }
-template <int RP, int BN, int CP, typename Fn>
+template <int RP, int BN, int CP, int NT, typename Fn>
 VLA_DEV void epi_rows_glu(const float* ct, int rows, int f0, int F, Fn&& f) {
-  constexpr int TPR = BN / 8, IT = (RP * TPR + 255) / 256;
+  constexpr int TPR = BN / 8, IT = (RP * TPR + NT - 1) / NT;
   float4 g[IT], u[IT];
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const int idx = threadIdx.x + 256 * j;
+    const int idx = threadIdx.x + NT * j;
     const int r = idx / TPR, c = (idx % TPR) * 4;
     const int cg = (c >> 4) * 32 + (c & 15);
     g[j] = (r < RP) ? *reinterpret_cast<const float4*>(ct + r * CP + cg) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -299,13 +302,13 @@ VLA_DEV void epi_rows_glu(const float* ct, int rows, int f0, int F, Fn&& f) {
   }
 #pragma unroll
   for (int j = 0; j < IT; ++j) {
-    const int idx = threadIdx.x + 256 * j;
+    const int idx = threadIdx.x + NT * j;
     const int r = idx / TPR, c = (idx % TPR) * 4;
     if (r < rows && f0 + c < F) f(r, f0 + c, F - (f0 + c), g[j], u[j]);
   }
 }
 
-template <int RP, int BN, int CP>
+template <int RP, int BN, int CP, int NT = 256>
 VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, int split) {
   const int M = a.M, N = a.N;
   const int rows = min(RP, M - m0);
@@ -321,7 +324,7 @@ VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, i
         if (a.out_f32) store4n(reinterpret_cast<float*>(a.out) + o, h, nv, vec);
         else store4n(reinterpret_cast<bf16_t*>(a.out) + o, h, nv, vec);
       };
-      epi_rows_glu<RP, BN, CP>(ct, rows, n0 / 2, N / 2, f);
+      epi_rows_glu<RP, BN, CP, NT>(ct, rows, n0 / 2, N / 2, f);
       break;
     }
     case EPI_STORE: {
@@ -337,14 +340,14 @@ VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, i
         if (a.out_f32) store4n(reinterpret_cast<float*>(a.out) + o, v, nv, vec);
         else store4n(reinterpret_cast<bf16_t*>(a.out) + o, v, nv, vec);
       };
-      epi_rows<RP, BN, CP>(ct, rows, n0, N, f);
+      epi_rows<RP, BN, CP, NT>(ct, rows, n0, N, f);
       break;
     }
     case EPI_PARTIAL: {
       float* out = reinterpret_cast<float*>(a.out) + (size_t)split * M * a.ldo;
       const bool vec = (a.ldo & 3) == 0;
       auto f = [&](int r, int n, int nv, float4 v) { store4n(out + (size_t)(m0 + r) * a.ldo + n, v, nv, vec); };
-      epi_rows<RP, BN, CP>(ct, rows, n0, N, f);
+      epi_rows<RP, BN, CP, NT>(ct, rows, n0, N, f);
       break;
     }
     case EPI_RESID: {
@@ -353,7 +356,7 @@ VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, i
         const float e[4] = {v.x, v.y, v.z, v.w};
         for (int j = 0; j < 4 && j < nv; ++j) xp[j] = xp[j] + a.alpha[n + j] * e[j];
       };
-      epi_rows<RP, BN, CP>(ct, rows, n0, N, f);
+      epi_rows<RP, BN, CP, NT>(ct, rows, n0, N, f);
       break;
     }
     case EPI_KVCACHE: {
@@ -372,7 +375,7 @@ VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, i
           reinterpret_cast<bf16_t*>(a.cache)[o] = f2bf(e[j]);
         }
       };
-      epi_rows<RP, BN, CP>(ct, rows, n0, N, f);
+      epi_rows<RP, BN, CP, NT>(ct, rows, n0, N, f);
       break;
     }
     case EPI_EULER: {
@@ -398,7 +401,7 @@ VLA_DEV void tile_epilogue(const GemmArgs& a, const float* ct, int m0, int n0, i
           }
         }
       };
-      epi_rows<RP, BN, CP>(ct, rows, n0, N, f);
+      epi_rows<RP, BN, CP, NT>(ct, rows, n0, N, f);
       break;
     }
     default:
@@ -522,21 +525,31 @@ __global__ __launch_bounds__(256) void gemm_tile_rs(GemmArgs a) {
 // time, so the compiler can tell the stage being read from the ones still in
 // flight and does not wait for those.  Requires K % 64 == 0 (rows beyond M
 // or N are loaded from a valid row and never stored).
-template <int MS, int NS>
+//
+// NWV = 4 waves in 2 x 2, or 8 waves in 2 x 4 for the 256 x 256 tile: the
+// same 128 x 64 wave tile, so each output sums its k-products in the same
+// order, while a workgroup's 64 KB slice feeds 128 FLOP per byte instead of
+// 85 (256 x 128).  Two stages of 64 KB fit in LDS; a slice's MFMAs (two
+// waves per SIMD) cover the next slice's load.
+template <int MS, int NS, int NWV = 4>
 struct Ring {
   static constexpr int BM = 32 * MS, BN = 32 * NS, ROWS = BM + BN;
-  static constexpr int NST = ROWS <= 256 ? 4 : 3;       // stages (LDS <= 144 KB)
-  static constexpr int LPT = ROWS * 8 / 256;            // load instructions per thread and slice
+  static constexpr int NST = ROWS <= 256 ? 4 : (ROWS <= 384 ? 3 : 2);   // stages (LDS <= 144 KB)
+  static constexpr int LPT = ROWS * 8 / (64 * NWV);     // load instructions per thread and slice
   static constexpr int SB = ROWS * 8;                   // 16-byte slots per stage
   // rows of the fp32 output tile per epilogue pass (the tile goes through stage 0)
   static constexpr int RP = (64 * (BN + 4) * 4 <= SB * 16) ? 64 : (32 * (BN + 4) * 4 <= SB * 16 ? 32 : 16);
 };
 
-template <int MS, int NS>
-__global__ __launch_bounds__(256) void gemm_tile(GemmArgs a) {
-  using R = Ring<MS, NS>;
+template <int MS, int NS, int NWV = 4>
+__global__ __launch_bounds__(64 * NWV) void gemm_tile(GemmArgs a) {
+  using R = Ring<MS, NS, NWV>;
   constexpr int BM = R::BM, BN = R::BN, NST = R::NST, LPT = R::LPT, SB = R::SB, D = NST - 1;
-  __shared__ v4u st0[SB], st1[SB], st2[SB], st3[NST > 3 ? SB : 1];
+  constexpr int WN = NWV / 2;                          // waves along N (2 along M)
+  constexpr int MSW = BM / 32, NSW = BN / (16 * WN);   // 16-row / 16-column subtiles of a wave
+  constexpr int KKB = NWV == 8 ? 1 : 2;                // k-halves whose operands are read at once
+  static_assert(LPT * 64 * NWV == R::ROWS * 8, "tile rows");
+  __shared__ v4u st0[SB], st1[SB], st2[NST > 2 ? SB : 1], st3[NST > 3 ? SB : 1];
   auto stage = [&](auto j) -> v4u* {
     constexpr int J = decltype(j)::value;
     if constexpr (J == 0) return st0;
@@ -547,7 +560,7 @@ __global__ __launch_bounds__(256) void gemm_tile(GemmArgs a) {
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int r16 = lane & 15, g4 = lane >> 4;
-  const int wm = wave >> 1, wn = wave & 1;
+  const int wm = wave / WN, wn = wave % WN;
   const int M = a.M, N = a.N, K = a.K;
   const int per = gridDim.x >> 3;
   const int u = (blockIdx.x & 7) * per + (blockIdx.x >> 3);
@@ -559,11 +572,11 @@ __global__ __launch_bounds__(256) void gemm_tile(GemmArgs a) {
   const int k0 = split * a.kper;
   const int nsl = (min(K, k0 + a.kper) - k0) / 64;
 
-  // source of this lane's slot in load instruction i: row (i*4 + wave)*8 + lane/8
+  // source of this lane's slot in load instruction i: row (i*NWV + wave)*8 + lane/8
   const bf16_t* src[LPT];
 #pragma unroll
   for (int i = 0; i < LPT; ++i) {
-    const int row = (i * 4 + wave) * 8 + (lane >> 3);
+    const int row = (i * NWV + wave) * 8 + (lane >> 3);
     const int chunk = (lane & 7) ^ (row & 7);
     if (row < BM) {
       const int m = min(m0 + row, M - 1);
@@ -576,43 +589,49 @@ __global__ __launch_bounds__(256) void gemm_tile(GemmArgs a) {
   auto issue = [&](auto j, int sl) {
     v4u* b = stage(j);
 #pragma unroll
-    for (int i = 0; i < LPT; ++i) dma16(src[i] + sl * 64, b + (i * 4 + wave) * 64);
+    for (int i = 0; i < LPT; ++i) dma16(src[i] + sl * 64, b + (i * NWV + wave) * 64);
   };
 
-  f32x4 acc[MS][NS];
+  f32x4 acc[MSW][NSW];
 #pragma unroll
-  for (int ms = 0; ms < MS; ++ms)
+  for (int ms = 0; ms < MSW; ++ms)
 #pragma unroll
-    for (int ns = 0; ns < NS; ++ns) acc[ms][ns] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int ns = 0; ns < NSW; ++ns) acc[ms][ns] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  // operand rows of this lane and their swizzled slot for logical chunk c
-  // every fragment of the slice is read before the first MFMA, so the LDS
-  // latency of the second k-half hides behind the first half's MFMAs
+  // operand rows of this lane and their swizzled slot for logical chunk c.
+  // With four waves every fragment of the slice is read before the first
+  // MFMA, so the LDS latency of the second k-half hides behind the first
+  // half's MFMAs; with eight the other wave of the SIMD hides it, and one
+  // k-half at a time keeps the registers under the two-wave limit.
   auto compute = [&](const v4u* b) {
-    v4u af[2][MS], bq[2][NS];
 #pragma unroll
-    for (int kk = 0; kk < 2; ++kk) {
-      const int c = kk * 4 + g4;
+    for (int k2 = 0; k2 < 2; k2 += KKB) {
+      v4u af[KKB][MSW], bq[KKB][NSW];
 #pragma unroll
-      for (int ms = 0; ms < MS; ++ms) {
-        const int row = wm * 16 * MS + ms * 16 + r16;
-        af[kk][ms] = b[row * 8 + (c ^ (row & 7))];
+      for (int kq = 0; kq < KKB; ++kq) {
+        const int c = (k2 + kq) * 4 + g4;
+#pragma unroll
+        for (int ms = 0; ms < MSW; ++ms) {
+          const int row = wm * 16 * MSW + ms * 16 + r16;
+          af[kq][ms] = b[row * 8 + (c ^ (row & 7))];
+        }
+#pragma unroll
+        for (int ns = 0; ns < NSW; ++ns) {
+          const int row = BM + wn * 16 * NSW + ns * 16 + r16;
+          bq[kq][ns] = b[row * 8 + (c ^ (row & 7))];
+        }
       }
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int ns = 0; ns < NS; ++ns) {
-        const int row = BM + wn * 16 * NS + ns * 16 + r16;
-        bq[kk][ns] = b[row * 8 + (c ^ (row & 7))];
-      }
+      for (int kq = 0; kq < KKB; ++kq)
+#pragma unroll
+        for (int ms = 0; ms < MSW; ++ms)
+#pragma unroll
+          for (int ns = 0; ns < NSW; ++ns)
+            acc[ms][ns] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[kq][ms]),
+                                                                  __builtin_bit_cast(bf16x8_t, bq[kq][ns]), acc[ms][ns],
+                                                                  0, 0, 0);
     }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int kk = 0; kk < 2; ++kk)
-#pragma unroll
-      for (int ms = 0; ms < MS; ++ms)
-#pragma unroll
-        for (int ns = 0; ns < NS; ++ns)
-          acc[ms][ns] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, af[kk][ms]),
-                                                                __builtin_bit_cast(bf16x8_t, bq[kk][ns]), acc[ms][ns], 0, 0, 0);
   };
 
   // prologue: slices 0 .. D-1 in flight
@@ -648,18 +667,18 @@ __global__ __launch_bounds__(256) void gemm_tile(GemmArgs a) {
 #pragma unroll
   for (int p = 0; p < BM / RP; ++p) {
 #pragma unroll
-    for (int ms = 0; ms < MS; ++ms) {
-      const int rb = wm * 16 * MS + ms * 16;  // first row of subtile ms
+    for (int ms = 0; ms < MSW; ++ms) {
+      const int rb = wm * 16 * MSW + ms * 16;  // first row of subtile ms
       if (rb / RP == p) {
 #pragma unroll
-        for (int ns = 0; ns < NS; ++ns)
+        for (int ns = 0; ns < NSW; ++ns)
 #pragma unroll
           for (int i = 0; i < 4; ++i)
-            ct[(rb - p * RP + g4 * 4 + i) * CP + wn * 16 * NS + ns * 16 + r16] = acc[ms][ns][i];
+            ct[(rb - p * RP + g4 * 4 + i) * CP + wn * 16 * NSW + ns * 16 + r16] = acc[ms][ns][i];
       }
     }
     lds_barrier();  // LDS only: the epilogue's global stores need not complete here
-    tile_epilogue<RP, BN, CP>(a, ct, m0 + p * RP, n0, split);
+    tile_epilogue<RP, BN, CP, 64 * NWV>(a, ct, m0 + p * RP, n0, split);
     lds_barrier();
   }
 }
@@ -737,12 +756,13 @@ hipError_t wide_t(const WideShape& sh, const GemmArgs& a, hipStream_t s) {
 }
 
 
-template <int MS, int NS>
+template <int MS, int NS, int NWV = 4>
 hipError_t launch_tile_t(const TileShape& sh, const GemmArgs& a, hipStream_t s) {
   if (a.K % 64 == 0) {  // direct-to-LDS ring (static LDS)
-    hipLaunchKernelGGL((gemm_tile<MS, NS>), dim3(sh.grid), dim3(256), 0, s, a);
+    hipLaunchKernelGGL((gemm_tile<MS, NS, NWV>), dim3(sh.grid), dim3(64 * NWV), 0, s, a);
     return hipGetLastError();
   }
+  if (NWV != 4) return hipErrorInvalidValue;   // the register-staged kernel has four waves
   static bool attr = false;
   if (!attr) {
     hipError_t e = set_lds_attr(&gemm_tile_rs<MS, NS>);
@@ -759,7 +779,9 @@ hipError_t launch_tile_t(const TileShape& sh, const GemmArgs& a, hipStream_t s) 
 // compute unit: bound by the ~50-60 GB/s a compute unit ingests from L2) and
 // the fixed cost of a workgroup (pipeline fill, epilogue).
 struct TileCand { int ms, ns; double slice_us, fixed_us; };
-constexpr TileCand kTiles[4] = {{2, 4, 0.40, 4.0}, {4, 4, 0.55, 5.0}, {8, 4, 0.94, 6.0}, {4, 8, 0.94, 6.0}};
+constexpr int kNumTiles = 5;
+constexpr TileCand kTiles[kNumTiles] = {{2, 4, 0.40, 4.0}, {4, 4, 0.55, 5.0}, {8, 4, 0.94, 6.0}, {4, 8, 0.94, 6.0},
+                                        {8, 8, GEMM_TILE88_SLICE_US, 8.0}};   // 256 x 256: eight waves, K % 64 == 0
 
 int cdiv_i(int a, int b) { return (a + b - 1) / b; }
 
@@ -834,12 +856,13 @@ hipError_t launch_gemm_wide(int et, const WideShape& sh, GemmArgs a, hipStream_t
 }
 
 bool tile_plan(int et, int M, int N, int K, bool allow_split, int force, TileShape* sh) {
-  if (et != ET_BF16 || M <= 128 || K % 8 || force > 3) return false;
+  if (et != ET_BF16 || M <= 128 || K % 8 || force >= kNumTiles) return false;
   const int slices = cdiv_i(K, TBK);
   double best = 1e30;
-  for (int c = 0; c < 4; ++c) {
+  for (int c = 0; c < kNumTiles; ++c) {
     if (force >= 0 && c != force) continue;
     const TileCand& tc = kTiles[c];
+    if (tc.ms * tc.ns > 32 && K % 64) continue;   // the eight-wave tile runs on the direct-to-LDS ring only
     const int BM = 32 * tc.ms, BN = 32 * tc.ns;
     const int mt = cdiv_i(M, BM), nt = cdiv_i(N, BN);
     const int max_split = (allow_split && force < 0) ? std::min(8, slices) : 1;
@@ -865,7 +888,8 @@ bool tile_plan(int et, int M, int N, int K, bool allow_split, int force, TileSha
     case 24: sh->lds = tile_lds_bytes<2, 4>(); break;
     case 44: sh->lds = tile_lds_bytes<4, 4>(); break;
     case 84: sh->lds = tile_lds_bytes<8, 4>(); break;
-    default: sh->lds = tile_lds_bytes<4, 8>(); break;
+    case 48: sh->lds = tile_lds_bytes<4, 8>(); break;
+    default: sh->lds = 0; break;   // 256 x 256: static LDS only
   }
   return true;
 }
@@ -881,6 +905,7 @@ hipError_t launch_gemm_tile(const TileShape& sh, GemmArgs a, hipStream_t s) {
     case 44: return launch_tile_t<4, 4>(sh, a, s);
     case 84: return launch_tile_t<8, 4>(sh, a, s);
     case 48: return launch_tile_t<4, 8>(sh, a, s);
+    case 88: return launch_tile_t<8, 8, 8>(sh, a, s);
   }
   return hipErrorInvalidValue;
 }

@@ -1525,8 +1525,8 @@ int32_t vla_test_persist_trace(vla_model* m, uint64_t* out, int32_t max_per_team
 vla_status vla_test_gemm(int32_t elem, const void* x, const void* w, int32_t M, int32_t N, int32_t K,
                          int32_t variant, float* y, void* stream) {
   if (elem != 0 && elem != 1) return fail(VLA_E_ARG, "elem must be 0 or 1");
-  if (variant < 0 || (variant > 4 && variant < 10) || variant > 13)
-    return fail(VLA_E_ARG, "variant must be 0..4 or 10..13");
+  if (variant < 0 || (variant > 4 && variant < 10) || variant > 14)
+    return fail(VLA_E_ARG, "variant must be 0..4 or 10..14");
   if (!x || !w || !y || !al16(x) || !al16(w) || !al16(y)) return fail(VLA_E_ARG, "bad buffer");
   if (M < 1 || N < 1 || K < 1 || K % (elem ? 8 : 4)) return fail(VLA_E_SHAPE, "bad GEMM shape");
   const int et = elem ? ET_BF16 : ET_F32;

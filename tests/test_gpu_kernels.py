@@ -47,8 +47,8 @@ GEMM_SHAPES = [
 ]
 
 # 0 runtime choice, 1 wide, 2 skinny, 3 tiled (runtime tile), 4 split-K partials (the residual
-# projections' launch) summed by the library, 10..13 tiled with a fixed tile
-GEMM_VARIANTS = (0, 1, 2, 3, 4, 10, 11, 12, 13)
+# projections' launch) summed by the library, 10..14 tiled with a fixed tile (14: 256 x 256, eight waves)
+GEMM_VARIANTS = (0, 1, 2, 3, 4, 10, 11, 12, 13, 14)
 
 
 @pytest.mark.parametrize("elem", [1, 0])
@@ -70,7 +70,8 @@ def test_gemm_parity(torch, elem, M, N, K):
         except vla.VlaError as e:
             # shape outside the skinny kernel, or not a bf16 GEMM with M > 128 for the tiled one
             assert e.status == 3 and (variant == 2 or (variant == 4 and not bf and M > 128)
-                                      or (variant == 3 or variant >= 10) and (not bf or M <= 128)), e
+                                      or (variant == 3 or variant >= 10) and (not bf or M <= 128)
+                                      or variant == 14 and K % 64), e
             continue
         got = y.cpu().numpy().astype(np.float64)
         err = np.abs(got - ref)
