@@ -450,21 +450,26 @@ namespace {
 // the banks.  Right before its MFMA a lane widens its 16 weights (one dword) to
 // signed int8, so v_mfma_i32_16x16x64_i8 sums q * w directly (exact int32).
 // Requires K % 128 == 0; rows past M or N load a valid row and are not stored.
-template <int MS>
+// NWV waves of 32 columns each: a 128-column tile on four waves, or a
+// 256-column one on eight, whose K-slice (codes + weights) then feeds twice
+// the MFMAs for 1.2x (MS = 4) the bytes.
+template <int MS, int NWV = 4>
 struct TRing {
-  static constexpr int BM = 32 * MS, BN = 128;
+  static constexpr int BM = 32 * MS, BN = 32 * NWV;
   static constexpr int SX = BM * 8;        // 16-byte slots of codes per stage
   static constexpr int SW = BN * 2;        // 16-byte slots of packed weights per stage
   static constexpr int SB = SX + SW;
-  // 80 / 48 / 32 KB of LDS (MS = 4 / 2 / 1): two or more workgroups fit a CU.
-  // Eight stages time the same as four here.
+  // 80 / 48 / 32 KB of LDS (MS = 4 / 2 / 1, four waves): two or more
+  // workgroups fit a CU; 96 KB for MS = 4 on eight waves.  Eight stages time
+  // the same as four.
   static constexpr int NST = 4;
-  static constexpr int LX = SX / 256;      // code loads per thread and slice (weights: one)
+  static constexpr int LX = SX / (64 * NWV);   // code loads per thread and slice (weights: one)
+  static_assert(LX >= 1 && LX * 64 * NWV == SX, "code rows per wave");
 };
 
-template <int MS>
-__global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
-  using R = TRing<MS>;
+template <int MS, int NWV = 4>
+__global__ __launch_bounds__(64 * NWV) void tern_tile(TernArgs a) {
+  using R = TRing<MS, NWV>;
   constexpr int BM = R::BM, BN = R::BN, SX = R::SX, SB = R::SB, NST = R::NST, LX = R::LX, D = NST - 1;
   static_assert((D - 1) * (LX + 1) < 64, "vmcnt range");
   __shared__ v4u ring[NST][SB];
@@ -481,12 +486,12 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
   const int m0 = mtile * BM, n0 = ntile * BN;
   const int nsl = K / 128;
 
-  // sources of this lane's slots: codes (instruction i: row (4 i + wave) * 8 + lane / 8),
+  // sources of this lane's slots: codes (instruction i: row (NWV i + wave) * 8 + lane / 8),
   // weights (row wave * 32 + lane / 2, half lane % 2)
   const int8_t* xsrc[LX];
 #pragma unroll
   for (int i = 0; i < LX; ++i) {
-    const int row = (i * 4 + wave) * 8 + (lane >> 3);
+    const int row = (i * NWV + wave) * 8 + (lane >> 3);
     const int c = (lane & 7) ^ (row & 7);
     xsrc[i] = a.x + (size_t)min(m0 + row, M - 1) * K + c * 16;
   }
@@ -495,7 +500,7 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
   auto issue = [&](auto j, int sl) {
     v4u* b = stage(j);
 #pragma unroll
-    for (int i = 0; i < LX; ++i) dma16(xsrc[i] + sl * 128, b + (i * 4 + wave) * 64);
+    for (int i = 0; i < LX; ++i) dma16(xsrc[i] + sl * 128, b + (i * NWV + wave) * 64);
     dma16(wsrc + sl * 32, b + SX + wave * 64);
   };
 
@@ -603,14 +608,14 @@ __global__ __launch_bounds__(256) void tern_tile(TernArgs a) {
   }
 }
 
-template <int MS>
+template <int MS, int NWV = 4>
 hipError_t tile_launch(const TernArgs& a0, hipStream_t s) {
   TernArgs a = a0;
   a.m_tiles = (a.M + 32 * MS - 1) / (32 * MS);
-  a.n_tiles = (a.N + 127) / 128;
+  a.n_tiles = (a.N + 32 * NWV - 1) / (32 * NWV);
   const int tiles = a.m_tiles * a.n_tiles;
   const int grid = (tiles + 7) / 8 * 8;
-  hipLaunchKernelGGL((tern_tile<MS>), dim3(grid), dim3(256), 0, s, a);
+  hipLaunchKernelGGL((tern_tile<MS, NWV>), dim3(grid), dim3(64 * NWV), 0, s, a);
   return hipGetLastError();
 }
 
@@ -618,13 +623,15 @@ hipError_t tile_launch(const TernArgs& a0, hipStream_t s) {
 
 bool tern_tile_eligible(int M, int N, int K) { return M >= 128 && N >= 1 && K >= 128 && K % 128 == 0; }
 
-hipError_t launch_ternary_tile(const TernArgs& a, int ms, hipStream_t s) {
+hipError_t launch_ternary_tile(const TernArgs& a, int ms, int waves, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (!tern_tile_eligible(a.M, a.N, a.K) || a.nsplit > 1) return hipErrorInvalidValue;
-  switch (ms) {
-    case 1: return tile_launch<1>(a, s);
-    case 2: return tile_launch<2>(a, s);
-    case 4: return tile_launch<4>(a, s);
+  switch (ms * 10 + waves) {
+    case 14: return tile_launch<1>(a, s);
+    case 24: return tile_launch<2>(a, s);
+    case 44: return tile_launch<4>(a, s);
+    case 28: return tile_launch<2, 8>(a, s);
+    case 48: return tile_launch<4, 8>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -640,10 +647,14 @@ hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t
   }
   const int nsub = (a.rscale != nullptr && a.e.epi == EPI_GLU) ? 2 : 1;
   if (a.nsplit <= 1 && tern_tile_eligible(a.M, a.N, a.K)) {
-    // many token rows: the tiled kernel; 128-row tiles once they fill the
-    // device, 32-row tiles when 64-row ones would leave half of it idle
-    const long long nt = (a.N + 127) / 128;
+    // many token rows: the tiled kernel; 64 x 256 tiles on eight waves when
+    // they still fill the device (the wide gate/up shape), else 128-row
+    // tiles once they do, 32-row tiles when 64-row ones would leave half of
+    // it idle
+    const long long nt = (a.N + 127) / 128, nt2 = (a.N + 255) / 256;
     const long long t4 = (long long)((a.M + 127) / 128) * nt, t2 = (long long)((a.M + 63) / 64) * nt;
+    const long long t28 = (long long)((a.M + 63) / 64) * nt2;
+    if (t28 >= 256) return tile_launch<2, 8>(a, s);
     return t4 >= 256 ? tile_launch<4>(a, s) : t2 >= 128 ? tile_launch<2>(a, s) : tile_launch<1>(a, s);
   }
   if (a.rscale != nullptr && a.M <= 64) {  // token rows of the denoise loop: the skinny kernel

@@ -1726,7 +1726,7 @@ vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t*
                                  float* us_per_launch, void* stream) {
   if (!q || !r || !w_packed || !wscale || !y || !al16(q) || !al16(w_packed) || !al16(y))
     return fail(VLA_E_ARG, "bad buffer");
-  if (variant < 0 || variant > 4) return fail(VLA_E_ARG, "variant must be 0 (MFMA), 1 (dot4) or 2..4 (row tile)");
+  if (variant < 0 || variant > 6) return fail(VLA_E_ARG, "variant must be 0 (MFMA), 1 (dot4) or 2..6 (tile)");
   if (variant >= 2 && !tern_tile_eligible(M, N, K))
     return fail(VLA_E_SHAPE, "the tiled kernel needs M >= 128 and K % 128 == 0");
   if (iters < 1 || iters > 10000) return fail(VLA_E_ARG, "iters must be 1..10000");
@@ -1738,7 +1738,8 @@ vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t*
   a.ks = t.nc * 256; a.nsplit = 1; a.n_tiles = t.n_tiles;
   a.e.M = M; a.e.N = N; a.e.K = K; a.e.epi = EPI_STORE; a.e.out = y; a.e.ldo = N; a.e.out_f32 = 1;
   auto run = [&]() {
-    if (variant >= 2) return launch_ternary_tile(a, 1 << (variant - 2), s);
+    static const int tile_cfg[5][2] = {{1, 4}, {2, 4}, {4, 4}, {2, 8}, {4, 8}};   // (row tile / 32, waves)
+    if (variant >= 2) return launch_ternary_tile(a, tile_cfg[variant - 2][0], tile_cfg[variant - 2][1], s);
     return variant == 0 ? launch_ternary_gemm(a, t.ms, t.units, s) : launch_ternary_dot4(a, s);
   };
   hipEvent_t e0 = nullptr, e1 = nullptr;

@@ -123,7 +123,7 @@ def test_call_validation_without_device():
     # test entries validate too
     assert vla.STATUS[L.vla_test_gemm(2, 16, 16, 1, 1, 8, 0, 16, None)] == "VLA_E_ARG"
     assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 5, 16, None)] == "VLA_E_ARG"
-    assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 14, 16, None)] == "VLA_E_ARG"
+    assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 15, 16, None)] == "VLA_E_ARG"
     # the tiled kernel takes bf16 with M > 128 only, refused before any device work
     assert vla.STATUS[L.vla_test_gemm(1, 16, 16, 1, 1, 8, 3, 16, None)] == "VLA_E_UNSUPPORTED"
     assert vla.STATUS[L.vla_test_gemm(0, 16, 16, 200, 1, 8, 12, 16, None)] == "VLA_E_UNSUPPORTED"

@@ -417,7 +417,8 @@ def test_ternary_gemm_dot4_matches_mfma(torch, M, N, K):
     np.testing.assert_allclose(ys[1], ref, rtol=1e-6, atol=1e-7)
 
 
-TILE_VARIANTS = {2: "32-row tiles", 3: "64-row tiles", 4: "128-row tiles"}
+TILE_VARIANTS = {2: "32-row tiles", 3: "64-row tiles", 4: "128-row tiles", 5: "64 x 256 tiles (eight waves)",
+                 6: "128 x 256 tiles (eight waves)"}
 
 
 @pytest.mark.parametrize("M,N,K", [(512, 2560, 2560), (512, 2560, 6912), (512, 3840, 2560), (300, 200, 640),
