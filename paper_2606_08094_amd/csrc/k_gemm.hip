@@ -228,9 +228,6 @@ __global__ __launch_bounds__(256) void gemm_wide(GemmArgs a) {
 
 // ---------------------------------------------------------------------------
 constexpr int TBK = 64;           // K-slice of gemm_tile
-#ifndef GEMM_TILE88_SLICE_US
-#define GEMM_TILE88_SLICE_US 1.6   // modelled time of one 64-wide K-slice of the 256 x 256 tile
-#endif
 constexpr int TPITCH = TBK + 8;   // LDS row pitch in elements (16 bytes of padding)
 
 // LDS of gemm_tile_rs: two K-slice buffers of X and W rows, reused for the
@@ -526,11 +523,11 @@ __global__ __launch_bounds__(256) void gemm_tile_rs(GemmArgs a) {
 // flight and does not wait for those.  Requires K % 64 == 0 (rows beyond M
 // or N are loaded from a valid row and never stored).
 //
-// NWV = 4 waves in 2 x 2, or 8 waves in 2 x 4 for the 256 x 256 tile: the
-// same 128 x 64 wave tile, so each output sums its k-products in the same
-// order, while a workgroup's 64 KB slice feeds 128 FLOP per byte instead of
-// 85 (256 x 128).  Two stages of 64 KB fit in LDS; a slice's MFMAs (two
-// waves per SIMD) cover the next slice's load.
+// NWV waves: 4 in 2 x 2, or 8 in 2 x 4 (two per SIMD).  Every wave sums its
+// outputs' k-products slice by slice in the same order, so the wave layout
+// does not change a result.  The 256 x 256 tile (eight waves, 128 x 64 per
+// wave) feeds 128 FLOP per staged byte instead of 85 (256 x 128); its two
+// 64 KB stages fill the LDS, and a slice's MFMAs cover the next slice's load.
 template <int MS, int NS, int NWV = 4>
 struct Ring {
   static constexpr int BM = 32 * MS, BN = 32 * NS, ROWS = BM + BN;
@@ -756,32 +753,38 @@ hipError_t wide_t(const WideShape& sh, const GemmArgs& a, hipStream_t s) {
 }
 
 
-template <int MS, int NS, int NWV = 4>
+// K % 64 == 0: the direct-to-LDS ring on eight waves (two per SIMD, so one
+// wave's LDS and load waits hide behind the other's MFMAs: 12-17% faster than
+// four waves on every tile); else the register-staged kernel on four.
+template <int MS, int NS>
 hipError_t launch_tile_t(const TileShape& sh, const GemmArgs& a, hipStream_t s) {
-  if (a.K % 64 == 0) {  // direct-to-LDS ring (static LDS)
-    hipLaunchKernelGGL((gemm_tile<MS, NS, NWV>), dim3(sh.grid), dim3(64 * NWV), 0, s, a);
+  if (a.K % 64 == 0) {
+    hipLaunchKernelGGL((gemm_tile<MS, NS, 8>), dim3(sh.grid), dim3(512), 0, s, a);
     return hipGetLastError();
   }
-  if (NWV != 4) return hipErrorInvalidValue;   // the register-staged kernel has four waves
-  static bool attr = false;
-  if (!attr) {
-    hipError_t e = set_lds_attr(&gemm_tile_rs<MS, NS>);
-    if (e != hipSuccess) return e;
-    attr = true;
+  if constexpr (MS * NS > 32) {   // 256 x 256: the ring only
+    return hipErrorInvalidValue;
+  } else {
+    static bool attr = false;
+    if (!attr) {
+      hipError_t e = set_lds_attr(&gemm_tile_rs<MS, NS>);
+      if (e != hipSuccess) return e;
+      attr = true;
+    }
+    const size_t lds = tile_lds_bytes<MS, NS>();
+    hipLaunchKernelGGL((gemm_tile_rs<MS, NS>), dim3(sh.grid), dim3(256), lds, s, a);
+    return hipGetLastError();
   }
-  const size_t lds = tile_lds_bytes<MS, NS>();
-  hipLaunchKernelGGL((gemm_tile_rs<MS, NS>), dim3(sh.grid), dim3(256), lds, s, a);
-  return hipGetLastError();
 }
 
 // The tiles gemm_tile is instantiated for, as (MS, NS), with the measured
-// time of one 64-wide K-slice of a workgroup (microseconds, one workgroup per
-// compute unit: bound by the ~50-60 GB/s a compute unit ingests from L2) and
-// the fixed cost of a workgroup (pipeline fill, epilogue).
+// time of one 64-wide K-slice of a workgroup on eight waves (microseconds, one
+// workgroup per compute unit: bound by the operand bytes a compute unit takes
+// in from L2) and the fixed cost of a workgroup (pipeline fill, epilogue).
 struct TileCand { int ms, ns; double slice_us, fixed_us; };
 constexpr int kNumTiles = 5;
-constexpr TileCand kTiles[kNumTiles] = {{2, 4, 0.40, 4.0}, {4, 4, 0.55, 5.0}, {8, 4, 0.94, 6.0}, {4, 8, 0.94, 6.0},
-                                        {8, 8, GEMM_TILE88_SLICE_US, 8.0}};   // 256 x 256: eight waves, K % 64 == 0
+constexpr TileCand kTiles[kNumTiles] = {{2, 4, 0.34, 4.0}, {4, 4, 0.47, 5.0}, {8, 4, 0.80, 6.0}, {4, 8, 0.80, 6.0},
+                                        {8, 8, 1.6, 8.0}};   // 256 x 256: K % 64 == 0 only
 
 int cdiv_i(int a, int b) { return (a + b - 1) / b; }
 
@@ -905,7 +908,7 @@ hipError_t launch_gemm_tile(const TileShape& sh, GemmArgs a, hipStream_t s) {
     case 44: return launch_tile_t<4, 4>(sh, a, s);
     case 84: return launch_tile_t<8, 4>(sh, a, s);
     case 48: return launch_tile_t<4, 8>(sh, a, s);
-    case 88: return launch_tile_t<8, 8, 8>(sh, a, s);
+    case 88: return launch_tile_t<8, 8>(sh, a, s);
   }
   return hipErrorInvalidValue;
 }
