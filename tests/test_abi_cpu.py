@@ -186,3 +186,16 @@ def test_backbone_calls_rejected_before_device_use():
     assert vla.STATUS[L.vla_backbone_create(ctypes.byref(c), table, n - 1, ctypes.byref(h))] == "VLA_E_ARG"
     assert vla.STATUS[L.vla_prefix_prefill(None, 16, 1, 1, 16, None)] == "VLA_E_ARG"
     assert vla.STATUS[L.vla_prefix_kv_build_noalloc(None, 16, 1, 1, 16, 0, None)] == "VLA_E_ARG"
+
+
+def test_diffusion_head_starts_from_uniform_noise():
+    """Algorithm 1 draws the chunk's start a_0 from N(0, I), or uniformly for a
+    diffusion head: the GR00T-shaped workload (diffusion-transformer head)
+    draws U(-1, 1) per element, the flow-matching workloads N(0, 1)."""
+    import numpy as np
+    g = wl.make_batch(wl.CONFIGS["gr00t_alt_bf16"], 4)["noise"]
+    assert g.shape == (4, 16, 32)
+    assert g.min() >= -1.0 and g.max() < 1.0
+    assert abs(float(g.mean())) < 0.05 and abs(float(g.var()) - 1.0 / 3.0) < 0.03
+    p = wl.make_batch(wl.CONFIGS["pi0_bf16"], 1)["noise"]
+    assert np.abs(p).max() > 2.0 and abs(float(p.var()) - 1.0) < 0.1

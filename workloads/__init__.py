@@ -8,7 +8,8 @@ the 2-bit packing of ternary codes.  None of the method's arithmetic lives here.
 The five workloads stand in for the paper's deployment shapes (the pi0,
 SmolVLA and BitVLA rows of the served-architecture table, Appendix A); the
 paper's LIBERO suites and trained checkpoints are not used.  Every weight and
-bias is N(0, 0.02^2), prefix hidden states and noise are N(0, 1), the
+bias is N(0, 0.02^2), prefix hidden states and noise are N(0, 1) (the
+diffusion-style GR00T-shaped head starts from U(-1, 1) noise instead), the
 proprioceptive state is U(-1, 1) and the solver schedule is uniform from
 t = 1 down to t = 0.
 """
@@ -51,6 +52,9 @@ class ExpertConfig:
     # variant: the state enters as its own token ahead of the n action tokens
     # (pi0-style) instead of being added to every action token
     state_token: bool = False
+    # the chunk's starting draw a_0: "normal" N(0, I) for flow-matching heads,
+    # "uniform" U(-1, 1) per element for the diffusion head (Algorithm 1)
+    start: str = "normal"
     rms_eps: float = 1e-6
     # workload
     prefix_len: int = 64
@@ -133,7 +137,7 @@ STRESS_PI0 = PI0_BF16.with_(name="stress_pi0", n_action=100, prefix_len=2048, n_
 GR00T_ALT_BF16 = ExpertConfig(
     name="gr00t_alt_bf16", n_layers=32, d_model=1024, n_heads=16, head_dim=64, n_kv_heads=16,
     d_ff=4096, d_prefix=2048, n_action=16, d_action=32, d_state=32,
-    pattern="alt", mlp="gelu", wtype="bf16",
+    pattern="alt", mlp="gelu", wtype="bf16", start="uniform",
     prefix_len=200, n_steps=4, seed_base=6000)
 
 EVO1_CROSS_BF16 = ExpertConfig(
@@ -296,7 +300,10 @@ def make_inputs(cfg: ExpertConfig, request: int = 0) -> Dict[str, np.ndarray]:
     prefix = rp.standard_normal(size=(cfg.prefix_len, cfg.d_prefix)).astype(np.float32)
     if cfg.wtype != "f32":
         prefix = round_bf16(prefix)
-    noise = rn.standard_normal(size=(cfg.n_action, cfg.d_action)).astype(np.float32)
+    if cfg.start == "uniform":
+        noise = rn.uniform(-1.0, 1.0, size=(cfg.n_action, cfg.d_action)).astype(np.float32)
+    else:
+        noise = rn.standard_normal(size=(cfg.n_action, cfg.d_action)).astype(np.float32)
     if cfg.head_regression:
         noise[:] = 0.0      # the single-pass regression head has no noise input
     state = rs.uniform(-1.0, 1.0, size=(cfg.d_state,)).astype(np.float32)
