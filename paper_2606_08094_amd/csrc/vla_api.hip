@@ -309,7 +309,9 @@ struct Builder {
     const double es = esize(et);
     const double xb = es;
     double ob = a.out_f32 ? 4.0 : es;
-    if (a.epi == EPI_PARTIAL) ob = 4.0 * dl.splits();
+    // split-K partials are this implementation's traffic, not the method's:
+    // the projection's output counts once, as one fp32 array
+    if (a.epi == EPI_PARTIAL) ob = 4.0;
     if (a.epi == EPI_RESID) ob = 8.0;                           // residual read + write
     if (a.epi == EPI_GLU) ob = es * 0.5;                        // one output per gate/up pair
     const double bytes = (double)a.N * a.K * es + (double)a.M * a.K * xb + (double)a.M * a.N * ob;
@@ -372,7 +374,7 @@ struct Builder {
   void row_norm(RowNormArgs r) {
     const int et = m->et;
     const double es = esize(et);
-    const double bytes = (double)r.M * r.d * (8.0 + 4.0 * r.nsplit + (r.u_f32 ? 4.0 : es)) +
+    const double bytes = (double)r.M * r.d * (8.0 + 4.0 * std::min(r.nsplit, 1) + (r.u_f32 ? 4.0 : es)) +
                          (r.mode == 1 ? (double)r.d * (r.A + r.n) * es : 0.0);
     ops->push_back(Op{[=](hipStream_t s) { return launch_row_norm(et, r, s); },
                       op_info(VLA_OP_SMALL, r.M, r.d, r.nsplit, bytes, 0.0)});
@@ -791,7 +793,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
         }
         // finish the residual stream and normalise for the next sublayer
         float** partp = &p->part;
-        const double bytes = (double)M * d * (8.0 + 4.0 * nr.nsplit + (u32 ? 4.0 : es));
+        const double bytes = (double)M * d * (8.0 + 4.0 * std::min(nr.nsplit, 1) + (u32 ? 4.0 : es));
         bld.ops->push_back(Op{[=](hipStream_t s) {
                                 RowNormArgs r = nr;
                                 r.part = *partp;
@@ -2033,7 +2035,7 @@ vla_status build_prefill_plan(vla_backbone* bb, PrefillPlan* p) {
   // row kernel finishing a residual update and normalising for what follows;
   // after the last layer it writes the final norm into the call's output
   auto norm_op = [&](RowNormArgs nr, bool final_out) {
-    const double bytes = (double)M * d * (8.0 + 4.0 * nr.nsplit + (nr.u_f32 ? 4.0 : es));
+    const double bytes = (double)M * d * (8.0 + 4.0 * std::min(nr.nsplit, 1) + (nr.u_f32 ? 4.0 : es));
     bld.ops->push_back(Op{[=](hipStream_t s) {
                             RowNormArgs r = nr;
                             r.part = *partp;
