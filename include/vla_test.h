@@ -80,8 +80,9 @@ vla_status vla_test_rope(int32_t elem, void* x, int32_t rows, int32_t rows_per_r
  *   variant 0: the library's W2A8 launch (int8 MFMA); 1: the vector-ALU
  *   sdot4 kernel; 2, 3, 4: the many-row tiled kernel with 32-, 64- or
  *   128-row tiles of 128 columns; 5, 6: 64- or 128-row tiles of 256 columns
- *   on eight waves (2..6 need M >= 128 and K % 128 == 0).  All sum exactly
- *   in int32, so y is identical.
+ *   on eight waves; 7, 8, 9: 32-, 64- or 128-row tiles of 128 columns on
+ *   eight waves in two groups taking alternate K-slices (2..9 need M >= 128
+ *   and K % 128 == 0).  All sum exactly in int32, so y is identical.
  *   iters >= 1 (at most 10000): the GEMM runs once untimed, then iters times
  *   between two HIP events on `stream`; *us_per_launch (host, may be NULL)
  *   receives the mean time of one launch.  Synchronises the stream. */

@@ -608,6 +608,175 @@ __global__ __launch_bounds__(64 * NWV) void tern_tile(TernArgs a) {
   }
 }
 
+// tern_tile with two wave groups taking alternate K-slices: eight waves, two
+// per SIMD, so one wave's LDS and load waits hide behind the other's work,
+// while each packed weight dword is still widened by one wave only (wave
+// (g, w) owns columns 32 w .. 32 w + 31 of slices 2 p + g).  Slice pairs
+// stream into a ring of NPR pairs (each stage laid out as tern_tile's),
+// NPR - 1 pairs ahead of the MFMAs.  At the end group 1 hands its int32
+// sums to group 0 through LDS (exact), and group 0 runs the epilogue.
+template <int MS>
+__global__ __launch_bounds__(512) void tern_tile_kg(TernArgs a) {
+  using R = TRing<MS, 4>;
+  constexpr int BM = R::BM, BN = R::BN, SX = R::SX, SB = R::SB, LX = R::LX;
+  constexpr int NPR = 3;                   // slice pairs in the ring
+  constexpr int RS = 2 * MS;               // 16-row subtiles of the tile, all in every wave
+  __shared__ v4u ring[2 * NPR][SB];
+  static_assert((size_t)4 * RS * 2 * 64 <= (size_t)2 * NPR * SB, "reduction buffer");
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = wave >> 2, wl = wave & 3;
+  const int r16 = lane & 15, g4 = lane >> 4;
+  const int M = a.M, N = a.N, K = a.K, KB = K / 4;
+  const int per = gridDim.x >> 3;
+  const int u = (blockIdx.x & 7) * per + (blockIdx.x >> 3);   // tiles of one W column block stay on one XCD
+  const int tiles = a.m_tiles * a.n_tiles;
+  if (u >= tiles) return;
+  const int ntile = u / a.m_tiles, mtile = u - ntile * a.m_tiles;
+  const int m0 = mtile * BM, n0 = ntile * BN;
+  const int nsl = K / 128, npair = (nsl + 1) / 2;
+
+  // this wave's slots in its group's slice, as wave wl of tern_tile
+  const int8_t* xsrc[LX];
+#pragma unroll
+  for (int i = 0; i < LX; ++i) {
+    const int row = (i * 4 + wl) * 8 + (lane >> 3);
+    const int c = (lane & 7) ^ (row & 7);
+    xsrc[i] = a.x + (size_t)min(m0 + row, M - 1) * K + c * 16;
+  }
+  const int wrow = wl * 32 + (lane >> 1);
+  const uint8_t* wsrc = a.w + (size_t)min(n0 + wrow, N - 1) * KB + (((lane & 1) ^ ((wrow >> 3) & 1)) * 16);
+  auto mine = [&](int p) { return 2 * p + grp < nsl; };   // this group's slice of pair p exists
+  auto issue = [&](int p) {
+    if (!mine(p)) return;
+    const int sl = 2 * p + grp;
+    v4u* b = ring[2 * (p % NPR) + grp];
+#pragma unroll
+    for (int i = 0; i < LX; ++i) dma16(xsrc[i] + sl * 128, b + (i * 4 + wl) * 64);
+    dma16(wsrc + sl * 32, b + SX + wl * 64);
+  };
+
+  i32x4 acc[RS][2];
+#pragma unroll
+  for (int ms = 0; ms < RS; ++ms)
+#pragma unroll
+    for (int ns = 0; ns < 2; ++ns) acc[ms][ns] = i32x4{0, 0, 0, 0};
+
+  auto compute = [&](const v4u* b) {
+    v4u xf[2][RS];
+    uint32_t wp[2][2];
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk) {
+#pragma unroll
+      for (int ms = 0; ms < RS; ++ms) {
+        const int row = ms * 16 + r16;
+        xf[kk][ms] = b[row * 8 + ((kk * 4 + g4) ^ (row & 7))];
+      }
+#pragma unroll
+      for (int ns = 0; ns < 2; ++ns) {
+        const int row = wl * 32 + ns * 16 + r16;
+        const uint32_t* slot = reinterpret_cast<const uint32_t*>(b + SX + row * 2 + (kk ^ ((row >> 3) & 1)));
+        wp[kk][ns] = slot[g4];
+      }
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int kk = 0; kk < 2; ++kk)
+#pragma unroll
+      for (int ns = 0; ns < 2; ++ns) {
+        const i32x4 w = unpack_signed(wp[kk][ns]);
+#pragma unroll
+        for (int ms = 0; ms < RS; ++ms)
+          acc[ms][ns] = __builtin_amdgcn_mfma_i32_16x16x64_i8(__builtin_bit_cast(i32x4, xf[kk][ms]), w, acc[ms][ns],
+                                                               0, 0, 0);
+      }
+  };
+
+  for (int p = 0; p < NPR - 1 && p < npair; ++p) issue(p);
+  for (int p = 0; p < npair; ++p) {
+    // this wave's slice of pair p has landed once at most its slice of pair
+    // p + 1 (issued, if it exists) is pending
+    if (p + 1 < npair && mine(p + 1))
+      __builtin_amdgcn_s_waitcnt(vm_wait(LX + 1));
+    else
+      __builtin_amdgcn_s_waitcnt(vm_wait(0));
+    lds_barrier();
+    // the stages of pair p - 1 are free: refill them with pair p + NPR - 1
+    if (p + NPR - 1 < npair) issue(p + NPR - 1);
+    if (mine(p)) compute(ring[2 * (p % NPR) + grp]);
+  }
+  __builtin_amdgcn_s_waitcnt(vm_wait(0));
+  lds_barrier();
+
+  // group 1's sums to group 0 (lane-major, conflict free), exact int32
+  i32x4* red = reinterpret_cast<i32x4*>(&ring[0][0]);
+  if (grp == 1) {
+#pragma unroll
+    for (int ms = 0; ms < RS; ++ms)
+#pragma unroll
+      for (int ns = 0; ns < 2; ++ns) red[((wl * RS + ms) * 2 + ns) * 64 + lane] = acc[ms][ns];
+  }
+  lds_barrier();
+  if (grp == 1) return;
+#pragma unroll
+  for (int ms = 0; ms < RS; ++ms)
+#pragma unroll
+    for (int ns = 0; ns < 2; ++ns) acc[ms][ns] += red[((wl * RS + ms) * 2 + ns) * 64 + lane];
+
+  const int nw = n0 + wl * 32;
+  if (a.rscale == nullptr) {   // raw int32 sums
+#pragma unroll
+    for (int ms = 0; ms < RS; ++ms)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int m = m0 + ms * 16 + g4 * 4 + i;
+#pragma unroll
+        for (int ns = 0; ns < 2; ++ns) {
+          const int n = nw + ns * 16 + r16;
+          if (m < M && n < N) a.acc_out[(size_t)m * N + n] = acc[ms][ns][i];
+        }
+      }
+    return;
+  }
+  float sw[2];
+#pragma unroll
+  for (int ns = 0; ns < 2; ++ns) {
+    const int n = nw + ns * 16 + r16;
+    sw[ns] = (n < N) ? a.wscale[n] : 0.0f;
+  }
+  f32x4 y[RS][2];
+#pragma unroll
+  for (int ms = 0; ms < RS; ++ms)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int m = m0 + ms * 16 + g4 * 4 + i;
+      const float rm = (m < M) ? a.rscale[m] : 0.0f;
+#pragma unroll
+      for (int ns = 0; ns < 2; ++ns) y[ms][ns][i] = (float)acc[ms][ns][i] * (sw[ns] * rm / 127.0f);
+    }
+  if (a.e.epi == EPI_RESID) {         // one 16-column subtile at a time
+#pragma unroll
+    for (int ns = 0; ns < 2; ++ns) {
+      f32x4 y1[RS][1];
+#pragma unroll
+      for (int ms = 0; ms < RS; ++ms) y1[ms][0] = y[ms][ns];
+      wave_epilogue<bf16_t, RS, 1>(a.e, y1, m0, nw + 16 * ns, 0);
+    }
+  } else {                            // GLU: the wave's 32 columns are one gate / up pair of 16-row blocks
+    wave_epilogue<bf16_t, RS, 2>(a.e, y, m0, nw, 0);
+  }
+}
+
+template <int MS>
+hipError_t tile_kg_launch(const TernArgs& a0, hipStream_t s) {
+  TernArgs a = a0;
+  a.m_tiles = (a.M + 32 * MS - 1) / (32 * MS);
+  a.n_tiles = (a.N + 127) / 128;
+  const int tiles = a.m_tiles * a.n_tiles;
+  const int grid = (tiles + 7) / 8 * 8;
+  hipLaunchKernelGGL((tern_tile_kg<MS>), dim3(grid), dim3(512), 0, s, a);
+  return hipGetLastError();
+}
+
 template <int MS, int NWV = 4>
 hipError_t tile_launch(const TernArgs& a0, hipStream_t s) {
   TernArgs a = a0;
@@ -623,15 +792,18 @@ hipError_t tile_launch(const TernArgs& a0, hipStream_t s) {
 
 bool tern_tile_eligible(int M, int N, int K) { return M >= 128 && N >= 1 && K >= 128 && K % 128 == 0; }
 
-hipError_t launch_ternary_tile(const TernArgs& a, int ms, int waves, hipStream_t s) {
+hipError_t launch_ternary_tile(const TernArgs& a, int ms, int waves, int kgroups, hipStream_t s) {
   if (a.M <= 0 || a.N <= 0) return hipSuccess;
   if (!tern_tile_eligible(a.M, a.N, a.K) || a.nsplit > 1) return hipErrorInvalidValue;
-  switch (ms * 10 + waves) {
-    case 14: return tile_launch<1>(a, s);
-    case 24: return tile_launch<2>(a, s);
-    case 44: return tile_launch<4>(a, s);
-    case 28: return tile_launch<2, 8>(a, s);
-    case 48: return tile_launch<4, 8>(a, s);
+  switch (ms * 100 + waves * 10 + kgroups) {
+    case 141: return tile_launch<1>(a, s);
+    case 241: return tile_launch<2>(a, s);
+    case 441: return tile_launch<4>(a, s);
+    case 281: return tile_launch<2, 8>(a, s);
+    case 481: return tile_launch<4, 8>(a, s);
+    case 182: return tile_kg_launch<1>(a, s);
+    case 282: return tile_kg_launch<2>(a, s);
+    case 482: return tile_kg_launch<4>(a, s);
     default: return hipErrorInvalidValue;
   }
 }
@@ -649,13 +821,13 @@ hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t
   if (a.nsplit <= 1 && tern_tile_eligible(a.M, a.N, a.K)) {
     // many token rows: the tiled kernel; 64 x 256 tiles on eight waves when
     // they still fill the device (the wide gate/up shape), else 128-row
-    // tiles once they do, 32-row tiles when 64-row ones would leave half of
-    // it idle
+    // tiles once they do; below that, 64-row (or, when those would leave
+    // half the device idle, 32-row) tiles on eight waves in two K groups
     const long long nt = (a.N + 127) / 128, nt2 = (a.N + 255) / 256;
     const long long t4 = (long long)((a.M + 127) / 128) * nt, t2 = (long long)((a.M + 63) / 64) * nt;
     const long long t28 = (long long)((a.M + 63) / 64) * nt2;
     if (t28 >= 256) return tile_launch<2, 8>(a, s);
-    return t4 >= 256 ? tile_launch<4>(a, s) : t2 >= 128 ? tile_launch<2>(a, s) : tile_launch<1>(a, s);
+    return t4 >= 256 ? tile_launch<4>(a, s) : t2 >= 128 ? tile_kg_launch<2>(a, s) : tile_kg_launch<1>(a, s);
   }
   if (a.rscale != nullptr && a.M <= 64) {  // token rows of the denoise loop: the skinny kernel
     const int sms = a.M <= 16 ? 1 : (a.M <= 32 ? 2 : 4);

@@ -1728,7 +1728,7 @@ vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t*
                                  float* us_per_launch, void* stream) {
   if (!q || !r || !w_packed || !wscale || !y || !al16(q) || !al16(w_packed) || !al16(y))
     return fail(VLA_E_ARG, "bad buffer");
-  if (variant < 0 || variant > 6) return fail(VLA_E_ARG, "variant must be 0 (MFMA), 1 (dot4) or 2..6 (tile)");
+  if (variant < 0 || variant > 9) return fail(VLA_E_ARG, "variant must be 0 (MFMA), 1 (dot4) or 2..9 (tile)");
   if (variant >= 2 && !tern_tile_eligible(M, N, K))
     return fail(VLA_E_SHAPE, "the tiled kernel needs M >= 128 and K % 128 == 0");
   if (iters < 1 || iters > 10000) return fail(VLA_E_ARG, "iters must be 1..10000");
@@ -1740,8 +1740,11 @@ vla_status vla_test_ternary_gemm(const int8_t* q, const float* r, const uint8_t*
   a.ks = t.nc * 256; a.nsplit = 1; a.n_tiles = t.n_tiles;
   a.e.M = M; a.e.N = N; a.e.K = K; a.e.epi = EPI_STORE; a.e.out = y; a.e.ldo = N; a.e.out_f32 = 1;
   auto run = [&]() {
-    static const int tile_cfg[5][2] = {{1, 4}, {2, 4}, {4, 4}, {2, 8}, {4, 8}};   // (row tile / 32, waves)
-    if (variant >= 2) return launch_ternary_tile(a, tile_cfg[variant - 2][0], tile_cfg[variant - 2][1], s);
+    // (row tile / 32, waves, K groups)
+    static const int tile_cfg[8][3] = {{1, 4, 1}, {2, 4, 1}, {4, 4, 1}, {2, 8, 1}, {4, 8, 1}, {1, 8, 2}, {2, 8, 2},
+                                       {4, 8, 2}};
+    if (variant >= 2)
+      return launch_ternary_tile(a, tile_cfg[variant - 2][0], tile_cfg[variant - 2][1], tile_cfg[variant - 2][2], s);
     return variant == 0 ? launch_ternary_gemm(a, t.ms, t.units, s) : launch_ternary_dot4(a, s);
   };
   hipEvent_t e0 = nullptr, e1 = nullptr;

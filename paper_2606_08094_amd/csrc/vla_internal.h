@@ -249,9 +249,11 @@ hipError_t launch_ternary_dot4(const TernArgs& a, hipStream_t s);   // VALU sdot
 // The tiled W2A8 kernel takes the shape (many token rows, K % 128 == 0).
 bool tern_tile_eligible(int M, int N, int K);
 // The tiled W2A8 kernel with (32 ms)-row tiles (ms 1, 2 or 4) on `waves`
-// waves of 32 columns (4; or 8 with ms 2 or 4): the same sums as every other
+// waves: kgroups 1 = waves of 32 columns each (4, or 8 with ms 2 or 4 for a
+// 256-column tile); kgroups 2 = eight waves of a 128-column tile in two
+// groups taking alternate K-slices.  The same sums as every other
 // configuration; hipErrorInvalidValue for shapes or tiles it does not take.
-hipError_t launch_ternary_tile(const TernArgs& a, int ms, int waves, hipStream_t s);
+hipError_t launch_ternary_tile(const TernArgs& a, int ms, int waves, int kgroups, hipStream_t s);
 hipError_t launch_ternary_gemm(const TernArgs& a, int ms, int units, hipStream_t s);
 hipError_t launch_check_finite(const float* x, size_t n, int* flag, hipStream_t s);
 hipError_t launch_fill_u32(unsigned* p, unsigned v, size_t n, hipStream_t s);

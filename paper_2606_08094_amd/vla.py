@@ -344,7 +344,9 @@ def test_ternary_gemm(q, r, w_packed, wscale, M: int, N: int, K: int, variant: i
     """The W2A8 GEMM alone on int8 codes: variant 0 the int8-MFMA launch, 1 the
     VALU sdot4 kernel, 2 / 3 / 4 the many-row tiled kernel with 32- / 64- /
     128-row tiles of 128 columns, 5 / 6 with 64- / 128-row tiles of 256 columns
-    (eight waves).  Returns the mean microseconds of one of `iters` launches."""
+    (eight waves), 7 / 8 / 9 with 32- / 64- / 128-row tiles of 128 columns on
+    eight waves in two K-slice groups.  Returns the mean microseconds of one of
+    `iters` launches."""
     us = ctypes.c_float(0.0)
     _check(lib().vla_test_ternary_gemm(_ptr(q), _ptr(r), _ptr(w_packed), _ptr(wscale), M, N, K, variant, iters,
                                        _ptr(y), ctypes.byref(us), _stream(stream)))

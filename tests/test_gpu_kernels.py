@@ -418,7 +418,8 @@ def test_ternary_gemm_dot4_matches_mfma(torch, M, N, K):
 
 
 TILE_VARIANTS = {2: "32-row tiles", 3: "64-row tiles", 4: "128-row tiles", 5: "64 x 256 tiles (eight waves)",
-                 6: "128 x 256 tiles (eight waves)"}
+                 6: "128 x 256 tiles (eight waves)", 7: "32-row tiles, two K groups", 8: "64-row tiles, two K groups",
+                 9: "128-row tiles, two K groups"}
 
 
 @pytest.mark.parametrize("M,N,K", [(512, 2560, 2560), (512, 2560, 6912), (512, 3840, 2560), (300, 200, 640),
