@@ -477,3 +477,43 @@ def test_stress_batch16_sampled_requests_vs_oracle(torch):
         err = np.abs(got[r] - ref[0]).max()
         print(f"stress B=16 request {r} (T=2): max|d| vs oracle = {err:.3e}", flush=True)
         assert np.all(np.isfinite(got[r])) and err <= 2e-2
+
+
+# Degenerate and limit shapes: one action token and one prefix row (every
+# attention has a single query or a single prefix key, every row tile is
+# ragged), action and state width 1, one or two solver steps; and the
+# persistent kernel's largest chunk (64 action tokens) over a 1000-row prefix
+# (18 key splits).  Loop mode 2 runs the persistent kernel where the model
+# fits it and the graph driver otherwise.
+_PI0_SMALL = wl.PI0_BF16.with_(n_layers=2, d_model=512, head_dim=64, d_ff=2048, d_prefix=512)
+EDGE = {
+    "f32_single": wl.TINY_F32.with_(name="edge_f32", n_action=1, prefix_len=1, d_action=1, d_state=1,
+                                    n_steps=1, seed_base=9100),
+    "alt_single": wl.SMOLVLA_BF16.with_(name="edge_alt", n_layers=2, n_action=1, prefix_len=1, d_action=1,
+                                        d_state=1, n_steps=2, seed_base=9200),
+    "joint_single": _PI0_SMALL.with_(name="edge_joint", n_action=1, prefix_len=1, d_action=1, d_state=1,
+                                     n_steps=2, seed_base=9300),
+    "joint_max_chunk": _PI0_SMALL.with_(name="edge_joint_max", n_action=64, prefix_len=1000, n_steps=2,
+                                        seed_base=9400),
+}
+
+
+@pytest.mark.parametrize("loop_mode", [1, 2])
+@pytest.mark.parametrize("name", sorted(EDGE))
+def test_degenerate_and_limit_shapes(torch, name, loop_mode):
+    cfg = EDGE[name]
+    W = wl.make_weights(cfg)
+    inp = wl.make_batch(cfg, 1)
+    tau = wl.uniform_schedule(cfg.n_steps)
+    cache_ref, ref = _oracle(cfg, W, inp, tau)
+    pipe = _pipe(cfg, W, inp, loop_mode)
+    try:
+        pipe.build_cache()
+        got = pipe.denoise(tau).cpu().numpy().astype(np.float64)
+        _check_cache(pipe, cache_ref, cfg)
+    finally:
+        pipe.close()
+    err = np.abs(got - ref).max()
+    print(f"{name} (loop mode {loop_mode}): max|d| = {err:.3e} (tol {TOL[cfg.wtype]})")
+    assert np.all(np.isfinite(got))
+    assert err <= TOL[cfg.wtype]

@@ -205,3 +205,21 @@ def test_ternary_prefill_full_depth(torch):
         W0[f"B{l}.W_o.scale"] = np.float32(0.0)
         W0[f"B{l}.W_d.scale"] = np.float32(0.0)
     assert np.abs(ref - O.prefix_prefill(bcfg, W0, e)).mean() > 0.3
+
+
+@pytest.mark.parametrize("wtype", ["bf16", "ternary"])
+def test_prefill_single_prefix_row(torch, wtype):
+    """A prefix of one row per request (two requests): attention over a single
+    key (weight 1), RoPE at position 0 only, every GEMM with M = 2."""
+    if wtype == "bf16":
+        bcfg = SMALL.with_(name="one_row", prefix_len=1, seed_base=8500)
+        tol = (8e-2, 1.2e-2)
+    else:
+        bcfg = wl.BITNET_W2A8.with_(name="one_row_tern", n_layers=2, d_model=512, n_heads=4, head_dim=128,
+                                    n_kv_heads=2, d_ff=1536, prefix_len=1, seed_base=8600)
+        tol = (4e-2, 6e-3)
+    W = wl.make_backbone_weights(bcfg)
+    e = wl.make_prefix_embeds(bcfg, 2)
+    got = _prefill(bcfg, W, e)
+    ref = O.prefix_prefill(bcfg, W, e)
+    _cmp(f"one prefix row ({wtype})", got, ref, *tol)
