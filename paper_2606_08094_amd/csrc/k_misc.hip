@@ -10,21 +10,56 @@ __global__ void set_params_kernel(CallParams* dst, CallParams src) {
   if (threadIdx.x == 0) *dst = src;
 }
 
-// a <- noise; xs[b] = b_in + b_s + state[b] W_s^T (the per-request constant part
-// of the input embedding).
+// Chunk start, one launch: a <- noise; xs[b] = b_in + b_s + state[b] W_s^T
+// (the per-request constant part of the input embedding); and, when e is set,
+// the sinusoidal embedding of every solver time: e[k] = [sin(2 pi tau_k / p_j),
+// cos(2 pi tau_k / p_j)], p_j geometric from 4e-3 to 4, with rows T..Tpad-1
+// zero and the angle formed in double precision.  Workgroups [0, B * XB) take
+// 64 columns of one request's xs each (four threads split the state sum) and
+// a share of its noise copy; the next Tpad * EB take 256 frequency pairs of
+// one time row each.
+constexpr int XCOLS = 64;
 template <typename T>
-__global__ __launch_bounds__(256) void init_chunk_kernel(const CallParams* cp, float* a, float* xs,
+__global__ __launch_bounds__(256) void chunk_start_kernel(const CallParams* cp, float* a, float* xs,
                                                           const T* W_s, const float* b_s,
-                                                          const float* b_in, int n, int A, int S, int d) {
-  const int b = blockIdx.x;
-  const float* st = cp->state + (size_t)b * S;
-  for (int j = threadIdx.x; j < d; j += 256) {
-    float acc = (b_in ? b_in[j] : 0.0f) + b_s[j];   // b_in NULL: the state token's own row
-    for (int s = 0; s < S; ++s) acc += st[s] * ElemTraits<T>::to_f(W_s[(size_t)j * S + s]);
-    xs[(size_t)b * d + j] = acc;
+                                                          const float* b_in, int B, int n, int A, int S, int d,
+                                                          T* e, int T_, int Tpad) {
+  const int XB = (d + XCOLS - 1) / XCOLS;
+  const int tid = threadIdx.x;
+  int blk = blockIdx.x;
+  if (blk < B * XB) {
+    __shared__ float red[4][XCOLS];
+    const int b = blk / XB, cb = blk - b * XB;
+    const int c = tid % XCOLS, part = tid / XCOLS;
+    const int j = cb * XCOLS + c;
+    const float* st = cp->state + (size_t)b * S;
+    float acc = 0.0f;
+    if (j < d)
+      for (int s2 = part; s2 < S; s2 += 4) acc += st[s2] * ElemTraits<T>::to_f(W_s[(size_t)j * S + s2]);
+    red[part][c] = acc;
+    __syncthreads();
+    if (part == 0 && j < d)   // b_in NULL: the state token's own row
+      xs[(size_t)b * d + j] = (b_in ? b_in[j] : 0.0f) + b_s[j] + red[0][c] + red[1][c] + red[2][c] + red[3][c];
+    const float* nz = cp->noise + (size_t)b * n * A;
+    const int per = (n * A + XB - 1) / XB;
+    const int i1 = min(n * A, (cb + 1) * per);
+    for (int i = cb * per + tid; i < i1; i += 256) a[(size_t)b * n * A + i] = nz[i];
+    return;
   }
-  const float* nz = cp->noise + (size_t)b * n * A;
-  for (int i = threadIdx.x; i < n * A; i += 256) a[(size_t)b * n * A + i] = nz[i];
+  blk -= B * XB;
+  const int half = d / 2, EB = (half + 255) / 256;
+  const int k = blk / EB, j = (blk - k * EB) * 256 + tid;
+  if (e == nullptr || k >= Tpad || j >= half) return;
+  float sv = 0.0f, cv = 0.0f;
+  if (k < T_) {
+    const double frac = (double)j / (double)(half > 1 ? half - 1 : 1);
+    const double period = 4e-3 * pow(1000.0, frac);
+    const double ang = 2.0 * 3.14159265358979323846 * (double)cp->tau[k] / period;
+    sv = (float)sin(ang);
+    cv = (float)cos(ang);
+  }
+  e[(size_t)k * d + j] = ElemTraits<T>::from_f(sv);
+  e[(size_t)k * d + j + half] = ElemTraits<T>::from_f(cv);
 }
 
 // One workgroup per token row: finish the residual stream x (add the split-K
@@ -189,26 +224,6 @@ __global__ __launch_bounds__(256) void row_norm_kernel(RowNormArgs a) {
   if (t == 0) a.qr[m] = r;
 }
 
-// e[k] = [sin(2 pi tau_k / p_j), cos(2 pi tau_k / p_j)], p_j geometric from
-// 4e-3 to 4; rows T..Tpad-1 are zero.  The angle is formed in double precision.
-template <typename T>
-__global__ __launch_bounds__(256) void time_embed_kernel(const CallParams* cp, T* e, int T_, int d) {
-  const int k = blockIdx.x;
-  const int half = d / 2;
-  for (int j = threadIdx.x; j < half; j += 256) {
-    float sv = 0.0f, cv = 0.0f;
-    if (k < T_) {
-      const double frac = (double)j / (double)(half > 1 ? half - 1 : 1);
-      const double period = 4e-3 * pow(1000.0, frac);
-      const double ang = 2.0 * 3.14159265358979323846 * (double)cp->tau[k] / period;
-      sv = (float)sin(ang);
-      cv = (float)cos(ang);
-    }
-    e[(size_t)k * d + j] = ElemTraits<T>::from_f(sv);
-    e[(size_t)k * d + j + half] = ElemTraits<T>::from_f(cv);
-  }
-}
-
 __global__ void copy_f32_kernel(float* dst, const float* src, size_t n) {
   for (size_t i = blockIdx.x * (size_t)blockDim.x + threadIdx.x; i < n; i += (size_t)gridDim.x * blockDim.x)
     dst[i] = src[i];
@@ -349,15 +364,20 @@ hipError_t launch_set_params(CallParams* dst, const CallParams& src, hipStream_t
   return hipGetLastError();
 }
 
-hipError_t launch_init_chunk(int et, const CallParams* cp, float* a, float* xs, const void* W_s,
-                             const float* b_s, const float* b_in, int B, int n, int A, int S, int d,
-                             hipStream_t s) {
+hipError_t launch_chunk_start(int et, const CallParams* cp, float* a, float* xs, const void* W_s,
+                              const float* b_s, const float* b_in, int B, int n, int A, int S, int d, void* e,
+                              int T, int Tpad, hipStream_t s) {
+  const int XB = (d + XCOLS - 1) / XCOLS, EB = (d / 2 + 255) / 256;
+  const int blocks = B * XB + (e ? Tpad * EB : 0);
+  if (blocks <= 0) return hipSuccess;
   if (et == ET_BF16)
-    hipLaunchKernelGGL(init_chunk_kernel<bf16_t>, dim3(B), dim3(256), 0, s, cp, a, xs,
-                       reinterpret_cast<const bf16_t*>(W_s), b_s, b_in, n, A, S, d);
+    hipLaunchKernelGGL(chunk_start_kernel<bf16_t>, dim3(blocks), dim3(256), 0, s, cp, a, xs,
+                       reinterpret_cast<const bf16_t*>(W_s), b_s, b_in, B, n, A, S, d,
+                       reinterpret_cast<bf16_t*>(e), T, Tpad);
   else
-    hipLaunchKernelGGL(init_chunk_kernel<float>, dim3(B), dim3(256), 0, s, cp, a, xs,
-                       reinterpret_cast<const float*>(W_s), b_s, b_in, n, A, S, d);
+    hipLaunchKernelGGL(chunk_start_kernel<float>, dim3(blocks), dim3(256), 0, s, cp, a, xs,
+                       reinterpret_cast<const float*>(W_s), b_s, b_in, B, n, A, S, d,
+                       reinterpret_cast<float*>(e), T, Tpad);
   return hipGetLastError();
 }
 
@@ -372,13 +392,7 @@ hipError_t launch_row_norm(int et, const RowNormArgs& a, hipStream_t s) {
 }
 
 hipError_t launch_time_embed(int et, const CallParams* cp, void* e, int T, int Tpad, int d, hipStream_t s) {
-  if (et == ET_BF16)
-    hipLaunchKernelGGL(time_embed_kernel<bf16_t>, dim3(Tpad), dim3(256), 0, s, cp,
-                       reinterpret_cast<bf16_t*>(e), T, d);
-  else
-    hipLaunchKernelGGL(time_embed_kernel<float>, dim3(Tpad), dim3(256), 0, s, cp, reinterpret_cast<float*>(e),
-                       T, d);
-  return hipGetLastError();
+  return launch_chunk_start(et, cp, nullptr, nullptr, nullptr, nullptr, nullptr, 0, 0, 0, 0, d, e, T, Tpad, s);
 }
 
 hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s) {

@@ -481,14 +481,14 @@ vla_status build_plan(vla_model* m, Plan* p) {
   CallParams* cp = p->cp;
   size_t part_need = 0;
 
+  // chunk start and (flow heads) the time embedding of every solver step, one launch;
+  // with the state token b_in belongs to the action rows only, added by the embedding
+  void* temb = c.head_regression ? nullptr : p->e;
   bld.small([=](hipStream_t s) {
-    // with the state token b_in belongs to the action rows only, added by the embedding
-    return launch_init_chunk(et, cp, p->a, p->xs, m->W_s, m->b_s, stok ? nullptr : m->b_in, B, n, A,
-                             S, d, s);
-  }, B, d, S, (double)d * S * es + (double)B * (S + d) * 4 + (double)B * n * A * 8);
+    return launch_chunk_start(et, cp, p->a, p->xs, m->W_s, m->b_s, stok ? nullptr : m->b_in, B, n, A, S, d,
+                              temb, T, T, s);
+  }, B, d, S, (double)d * S * es + (double)B * (S + d) * 4 + (double)B * n * A * 8 + (temb ? (double)T * d * es : 0.0));
   if (!c.head_regression) {
-    bld.small([=](hipStream_t s) { return launch_time_embed(et, cp, p->e, T, T, d, s); }, T, d, 0,
-              (double)T * d * es);
     GemmArgs g = gemm_base(m, T, d, d, p->e, d, m->W_t1);
     g.epi = EPI_STORE;
     g.bias = m->b_t1;

@@ -238,9 +238,11 @@ size_t attention_part_bytes(int et, const AttnArgs& a);
 size_t attention_stats_bytes(const AttnArgs& a);
 
 hipError_t launch_set_params(CallParams* dst, const CallParams& src, hipStream_t s);
-hipError_t launch_init_chunk(int et, const CallParams* cp, float* a, float* xs, const void* W_s,
-                             const float* b_s, const float* b_in, int B, int n, int A, int S, int d,
-                             hipStream_t s);
+// Chunk start: a <- noise and xs (per-request constant embedding) for B
+// requests, plus the time embedding rows e[Tpad][d] when e is not null.
+hipError_t launch_chunk_start(int et, const CallParams* cp, float* a, float* xs, const void* W_s,
+                              const float* b_s, const float* b_in, int B, int n, int A, int S, int d, void* e,
+                              int T, int Tpad, hipStream_t s);
 hipError_t launch_row_norm(int et, const RowNormArgs& a, hipStream_t s);
 hipError_t launch_time_embed(int et, const CallParams* cp, void* e, int T, int Tpad, int d, hipStream_t s);
 hipError_t launch_copy_f32(float* dst, const float* src, size_t n, hipStream_t s);
