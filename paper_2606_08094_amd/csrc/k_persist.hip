@@ -29,6 +29,7 @@
 // L2 write-back or invalidate is needed.  Barriers are relaxed agent-scope
 // counters; every wait is bounded, and a timeout sets *err, writes NaN into
 // the chunk and makes every workgroup leave.
+#include <utility>
 #include "device_common.h"
 
 namespace {
@@ -194,39 +195,78 @@ VLA_DEV void prefetch_w(WTile<NS>& t, rsrc_t W, int ldw, int kofs, int K, const 
 // rows x 64 contiguous bytes = 1 KB); rows past M read zero.
 VLA_DEV unsigned xtile_off(int m, int k, int M) { return (unsigned)(((k >> 5) * M + m) * 64 + (k & 31) * 2); }
 
+// The X operand is staged through LDS: the wave copies its CPW x VPL x 4
+// blocks of 1 KB (16 rows x 32 k) with direct-to-LDS buffer loads, all in
+// flight at once and holding no registers, into its own XSTAGE-byte slice;
+// lane l of a block lands at byte 16 l, which is the 16 bytes lane l feeds to
+// the MFMA.  Each (j, v) group is read back after its own loads have landed
+// (in-order vmcnt), so the MFMAs of early groups overlap the later loads.
+// Lanes of absent rows and chunks past K get offsets past the buffer, and an
+// out-of-range direct-to-LDS load writes zeros, so those operands are zero
+// (the weights of chunks past K are zero too).  Every acc[ms][s] sums its
+// k-products in the order (j, v), as a register-staged form would.
+constexpr int XSTAGE = CPW * VPL * 4 * 1024;   // LDS bytes per wave
+
+// Buffer descriptor words of [base, base + bytes) in SGPRs (the layout
+// mkr builds: stride 0, bounds-checked, zero past the end).
+VLA_DEV u32x4_t rsrc_words(const void* base, unsigned bytes) {
+  const unsigned long long p = (unsigned long long)(uintptr_t)base;
+  return u32x4_t{(unsigned)__builtin_amdgcn_readfirstlane((unsigned)p),
+                 (unsigned)__builtin_amdgcn_readfirstlane((unsigned)(p >> 32)) & 0xffffu,
+                 (unsigned)__builtin_amdgcn_readfirstlane(bytes), 0x00020000u};
+}
+// One wave-wide device-coherent (sc1) buffer load of 16 bytes per lane into
+// LDS at the wave-uniform lds + 16 lane.  Written as asm so that the compiler
+// adds no waits of its own for it; the caller's vmcnt waits order it.
+VLA_DEV void dma_x16(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned char* lds) {
+  typedef __attribute__((address_space(3))) unsigned char lds_u8;
+  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
+               : : "s"(lb), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
+}
+template <int N>
+VLA_DEV void vm_wait_mem() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
+
 template <int NS>
-VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, rsrc_t X, int K, int M) {
+VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase, unsigned xbytes, int K, int M,
+                      unsigned char* stage) {
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g4 = lane >> 4;
-  // offset = lane part (row r16 of subtile ms, 16-byte group g4) + a
-  // wave-uniform part (32-column block, subtile); absent rows and chunks
-  // past K get offsets beyond the buffer
+  unsigned char* ws = stage + wave * XSTAGE;
+  const u32x4_t rs = rsrc_words(xbase, xbytes);
   unsigned vo[4];
 #pragma unroll
   for (int ms = 0; ms < 4; ++ms) vo[ms] = (16 * ms + r16 < M) ? (unsigned)(r16 * 64 + g4 * 16) : 0x7ffffff0u;
-  uint4 xr[CPW][4][VPL];
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
     const int kc = 128 * (wave + NW * j);
 #pragma unroll
-    for (int ms = 0; ms < 4; ++ms)
+    for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int v = 0; v < VPL; ++v) {
+      for (int ms = 0; ms < 4; ++ms) {
         const unsigned so = kc < K ? (unsigned)(((kc >> 5) + v) * M * 64 + ms * 16 * 64) : 0x7ffffff0u;
-        const u32x4_t x = __builtin_amdgcn_raw_buffer_load_b128(X, (int)vo[ms], (int)so, LDX);
-        xr[j][ms][v] = make_uint4(x.x, x.y, x.z, x.w);
+        dma_x16(rs, vo[ms], so, ws + ((j * VPL + v) * 4 + ms) * 1024);
       }
   }
 #pragma unroll
   for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      acc[ms][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int s = 0; s < NS; ++s) acc[ms][s] = f32x4{0.f, 0.f, 0.f, 0.f};
+  // group g = (j, v): wait until only the later groups' loads are in flight
+  auto group = [&]<int G>(std::integral_constant<int, G>) {
+    constexpr int j = G / VPL, v = G % VPL;
+    vm_wait_mem<4 * (CPW * VPL - 1 - G)>();
+    uint4 x[4];
 #pragma unroll
-      for (int j = 0; j < CPW; ++j)
+    for (int ms = 0; ms < 4; ++ms) x[ms] = *reinterpret_cast<const uint4*>(ws + (G * 4 + ms) * 1024 + lane * 16);
 #pragma unroll
-        for (int v = 0; v < VPL; ++v) mma16(acc[ms][s], xr[j][ms][v], t.w[j][s][v], bf16_t());
-    }
+    for (int ms = 0; ms < 4; ++ms)
+#pragma unroll
+      for (int s = 0; s < NS; ++s) mma16(acc[ms][s], x[ms], t.w[j][s][v], bf16_t());
+  };
+  [&]<int... G>(std::integer_sequence<int, G...>) {
+    (group(std::integral_constant<int, G>{}), ...);
+  }(std::make_integer_sequence<int, CPW * VPL>{});
 }
 
 // Sum the 4 waves' tiles through LDS (red: 4 * 4 * NS * 64 f32x4); afterwards
@@ -328,6 +368,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   const rsrc_t APr = mkr((const bf16_t*)a.apart + (size_t)team * S * n * HTD, (size_t)S * n * HTD * 2);
   const rsrc_t ASr = mkr(a.astat + (size_t)team * S * n * HT * 2, (size_t)S * n * HT * 8);
   const rsrc_t Hr = mkr((const bf16_t*)a.hbuf + (size_t)team * n * F8, (size_t)n * F8 * 2);
+  const void* ubase = (const bf16_t*)a.u + (size_t)team * n * d;     // the GEMM phases' X operands
+  const void* hbase = (const bf16_t*)a.hbuf + (size_t)team * n * F8;
   const rsrc_t OMr = mkr((const bf16_t*)a.omerged + (size_t)team * n * HTD, (size_t)n * HTD * 2);
   const rsrc_t Dr = mkr(a.delta, (size_t)2 * NTEAM * n * d * 4);   // [buf][team][n][d]
 
@@ -662,7 +704,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         int wr[2], oc[2];
         qkv_rows(wr, oc);
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wq, Ur, d, n);
+        tile_mma<2>(acc, wq, ubase, (unsigned)(n * d * 2), d, n, smem);
+        __syncthreads();
         tile_reduce<2>(acc, red);
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
@@ -952,7 +995,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       // ---- G: u -> h of the team's MLP columns ------------------------------------
       {
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wg, Ur, d, n);
+        tile_mma<2>(acc, wg, ubase, (unsigned)(n * d * 2), d, n, smem);
+        __syncthreads();
         tile_reduce<2>(acc, red);
         if (rank < npairs) {
           const int f = 16 * rank + r16;
@@ -1002,7 +1046,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         int wr[2];
         dn_rows(wr);
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wd, Hr, F8, n);
+        tile_mma<2>(acc, wd, hbase, (unsigned)(n * F8 * 2), F8, n, smem);
+        __syncthreads();
         tile_reduce<2>(acc, red);
 #pragma unroll
         for (int s = 0; s < 2; ++s) {
@@ -1082,7 +1127,9 @@ bool persist_supported(int d, int hd, int H, int G, int F, int n, int P, int A, 
 size_t persist_lds_bytes(int hd, int HT) {
   const size_t otile = (size_t)64 * (HT * hd + 8) * 2;
   const size_t mainb = lds_main(hd);
-  return mainb > otile ? mainb : otile;
+  const size_t xst = (size_t)NW * XSTAGE;   // the GEMM phases' staged activations
+  const size_t m2 = mainb > otile ? mainb : otile;
+  return m2 > xst ? m2 : xst;
 }
 
 namespace {
