@@ -234,6 +234,12 @@ VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase
   const int r16 = lane & 15, g4 = lane >> 4;
   unsigned char* ws = stage + wave * XSTAGE;
   const u32x4_t rs = rsrc_words(xbase, xbytes);
+  // The weight tile (and every other load in flight) must land before the
+  // first MFMA anyway.  Waiting here, with a wait the compiler sees, clears
+  // its count of outstanding loads, so it adds no vmcnt(0) of its own after
+  // the asm loads below, which it cannot count and which would stall every
+  // group until the last one has landed.
+  __builtin_amdgcn_s_waitcnt(vm_wait(0));
   unsigned vo[4];
 #pragma unroll
   for (int ms = 0; ms < 4; ++ms) vo[ms] = (16 * ms + r16 < M) ? (unsigned)(r16 * 64 + g4 * 16) : 0x7ffffff0u;
