@@ -174,7 +174,9 @@ struct WTile {
 // W: [rows][ldw] bf16 (rsrc over the matrix), columns kofs + k; wrow[s] < 0: tile s absent.
 template <int NS>
 VLA_DEV void prefetch_w(WTile<NS>& t, rsrc_t W, int ldw, int kofs, int K, const int (&wrow)[NS]) {
-  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  // the wave index in a scalar register: the row-block offsets derived from it
+  // are scalar, so each load is one instruction (no loop over lane values)
+  const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g4 = lane >> 4;
 #pragma unroll
   for (int j = 0; j < CPW; ++j) {
@@ -326,7 +328,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   __shared__ float hv[2][NW][32];          // head partial sums per wave
   __shared__ PLayer lt[PERSIST_MAX_LAYERS];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int r16 = lane & 15, g4 = lane >> 4;
   // Team = the XCD this workgroup runs on, rank = its arrival order there, so
   // the team-local exchange through the XCD's L2 is coherent whatever order
