@@ -230,8 +230,8 @@ vla_status vla_ternary_gemm(const int8_t* x, const uint8_t* w_packed, int32_t M,
  *    layout.  0 (default) = the paper's embedding.  Discards the cached plans;
  *    such models run on loop modes 0 and 1.
  *  VLA_OPT_PERSIST_SPIN_LIMIT: polls of one barrier wait of the persistent
- *    step kernel before it gives up (value >= 0; -1 = the default, about
- *    0.2 s).  For tests of the failure path: a small value makes waits time
+ *    step kernel before it gives up (value >= 0; -1 = the default, 2^20
+ *    polls, about 0.25 s).  For tests of the failure path: a small value makes waits time
  *    out, which every workgroup survives (see vla_denoise). */
 enum { VLA_OPT_LOOP_MODE = 0, VLA_OPT_PROFILE = 1, VLA_OPT_TRACE = 2, VLA_OPT_ATTN_SPLITS = 3,
        VLA_OPT_CAUSAL_SELF = 4, VLA_OPT_ROPE_BASE = 5, VLA_OPT_STATE_TOKEN = 6,

@@ -137,7 +137,9 @@ VLA_DEV bool wait_flags(Sync& s, int team, int* lds_flag, unsigned peek) {
     if (!__all(peek >= target)) {
       long it = 0;
       while (true) {
-        __builtin_amdgcn_s_sleep(1);
+        // about 256 clocks between polls: fewer polls on the 8 hot flag lines
+        // let the flag stores through sooner (measured best among 1, 2, 4, 8, 16)
+        __builtin_amdgcn_s_sleep(4);
         if (__all(flag_peek<GRID>(s, team) >= target)) break;
         if (++it > s.spin_limit) {
           if (threadIdx.x == 0) __hip_atomic_fetch_or(s.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);

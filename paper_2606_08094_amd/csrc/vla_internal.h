@@ -206,7 +206,7 @@ struct PersistArgs {
 constexpr int PERSIST_RANK_OFF = 8 * 32;          // 8 per-XCD arrival counters (team ranks)
 constexpr int PERSIST_ERR_OFF = 8 * 32 + 32;      // the error word, on a line of its own
 constexpr int PERSIST_SYNC_WORDS = 8 * 32 + 64;   // barrier flags [8][32], rank counters, error word
-constexpr long PERSIST_SPIN_DEFAULT = 1L << 21;   // barrier polls before a timeout (about 0.2 s)
+constexpr long PERSIST_SPIN_DEFAULT = 1L << 20;   // barrier polls before a timeout (about 0.25 s)
 constexpr int PERSIST_TRACE_MAX = 8192;
 constexpr int PERSIST_TRACE_WG = 8 * PERSIST_TRACE_MAX / 256;   // marks per workgroup when all record
 constexpr int PERSIST_MAX_LAYERS = 64;
