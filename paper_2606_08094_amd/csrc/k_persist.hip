@@ -120,10 +120,10 @@ VLA_DEV unsigned flag_peek(const Sync& s, int team) {
   const int t = threadIdx.x;
   if (t >= 64) return 0xffffffffu;
   if (GRID) {
-    unsigned v[4];
-#pragma unroll
-    for (int i = 0; i < 4; ++i) v[i] = __hip_atomic_load(s.flag + 4 * t + i, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    return min(min(v[0], v[1]), min(v[2], v[3]));
+    // one 16-byte device-coherent load per lane: the 256 flags in one
+    // instruction (a quarter of the requests of four 4-byte loads)
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(mkr(s.flag, (size_t)NWG * 4), t * 16, 0, LDX);
+    return min(min(v.x, v.y), min(v.z, v.w));
   }
   return t < TSIZE ? __hip_atomic_load(s.flag + team * 32 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0xffffffffu;
 }
