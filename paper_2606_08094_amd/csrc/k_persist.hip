@@ -91,26 +91,34 @@ VLA_DEV unsigned xcc_id() {
 }
 
 // ---------------------------------------------------------------------------
-// Barriers, without atomics.  Every workgroup owns one flag word holding the
-// number of barriers (team and grid alike) it has arrived at; the flags of a
-// team are one 128-byte line, flag[team * 32 + rank].  Arriving = waiting
-// until this workgroup's stores have completed, then a device-coherent store
-// of the new count.  A team barrier waits until the team's 32 flags reach the
-// count (one load per lane of the first wave), a grid barrier until all 256 do
-// (lane l reads flags 4l .. 4l+3).  Flags only grow, so a workgroup that is
-// already past the barrier also satisfies it.
+// Barriers, without atomics.  Every workgroup owns two flag words holding the
+// number of barriers it has arrived at: a team flag, stored at team barriers
+// with a plain store (only workgroups of the same XCD read it, from that XCD's
+// L2, where the line stays), and a grid flag, stored at grid barriers with a
+// device-coherent store that other XCDs can see.  The flags of a team are one
+// 128-byte line, flag[team * 32 + rank].  Arriving = waiting until this
+// workgroup's stores have completed, then the store of the new count.  A team
+// barrier waits until the team's 32 team flags reach the count (one load per
+// lane of the first wave), a grid barrier until all 256 grid flags do (one
+// 16-byte load per lane).  Flags only grow, so a workgroup that is already
+// past the barrier also satisfies it.
 struct Sync {
-  unsigned* flag;   // [8][32]
+  unsigned* flag;   // [8][32]: grid barriers (device-coherent stores: other XCDs read them)
+  unsigned* tflag;  // [8][32]: team barriers (plain stores: only the team's XCD reads them, from its L2)
   int* err;
   unsigned bk;      // barriers this workgroup has arrived at
   long spin_limit;  // polls before a wait gives up
 };
 
+template <bool GRID>
 VLA_DEV void arrive(Sync& s, int team, int rank) {
   __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
   __syncthreads();
   ++s.bk;
-  if (threadIdx.x == 0) __hip_atomic_store(s.flag + team * 32 + rank, s.bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+  if (threadIdx.x == 0) {
+    if (GRID) __hip_atomic_store(s.flag + team * 32 + rank, s.bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    else __builtin_amdgcn_raw_buffer_store_b32(s.bk, mkr(s.tflag, (size_t)NWG * 4), (team * 32 + rank) * 4, 0, 0);
+  }
 }
 
 // Smallest flag this lane of the first wave watches (team: lane < 32 reads
@@ -125,7 +133,7 @@ VLA_DEV unsigned flag_peek(const Sync& s, int team) {
     const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(mkr(s.flag, (size_t)NWG * 4), t * 16, 0, LDX);
     return min(min(v.x, v.y), min(v.z, v.w));
   }
-  return t < TSIZE ? __hip_atomic_load(s.flag + team * 32 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0xffffffffu;
+  return t < TSIZE ? __hip_atomic_load(s.tflag + team * 32 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0xffffffffu;
 }
 
 // Returns false (in every thread) if the run must stop.
@@ -357,7 +365,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   for (int i = tid; i < a.L; i += NTHR) lt[i] = a.layers[i];
   const bf16_t* kvbase = reinterpret_cast<const bf16_t*>(a.cp->kv_cache);
 
-  Sync sy{a.sync, a.err, 0u, a.spin_limit};
+  Sync sy{a.sync, a.sync + PERSIST_TFLAG_OFF, a.err, 0u, a.spin_limit};
   unsigned long long* trace = !a.trace ? nullptr
                               : a.trace_all ? a.trace + (size_t)(team * TSIZE + rank) * PERSIST_TRACE_WG
                               : (rank == 0 ? a.trace + (size_t)team * PERSIST_TRACE_MAX : nullptr);
@@ -702,7 +710,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   embed();
   norm_store(gam(0, 0, 0), gam(0, 0, 0) + d);
   mark();
-  arrive(sy, team, rank);
+  arrive<false>(sy, team, rank);
       if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
   mark();
 
@@ -728,7 +736,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      arrive(sy, team, rank);
+      arrive<false>(sy, team, rank);
       const unsigned pk1 = flag_peek<false>(sy, team);
       prefetch_kv(l);
       if (att_on) stage_prefix();   // independent of this step: done while the team arrives
@@ -871,7 +879,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      arrive(sy, team, rank);
+      arrive<false>(sy, team, rank);
       const unsigned pk2 = flag_peek<false>(sy, team);
       prefetch_wo(l);
       if (!wait_flags<false>(sy, team, &flag, pk2)) return bail();
@@ -938,7 +946,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      arrive(sy, team, rank);
+      arrive<false>(sy, team, rank);
       if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
       mark();
 
@@ -984,7 +992,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      arrive(sy, team, rank);
+      arrive<true>(sy, team, rank);
       const unsigned pk3 = flag_peek<true>(sy, team);
       {
         int wr[2];
@@ -998,7 +1006,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       resid(0, gam(k, l, 0) + 2 * d);
       norm_store(gam(k, l, 1), gam(k, l, 1) + d);
       mark();
-      arrive(sy, team, rank);
+      arrive<false>(sy, team, rank);
       if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
       mark();
 
@@ -1041,7 +1049,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         }
       }
       mark();
-      arrive(sy, team, rank);
+      arrive<false>(sy, team, rank);
       const unsigned pk4 = flag_peek<false>(sy, team);
       {
         int wr[2];
@@ -1073,7 +1081,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       const bool last_layer = l == a.L - 1;
       const bool last = last_layer && k == a.T - 1;
       mark();
-      arrive(sy, team, rank);
+      arrive<true>(sy, team, rank);
       const unsigned pk5 = flag_peek<true>(sy, team);
       {
         int wr[2], oc[2];
@@ -1097,7 +1105,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       }
       if (!last) {
         mark();
-        arrive(sy, team, rank);
+        arrive<false>(sy, team, rank);
       if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
         mark();
       }
