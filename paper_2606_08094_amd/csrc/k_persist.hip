@@ -755,24 +755,25 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         const unsigned qb = (unsigned)(qrow * QW + hh * HD + g4 * (HD / 4)) * 2u;
 #pragma unroll
         for (int c = 0; c < NQV; ++c) qf[c] = ld16<LDX>(Qr, qwave ? qb + 16u * c : OOB);
-        uint4 kch[NKI], vch[NKI];
+        // A split holding chunk-token keys holds one block of them (jbeg >=
+        // nbp): one block's items per thread (every wave-wide load costs the
+        // address unit about as much whether its lanes are in range or not).
+        constexpr int NKC = 32 * VPR / NTHR;
+        const bool chunk = jbeg >= nbp;
+        uint4 kch[NKC], vch[NKC];
 #pragma unroll
-        for (int q = 0; q < NKI; ++q) {
+        for (int q = 0; q < NKC; ++q) {
           const int i = tid + q * NTHR;
-          const int jb = i / (32 * VPR), rr = i - jb * 32 * VPR;
-          const int kr = rr / VPR, cv = rr - kr * VPR;
-          const int j = jbeg + jb, key = (j - nbp) * 32 + kr;
-          const bool ok = i < nblk * 32 * VPR && j >= nbp;
+          const int kr = i / VPR, cv = i - kr * VPR;
+          const int key = (jbeg - nbp) * 32 + kr;
+          const bool ok = chunk && key < nself;
           const unsigned off = ok ? (unsigned)(key * QW + HTD + cv * 8) * 2u : OOB;
           kch[q] = ld16<LDX>(Qr, off);
           vch[q] = ld16<LDX>(Qr, ok ? off + HD * 2u : OOB);
         }
-        if (jbeg + nblk > nbp) {   // the split holds chunk-token keys
+        if (chunk) {
 #pragma unroll
-          for (int q = 0; q < NKI; ++q) {
-            const int i = tid + q * NTHR;
-            if (i < nblk * 32 * VPR && jbeg + i / (32 * VPR) >= nbp) put_kv(i, kch[q], vch[q]);
-          }
+          for (int q = 0; q < NKC; ++q) put_kv(tid + q * NTHR, kch[q], vch[q]);
         }
         __syncthreads();
         if (qwave) {
