@@ -91,33 +91,40 @@ VLA_DEV unsigned xcc_id() {
 }
 
 // ---------------------------------------------------------------------------
-// Barriers, without atomics.  Every workgroup owns two flag words holding the
+// Barriers, without atomics.  Every workgroup owns flag words holding the
 // number of barriers it has arrived at: a team flag, stored at team barriers
 // with a plain store (only workgroups of the same XCD read it, from that XCD's
-// L2, where the line stays), and a grid flag, stored at grid barriers with a
-// device-coherent store that other XCDs can see.  The flags of a team are one
-// 128-byte line, flag[team * 32 + rank].  Arriving = waiting until this
-// workgroup's stores have completed, then the store of the new count.  A team
-// barrier waits until the team's 32 team flags reach the count (one load per
-// lane of the first wave), a grid barrier until all 256 grid flags do (one
-// 16-byte load per lane).  Flags only grow, so a workgroup that is already
-// past the barrier also satisfies it.
+// L2, where the line stays), and a grid flag, stored at grid barriers with
+// device-coherent stores that other XCDs can see, into eight copies of the
+// grid flags 4 KB apart: team x polls copy x, so each copy's lines have 32
+// pollers instead of 256 and the copies sit in different memory channels.
+// The flags of a team are one 128-byte line, flag[team * 32 + rank].
+// Arriving = waiting until this workgroup's stores have completed, then the
+// store of the new count.  A team barrier waits until the team's 32 team flags
+// reach the count (one load per lane of the first wave), a grid barrier until
+// all 256 grid flags of the team's copy do (one 16-byte load per lane).  Flags
+// only grow, so a workgroup that is already past the barrier also satisfies it.
 struct Sync {
-  unsigned* flag;   // [8][32]: grid barriers (device-coherent stores: other XCDs read them)
+  unsigned* flag;   // 8 copies of [8][32], PERSIST_GFLAG_STRIDE words apart: grid barriers (device-coherent)
   unsigned* tflag;  // [8][32]: team barriers (plain stores: only the team's XCD reads them, from its L2)
   int* err;
   unsigned bk;      // barriers this workgroup has arrived at
   long spin_limit;  // polls before a wait gives up
 };
 
+// drain = false: this workgroup stored nothing since its last arrival, so its
+// loads in flight need not land first.
 template <bool GRID>
-VLA_DEV void arrive(Sync& s, int team, int rank) {
-  __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
+VLA_DEV void arrive(Sync& s, int team, int rank, bool drain = true) {
+  if (drain) __builtin_amdgcn_s_waitcnt(0);  // this thread's stores have completed
   __syncthreads();
   ++s.bk;
-  if (threadIdx.x == 0) {
-    if (GRID) __hip_atomic_store(s.flag + team * 32 + rank, s.bk, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    else __builtin_amdgcn_raw_buffer_store_b32(s.bk, mkr(s.tflag, (size_t)NWG * 4), (team * 32 + rank) * 4, 0, 0);
+  if (GRID) {
+    if (threadIdx.x < NTEAM)   // one copy per thread
+      __hip_atomic_store(s.flag + threadIdx.x * PERSIST_GFLAG_STRIDE + team * 32 + rank, s.bk, __ATOMIC_RELAXED,
+                         __HIP_MEMORY_SCOPE_AGENT);
+  } else if (threadIdx.x == 0) {
+    __builtin_amdgcn_raw_buffer_store_b32(s.bk, mkr(s.tflag, (size_t)NWG * 4), (team * 32 + rank) * 4, 0, 0);
   }
 }
 
@@ -130,7 +137,8 @@ VLA_DEV unsigned flag_peek(const Sync& s, int team) {
   if (GRID) {
     // one 16-byte device-coherent load per lane: the 256 flags in one
     // instruction (a quarter of the requests of four 4-byte loads)
-    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(mkr(s.flag, (size_t)NWG * 4), t * 16, 0, LDX);
+    const u32x4_t v =
+        __builtin_amdgcn_raw_buffer_load_b128(mkr(s.flag + team * PERSIST_GFLAG_STRIDE, (size_t)NWG * 4), t * 16, 0, LDX);
     return min(min(v.x, v.y), min(v.z, v.w));
   }
   return t < TSIZE ? __hip_atomic_load(s.tflag + team * 32 + t, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) : 0xffffffffu;
@@ -235,6 +243,15 @@ VLA_DEV void dma_x16(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned c
   const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
                : : "s"(lb), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
+}
+// One wave-wide load of 4 bytes per lane into LDS at the wave-uniform
+// lds + 4 lane, with the default cache policy.  Used only to bring lines into
+// the XCD's L2 (the LDS copy is never read); asm, like dma_x16, and waited for
+// by the next full wait.
+VLA_DEV void touch_l2(const u32x4_t& rs, unsigned voff, unsigned char* lds) {
+  typedef __attribute__((address_space(3))) unsigned char lds_u8;
+  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "s"(lb), "v"(voff), "s"(rs) : "memory", "m0");
 }
 template <int N>
 VLA_DEV void vm_wait_mem() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
@@ -878,9 +895,32 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
                    __float_as_uint(lrun));
           }
         }
+      } else if (S < TSIZE) {
+        // A rank without a key split brings its share of the team's MLP
+        // weights of this layer into the XCD's L2 (one 4-byte load per 64
+        // bytes): the gate / up rows, then the down projection's columns.  The
+        // G and D phases' weight loads, issued at the barriers before them,
+        // then hit there instead of waiting for HBM, and the polls queued
+        // behind those loads return sooner.  Started about 1 us into the
+        // phase, after the key splits' own loads; not waited for (see below).
+        const int nwv = (TSIZE - S) * NW, w0 = (rank - S) * NW + wave;
+        const size_t gurows = (size_t)(a.glu ? 2 : 1) * F8;
+        const unsigned gub = (unsigned)(gurows * d * 2);
+        const u32x4_t rg = rsrc_words((const bf16_t*)ly.wgu + (size_t)team * gurows * d, gub);
+        const u32x4_t rd = rsrc_words((const bf16_t*)ly.wd + (size_t)team * F8, (unsigned)((size_t)(d - 1) * a.F * 2 + F8 * 2));
+        const int lpr = F8 * 2 / 64;       // 64-byte pieces of a down-projection row
+        __builtin_amdgcn_s_sleep(40);
+        for (int it = w0; it < (int)(gub / 4096u); it += nwv) touch_l2(rg, (unsigned)it * 4096u + lane * 64u, smem + wave * 256);
+        for (int it = w0; it < d * lpr / 64; it += nwv) {
+          const int pc = it * 64 + lane, row = pc / lpr;
+          touch_l2(rd, (unsigned)(row * a.F * 2 + (pc - row * lpr) * 64), smem + wave * 256);
+        }
       }
       mark();
-      arrive<false>(sy, team, rank);
+      // A rank without a key split stored nothing here and arrives at once;
+      // its L2 loads land before the merge phase's loads (in-order returns) and
+      // before its next full wait, ahead of the O phase's LDS use.
+      arrive<false>(sy, team, rank, __builtin_amdgcn_readfirstlane(att_on ? 1 : 0) != 0);
       const unsigned pk2 = flag_peek<false>(sy, team);
       prefetch_wo(l);
       if (!wait_flags<false>(sy, team, &flag, pk2)) return bail();

@@ -203,10 +203,14 @@ struct PersistArgs {
   unsigned long long* trace;
   int trace_all;             // 1: every workgroup records its first PERSIST_TRACE_WG marks (row team * 32 + rank)
 };
+// Grid barrier flags [8][32] in 8 copies, 4 KB apart (team x polls copy x);
+// the first copy's 4 KB also holds the rank counters, the error word and the
+// team barrier flags.
+constexpr int PERSIST_GFLAG_STRIDE = 1024;        // words between two copies of the grid flags
 constexpr int PERSIST_RANK_OFF = 8 * 32;          // 8 per-XCD arrival counters (team ranks)
 constexpr int PERSIST_ERR_OFF = 8 * 32 + 32;      // the error word, on a line of its own
 constexpr int PERSIST_TFLAG_OFF = 8 * 32 + 64;    // team barrier flags [8][32], one 128-byte line per team
-constexpr int PERSIST_SYNC_WORDS = 16 * 32 + 64;  // grid flags [8][32], rank counters, error word, team flags
+constexpr int PERSIST_SYNC_WORDS = 8 * PERSIST_GFLAG_STRIDE;
 constexpr long PERSIST_SPIN_DEFAULT = 1L << 20;   // barrier polls before a timeout (about 0.25 s)
 constexpr int PERSIST_TRACE_MAX = 8192;
 constexpr int PERSIST_TRACE_WG = 8 * PERSIST_TRACE_MAX / 256;   // marks per workgroup when all record
