@@ -215,8 +215,8 @@ VLA_DEV void prefetch_w(WTile<NS>& t, rsrc_t W, int ldw, int kofs, int K, const 
 // rows x 64 contiguous bytes = 1 KB); rows past M read zero.
 VLA_DEV unsigned xtile_off(int m, int k, int M) { return (unsigned)(((k >> 5) * M + m) * 64 + (k & 31) * 2); }
 
-// The X operand is staged through LDS: the wave copies its CPW x VPL x 4
-// blocks of 1 KB (16 rows x 32 k) with direct-to-LDS buffer loads, all in
+// The X operand is staged through LDS: the wave copies its NCH x VPL groups
+// of 4 blocks of 1 KB (16 rows x 32 k) with direct-to-LDS buffer loads, all in
 // flight at once and holding no registers, into its own XSTAGE-byte slice;
 // lane l of a block lands at byte 16 l, which is the 16 bytes lane l feeds to
 // the MFMA.  Each (j, v) group is read back after its own loads have landed
@@ -256,9 +256,17 @@ VLA_DEV void touch_l2(const u32x4_t& rs, unsigned voff, unsigned char* lds) {
 template <int N>
 VLA_DEV void vm_wait_mem() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
 
-template <int NS>
+// NCH: the wave's K chunks (K <= 128 NW NCH); FOLD (M <= 50): the fourth
+// 16-row subtile holds at most rows 48 and 49, and those rows of all the
+// wave's groups come in with one load (lane l: group l / 8, row 48 + (l / 4) % 2,
+// k part l % 4) instead of one mostly out-of-range load per group.  A load
+// costs the address unit the same whether its lanes are in range or not.
+template <int NS, int NCH, bool FOLD>
 VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase, unsigned xbytes, int K, int M,
                       unsigned char* stage) {
+  static_assert(NCH >= 1 && NCH <= CPW && (!FOLD || NCH * VPL <= 8), "tile_mma shape");
+  constexpr int NG = NCH * VPL;            // (j, v) groups of the wave
+  constexpr int LPG = FOLD ? 3 : 4;        // loads per group
   const int lane = threadIdx.x & 63, wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
   const int r16 = lane & 15, g4 = lane >> 4;
   unsigned char* ws = stage + wave * XSTAGE;
@@ -269,16 +277,24 @@ VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase
   // the asm loads below, which it cannot count and which would stall every
   // group until the last one has landed.
   __builtin_amdgcn_s_waitcnt(vm_wait(0));
+  if constexpr (FOLD) {   // rows 48, 49 of every group, into group 0's fourth block
+    const int gg = lane >> 3, rr = 48 + ((lane >> 2) & 1);
+    const int kc = 128 * (wave + NW * (gg / VPL));
+    const unsigned off = (gg < NG && kc < K && rr < M)
+                             ? (unsigned)((((kc >> 5) + gg % VPL) * M + rr) * 64 + (lane & 3) * 16)
+                             : 0x7ffffff0u;
+    dma_x16(rs, off, 0u, ws + 3 * 1024);
+  }
   unsigned vo[4];
 #pragma unroll
   for (int ms = 0; ms < 4; ++ms) vo[ms] = (16 * ms + r16 < M) ? (unsigned)(r16 * 64 + g4 * 16) : 0x7ffffff0u;
 #pragma unroll
-  for (int j = 0; j < CPW; ++j) {
+  for (int j = 0; j < NCH; ++j) {
     const int kc = 128 * (wave + NW * j);
 #pragma unroll
     for (int v = 0; v < VPL; ++v)
 #pragma unroll
-      for (int ms = 0; ms < 4; ++ms) {
+      for (int ms = 0; ms < LPG; ++ms) {
         const unsigned so = kc < K ? (unsigned)(((kc >> 5) + v) * M * 64 + ms * 16 * 64) : 0x7ffffff0u;
         dma_x16(rs, vo[ms], so, ws + ((j * VPL + v) * 4 + ms) * 1024);
       }
@@ -288,12 +304,17 @@ VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase
 #pragma unroll
     for (int s = 0; s < NS; ++s) acc[ms][s] = f32x4{0.f, 0.f, 0.f, 0.f};
   // group g = (j, v): wait until only the later groups' loads are in flight
+  // (the folded load is older than all of them)
   auto group = [&]<int G>(std::integral_constant<int, G>) {
     constexpr int j = G / VPL, v = G % VPL;
-    vm_wait_mem<4 * (CPW * VPL - 1 - G)>();
+    vm_wait_mem<LPG * (NG - 1 - G)>();
     uint4 x[4];
 #pragma unroll
-    for (int ms = 0; ms < 4; ++ms) x[ms] = *reinterpret_cast<const uint4*>(ws + (G * 4 + ms) * 1024 + lane * 16);
+    for (int ms = 0; ms < LPG; ++ms) x[ms] = *reinterpret_cast<const uint4*>(ws + (G * 4 + ms) * 1024 + lane * 16);
+    if constexpr (FOLD) {
+      const uint4 f = *reinterpret_cast<const uint4*>(ws + 3 * 1024 + (G * 8 + (r16 & 1) * 4 + g4) * 16);
+      x[3] = r16 < 2 ? f : make_uint4(0, 0, 0, 0);
+    }
 #pragma unroll
     for (int ms = 0; ms < 4; ++ms)
 #pragma unroll
@@ -301,7 +322,7 @@ VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase
   };
   [&]<int... G>(std::integer_sequence<int, G...>) {
     (group(std::integral_constant<int, G>{}), ...);
-  }(std::make_integer_sequence<int, CPW * VPL>{});
+  }(std::make_integer_sequence<int, NG>{});
 }
 
 // Sum the 4 waves' tiles through LDS (red: 4 * 4 * NS * 64 f32x4); afterwards
@@ -339,7 +360,8 @@ size_t lds_main(int hd) {
   return att > red2 ? att : red2;
 }
 
-template <int HD, int DPT>
+// FOLD: the chunk has at most 50 rows (see tile_mma).
+template <int HD, int DPT, bool FOLD>
 __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   using L = PLds<HD>;
   constexpr int VPR = HD / 8;              // 16-byte vectors per K/V row
@@ -739,7 +761,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         int wr[2], oc[2];
         qkv_rows(wr, oc);
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wq, ubase, (unsigned)(n * d * 2), d, n, smem);
+        tile_mma<2, DPT / 2, FOLD>(acc, wq, ubase, (unsigned)(n * d * 2), d, n, smem);
         __syncthreads();
         tile_reduce<2>(acc, red);
 #pragma unroll
@@ -1054,7 +1076,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       // ---- G: u -> h of the team's MLP columns ------------------------------------
       {
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wg, ubase, (unsigned)(n * d * 2), d, n, smem);
+        tile_mma<2, DPT / 2, FOLD>(acc, wg, ubase, (unsigned)(n * d * 2), d, n, smem);
         __syncthreads();
         tile_reduce<2>(acc, red);
         if (rank < npairs) {
@@ -1105,7 +1127,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         int wr[2];
         dn_rows(wr);
         f32x4 acc[4][2];
-        tile_mma<2>(acc, wd, hbase, (unsigned)(n * F8 * 2), F8, n, smem);
+        tile_mma<2, 1, FOLD>(acc, wd, hbase, (unsigned)(n * F8 * 2), F8, n, smem);   // K = F / 8 <= 512
         __syncthreads();
         tile_reduce<2>(acc, red);
 #pragma unroll
@@ -1192,31 +1214,37 @@ size_t persist_lds_bytes(int hd, int HT) {
 }
 
 namespace {
-const void* persist_fn(int hd, int d) {
-  const int dpt = d / NTHR;
+template <bool FOLD>
+const void* persist_fn_t(int hd, int dpt) {
   switch (hd * 10 + dpt) {
-    case 2564: return reinterpret_cast<const void*>(&persist_kernel<256, 4>);
-    case 2562: return reinterpret_cast<const void*>(&persist_kernel<256, 2>);
-    case 1284: return reinterpret_cast<const void*>(&persist_kernel<128, 4>);
-    case 1282: return reinterpret_cast<const void*>(&persist_kernel<128, 2>);
-    case 644: return reinterpret_cast<const void*>(&persist_kernel<64, 4>);
-    case 642: return reinterpret_cast<const void*>(&persist_kernel<64, 2>);
+    case 2564: return reinterpret_cast<const void*>(&persist_kernel<256, 4, FOLD>);
+    case 2562: return reinterpret_cast<const void*>(&persist_kernel<256, 2, FOLD>);
+    case 1284: return reinterpret_cast<const void*>(&persist_kernel<128, 4, FOLD>);
+    case 1282: return reinterpret_cast<const void*>(&persist_kernel<128, 2, FOLD>);
+    case 644: return reinterpret_cast<const void*>(&persist_kernel<64, 4, FOLD>);
+    case 642: return reinterpret_cast<const void*>(&persist_kernel<64, 2, FOLD>);
     default: return nullptr;
   }
+}
+// chunks of at most 50 rows take the folded-tail form of the GEMM phases
+const void* persist_fn(int hd, int d, int n) {
+  return n <= 50 ? persist_fn_t<true>(hd, d / NTHR) : persist_fn_t<false>(hd, d / NTHR);
 }
 }  // namespace
 
 bool persist_resident(int d, int hd, int HT) {
-  const void* fn = persist_fn(hd, d);
-  if (!fn) return false;
+  const void* fns[2] = {persist_fn(hd, d, 1), persist_fn(hd, d, 64)};
+  if (!fns[0] || !fns[1]) return false;
   int dev = 0, cus = 0, nb = 0;
   if (hipGetDevice(&dev) != hipSuccess) return false;
   if (hipDeviceGetAttribute(&cus, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || cus != NWG)
     return false;
   const size_t lds = persist_lds_bytes(hd, HT);
-  if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) return false;
-  if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, NTHR, lds) != hipSuccess) return false;
-  return nb >= 1;
+  for (const void* fn : fns) {
+    if (hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds) != hipSuccess) return false;
+    if (hipOccupancyMaxActiveBlocksPerMultiprocessor(&nb, fn, NTHR, lds) != hipSuccess || nb < 1) return false;
+  }
+  return true;
 }
 
 // A plain launch: the plan builder has checked that every workgroup fits on
@@ -1226,7 +1254,7 @@ bool persist_resident(int d, int hd, int HT) {
 hipError_t launch_persist(const PersistArgs& a, hipStream_t s) {
   const size_t lds = persist_lds_bytes(a.hd, a.HT);
   void* args[] = {const_cast<PersistArgs*>(&a)};
-  const void* fn = persist_fn(a.hd, a.d);
+  const void* fn = persist_fn(a.hd, a.d, a.n);
   if (!fn) return hipErrorInvalidValue;
   hipError_t e = hipFuncSetAttribute(fn, hipFuncAttributeMaxDynamicSharedMemorySize, (int)lds);
   if (e != hipSuccess) return e;

@@ -30,6 +30,12 @@ CASES = {
                                              prefix_len=70, d_action=7, d_state=7, n_steps=2, seed_base=6200),
     "d1024_hd128_t1": SMALL.with_(name="d1024", d_model=1024, head_dim=128, d_ff=4096, d_prefix=1024,
                                   n_action=33, prefix_len=129, n_steps=1, seed_base=6300),
+    # chunks of up to 50 rows fold rows 48-49 of the GEMM phases' operand into
+    # one load per wave; longer chunks (51..64 rows) take the unfolded form
+    "chunk49_one_tail_row": SMALL.with_(name="n49", n_action=49, prefix_len=64, n_steps=2, seed_base=6400),
+    "chunk61_unfolded": SMALL.with_(name="n61", n_action=61, prefix_len=45, n_steps=2, seed_base=6500),
+    "chunk64_unfolded_d1024": SMALL.with_(name="n64", d_model=1024, head_dim=128, d_ff=4096, d_prefix=1024,
+                                          n_action=64, prefix_len=90, n_steps=1, seed_base=6600),
 }
 
 
@@ -41,17 +47,23 @@ def torch():
     return t
 
 
-def _run(cfg, W, inp, tau, loop_mode, reps=1):
+def _run(cfg, W, inp, tau, loop_mode, reps=1, expect_persist=True):
     from vla_testlib import Pipeline
     pipe = Pipeline(cfg, W, inp, loop_mode)
     import torch
     try:
         pipe.build_cache()
+        if loop_mode == 2:
+            pipe.model.set_trace(1)   # the persistent kernel's marks show that it ran
         outs = []
         for _ in range(reps):
             out = pipe.denoise(tau)
             torch.cuda.synchronize()
             outs.append(out.cpu().numpy().astype(np.float64).copy())
+        if loop_mode == 2:
+            tr = pipe.model.trace_read()
+            ran = tr is not None and bool(tr.any())
+            assert ran == expect_persist, f"persistent kernel ran: {ran}, expected {expect_persist}"
         return outs
     finally:
         pipe.close()
@@ -104,7 +116,7 @@ def test_ineligible_model_falls_back(torch):
     W = wl.make_weights(cfg)
     inp = wl.make_batch(cfg, 2)
     tau = wl.uniform_schedule(cfg.n_steps)
-    a = _run(cfg, W, inp, tau, loop_mode=2)[0]
+    a = _run(cfg, W, inp, tau, loop_mode=2, expect_persist=False)[0]
     b = _run(cfg, W, inp, tau, loop_mode=1)[0]
     assert np.array_equal(a, b)
 
