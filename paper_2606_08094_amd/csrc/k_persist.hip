@@ -681,6 +681,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   // split that holds them is the phase's longest path).
   const int nps = (nbp + a.kba - 1) / a.kba;
   const bool att_on = rank < S;
+  const bool pre_split = __builtin_amdgcn_readfirstlane(rank < nps ? 1 : 0) != 0;   // holds prefix keys
   const int jbeg = rank < nps ? rank * a.kba : nbp + (rank - nps);
   const int nblk = att_on ? (rank < nps ? min(nbp, jbeg + a.kba) : jbeg + 1) - jbeg : 0;
   uint4 kpre[NKI], vpre[NKI];
@@ -777,8 +778,13 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       mark();
       arrive<false>(sy, team, rank);
       const unsigned pk1 = flag_peek<false>(sy, team);
-      prefetch_kv(l);
-      if (att_on) stage_prefix();   // independent of this step: done while the team arrives
+      // Prefix K / V of a prefix split, independent of this step: loaded and
+      // staged while the team arrives.  Other ranks load nothing here (a
+      // chunk split's block is filled after the barrier).
+      if (pre_split) {
+        prefetch_kv(l);
+        stage_prefix();
+      }
       if (!wait_flags<false>(sy, team, &flag, pk1)) return bail();
       mark();
 
