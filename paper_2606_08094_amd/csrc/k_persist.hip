@@ -959,6 +959,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       // threads share each 8-column vector: thread quarter q merges splits
       // q, q+4, ... (one round of loads), then the four combine through lane
       // shuffles.
+      // a merge thread loads splits qtr, qtr + 4, ...: MBX = 4 covers up to 16 splits
+      auto merge = [&]<int MBX>(std::integral_constant<int, MBX>) {
       if (ot < QT) {
         const int cw8 = HTD / 8;                          // merged columns per rank (8 .. 32)
         const int nv = 16 * (cw8 / 8);                    // 16-byte vectors (<= 64)
@@ -972,17 +974,17 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
 #pragma unroll
           for (int e = 0; e < 8; ++e) acc8[e] = 0.f;
           float mx = -INFINITY, tot = 0.f;
-          uint4 v[MB];
-          float2 st[MB];
+          uint4 v[MBX];
+          float2 st[MBX];
 #pragma unroll
-          for (int q = 0; q < MB; ++q) {
+          for (int q = 0; q < MBX; ++q) {
             const int sp = qtr + 4 * q;
             const bool ok = live && sp < S;   // absent splits read (0, 0): skipped below
             st[q] = ld8f<LDX>(ASr, ok ? (unsigned)(((sp * n + m) * HT + hh) * 2) * 4u : OOB);
             v[q] = ld16<LDX>(APr, ok ? (unsigned)((sp * n + m) * HTD + cv * 8) * 2u : OOB);
           }
 #pragma unroll
-          for (int q = 0; q < MB; ++q) {
+          for (int q = 0; q < MBX; ++q) {
             if (st[q].y <= 0.f) continue;
             const float mnew = fmaxf(mx, st[q].x);
             const float corr = exp2f(mx - mnew);
@@ -1014,6 +1016,9 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
           }
         }
       }
+      };
+      if (S <= 16) merge(std::integral_constant<int, 4>{});
+      else merge(std::integral_constant<int, MB>{});
       mark();
       arrive<false>(sy, team, rank);
       if (!wait_flags<false>(sy, team, &flag, flag_peek<false>(sy, team))) return bail();
