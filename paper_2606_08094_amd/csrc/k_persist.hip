@@ -153,9 +153,10 @@ VLA_DEV bool wait_flags(Sync& s, int team, int* lds_flag, unsigned peek) {
     if (!__all(peek >= target)) {
       long it = 0;
       while (true) {
-        // about 256 clocks between polls: fewer polls on the 8 hot flag lines
-        // let the flag stores through sooner (measured best among 1, 2, 4, 8, 16)
-        __builtin_amdgcn_s_sleep(4);
+        // Grid polls about 256 clocks apart: fewer polls on the flag lines in
+        // far memory let the flag stores through sooner.  Team polls read the
+        // XCD's L2 and go back to back.
+        if (GRID) __builtin_amdgcn_s_sleep(4);
         if (__all(flag_peek<GRID>(s, team) >= target)) break;
         if (++it > s.spin_limit) {
           if (threadIdx.x == 0) __hip_atomic_fetch_or(s.err, 1, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
