@@ -254,6 +254,13 @@ VLA_DEV void touch_l2(const u32x4_t& rs, unsigned voff, unsigned char* lds) {
   const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "s"(lb), "v"(voff), "s"(rs) : "memory", "m0");
 }
+// As dma_x16, with the default cache policy (read-only data).
+VLA_DEV void dma_x16_ro(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned char* lds) {
+  typedef __attribute__((address_space(3))) unsigned char lds_u8;
+  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
+  asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
+               : : "s"(lb), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
+}
 template <int N>
 VLA_DEV void vm_wait_mem() { asm volatile("s_waitcnt vmcnt(%0)" : : "n"(N) : "memory"); }
 
@@ -724,20 +731,24 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
   };
 
   WTile<2> wq, wg, wd;
-  uint4 wo[OTW][OKS];                      // O: this wave's W_o rows (OTW tiles of 16) over K = HT * hd
   const int CW = d / TSIZE;                // O-projection columns per rank (16 or 32)
   const int ot = rank / 8, ocb = rank % 8; // merge: query tile and column eighth of this rank
+  // The rank's W_o rows (OTW tiles of 16) over K = HT * hd, loaded once per
+  // workgroup by direct-to-LDS loads (every wave of the O phase uses the same
+  // operand) into the LDS past the O phase's activation tile: block
+  // (t, ks) of 1 KB holds the 16 bytes lane l feeds to the MFMA at byte 16 l.
+  // Absent blocks read zero.  Nothing in the merge phase uses that LDS, and
+  // the merge's arrival waits for these loads.
+  constexpr int WOFF = 64 * (256 + 8) * 2;   // past the largest activation tile
   auto prefetch_wo = [&](int l) {
-    const rsrc_t W = mkr(lt[l].wo, (size_t)d * dq * 2);
+    const u32x4_t rs = rsrc_words(lt[l].wo, (unsigned)((size_t)d * dq * 2));
     const unsigned vb = (unsigned)(r16 * dq + team * HTD + 8 * g4) * 2u;
 #pragma unroll
-    for (int t = 0; t < OTW; ++t) {
-      const int cl = 16 * t;
-      const bool on = wave < QT && cl < CW;
-      const unsigned sb = on ? (unsigned)(rank * CW + cl) * (unsigned)dq * 2u : 0u;
-#pragma unroll
-      for (int ks = 0; ks < OKS; ++ks)
-        wo[t][ks] = (on && 32 * ks < HTD) ? bld16(W, vb + 64u * ks, sb, 0) : make_uint4(0, 0, 0, 0);
+    for (int i = 0; i < OTW * OKS / NW; ++i) {
+      const int b = wave + NW * i, t = b / OKS, ks = b - t * OKS;
+      const bool on = 16 * t < CW && 32 * ks < HTD;
+      const unsigned so = on ? (unsigned)(rank * CW + 16 * t) * (unsigned)dq * 2u : 0x7ffffff0u;
+      dma_x16_ro(rs, vb + 64u * ks, so, smem + WOFF + b * 1024);
     }
   };
 
@@ -1055,7 +1066,8 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
             for (int ks = 0; ks < OKS; ++ks) {
               if (32 * ks >= HTD) break;
               const uint4 av = *reinterpret_cast<const uint4*>(otile + (16 * wave + r16) * OP + 32 * ks + 8 * g4);
-              mma16(acc, av, wo[t][ks], bf16_t());
+              const uint4 wv = *reinterpret_cast<const uint4*>(smem + WOFF + (t * OKS + ks) * 1024 + lane * 16);
+              mma16(acc, av, wv, bf16_t());
             }
             const int col = rank * CW + cl + r16;
 #pragma unroll
