@@ -237,27 +237,27 @@ VLA_DEV u32x4_t rsrc_words(const void* base, unsigned bytes) {
                  (unsigned)__builtin_amdgcn_readfirstlane(bytes), 0x00020000u};
 }
 // One wave-wide device-coherent (sc1) buffer load of 16 bytes per lane into
-// LDS at the wave-uniform lds + 16 lane.  Written as asm so that the compiler
+// LDS at base + off + 16 lane (off wave-uniform; the LDS address is taken from
+// base, the kernel's LDS array, and offset, so the compiler needs no null check).  Written as asm so that the compiler
 // adds no waits of its own for it; the caller's vmcnt waits order it.
-VLA_DEV void dma_x16(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned char* lds) {
+VLA_DEV void dma_x16(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned char* base, unsigned off) {
   typedef __attribute__((address_space(3))) unsigned char lds_u8;
-  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
+  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)base + off);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen sc1 lds"
                : : "s"(lb), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
 }
-// One wave-wide load of 4 bytes per lane into LDS at the wave-uniform
-// lds + 4 lane, with the default cache policy.  Used only to bring lines into
+// One wave-wide load of 4 bytes per lane into LDS at base + off + 4 lane, with the default cache policy.  Used only to bring lines into
 // the XCD's L2 (the LDS copy is never read); asm, like dma_x16, and waited for
 // by the next full wait.
-VLA_DEV void touch_l2(const u32x4_t& rs, unsigned voff, unsigned char* lds) {
+VLA_DEV void touch_l2(const u32x4_t& rs, unsigned voff, unsigned char* base, unsigned off) {
   typedef __attribute__((address_space(3))) unsigned char lds_u8;
-  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
+  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)base + off);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dword %1, %2, 0 offen lds" : : "s"(lb), "v"(voff), "s"(rs) : "memory", "m0");
 }
 // As dma_x16, with the default cache policy (read-only data).
-VLA_DEV void dma_x16_ro(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned char* lds) {
+VLA_DEV void dma_x16_ro(const u32x4_t& rs, unsigned voff, unsigned soff, unsigned char* base, unsigned off) {
   typedef __attribute__((address_space(3))) unsigned char lds_u8;
-  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)lds);
+  const unsigned lb = __builtin_amdgcn_readfirstlane((unsigned)(uintptr_t)(lds_u8*)base + off);
   asm volatile("s_mov_b32 m0, %0\n\tbuffer_load_dwordx4 %1, %2, %3 offen lds"
                : : "s"(lb), "v"(voff), "s"(rs), "s"(soff) : "memory", "m0");
 }
@@ -291,7 +291,7 @@ VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase
     const unsigned off = (gg < NG && kc < K && rr < M)
                              ? (unsigned)((((kc >> 5) + gg % VPL) * M + rr) * 64 + (lane & 3) * 16)
                              : 0x7ffffff0u;
-    dma_x16(rs, off, 0u, ws + 3 * 1024);
+    dma_x16(rs, off, 0u, stage, (unsigned)(wave * XSTAGE + 3 * 1024));
   }
   unsigned vo[4];
 #pragma unroll
@@ -304,7 +304,7 @@ VLA_DEV void tile_mma(f32x4 (&acc)[4][NS], const WTile<NS>& t, const void* xbase
 #pragma unroll
       for (int ms = 0; ms < LPG; ++ms) {
         const unsigned so = kc < K ? (unsigned)(((kc >> 5) + v) * M * 64 + ms * 16 * 64) : 0x7ffffff0u;
-        dma_x16(rs, vo[ms], so, ws + ((j * VPL + v) * 4 + ms) * 1024);
+        dma_x16(rs, vo[ms], so, stage, (unsigned)(wave * XSTAGE + ((j * VPL + v) * 4 + ms) * 1024));
       }
   }
 #pragma unroll
@@ -748,7 +748,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       const int b = wave + NW * i, t = b / OKS, ks = b - t * OKS;
       const bool on = 16 * t < CW && 32 * ks < HTD;
       const unsigned so = on ? (unsigned)(rank * CW + 16 * t) * (unsigned)dq * 2u : 0x7ffffff0u;
-      dma_x16_ro(rs, vb + 64u * ks, so, smem + WOFF + b * 1024);
+      dma_x16_ro(rs, vb + 64u * ks, so, smem, (unsigned)(WOFF + b * 1024));
     }
   };
 
@@ -950,10 +950,10 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         const u32x4_t rd = rsrc_words((const bf16_t*)ly.wd + (size_t)team * F8, (unsigned)((size_t)(d - 1) * a.F * 2 + F8 * 2));
         const int lpr = F8 * 2 / 64;       // 64-byte pieces of a down-projection row
         __builtin_amdgcn_s_sleep(40);
-        for (int it = w0; it < (int)(gub / 4096u); it += nwv) touch_l2(rg, (unsigned)it * 4096u + lane * 64u, smem + wave * 256);
+        for (int it = w0; it < (int)(gub / 4096u); it += nwv) touch_l2(rg, (unsigned)it * 4096u + lane * 64u, smem, (unsigned)wave * 256u);
         for (int it = w0; it < d * lpr / 64; it += nwv) {
           const int pc = it * 64 + lane, row = pc / lpr;
-          touch_l2(rd, (unsigned)(row * a.F * 2 + (pc - row * lpr) * 64), smem + wave * 256);
+          touch_l2(rd, (unsigned)(row * a.F * 2 + (pc - row * lpr) * 64), smem, (unsigned)wave * 256u);
         }
       }
       mark();
