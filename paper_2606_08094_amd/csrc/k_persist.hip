@@ -21,9 +21,7 @@
 // to a workgroup.  After the last layer R also runs the head, the Euler update
 // and the next step's input embedding.  Weights and cached prefix K/V do not
 // depend on the step's activations: a workgroup issues their loads before it
-// waits at the barrier that precedes the phase using them (into registers,
-// or, for W_o, which all four waves share, into LDS).  The ranks without an
-// attention split pull the layer's MLP weights into their XCD's L2 meanwhile.
+// waits at the barrier that precedes the phase using them.
 //
 // Memory model: data that one workgroup writes and another reads is stored
 // with plain (write-through) stores and read with device-coherent (sc1) buffer
