@@ -938,7 +938,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       } else if (S < TSIZE) {
         // A rank without a key split brings its share of the team's MLP
         // weights of this layer into the XCD's L2 (one 4-byte load per 64
-        // bytes): the gate / up rows, then the down projection's columns.  The
+        // bytes): the gate / up rows, then the down projection's block.  The
         // G and D phases' weight loads, issued at the barriers before them,
         // then hit there instead of waiting for HBM, and the polls queued
         // behind those loads return sooner.  Started about 1 us into the
@@ -947,14 +947,11 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
         const size_t gurows = (size_t)(a.glu ? 2 : 1) * F8;
         const unsigned gub = (unsigned)(gurows * d * 2);
         const u32x4_t rg = rsrc_words((const bf16_t*)ly.wgu + (size_t)team * gurows * d, gub);
-        const u32x4_t rd = rsrc_words((const bf16_t*)ly.wd + (size_t)team * F8, (unsigned)((size_t)(d - 1) * a.F * 2 + F8 * 2));
-        const int lpr = F8 * 2 / 64;       // 64-byte pieces of a down-projection row
+        const unsigned db = (unsigned)((size_t)d * F8 * 2);
+        const u32x4_t rd = rsrc_words((const bf16_t*)ly.wd + (size_t)team * d * F8, db);
         __builtin_amdgcn_s_sleep(40);
         for (int it = w0; it < (int)(gub / 4096u); it += nwv) touch_l2(rg, (unsigned)it * 4096u + lane * 64u, smem, (unsigned)wave * 256u);
-        for (int it = w0; it < d * lpr / 64; it += nwv) {
-          const int pc = it * 64 + lane, row = pc / lpr;
-          touch_l2(rd, (unsigned)(row * a.F * 2 + (pc - row * lpr) * 64), smem, (unsigned)wave * 256u);
-        }
+        for (int it = w0; it < (int)(db / 4096u); it += nwv) touch_l2(rd, (unsigned)it * 4096u + lane * 64u, smem, (unsigned)wave * 256u);
       }
       mark();
       // A rank without a key split stored nothing here and arrives at once;
@@ -1141,7 +1138,7 @@ __global__ __launch_bounds__(NTHR, 1) void persist_kernel(PersistArgs a) {
       {
         int wr[2];
         dn_rows(wr);
-        prefetch_w<2>(wd, mkr(ly.wd, (size_t)d * a.F * 2), a.F, team * F8, F8, wr);
+        prefetch_w<2>(wd, mkr((const bf16_t*)ly.wd + (size_t)team * d * F8, (size_t)d * F8 * 2), F8, 0, F8, wr);
       }
       if (!wait_flags<false>(sy, team, &flag, pk4)) return bail();
       mark();

@@ -135,6 +135,9 @@ struct vla_model {
   float *b_t1 = nullptr, *b_t2 = nullptr, *b_fm = nullptr, *b_mod = nullptr;
   float *mod_static = nullptr, *modf_static = nullptr;
   std::vector<std::vector<SubW>> layers;
+  // persistent kernel: each layer's W_d (or W2) once more, team-major (team t's
+  // d_ff / 8 columns as one [d][d_ff / 8] block); built on the first persistent plan
+  std::vector<const void*> wd_team;
   std::map<std::tuple<int, int, int, int>, std::unique_ptr<Plan>> plans;
   std::map<std::pair<int, int>, std::unique_ptr<PrefixWs>> prefix_ws;
   int loop_mode = 2;
@@ -531,6 +534,24 @@ vla_status build_plan(vla_model* m, Plan* p) {
     pa.eps = c.rms_eps;
     pa.scale = 1.0f / std::sqrt((float)hd);
     const size_t layer_block = (size_t)2 * B * c.n_kv_heads * P * hd;
+    // Team t reads only columns [t F / 8, (t + 1) F / 8) of W_d: one contiguous
+    // block per team instead of d pieces of F / 4 bytes, F * es bytes apart.
+    if (m->wd_team.empty()) {
+      Alloc am{m->allocs};
+      const size_t F8 = (size_t)F / 8;
+      std::vector<const void*> wt(L);
+      for (int l = 0; l < L; ++l) {
+        void* dst = nullptr;
+        VLA_TRY(am(&dst, (size_t)d * F * es));
+        const char* src = static_cast<const char*>(m->layers[l][1].dn);
+        for (int t = 0; t < 8; ++t)
+          HIP_TRY(hipMemcpy2D(static_cast<char*>(dst) + t * d * F8 * es, F8 * es, src + t * F8 * es, (size_t)F * es,
+                              F8 * es, d, hipMemcpyDeviceToDevice));
+        wt[l] = dst;
+      }
+      HIP_TRY(hipDeviceSynchronize());
+      m->wd_team = wt;
+    }
     std::vector<PLayer> hl(L);
     for (int l = 0; l < L; ++l) {
       const std::vector<SubW>& subs = m->layers[l];
@@ -539,7 +560,7 @@ vla_status build_plan(vla_model* m, Plan* p) {
       hl[l].wqkv = subs[0].qkv;
       hl[l].wo = subs[0].o;
       hl[l].wgu = subs[1].gu;
-      hl[l].wd = subs[1].dn;
+      hl[l].wd = m->wd_team[l];
       hl[l].cache_off = (size_t)subs[0].cache_idx * layer_block;
     }
     PLayer* dl = nullptr;

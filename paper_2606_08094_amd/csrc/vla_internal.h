@@ -167,7 +167,7 @@ struct PLayer {
   const void* wqkv;          // [d_q + 2 d_kv][d]
   const void* wo;            // [d][d_q]
   const void* wgu;           // GLU: gate/up interleaved in 16-row blocks [2F][d]; GELU: W1 [F][d]
-  const void* wd;            // [d][F]
+  const void* wd;            // [8][d][F / 8]: team t's columns of W_d [d][F] as one block
   size_t cache_off;          // element offset of this layer's K block in the cache
 };
 
